@@ -1,0 +1,362 @@
+/*
+ * rb.h - request batching for model serving on one MI355X (gfx950).
+ *
+ * The C boundary of the inter-request batching path of TensorFlow-Serving
+ * (Olston et al., 2017), section 2.2.1 "Inter-Request Batching": requests for
+ * a servable wait in that servable's batching queue; a batch is formed by
+ * concatenating the requests' input tensors; queues share one device and are
+ * served round-robin; the batched run is transparent to every caller, who
+ * gets back exactly its own rows. Servables are opaque to the batching layer
+ * (section 2, a servable is a black box behind a type-erased handle).
+ *
+ * Conventions
+ *  - Every call returns rb_status: RB_OK (0) or a negative error code.
+ *    Out-parameters are written only on RB_OK. No C++ exception crosses
+ *    this boundary. rb_status_str() names a code (static string).
+ *  - Host pointers are plain CPU memory; "device pointers" are addresses in
+ *    the context's GPU memory (e.g. a torch CUDA tensor's data_ptr()).
+ *  - Objects are created and destroyed by the caller; destroy calls accept
+ *    NULL. Objects are not thread-safe: one host thread drives a scheduler.
+ *  - Times are int64 nanoseconds of a simulated clock (see rb_sim_run).
+ *  - All row-major. Floats are IEEE binary32; "bf16" storage is bfloat16
+ *    rounded to nearest even, with fp32 accumulation.
+ */
+#ifndef RB_H
+#define RB_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef int32_t rb_status;
+#define RB_OK 0
+#define RB_EINVAL (-1)  /* bad argument, shape or option */
+#define RB_EBUSY (-2)   /* object still in use (bound queues, pending tasks) */
+#define RB_EAGAIN (-3)  /* result not ready yet */
+#define RB_EEMPTY (-4)  /* nothing to run */
+#define RB_ESIZE (-5)   /* destination buffer too small */
+#define RB_ENOENT (-6)  /* unknown or already collected request */
+#define RB_EDEVICE (-7) /* HIP runtime error, or no device in this mode */
+#define RB_ENOMEM (-8)  /* host or device allocation failed */
+#define RB_ERANGE (-9)  /* the device found an id or length outside its bounds */
+
+const char* rb_status_str(rb_status s);
+
+typedef struct rb_ctx rb_ctx;
+typedef struct rb_model rb_model;
+typedef struct rb_sched rb_sched;
+typedef struct rb_queue rb_queue;
+
+/* ---------------------------------------------------------------- context */
+
+/* hip_device >= 0: bind to that GPU. hip_device < 0: host-only context; models
+ * and schedulers created in it can only run in RB_MODE_NO_DEVICE.
+ * RB_EDEVICE if the device cannot be initialised. */
+rb_status rb_ctx_create(int32_t hip_device, rb_ctx** out);
+/* RB_EBUSY while models or schedulers created in it are alive. */
+rb_status rb_ctx_destroy(rb_ctx* ctx);
+
+/* ---------------------------------------------------------------- models */
+
+enum { RB_MODEL_MLP = 0, RB_MODEL_RANKING = 1, RB_MODEL_SEQPOOL = 2 };
+enum { RB_DT_F32 = 0, RB_DT_BF16 = 1 };
+enum { RB_ACT_NONE = 0, RB_ACT_RELU = 1, RB_ACT_SIGMOID = 2, RB_ACT_SOFTMAX = 3 };
+
+/* One dense layer y = act(x W^T + b). w: host [fan_out, fan_in] fp32,
+ * b: host [fan_out] fp32. */
+typedef struct {
+  int32_t fan_in, fan_out, act;
+  const float* w;
+  const float* b;
+} rb_layer_desc;
+
+/* A servable's model (opaque to the queues and the scheduler).
+ *   RB_MODEL_MLP      request rows of layers[0].fan_in floats -> layers.
+ *   RB_MODEL_RANKING  per row: n_tables sum-pooled embedding bags of emb_dim
+ *                     (one per table, in table order) followed by n_dense
+ *                     floats -> layers; layers[0].fan_in must equal
+ *                     n_tables*emb_dim + n_dense. Tables are host
+ *                     [table_rows, emb_dim] fp32 arrays.
+ *   RB_MODEL_SEQPOOL  per sequence: layers on every token, mean over the
+ *                     sequence's tokens, then `head` (act RB_ACT_SOFTMAX or
+ *                     RB_ACT_NONE).
+ * dtype RB_DT_BF16 stores weights and tables as bf16 (rounded to nearest even
+ * from the given fp32), rounds every layer input to bf16 and accumulates in
+ * fp32; the last layer's output stays fp32. RB_DT_F32 keeps fp32 throughout.
+ * RB_ACT_SIGMOID and RB_ACT_SOFTMAX are allowed only on the last layer (MLP
+ * and ranking: sigmoid with fan_out 1) and on the head.
+ * All host arrays are copied; the caller may free them when this returns.
+ * RB_EINVAL on inconsistent shapes. */
+typedef struct {
+  int32_t kind, dtype;
+  int32_t n_layers;
+  const rb_layer_desc* layers;
+  int32_t n_tables;
+  int64_t table_rows;
+  int32_t emb_dim;
+  int32_t n_dense;
+  const float* const* tables;
+  rb_layer_desc head;
+} rb_model_desc;
+
+rb_status rb_model_create(rb_ctx* ctx, const rb_model_desc* desc, rb_model** out);
+/* d_in: floats per request row (tokens: per token); d_out: floats per output row
+ * (seqpool: per sequence). */
+rb_status rb_model_info(const rb_model* m, int32_t* d_in, int32_t* d_out);
+/* RB_EBUSY while a queue is bound to the model. Device memory is released by
+ * the context's deleter thread once work already enqueued has finished, never
+ * on the caller's thread (a large free must not stall inference). */
+rb_status rb_model_destroy(rb_model* m);
+
+/* ---------------------------------------------------------------- scheduler */
+
+enum { RB_MODE_DEVICE = 0, RB_MODE_NO_DEVICE = 1 };
+
+typedef struct {
+  int32_t mode;
+  /* Device mode: dispatched batches are handed to the device in windows of
+   * up to window_batches batches (>= 1); the batches of one model in a window
+   * run in one launch chain (their rows stay in separate, separately padded
+   * batches). 1 runs every batch on its own. */
+  int32_t window_batches;
+  /* Value written into padding rows (and padding tokens) before the forward
+   * pass. 0 in production; NaN shows that padding never reaches an output. */
+  float pad_value;
+  /* Nonzero: time every kernel launch with HIP events (rb_sched_kernel_stats). */
+  int32_t profile;
+} rb_sched_opts;
+
+/* One scheduler owns one HIP stream of the context's device (device mode) and
+ * round-robins its queues onto it. */
+rb_status rb_sched_create(rb_ctx* ctx, const rb_sched_opts* opts, rb_sched** out);
+/* RB_EBUSY while queues exist. Waits for the scheduler's device work. */
+rb_status rb_sched_destroy(rb_sched* s);
+/* Blocks until all device work of the scheduler has finished. RB_ERANGE if a
+ * kernel found an id or a sequence length outside its request's bounds since
+ * the last rb_sync (the offending values contributed nothing). */
+rb_status rb_sync(rb_sched* s);
+/* Kernel timings of a profiling scheduler since its creation (after rb_sync):
+ * kernel names are those of rb_k_* without the prefix ("embbag", ...). */
+rb_status rb_sched_kernel_stats(rb_sched* s, const char* kernel, int64_t* launches, double* total_ms);
+/* The scheduler's HIP stream (hipStream_t), for callers that order their own
+ * work after the scheduler's. */
+rb_status rb_sched_stream(rb_sched* s, void** stream);
+
+/* ---------------------------------------------------------------- queues */
+
+typedef struct {
+  int32_t max_batch_size;            /* rows (sequences for seqpool) per batch, >= 1 */
+  const int32_t* allowed_batch_sizes;/* strictly ascending, last == max_batch_size */
+  int32_t n_allowed;                 /* 0: batches run at their real size */
+  int64_t batch_timeout_ns;          /* > 0; INT64_MAX: batches close by count only */
+  int32_t bucket_len;                /* seqpool: sequences up to this many tokens; else 0 */
+  /* Simulated device time of a batch of padded size P is service_ns[P],
+   * 0 <= P <= max_batch_size (n_service = max_batch_size + 1); NULL: 0. */
+  const int64_t* service_ns;
+  int32_t n_service;
+} rb_queue_opts;
+
+/* Queues may be created and destroyed while the scheduler runs (the set of
+ * queues follows the servables and versions being served); queue ids are
+ * assigned in creation order and round-robin follows them. */
+rb_status rb_queue_create(rb_sched* s, rb_model* m, const rb_queue_opts* opts, rb_queue** out);
+/* RB_EBUSY while the queue holds requests that have not run. */
+rb_status rb_queue_destroy(rb_queue* q);
+rb_status rb_queue_id(const rb_queue* q, int32_t* id);
+
+/* ---------------------------------------------------------------- serving */
+
+/* One request's input tensors (host memory; copied before rb_submit returns).
+ *   MLP:      dense [n_rows, d_in]
+ *   RANKING:  dense [n_rows, n_dense]; lens [n_rows, n_tables] ids per bag;
+ *             ids [sum(lens)] table rows, row after row, bag after bag
+ *   SEQPOOL:  n_rows sequences; lens [n_rows] tokens per sequence (>= 1);
+ *             dense [sum(lens), d_in] tokens, sequence after sequence
+ * n_dense/n_lens/n_ids are element counts. */
+typedef struct {
+  int32_t n_rows;
+  const float* dense;
+  int64_t n_dense;
+  const int32_t* lens;
+  int64_t n_lens;
+  const int32_t* ids;
+  int64_t n_ids;
+} rb_request;
+
+/* Enqueue a request arriving at arrival_ns (non-decreasing per scheduler).
+ * Timeouts due at or before arrival_ns fire first. RB_EINVAL if n_rows < 1 or
+ * > max_batch_size, shapes mismatch, an id is outside its table, or a
+ * sequence is longer than the queue's bucket. Request ids are dense per
+ * scheduler, in submission order. */
+rb_status rb_submit(rb_queue* q, const rb_request* r, int64_t arrival_ns, uint64_t* out_req_id);
+/* Advance the simulated clock, firing batch timeouts due at or before now_ns. */
+rb_status rb_advance(rb_sched* s, int64_t now_ns);
+/* Close the queue's open batch now (no-op if empty). */
+rb_status rb_flush(rb_queue* q);
+
+typedef struct {
+  uint64_t batch_id;
+  int32_t queue;        /* queue id */
+  int32_t real_rows;    /* s */
+  int32_t padded_rows;  /* P */
+  int32_t n_req;
+  int64_t close_ns, dispatch_ns, done_ns;
+  const uint64_t* req_ids; /* valid until the next rb_run_next */
+} rb_batch_info;
+
+/* Dispatch the next closed batch (round-robin over queues, oldest first in a
+ * queue) at max(clock, simulated device free time) and, in device mode,
+ * enqueue its assemble -> forward -> split on the scheduler's stream
+ * (asynchronous). RB_EEMPTY if no queue has a closed batch. */
+rb_status rb_run_next(rb_sched* s, rb_batch_info* out);
+/* Copy request req_id's output rows ([n_rows, d_out] fp32) to dst (host).
+ * RB_EAGAIN if its batch has not finished; RB_ESIZE if dst_bytes is too
+ * small; RB_ENOENT if unknown or already collected. The library drops its copy
+ * after a successful collect. */
+rb_status rb_collect(rb_sched* s, uint64_t req_id, float* dst, size_t dst_bytes, int32_t* out_rows);
+
+/* ---------------------------------------------------------------- trace replay */
+
+/* A servable: its queues (one, or one per length bucket for seqpool; a request
+ * goes to the smallest bucket that holds its longest sequence). */
+typedef struct {
+  int32_t n_queues;
+  rb_queue* const* queues;
+} rb_servable;
+
+/* A whole request trace whose payloads are already in device memory.
+ * Host arrays: servable, arrival_ns, n_rows, max_len (seqpool; else NULL),
+ *   and the [n_requests + 1] element offsets *_off of each request's slice of
+ *   the device arenas (the last entry is the arena's length).
+ * Device arrays: dense (fp32), lens (i32), ids (i32) arenas laid out per
+ *   request as in rb_request, and out, the fp32 output arena receiving
+ *   request r's [n_rows, d_out] rows at out_off[r].
+ * In RB_MODE_NO_DEVICE the device arrays may be NULL. */
+typedef struct {
+  int32_t n_requests;
+  const int32_t* servable;
+  const int64_t* arrival_ns;
+  const int32_t* n_rows;
+  const int32_t* max_len;
+  const float* dense;
+  const int64_t* dense_off;
+  const int32_t* lens;
+  const int64_t* lens_off;
+  const int32_t* ids;
+  const int64_t* ids_off;
+  float* out;
+  const int64_t* out_off;
+} rb_trace;
+
+/* Batch log of a replay (host arrays allocated by the caller).
+ *   req_done_ns [n_requests], req_queue [n_requests] (queue id);
+ *   per batch, in dispatch order, up to max_batches:
+ *   b_queue, b_real, b_padded, b_close_ns, b_dispatch_ns, b_done_ns,
+ *   b_req_begin [max_batches + 1] offsets into b_reqs [n_requests]. */
+typedef struct {
+  int64_t* req_done_ns;
+  int32_t* req_queue;
+  int64_t max_batches;
+  int64_t n_batches; /* out */
+  int32_t* b_queue;
+  int32_t* b_real;
+  int32_t* b_padded;
+  int64_t* b_close_ns;
+  int64_t* b_dispatch_ns;
+  int64_t* b_done_ns;
+  int64_t* b_req_begin;
+  int32_t* b_reqs;
+} rb_log;
+
+/* Replay a trace through the queues with the simulated clock (events at one
+ * timestamp: timeouts in queue-id order, then arrivals in request order, then
+ * the end-of-trace close of count-only queues at the last arrival, then
+ * dispatch while the simulated device is free), and in device mode enqueue
+ * every batch's device work (asynchronous; rb_sync waits). The queues must be
+ * empty; the replay leaves them empty. RB_ESIZE if max_batches is too small. */
+rb_status rb_sim_run(rb_sched* s, const rb_servable* servables, int32_t n_servables,
+                     const rb_trace* trace, rb_log* log);
+
+/* ---------------------------------------------------------------- kernel ABI */
+/* Single kernels of the device path, for tests and measurement. All pointers
+ * are device pointers, `stream` is a hipStream_t (NULL: the null stream), and
+ * launches are asynchronous. The group descriptors (rb_k_req, rb_k_batch) are
+ * device arrays too. */
+
+/* A request of a launch group: [dense_off, dense_end) of the dense arena,
+ * lens from lens_off, [ids_off, ids_end) of the ids arena, output at out_off. */
+typedef struct {
+  int64_t dense_off, dense_end, lens_off, ids_off, ids_end, out_off;
+  int32_t n_rows, pad_;
+} rb_k_req;
+
+typedef struct {
+  int32_t req_begin, n_req; /* requests [req_begin, req_begin + n_req) of the group */
+  int32_t row_base;         /* first row of this batch in the group's row space */
+  int32_t padded;           /* P */
+  int32_t real;             /* s */
+  int32_t seq_T;            /* seqpool: tokens per sequence slot (bucket), else 0 */
+} rb_k_batch;
+
+/* Per padded row: src = element offset of the row's dense input (-1: padding),
+ * aux = ranking: offset of the row's first id; seqpool: sequence length,
+ * lens = ranking: offset of the row's bag lengths, out = offset of the row's
+ * output (-1: padding). */
+typedef struct {
+  int64_t src, aux, lens, out;
+} rb_k_row;
+
+/* Row routing (exclusive prefix scans): fills rows[row_base .. row_base + P)
+ * of every batch. kind = RB_MODEL_*; d_in floats per row (per token for
+ * seqpool); d_out floats per output row; n_tables bags per ranking row.
+ * A request whose payload does not match its n_rows (dense length, bag
+ * lengths vs ids, sequence lengths outside [1, seq_T]) sets *err = 1 and
+ * contributes no ids / no tokens. */
+rb_status rb_k_route(void* stream, int32_t kind, const rb_k_batch* batches, int32_t n_batches,
+                     const rb_k_req* reqs, const int32_t* lens, int32_t d_in, int32_t d_out,
+                     int32_t n_tables, rb_k_row* rows, int32_t* err);
+/* Gather rows into X [n_rows_total, ldx] (ldx >= d_in, columns [d_in, ldx)
+ * zeroed), padding rows set to pad; out_bf16 != 0 writes bf16 (RNE), else fp32.
+ * Seqpool (seq_T > 0): row r*T + t is token t of sequence slot r (pad past L). */
+rb_status rb_k_assemble(void* stream, const rb_k_row* rows, int32_t n_rows_total, int32_t seq_T,
+                        const float* dense, int64_t dense_len, int32_t d_in, void* X, int32_t ldx,
+                        int32_t out_bf16, float pad, int32_t* err);
+/* Ranking input: X[r] = [bf16(sum of bag f of row r from table f), f = 0..n_tables-1 |
+ * bf16(dense) | 0 ...] with row stride ldx; tables: n_tables device pointers
+ * (in a device array) to [table_rows, emb_dim] bf16. emb_dim must be 64. */
+rb_status rb_k_embbag(void* stream, const rb_k_row* rows, int32_t n_rows_total, const int32_t* lens,
+                      const int32_t* ids, const void* const* tables, int32_t n_tables, int64_t table_rows,
+                      int32_t emb_dim, const float* dense, int32_t n_dense, void* X, int32_t ldx,
+                      float pad, int32_t* err);
+/* Y[M, N] = act(X[M, K] W[N, K]^T + b), bf16 X and W (row strides ldx, ldw),
+ * fp32 accumulation; Y bf16 (out_f32 == 0) or fp32, row stride ldy. K % 64 == 0,
+ * N % 64 == 0. act: RB_ACT_NONE or RB_ACT_RELU. */
+rb_status rb_k_gemm_bf16(void* stream, const void* X, int32_t ldx, const void* W, int32_t ldw,
+                         const float* b, void* Y, int32_t ldy, int32_t M, int32_t N, int32_t K,
+                         int32_t act, int32_t out_f32);
+/* fp32 variant (fp32 MFMA); same layout rules. */
+rb_status rb_k_gemm_f32(void* stream, const float* X, int32_t ldx, const float* W, int32_t ldw,
+                        const float* b, float* Y, int32_t ldy, int32_t M, int32_t N, int32_t K, int32_t act);
+/* Narrow last layer fused with the split: out[rows[r].out] = act(H[r, :K] . w + b)
+ * for real rows (act RB_ACT_SIGMOID or RB_ACT_NONE); H bf16 [n_rows_total, ldh],
+ * w bf16 [K]. */
+rb_status rb_k_head(void* stream, const rb_k_row* rows, int32_t n_rows_total, const void* H, int32_t ldh,
+                    const void* w, float b, int32_t K, int32_t act, float* out);
+/* Seqpool head fused with the split: per sequence slot r with L = rows[r].aux
+ * real tokens, pooled = mean of H[r*T + t, :D] over t < L (fp32; tokens past L
+ * are never read), then out[rows[r].out + j] = act(Wh pooled + bh)[j], j < n_out
+ * (act RB_ACT_SOFTMAX or RB_ACT_NONE; D <= 1024, n_out <= 16). */
+rb_status rb_k_seqpool(void* stream, const rb_k_row* rows, int32_t n_seqs, int32_t seq_T, const float* H,
+                       int32_t ldh, int32_t D, const float* Wh, const float* bh, int32_t n_out, int32_t act,
+                       float* out);
+/* Split: out[rows[r].out + j] = Y[r, j] for real rows, j < d_out. */
+rb_status rb_k_split(void* stream, const rb_k_row* rows, int32_t n_rows_total, const float* Y, int32_t ldy,
+                     int32_t d_out, float* out);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* RB_H */

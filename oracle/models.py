@@ -103,10 +103,11 @@ class OracleModel:
 
     def forward(self, payload) -> np.ndarray:
         """Output rows [n, d_out] (float32) of one request run on its own."""
+        m = self.model
         if self.kind == "mlp":
-            return self.mlp(self._round_in(payload.dense)).astype(np.float32)
+            return self.mlp(self._round_in(np.asarray(payload.dense).reshape(-1, m.d_in))).astype(np.float32)
         if self.kind == "ranking":
-            X = self.ranking_input(payload.dense, payload.lens, payload.ids)
+            X = self.ranking_input(np.asarray(payload.dense).reshape(-1, m.n_dense), payload.lens, payload.ids)
             return self.mlp(X).astype(np.float32)
         # seqpool: each sequence on its own, over its own tokens only
         lens = np.asarray(payload.lens, np.int64)

@@ -1,0 +1,729 @@
+// Device kernels of the batched inference path, written for gfx950 (CDNA4,
+// wave64, MFMA, 160 KB LDS per CU).
+//
+// A launch group is a set of dispatched batches of one queue. Its rows live in
+// one row space: batch b owns rows [row_base_b, row_base_b + P_b), the first
+// s_b of them real, the rest padding (the batch axis padded to an allowed
+// size). The kernels, in the order a group runs them:
+//
+//   route     per-batch exclusive prefix scans: which request row (or padding)
+//             every row is, where its input and output live (the paper's
+//             concatenation of input tensors, section 2.2.1, as an index map)
+//   assemble  gather request rows into the padded batch tensor (optional
+//             fp32 -> bf16 cast), or
+//   embbag    sum-pool each row's embedding bags (ranking models)
+//   gemm      dense layers with fused bias + activation (bf16 or fp32 MFMA)
+//   head /    narrow last layer or masked mean-pool + softmax head, writing
+//   seqpool   straight to each request's output rows
+//   split     copy real rows to their requests' outputs (padding dropped)
+//
+// Every row is computed the same way whatever batch it sits in (one tile
+// shape and k order per layer, no row-count-dependent split of the sum), so a
+// request's result does not depend on how its batch was composed.
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "../../include/rb.h"
+
+namespace {
+
+typedef uint16_t bf16_t;
+typedef __attribute__((__vector_size__(8 * sizeof(short)))) short bf16x8_t;
+typedef __attribute__((__vector_size__(4 * sizeof(float)))) float floatx4_t;
+typedef __attribute__((__vector_size__(16 * sizeof(float)))) float floatx16_t;
+typedef unsigned int u32x4_t __attribute__((ext_vector_type(4)));
+
+__device__ __forceinline__ bf16_t f2bf(float f) {
+  // round to nearest even on the 16 dropped bits; NaN stays a (quiet) NaN
+  uint32_t u = __float_as_uint(f);
+  if ((u & 0x7fffffffu) > 0x7f800000u) return (bf16_t)((u >> 16) | 0x40u);
+  u += 0x7fffu + ((u >> 16) & 1u);
+  return (bf16_t)(u >> 16);
+}
+
+__device__ __forceinline__ float bf2f(uint32_t h) { return __uint_as_float(h << 16); }
+
+__device__ __forceinline__ uint32_t pack2(float a, float b) {
+  return (uint32_t)f2bf(a) | ((uint32_t)f2bf(b) << 16);
+}
+
+template <int ACT>
+__device__ __forceinline__ float act_fn(float z) {
+  if (ACT == RB_ACT_RELU) return z > 0.f ? z : 0.f;
+  if (ACT == RB_ACT_SIGMOID) return 1.f / (1.f + expf(-z));
+  return z;
+}
+
+__device__ __forceinline__ float wave_sum(float v) {
+  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o);
+  return v;
+}
+
+// ---------------------------------------------------------------- route
+
+// One workgroup per batch. Phase 1: block-wide exclusive scan of the
+// requests' row counts (256 requests per pass, carried across passes) gives
+// each request's first row in the batch. Phase 2: the thread owning a request
+// validates its payload and writes its rows' entries (ranking: a running sum
+// of the rows' bag lengths gives each row's first id; seqpool: a running sum
+// of sequence lengths gives each sequence's first token). Phase 3: padding.
+__global__ __launch_bounds__(256) void k_route(int kind, const rb_k_batch* __restrict__ batches,
+                                               const rb_k_req* __restrict__ reqs,
+                                               const int32_t* __restrict__ lens, int d_in, int d_out,
+                                               int n_tables, rb_k_row* __restrict__ rows,
+                                               int* __restrict__ err) {
+  const rb_k_batch b = batches[blockIdx.x];
+  const int tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
+  __shared__ int s_wsum[4];
+  __shared__ int s_carry;
+  if (tid == 0) s_carry = 0;
+  __syncthreads();
+  for (int base = 0; base < b.n_req; base += 256) {
+    const int i = base + tid;
+    rb_k_req rq = {};
+    int n = 0;
+    if (i < b.n_req) {
+      rq = reqs[b.req_begin + i];
+      n = rq.n_rows;
+    }
+    int incl = n;
+    for (int o = 1; o < 64; o <<= 1) {
+      int v = __shfl_up(incl, o);
+      if (lane >= o) incl += v;
+    }
+    if (lane == 63) s_wsum[wid] = incl;
+    __syncthreads();
+    int wofs = 0;
+    for (int w = 0; w < wid; ++w) wofs += s_wsum[w];
+    const int carry = s_carry;
+    const int dst = carry + wofs + incl - n;
+    __syncthreads();
+    if (tid == 255) s_carry = carry + wofs + incl;
+    if (i < b.n_req) {
+      if (dst + n > b.padded) {
+        *err = 1;
+      } else if (kind == RB_MODEL_SEQPOOL) {
+        // rows are sequences; validate lengths against the bucket and the tokens
+        int64_t tok = 0;
+        bool ok = true;
+        for (int e = 0; e < n; ++e) {
+          int L = lens[rq.lens_off + e];
+          ok = ok && L >= 1 && L <= b.seq_T;
+          tok += L;
+        }
+        ok = ok && (tok * d_in == rq.dense_end - rq.dense_off);
+        if (!ok) *err = 1;
+        int64_t t0 = 0;
+        for (int e = 0; e < n; ++e) {
+          int L = lens[rq.lens_off + e];
+          rb_k_row rw;
+          rw.src = ok ? rq.dense_off + t0 * d_in : -1;
+          rw.aux = ok ? L : 0;
+          rw.lens = rq.lens_off + e;
+          rw.out = rq.out_off + (int64_t)e * d_out;
+          rows[b.row_base + dst + e] = rw;
+          t0 += ok ? L : 0;
+        }
+      } else {
+        bool ok = (int64_t)n * d_in == rq.dense_end - rq.dense_off;
+        bool ids_ok = true;
+        if (kind == RB_MODEL_RANKING) {
+          int64_t tot = 0;
+          for (int e = 0; e < n * n_tables; ++e) {
+            int L = lens[rq.lens_off + e];
+            ids_ok = ids_ok && L >= 0;
+            tot += L;
+          }
+          ids_ok = ids_ok && tot == rq.ids_end - rq.ids_off;
+        }
+        if (!ok || !ids_ok) *err = 1;
+        int64_t id0 = rq.ids_off;
+        for (int e = 0; e < n; ++e) {
+          rb_k_row rw;
+          rw.src = ok ? rq.dense_off + (int64_t)e * d_in : -1;
+          rw.aux = id0;
+          rw.lens = (kind == RB_MODEL_RANKING && ids_ok) ? rq.lens_off + (int64_t)e * n_tables : -1;
+          rw.out = rq.out_off + (int64_t)e * d_out;
+          if (kind == RB_MODEL_RANKING && ids_ok)
+            for (int f = 0; f < n_tables; ++f) id0 += lens[rq.lens_off + (int64_t)e * n_tables + f];
+          rows[b.row_base + dst + e] = rw;
+        }
+      }
+    }
+    __syncthreads();
+  }
+  const int s = s_carry;
+  for (int p = s + tid; p < b.padded; p += 256) {
+    rb_k_row rw;
+    rw.src = -1;
+    rw.aux = 0;
+    rw.lens = -1;
+    rw.out = -1;
+    rows[b.row_base + p] = rw;
+  }
+}
+
+// ---------------------------------------------------------------- assemble
+
+// One thread per 8 output elements of a row: coalesced 16-byte stores of the
+// padded batch tensor. Padding rows (and padding tokens) get `pad` in their
+// d_in input columns; columns past d_in are always zero so that they add
+// nothing in the next contraction.
+template <bool BF16>
+__global__ __launch_bounds__(256) void k_assemble(const rb_k_row* __restrict__ rows, int n_rows_total,
+                                                  int seq_T, const float* __restrict__ dense,
+                                                  int64_t dense_len, int d_in, void* __restrict__ X,
+                                                  int ldx, float pad, int* __restrict__ err) {
+  const int chunks = ldx >> 3;
+  const int64_t gid = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  const int64_t r = gid / chunks;
+  if (r >= n_rows_total) return;
+  const int c0 = (int)(gid - r * chunks) * 8;
+  int64_t src;
+  if (seq_T > 0) {
+    const int64_t slot = r / seq_T;
+    const int t = (int)(r - slot * seq_T);
+    const rb_k_row rw = rows[slot];
+    src = (rw.src >= 0 && t < rw.aux) ? rw.src + (int64_t)t * d_in : -1;
+  } else {
+    src = rows[r].src;
+  }
+  float v[8];
+  if (src < 0) {
+#pragma unroll
+    for (int j = 0; j < 8; ++j) v[j] = (c0 + j < d_in) ? pad : 0.f;
+  } else if (src + d_in > dense_len) {
+    *err = 1;
+#pragma unroll
+    for (int j = 0; j < 8; ++j) v[j] = 0.f;
+  } else if ((d_in & 7) == 0 && (src & 3) == 0) {
+    if (c0 < d_in) {
+      const float4 a = *(const float4*)(dense + src + c0);
+      const float4 c = *(const float4*)(dense + src + c0 + 4);
+      v[0] = a.x; v[1] = a.y; v[2] = a.z; v[3] = a.w;
+      v[4] = c.x; v[5] = c.y; v[6] = c.z; v[7] = c.w;
+    } else {
+#pragma unroll
+      for (int j = 0; j < 8; ++j) v[j] = 0.f;
+    }
+  } else {
+#pragma unroll
+    for (int j = 0; j < 8; ++j) v[j] = (c0 + j < d_in) ? dense[src + c0 + j] : 0.f;
+  }
+  if (BF16) {
+    uint4 o;
+    o.x = pack2(v[0], v[1]);
+    o.y = pack2(v[2], v[3]);
+    o.z = pack2(v[4], v[5]);
+    o.w = pack2(v[6], v[7]);
+    *(uint4*)((bf16_t*)X + r * ldx + c0) = o;
+  } else {
+    float* y = (float*)X + r * ldx + c0;
+    *(float4*)y = make_float4(v[0], v[1], v[2], v[3]);
+    *(float4*)(y + 4) = make_float4(v[4], v[5], v[6], v[7]);
+  }
+}
+
+// ---------------------------------------------------------------- embedding bags
+
+constexpr int EMB_DIM = 64;       // one table row = 128 bytes of bf16
+constexpr int MAX_TABLES = 64;
+constexpr int STAGE_IDS = 2048;   // ids of one row staged in LDS (more: read from global)
+
+// One workgroup (4 waves) per row. The row's bag lengths are scanned in LDS
+// and its ids staged in LDS with coalesced loads. Each wave then pools whole
+// bags: 8 lane groups of 8 lanes take every 8th id of the bag, each lane
+// loading 16 bytes (8 dims) of the table row; the 8 partial sums are combined
+// by a butterfly over the groups (fixed order: deterministic per row), rounded
+// to bf16 and stored as one 128-byte row segment. The dense features follow
+// the pooled bags; columns past them are zero.
+__global__ __launch_bounds__(256) void k_embbag(const rb_k_row* __restrict__ rows,
+                                                const int32_t* __restrict__ lens,
+                                                const int32_t* __restrict__ ids,
+                                                const bf16_t* const* __restrict__ tables, int n_tables,
+                                                int64_t table_rows, const float* __restrict__ dense,
+                                                int n_dense, bf16_t* __restrict__ X, int ldx, float pad,
+                                                int* __restrict__ err) {
+  const int r = blockIdx.x;
+  const rb_k_row rw = rows[r];
+  bf16_t* xr = X + (int64_t)r * ldx;
+  const int tid = threadIdx.x;
+  const int demb = n_tables * EMB_DIM;
+  if (rw.src < 0) {
+    const bf16_t p = f2bf(pad);
+    for (int c = tid; c < ldx; c += 256) xr[c] = c < demb + n_dense ? p : (bf16_t)0;
+    return;
+  }
+  __shared__ int s_len[MAX_TABLES];
+  __shared__ int s_start[MAX_TABLES + 1];
+  __shared__ int s_ids[STAGE_IDS];
+  if (tid < n_tables) s_len[tid] = rw.lens >= 0 ? lens[rw.lens + tid] : 0;
+  __syncthreads();
+  if (tid < 64) {
+    // wave-level exclusive scan of the bag lengths
+    int v = tid < n_tables ? s_len[tid] : 0;
+    int incl = v;
+    for (int o = 1; o < 64; o <<= 1) {
+      int u = __shfl_up(incl, o);
+      if (tid >= o) incl += u;
+    }
+    if (tid < n_tables) s_start[tid] = incl - v;
+    if (tid == 63) s_start[n_tables] = incl;
+  }
+  __syncthreads();
+  const int total = s_start[n_tables];
+  const bool staged = total <= STAGE_IDS;
+  if (staged)
+    for (int i = tid; i < total; i += 256) s_ids[i] = ids[rw.aux + i];
+  __syncthreads();
+  const int lane = tid & 63, wid = tid >> 6, g = lane >> 3, l8 = lane & 7;
+  for (int f = wid; f < n_tables; f += 4) {
+    float acc[8];
+#pragma unroll
+    for (int k = 0; k < 8; ++k) acc[k] = 0.f;
+    const bf16_t* T = tables[f];
+    const int st = s_start[f], len = s_len[f];
+    for (int j = g; j < len; j += 8) {
+      const int id = staged ? s_ids[st + j] : ids[rw.aux + st + j];
+      if ((uint64_t)(int64_t)id >= (uint64_t)table_rows) {
+        *err = 1;
+        continue;
+      }
+      const uint4 q = *(const uint4*)(T + (int64_t)id * EMB_DIM + l8 * 8);
+      acc[0] += bf2f(q.x & 0xffffu); acc[1] += bf2f(q.x >> 16);
+      acc[2] += bf2f(q.y & 0xffffu); acc[3] += bf2f(q.y >> 16);
+      acc[4] += bf2f(q.z & 0xffffu); acc[5] += bf2f(q.z >> 16);
+      acc[6] += bf2f(q.w & 0xffffu); acc[7] += bf2f(q.w >> 16);
+    }
+#pragma unroll
+    for (int o = 8; o < 64; o <<= 1)
+#pragma unroll
+      for (int k = 0; k < 8; ++k) acc[k] += __shfl_xor(acc[k], o);
+    if (g == 0) {
+      uint4 o;
+      o.x = pack2(acc[0], acc[1]);
+      o.y = pack2(acc[2], acc[3]);
+      o.z = pack2(acc[4], acc[5]);
+      o.w = pack2(acc[6], acc[7]);
+      *(uint4*)(xr + f * EMB_DIM + l8 * 8) = o;
+    }
+  }
+  for (int c = demb + tid; c < ldx; c += 256)
+    xr[c] = c < demb + n_dense ? f2bf(dense[rw.src + (c - demb)]) : (bf16_t)0;
+}
+
+// ---------------------------------------------------------------- bf16 GEMM
+
+// Y = act(X W^T + b): X [M, K] and W [N, K] bf16, K contiguous. Workgroup tile
+// 128 x 128, k-step 64; four waves in a 2 x 2 grid, each owning 64 x 64 as
+// 2 x 2 v_mfma_f32_32x32x16_bf16 accumulators. LDS holds the A and B tiles
+// row-major with 16-byte chunks XOR-swizzled by row (bank-conflict-free
+// 16-byte reads), double-buffered so the next tile's global loads overlap the
+// current tile's MFMAs with one barrier per k-step.
+constexpr int G16_BM = 128, G16_BN = 128, G16_BK = 64;
+
+template <int ACT, bool OUT_F32>
+__global__ __launch_bounds__(256) void k_gemm_bf16(const bf16_t* __restrict__ X, int ldx,
+                                                   const bf16_t* __restrict__ W, int ldw,
+                                                   const float* __restrict__ bias, void* __restrict__ Y,
+                                                   int ldy, int M, int N, int K) {
+  __shared__ u32x4_t sA[2][G16_BM * G16_BK / 8];
+  __shared__ u32x4_t sB[2][G16_BN * G16_BK / 8];
+  const int tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
+  const int wm = wid >> 1, wn = wid & 1;
+  const int tiles_n = N / G16_BN;
+  const int bm = blockIdx.x / tiles_n, bn = blockIdx.x - bm * tiles_n;
+  const int m0 = bm * G16_BM, n0 = bn * G16_BN;
+
+  const int lrow = tid >> 3, lch = tid & 7;
+  const bf16_t* ag[4];
+  const bf16_t* bg[4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    int ra = m0 + lrow + 32 * i;
+    ra = ra < M ? ra : M - 1;  // rows past M are computed on a copy and never stored
+    ag[i] = X + (int64_t)ra * ldx + lch * 8;
+    bg[i] = W + (int64_t)(n0 + lrow + 32 * i) * ldw + lch * 8;
+  }
+  u32x4_t ra_[4], rb_[4];
+  floatx16_t acc[2][2];
+#pragma unroll
+  for (int i = 0; i < 2; ++i)
+#pragma unroll
+    for (int j = 0; j < 2; ++j)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
+
+  const int nk = K / G16_BK;
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    ra_[i] = *(const u32x4_t*)(ag[i]);
+    rb_[i] = *(const u32x4_t*)(bg[i]);
+  }
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const int r = lrow + 32 * i;
+    sA[0][r * 8 + (lch ^ (r & 7))] = ra_[i];
+    sB[0][r * 8 + (lch ^ (r & 7))] = rb_[i];
+  }
+  __syncthreads();
+  for (int kt = 0; kt < nk; ++kt) {
+    const int buf = kt & 1;
+    if (kt + 1 < nk) {
+      const int k0 = (kt + 1) * G16_BK;
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        ra_[i] = *(const u32x4_t*)(ag[i] + k0);
+        rb_[i] = *(const u32x4_t*)(bg[i] + k0);
+      }
+    }
+#pragma unroll
+    for (int kk = 0; kk < 4; ++kk) {
+      bf16x8_t a[2], bv[2];
+      const int ch = kk * 2 + (lane >> 5);
+#pragma unroll
+      for (int i = 0; i < 2; ++i) {
+        const int rA = wm * 64 + i * 32 + (lane & 31);
+        const int rB = wn * 64 + i * 32 + (lane & 31);
+        a[i] = __builtin_bit_cast(bf16x8_t, sA[buf][rA * 8 + (ch ^ (rA & 7))]);
+        bv[i] = __builtin_bit_cast(bf16x8_t, sB[buf][rB * 8 + (ch ^ (rB & 7))]);
+      }
+#pragma unroll
+      for (int i = 0; i < 2; ++i)
+#pragma unroll
+        for (int j = 0; j < 2; ++j)
+          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[i], bv[j], acc[i][j], 0, 0, 0);
+    }
+    if (kt + 1 < nk) {
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int r = lrow + 32 * i;
+        sA[buf ^ 1][r * 8 + (lch ^ (r & 7))] = ra_[i];
+        sB[buf ^ 1][r * 8 + (lch ^ (r & 7))] = rb_[i];
+      }
+    }
+    __syncthreads();
+  }
+  // accumulator (i, j) register r of lane l holds row 8*(r/4) + 4*(l/32) + r%4,
+  // column l%32 of the 32 x 32 block
+#pragma unroll
+  for (int i = 0; i < 2; ++i)
+#pragma unroll
+    for (int j = 0; j < 2; ++j) {
+      const int col = n0 + wn * 64 + j * 32 + (lane & 31);
+      const float bb = bias[col];
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const int row = m0 + wm * 64 + i * 32 + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
+        if (row < M) {
+          const float v = act_fn<ACT>(acc[i][j][r] + bb);
+          if (OUT_F32)
+            ((float*)Y)[(int64_t)row * ldy + col] = v;
+          else
+            ((bf16_t*)Y)[(int64_t)row * ldy + col] = f2bf(v);
+        }
+      }
+    }
+}
+
+// ---------------------------------------------------------------- fp32 GEMM
+
+// fp32 X [M, K], W [N, K]. Workgroup tile 64 x 64, k-step 32; 2 x 2 waves each
+// owning 32 x 32 with v_mfma_f32_32x32x2f32 (one k pair per instruction).
+// Tiles are kept k-major in LDS so that the 32 lanes reading one k read 32
+// consecutive floats.
+constexpr int G32_BM = 64, G32_BN = 64, G32_BK = 32, G32_PAD = 4;
+
+template <int ACT>
+__global__ __launch_bounds__(256) void k_gemm_f32(const float* __restrict__ X, int ldx,
+                                                  const float* __restrict__ W, int ldw,
+                                                  const float* __restrict__ bias, float* __restrict__ Y,
+                                                  int ldy, int M, int N, int K) {
+  __shared__ float sA[2][G32_BK][G32_BM + G32_PAD];
+  __shared__ float sB[2][G32_BK][G32_BN + G32_PAD];
+  const int tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
+  const int wm = wid >> 1, wn = wid & 1;
+  const int tiles_n = N / G32_BN;
+  const int bm = blockIdx.x / tiles_n, bn = blockIdx.x - bm * tiles_n;
+  const int m0 = bm * G32_BM, n0 = bn * G32_BN;
+  const int lrow = tid >> 3, lk = (tid & 7) * 4;
+  const float* ag[2];
+  const float* bg[2];
+#pragma unroll
+  for (int i = 0; i < 2; ++i) {
+    int ra = m0 + lrow + 32 * i;
+    ra = ra < M ? ra : M - 1;
+    ag[i] = X + (int64_t)ra * ldx + lk;
+    bg[i] = W + (int64_t)(n0 + lrow + 32 * i) * ldw + lk;
+  }
+  float4 ra_[2], rb_[2];
+  floatx16_t acc;
+#pragma unroll
+  for (int r = 0; r < 16; ++r) acc[r] = 0.f;
+  const int nk = K / G32_BK;
+  auto stage = [&](int buf) {
+#pragma unroll
+    for (int i = 0; i < 2; ++i) {
+      const int r = lrow + 32 * i;
+      sA[buf][lk + 0][r] = ra_[i].x; sA[buf][lk + 1][r] = ra_[i].y;
+      sA[buf][lk + 2][r] = ra_[i].z; sA[buf][lk + 3][r] = ra_[i].w;
+      sB[buf][lk + 0][r] = rb_[i].x; sB[buf][lk + 1][r] = rb_[i].y;
+      sB[buf][lk + 2][r] = rb_[i].z; sB[buf][lk + 3][r] = rb_[i].w;
+    }
+  };
+#pragma unroll
+  for (int i = 0; i < 2; ++i) {
+    ra_[i] = *(const float4*)(ag[i]);
+    rb_[i] = *(const float4*)(bg[i]);
+  }
+  stage(0);
+  __syncthreads();
+  for (int kt = 0; kt < nk; ++kt) {
+    const int buf = kt & 1;
+    if (kt + 1 < nk) {
+      const int k0 = (kt + 1) * G32_BK;
+#pragma unroll
+      for (int i = 0; i < 2; ++i) {
+        ra_[i] = *(const float4*)(ag[i] + k0);
+        rb_[i] = *(const float4*)(bg[i] + k0);
+      }
+    }
+#pragma unroll
+    for (int kk = 0; kk < G32_BK / 2; ++kk) {
+      const int k = kk * 2 + (lane >> 5);
+      const float a = sA[buf][k][wm * 32 + (lane & 31)];
+      const float bv = sB[buf][k][wn * 32 + (lane & 31)];
+      acc = __builtin_amdgcn_mfma_f32_32x32x2f32(a, bv, acc, 0, 0, 0);
+    }
+    if (kt + 1 < nk) stage(buf ^ 1);
+    __syncthreads();
+  }
+  const int col = n0 + wn * 32 + (lane & 31);
+  const float bb = bias[col];
+#pragma unroll
+  for (int r = 0; r < 16; ++r) {
+    const int row = m0 + wm * 32 + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
+    if (row < M) Y[(int64_t)row * ldy + col] = act_fn<ACT>(acc[r] + bb);
+  }
+}
+
+// ---------------------------------------------------------------- heads and split
+
+// One wave per row: a K-long dot product (lane-strided, then a butterfly),
+// bias, activation, and the store into the request's output row.
+template <int ACT>
+__global__ __launch_bounds__(256) void k_head(const rb_k_row* __restrict__ rows, int n,
+                                              const bf16_t* __restrict__ H, int ldh,
+                                              const bf16_t* __restrict__ w, float b, int K,
+                                              float* __restrict__ out) {
+  const int r = blockIdx.x * 4 + (threadIdx.x >> 6), lane = threadIdx.x & 63;
+  if (r >= n) return;
+  const int64_t o = rows[r].out;
+  if (o < 0) return;
+  const bf16_t* h = H + (int64_t)r * ldh;
+  float s = 0.f;
+  for (int k = lane; k < K; k += 64) s += bf2f(h[k]) * bf2f(w[k]);
+  s = wave_sum(s);
+  if (lane == 0) out[o] = act_fn<ACT>(s + b);
+}
+
+constexpr int POOL_MAX_D = 1024, POOL_MAX_OUT = 16;
+
+// One workgroup per sequence slot: each thread sums one feature over the
+// sequence's L real tokens (coalesced token rows; tokens past L are never
+// read, so padding cannot reach the mean), divides by L, then the block
+// computes the head logits with fixed-order reductions and thread 0 applies
+// the softmax and writes the request's output row.
+__global__ __launch_bounds__(256) void k_seqpool(const rb_k_row* __restrict__ rows, int n_seqs, int T,
+                                                 const float* __restrict__ H, int ldh, int D,
+                                                 const float* __restrict__ Wh,
+                                                 const float* __restrict__ bh, int n_out, int act,
+                                                 float* __restrict__ out) {
+  const int r = blockIdx.x;
+  const rb_k_row rw = rows[r];
+  if (rw.out < 0) return;
+  const int L = (int)rw.aux;
+  const int tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
+  __shared__ float pooled[POOL_MAX_D];
+  __shared__ float part[4][POOL_MAX_OUT];
+  const float* h = H + (int64_t)r * T * ldh;
+  for (int c = tid; c < D; c += 256) {
+    float s = 0.f;
+    for (int t = 0; t < L; ++t) s += h[(int64_t)t * ldh + c];
+    pooled[c] = s / (float)L;
+  }
+  __syncthreads();
+  for (int j = 0; j < n_out; ++j) {
+    float s = 0.f;
+    for (int c = tid; c < D; c += 256) s += Wh[(int64_t)j * D + c] * pooled[c];
+    s = wave_sum(s);
+    if (lane == 0) part[wid][j] = s;
+  }
+  __syncthreads();
+  if (tid == 0) {
+    float z[POOL_MAX_OUT];
+    float mx = -INFINITY;
+    for (int j = 0; j < n_out; ++j) {
+      z[j] = ((part[0][j] + part[1][j]) + (part[2][j] + part[3][j])) + bh[j];
+      mx = fmaxf(mx, z[j]);
+    }
+    if (act == RB_ACT_SOFTMAX) {
+      float den = 0.f;
+      for (int j = 0; j < n_out; ++j) {
+        z[j] = expf(z[j] - mx);
+        den += z[j];
+      }
+      for (int j = 0; j < n_out; ++j) out[rw.out + j] = z[j] / den;
+    } else {
+      for (int j = 0; j < n_out; ++j) out[rw.out + j] = z[j];
+    }
+  }
+}
+
+__global__ __launch_bounds__(256) void k_split(const rb_k_row* __restrict__ rows, int n,
+                                               const float* __restrict__ Y, int ldy, int d_out,
+                                               float* __restrict__ out) {
+  const int64_t gid = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  const int64_t r = gid / d_out;
+  if (r >= n) return;
+  const int c = (int)(gid - r * d_out);
+  const int64_t o = rows[r].out;
+  if (o < 0) return;
+  out[o + c] = Y[r * ldy + c];
+}
+
+inline rb_status launch_status() {
+  return hipGetLastError() == hipSuccess ? RB_OK : RB_EDEVICE;
+}
+
+inline unsigned blocks_for(int64_t threads) { return (unsigned)((threads + 255) / 256); }
+
+}  // namespace
+
+// ---------------------------------------------------------------- kernel ABI
+
+extern "C" {
+
+rb_status rb_k_route(void* stream, int32_t kind, const rb_k_batch* batches, int32_t n_batches,
+                     const rb_k_req* reqs, const int32_t* lens, int32_t d_in, int32_t d_out,
+                     int32_t n_tables, rb_k_row* rows, int32_t* err) {
+  if (n_batches < 0 || !batches || !rows || !err || d_in < 1 || d_out < 1) return RB_EINVAL;
+  if (kind < RB_MODEL_MLP || kind > RB_MODEL_SEQPOOL) return RB_EINVAL;
+  if (kind != RB_MODEL_MLP && !lens) return RB_EINVAL;
+  if (kind == RB_MODEL_RANKING && (n_tables < 1 || n_tables > MAX_TABLES)) return RB_EINVAL;
+  if (n_batches == 0) return RB_OK;
+  hipLaunchKernelGGL(k_route, dim3(n_batches), dim3(256), 0, (hipStream_t)stream, kind, batches, reqs, lens,
+                     d_in, d_out, n_tables, rows, err);
+  return launch_status();
+}
+
+rb_status rb_k_assemble(void* stream, const rb_k_row* rows, int32_t n_rows_total, int32_t seq_T,
+                        const float* dense, int64_t dense_len, int32_t d_in, void* X, int32_t ldx,
+                        int32_t out_bf16, float pad, int32_t* err) {
+  if (n_rows_total < 0 || seq_T < 0 || d_in < 1 || ldx < d_in || (ldx & 7) || !rows || !X || !err)
+    return RB_EINVAL;
+  if (n_rows_total == 0) return RB_OK;
+  const unsigned g = blocks_for((int64_t)n_rows_total * (ldx / 8));
+  if (out_bf16)
+    hipLaunchKernelGGL(k_assemble<true>, dim3(g), dim3(256), 0, (hipStream_t)stream, rows, n_rows_total, seq_T,
+                       dense, dense_len, d_in, X, ldx, pad, err);
+  else
+    hipLaunchKernelGGL(k_assemble<false>, dim3(g), dim3(256), 0, (hipStream_t)stream, rows, n_rows_total, seq_T,
+                       dense, dense_len, d_in, X, ldx, pad, err);
+  return launch_status();
+}
+
+rb_status rb_k_embbag(void* stream, const rb_k_row* rows, int32_t n_rows_total, const int32_t* lens,
+                      const int32_t* ids, const void* const* tables, int32_t n_tables, int64_t table_rows,
+                      int32_t emb_dim, const float* dense, int32_t n_dense, void* X, int32_t ldx, float pad,
+                      int32_t* err) {
+  if (emb_dim != EMB_DIM || n_tables < 1 || n_tables > MAX_TABLES || n_dense < 0 || table_rows < 1)
+    return RB_EINVAL;
+  if (n_rows_total < 0 || ldx < n_tables * EMB_DIM + n_dense || (ldx & 7) || !rows || !X || !err || !tables)
+    return RB_EINVAL;
+  if (n_rows_total == 0) return RB_OK;
+  hipLaunchKernelGGL(k_embbag, dim3(n_rows_total), dim3(256), 0, (hipStream_t)stream, rows, lens, ids,
+                     (const bf16_t* const*)tables, n_tables, table_rows, dense, n_dense, (bf16_t*)X, ldx, pad,
+                     err);
+  return launch_status();
+}
+
+rb_status rb_k_gemm_bf16(void* stream, const void* X, int32_t ldx, const void* W, int32_t ldw, const float* b,
+                         void* Y, int32_t ldy, int32_t M, int32_t N, int32_t K, int32_t act, int32_t out_f32) {
+  if (M < 0 || N <= 0 || K <= 0 || (N % G16_BN) || (K % G16_BK) || ldx < K || ldw < K || ldy < N) return RB_EINVAL;
+  if ((ldx & 7) || (ldw & 7) || !X || !W || !b || !Y) return RB_EINVAL;
+  if (act != RB_ACT_NONE && act != RB_ACT_RELU && act != RB_ACT_SIGMOID) return RB_EINVAL;
+  if (M == 0) return RB_OK;
+  const unsigned g = (unsigned)(((M + G16_BM - 1) / G16_BM) * (N / G16_BN));
+  hipStream_t s = (hipStream_t)stream;
+  const bf16_t* x = (const bf16_t*)X;
+  const bf16_t* w = (const bf16_t*)W;
+#define RB_G16(A, F) hipLaunchKernelGGL((k_gemm_bf16<A, F>), dim3(g), dim3(256), 0, s, x, ldx, w, ldw, b, Y, ldy, M, N, K)
+  if (out_f32) {
+    if (act == RB_ACT_RELU) RB_G16(RB_ACT_RELU, true);
+    else if (act == RB_ACT_SIGMOID) RB_G16(RB_ACT_SIGMOID, true);
+    else RB_G16(RB_ACT_NONE, true);
+  } else {
+    if (act == RB_ACT_RELU) RB_G16(RB_ACT_RELU, false);
+    else if (act == RB_ACT_SIGMOID) RB_G16(RB_ACT_SIGMOID, false);
+    else RB_G16(RB_ACT_NONE, false);
+  }
+#undef RB_G16
+  return launch_status();
+}
+
+rb_status rb_k_gemm_f32(void* stream, const float* X, int32_t ldx, const float* W, int32_t ldw, const float* b,
+                        float* Y, int32_t ldy, int32_t M, int32_t N, int32_t K, int32_t act) {
+  if (M < 0 || N <= 0 || K <= 0 || (N % G32_BN) || (K % G32_BK) || ldx < K || ldw < K || ldy < N) return RB_EINVAL;
+  if ((ldx & 3) || (ldw & 3) || !X || !W || !b || !Y) return RB_EINVAL;
+  if (act != RB_ACT_NONE && act != RB_ACT_RELU && act != RB_ACT_SIGMOID) return RB_EINVAL;
+  if (M == 0) return RB_OK;
+  const unsigned g = (unsigned)(((M + G32_BM - 1) / G32_BM) * (N / G32_BN));
+  hipStream_t s = (hipStream_t)stream;
+  if (act == RB_ACT_RELU)
+    hipLaunchKernelGGL(k_gemm_f32<RB_ACT_RELU>, dim3(g), dim3(256), 0, s, X, ldx, W, ldw, b, Y, ldy, M, N, K);
+  else if (act == RB_ACT_SIGMOID)
+    hipLaunchKernelGGL(k_gemm_f32<RB_ACT_SIGMOID>, dim3(g), dim3(256), 0, s, X, ldx, W, ldw, b, Y, ldy, M, N, K);
+  else
+    hipLaunchKernelGGL(k_gemm_f32<RB_ACT_NONE>, dim3(g), dim3(256), 0, s, X, ldx, W, ldw, b, Y, ldy, M, N, K);
+  return launch_status();
+}
+
+rb_status rb_k_head(void* stream, const rb_k_row* rows, int32_t n_rows_total, const void* H, int32_t ldh,
+                    const void* w, float b, int32_t K, int32_t act, float* out) {
+  if (n_rows_total < 0 || K < 1 || ldh < K || !rows || !H || !w || !out) return RB_EINVAL;
+  if (act != RB_ACT_NONE && act != RB_ACT_SIGMOID) return RB_EINVAL;
+  if (n_rows_total == 0) return RB_OK;
+  const unsigned g = (unsigned)((n_rows_total + 3) / 4);
+  if (act == RB_ACT_SIGMOID)
+    hipLaunchKernelGGL(k_head<RB_ACT_SIGMOID>, dim3(g), dim3(256), 0, (hipStream_t)stream, rows, n_rows_total,
+                       (const bf16_t*)H, ldh, (const bf16_t*)w, b, K, out);
+  else
+    hipLaunchKernelGGL(k_head<RB_ACT_NONE>, dim3(g), dim3(256), 0, (hipStream_t)stream, rows, n_rows_total,
+                       (const bf16_t*)H, ldh, (const bf16_t*)w, b, K, out);
+  return launch_status();
+}
+
+rb_status rb_k_seqpool(void* stream, const rb_k_row* rows, int32_t n_seqs, int32_t seq_T, const float* H,
+                       int32_t ldh, int32_t D, const float* Wh, const float* bh, int32_t n_out, int32_t act,
+                       float* out) {
+  if (n_seqs < 0 || seq_T < 1 || D < 1 || D > POOL_MAX_D || ldh < D || n_out < 1 || n_out > POOL_MAX_OUT)
+    return RB_EINVAL;
+  if (act != RB_ACT_NONE && act != RB_ACT_SOFTMAX) return RB_EINVAL;
+  if (!rows || !H || !Wh || !bh || !out) return RB_EINVAL;
+  if (n_seqs == 0) return RB_OK;
+  hipLaunchKernelGGL(k_seqpool, dim3(n_seqs), dim3(256), 0, (hipStream_t)stream, rows, n_seqs, seq_T, H, ldh, D,
+                     Wh, bh, n_out, act, out);
+  return launch_status();
+}
+
+rb_status rb_k_split(void* stream, const rb_k_row* rows, int32_t n_rows_total, const float* Y, int32_t ldy,
+                     int32_t d_out, float* out) {
+  if (n_rows_total < 0 || d_out < 1 || ldy < d_out || !rows || !Y || !out) return RB_EINVAL;
+  if (n_rows_total == 0) return RB_OK;
+  hipLaunchKernelGGL(k_split, dim3(blocks_for((int64_t)n_rows_total * d_out)), dim3(256), 0, (hipStream_t)stream,
+                     rows, n_rows_total, Y, ldy, d_out, out);
+  return launch_status();
+}
+
+}  // extern "C"

@@ -1,0 +1,1286 @@
+// Host runtime of the request-batching library: contexts, models, batching
+// queues, the round-robin scheduler on a simulated clock, and the executor
+// that turns dispatched batches into launch chains on a HIP stream.
+//
+// Paper, section 2.2.1: requests for each servable (version) wait in their own
+// batching queue, are merged by concatenating their inputs, and the queues
+// share one device in round-robin order; the set of queues changes as
+// servables come and go. Section 2.1 (and the introduction): a big free of a
+// servable's memory happens on a manager thread, never an inference thread.
+//
+// Formation, padding, clock and tie rules (the paper gives none):
+//  - next-fit in arrival order: a batch closes when full, when the next
+//    request would overflow it (that request opens the next batch), when its
+//    timeout (from its first request's arrival) expires, or, in a replay, at
+//    the last arrival for count-only queues;
+//  - padded size = smallest allowed size >= real size (or the real size);
+//  - one simulated serial device: when it is free, the first queue after the
+//    last-served one (cyclic in queue-id order) holding a closed batch gets its
+//    oldest closed batch dispatched, and the device is busy for the queue's
+//    service time at that padded size;
+//  - events at one timestamp: timeouts (queue-id order), arrivals (request
+//    order), end-of-trace close, then dispatch.
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <climits>
+#include <cmath>
+#include <condition_variable>
+#include <cstdint>
+#include <cstring>
+#include <deque>
+#include <map>
+#include <memory>
+#include <mutex>
+#include <new>
+#include <string>
+#include <thread>
+#include <vector>
+
+#include "../../include/rb.h"
+
+namespace {
+
+constexpr int64_t NO_TIMEOUT = INT64_MAX;
+constexpr int KPAD = 64;       // every contraction dimension is padded to a multiple of this
+constexpr int NPAD_BF16 = 128; // output widths: the bf16 GEMM tile is 128 wide, the fp32 one 64
+constexpr int NPAD_F32 = 64;
+constexpr int N_SLOTS = 4;     // host/device staging slots in flight
+constexpr int CHUNK_WINDOWS = 32;
+
+inline int64_t round_up(int64_t x, int64_t m) { return (x + m - 1) / m * m; }
+
+inline uint16_t host_f2bf(float f) {
+  uint32_t u;
+  std::memcpy(&u, &f, 4);
+  if ((u & 0x7fffffffu) > 0x7f800000u) return (uint16_t)((u >> 16) | 0x40u);
+  u += 0x7fffu + ((u >> 16) & 1u);
+  return (uint16_t)(u >> 16);
+}
+
+struct DevFree {
+  std::vector<hipEvent_t> events;
+  std::vector<void*> ptrs;
+};
+
+}  // namespace
+
+// ---------------------------------------------------------------- objects
+
+struct rb_ctx {
+  int device = -1;
+  int n_models = 0, n_scheds = 0;
+  int64_t next_model_id = 1;
+  std::vector<rb_model*> models;  // live models (a destroyed scheduler's stream leaves their use lists)
+  // deleter thread: frees device memory after the events it waits on
+  std::thread deleter;
+  std::mutex mu;
+  std::condition_variable cv;
+  std::deque<DevFree> pending;
+  bool stop = false;
+};
+
+struct DevLayer {
+  int K = 0, N = 0, Kp = 0, Np = 0, act = 0;
+  void* w = nullptr;   // [Np, Kp] bf16 or fp32, zero padded
+  float* b = nullptr;  // [Np] zero padded
+};
+
+struct rb_model {
+  rb_ctx* ctx = nullptr;
+  int64_t id = 0;
+  int kind = 0, dtype = 0;
+  int d_in = 0, d_out = 0;
+  std::vector<DevLayer> layers;
+  bool head_last = false;  // last layer (fan_out 1, bf16) runs as the fused head
+  float head_bias = 0.f;
+  int n_tables = 0, emb_dim = 0, n_dense = 0;
+  int64_t table_rows = 0;
+  std::vector<void*> tables;
+  void** tables_dev = nullptr;
+  float* sp_w = nullptr;
+  float* sp_b = nullptr;
+  int sp_in = 0, sp_out = 0, sp_act = 0;
+  int bound = 0;
+  std::vector<void*> allocs;
+  std::vector<hipStream_t> used;  // streams that ran this model
+};
+
+namespace {
+
+struct Batch {
+  int64_t seq = 0;           // batch id in dispatch order
+  std::vector<int64_t> reqs; // request indices (trace index, or serving request id)
+  int s = 0, P = 0;
+  int64_t close_ns = 0, dispatch_ns = 0, done_ns = 0;
+};
+
+// A served request submitted through rb_submit (host payload copied in).
+struct HostReq {
+  rb_queue* q = nullptr;
+  int32_t n_rows = 0;
+  std::vector<float> dense;
+  std::vector<int32_t> lens, ids;
+  std::vector<float> out;
+  int state = 0;      // 0 queued, 1 dispatched, 2 done, 3 collected
+  int slot = -1;      // staging slot holding its output while in flight
+  int64_t out_off = 0;  // offset of its rows in the slot's output staging
+};
+
+struct Work {  // per (scheduler, model) device buffers, sized for the largest group seen
+  int64_t rows_cap = 0, slots_cap = 0;
+  void* X = nullptr;
+  void* A = nullptr;
+  void* B = nullptr;
+  float* Y = nullptr;
+  rb_k_row* rows = nullptr;
+};
+
+struct Group {  // the batches of one queue inside one window
+  rb_queue* q = nullptr;
+  std::vector<rb_k_batch> batches;
+  std::vector<rb_k_req> reqs;
+  int64_t slots = 0;  // sum of padded sizes
+};
+
+struct Slot {
+  hipEvent_t ev = nullptr;
+  bool busy = false;
+  char* host = nullptr;
+  char* dev = nullptr;
+  size_t cap = 0;
+  // serving mode: payload arenas and the output staging of one batch
+  std::vector<int64_t> serving_reqs;
+  float* host_out = nullptr;
+  size_t out_cap = 0;
+};
+
+struct Prof {
+  std::string name;
+  hipEvent_t a, b;
+};
+
+}  // namespace
+
+struct rb_queue {
+  rb_sched* s = nullptr;
+  rb_model* m = nullptr;
+  int id = 0;
+  int B = 0;
+  std::vector<int> allowed;
+  int64_t T = NO_TIMEOUT;
+  int bucket = 0;
+  std::vector<int64_t> svc;
+  // open batch
+  std::vector<int64_t> open;
+  int open_s = 0;
+  int64_t open_t = 0;
+  std::deque<Batch> closed;
+  int64_t undispatched = 0;  // requests in the open batch or in closed batches
+};
+
+struct rb_sched {
+  rb_ctx* ctx = nullptr;
+  rb_sched_opts opts{};
+  hipStream_t stream = nullptr;
+  std::vector<rb_queue*> queues;  // by id; null once destroyed
+  int n_live_queues = 0;
+  int64_t now = INT64_MIN;
+  int64_t device_free = INT64_MIN;
+  int last_served = -1;
+  int64_t n_closed = 0;
+  int64_t batch_seq = 0;
+  // serving-mode requests, by request id
+  std::vector<HostReq> hreqs;
+  std::vector<int64_t> last_batch_ids;
+  std::vector<uint64_t> last_batch_u64;
+  // executor
+  std::map<int64_t, Work> work;
+  std::vector<Group> window;     // current window, one group per queue
+  int window_batches = 0;
+  std::vector<std::vector<Group>> chunk;  // closed windows waiting for a flush
+  Slot slots[N_SLOTS];
+  int next_slot = 0;
+  int* err_dev = nullptr;
+  // trace replay arenas (device pointers of the current rb_sim_run)
+  const float* a_dense = nullptr;
+  int64_t a_dense_len = 0;
+  const int32_t* a_lens = nullptr;
+  const int32_t* a_ids = nullptr;
+  float* a_out = nullptr;
+  // profiling
+  std::vector<Prof> prof_pending;
+  std::map<std::string, std::pair<int64_t, double>> prof;
+  std::vector<hipEvent_t> ev_pool;
+};
+
+namespace {
+
+bool hip_ok(hipError_t e) { return e == hipSuccess; }
+
+void deleter_main(rb_ctx* c) {
+  hipSetDevice(c->device);
+  std::unique_lock<std::mutex> lk(c->mu);
+  for (;;) {
+    c->cv.wait(lk, [c] { return c->stop || !c->pending.empty(); });
+    if (c->pending.empty() && c->stop) return;
+    DevFree f = std::move(c->pending.front());
+    c->pending.pop_front();
+    lk.unlock();
+    for (hipEvent_t e : f.events) {
+      hipEventSynchronize(e);
+      hipEventDestroy(e);
+    }
+    for (void* p : f.ptrs) hipFree(p);
+    lk.lock();
+  }
+}
+
+rb_status dev_alloc(rb_model* m, size_t bytes, void** out) {
+  void* p = nullptr;
+  if (!hip_ok(hipMalloc(&p, bytes))) return RB_ENOMEM;
+  m->allocs.push_back(p);
+  *out = p;
+  return RB_OK;
+}
+
+bool valid_hidden_act(int a) { return a == RB_ACT_NONE || a == RB_ACT_RELU; }
+bool valid_last_act(int a) { return a == RB_ACT_NONE || a == RB_ACT_RELU || a == RB_ACT_SIGMOID; }
+
+rb_status upload_layer(rb_model* m, const rb_layer_desc& L, DevLayer& d, bool bf16) {
+  d.K = L.fan_in;
+  d.N = L.fan_out;
+  d.act = L.act;
+  d.Kp = (int)round_up(L.fan_in, KPAD);
+  d.Np = (int)round_up(L.fan_out, bf16 ? NPAD_BF16 : NPAD_F32);
+  if (m->ctx->device < 0) return RB_OK;
+  const size_t n = (size_t)d.Np * d.Kp;
+  rb_status st;
+  if (bf16) {
+    std::vector<uint16_t> h(n, 0);
+    for (int j = 0; j < d.N; ++j)
+      for (int k = 0; k < d.K; ++k) h[(size_t)j * d.Kp + k] = host_f2bf(L.w[(size_t)j * d.K + k]);
+    if ((st = dev_alloc(m, n * 2, &d.w)) != RB_OK) return st;
+    if (!hip_ok(hipMemcpy(d.w, h.data(), n * 2, hipMemcpyHostToDevice))) return RB_EDEVICE;
+  } else {
+    std::vector<float> h(n, 0.f);
+    for (int j = 0; j < d.N; ++j) std::memcpy(&h[(size_t)j * d.Kp], L.w + (size_t)j * d.K, sizeof(float) * d.K);
+    if ((st = dev_alloc(m, n * 4, &d.w)) != RB_OK) return st;
+    if (!hip_ok(hipMemcpy(d.w, h.data(), n * 4, hipMemcpyHostToDevice))) return RB_EDEVICE;
+  }
+  std::vector<float> hb(d.Np, 0.f);
+  std::memcpy(hb.data(), L.b, sizeof(float) * d.N);
+  void* pb = nullptr;
+  if ((st = dev_alloc(m, (size_t)d.Np * 4, &pb)) != RB_OK) return st;
+  d.b = (float*)pb;
+  if (!hip_ok(hipMemcpy(d.b, hb.data(), (size_t)d.Np * 4, hipMemcpyHostToDevice))) return RB_EDEVICE;
+  return RB_OK;
+}
+
+void free_model_now(rb_model* m) {
+  for (void* p : m->allocs) hipFree(p);
+  m->allocs.clear();
+}
+
+int padded_size(const rb_queue* q, int s) {
+  if (q->allowed.empty()) return s;
+  for (int a : q->allowed)
+    if (a >= s) return a;
+  return q->allowed.back();  // unreachable: s <= B == allowed.back()
+}
+
+int64_t service(const rb_queue* q, int P) {
+  if (q->svc.empty()) return 0;
+  return q->svc[std::min<size_t>((size_t)P, q->svc.size() - 1)];
+}
+
+void close_open(rb_queue* q, int64_t t) {
+  Batch b;
+  b.reqs.swap(q->open);
+  b.s = q->open_s;
+  b.P = padded_size(q, b.s);
+  b.close_ns = t;
+  q->closed.push_back(std::move(b));
+  q->open_s = 0;
+  q->s->n_closed++;
+}
+
+// Next-fit arrival of a request of n rows at time t.
+void arrive(rb_queue* q, int64_t req, int n, int64_t t) {
+  if (q->open_s > 0 && q->open_s + n > q->B) close_open(q, t);
+  if (q->open_s == 0) q->open_t = t;
+  q->open.push_back(req);
+  q->open_s += n;
+  q->undispatched++;
+  if (q->open_s == q->B) close_open(q, t);
+}
+
+// Fire every timeout due at or before t (each queue's open batch closes at
+// its own due time).
+void fire_timeouts_upto(rb_sched* s, int64_t t) {
+  for (rb_queue* q : s->queues)
+    if (q && q->T != NO_TIMEOUT && q->open_s > 0 && q->open_t + q->T <= t) close_open(q, q->open_t + q->T);
+}
+
+// Timeouts due exactly at t, in queue-id order.
+void fire_timeouts_at(rb_sched* s, int64_t t) {
+  for (rb_queue* q : s->queues)
+    if (q && q->T != NO_TIMEOUT && q->open_s > 0 && q->open_t + q->T == t) close_open(q, t);
+}
+
+int64_t next_timeout(const rb_sched* s) {
+  int64_t best = INT64_MAX;
+  for (const rb_queue* q : s->queues)
+    if (q && q->T != NO_TIMEOUT && q->open_s > 0) best = std::min(best, q->open_t + q->T);
+  return best;
+}
+
+rb_queue* pick_round_robin(rb_sched* s) {
+  const int nq = (int)s->queues.size();
+  for (int k = 1; k <= nq; ++k) {
+    rb_queue* q = s->queues[(size_t)((s->last_served + k) % nq + nq) % nq];
+    if (q && !q->closed.empty()) return q;
+  }
+  return nullptr;
+}
+
+// ---------------------------------------------------------------- executor
+
+hipEvent_t ev_get(rb_sched* s) {
+  if (!s->ev_pool.empty()) {
+    hipEvent_t e = s->ev_pool.back();
+    s->ev_pool.pop_back();
+    return e;
+  }
+  hipEvent_t e = nullptr;
+  hipEventCreate(&e);
+  return e;
+}
+
+void prof_begin(rb_sched* s, hipEvent_t* a) {
+  if (!s->opts.profile) return;
+  *a = ev_get(s);
+  hipEventRecord(*a, s->stream);
+}
+
+void prof_end(rb_sched* s, const char* name, hipEvent_t a) {
+  if (!s->opts.profile) return;
+  hipEvent_t b = ev_get(s);
+  hipEventRecord(b, s->stream);
+  s->prof_pending.push_back(Prof{name, a, b});
+}
+
+void prof_collect(rb_sched* s) {
+  for (Prof& p : s->prof_pending) {
+    float ms = 0.f;
+    if (hipEventElapsedTime(&ms, p.a, p.b) == hipSuccess) {
+      auto& e = s->prof[p.name];
+      e.first += 1;
+      e.second += ms;
+    }
+    s->ev_pool.push_back(p.a);
+    s->ev_pool.push_back(p.b);
+  }
+  s->prof_pending.clear();
+}
+
+#define RB_LAUNCH(s, name, call)           \
+  do {                                     \
+    hipEvent_t ev_a_ = nullptr;            \
+    prof_begin(s, &ev_a_);                 \
+    rb_status st_ = (call);                \
+    prof_end(s, name, ev_a_);              \
+    if (st_ != RB_OK) return st_;          \
+  } while (0)
+
+int64_t group_rows(const rb_model* m, const rb_queue* q, int64_t slots) {
+  return m->kind == RB_MODEL_SEQPOOL ? slots * q->bucket : slots;
+}
+
+rb_status ensure_work(rb_sched* s, rb_model* m, int64_t rows, int64_t slots, Work** out) {
+  Work& w = s->work[m->id];
+  if (rows > w.rows_cap || slots > w.slots_cap) {
+    hipStreamSynchronize(s->stream);
+    hipFree(w.X);
+    hipFree(w.A);
+    hipFree(w.B);
+    hipFree(w.Y);
+    hipFree(w.rows);
+    w = Work{};
+    const int64_t R = std::max<int64_t>(rows, 64);
+    const int64_t S = std::max<int64_t>(slots, 64);
+    const size_t elt = m->dtype == RB_DT_BF16 ? 2 : 4;
+    int maxN = 0;
+    for (const DevLayer& L : m->layers) maxN = std::max(maxN, L.Np);
+    const int Kp0 = m->layers[0].Kp;
+    if (!hip_ok(hipMalloc(&w.X, (size_t)R * Kp0 * elt)) || !hip_ok(hipMalloc(&w.A, (size_t)R * maxN * elt)) ||
+        !hip_ok(hipMalloc(&w.B, (size_t)R * maxN * elt)) ||
+        !hip_ok(hipMalloc((void**)&w.Y, (size_t)R * m->layers.back().Np * 4)) ||
+        !hip_ok(hipMalloc((void**)&w.rows, (size_t)S * sizeof(rb_k_row))))
+      return RB_ENOMEM;
+    w.rows_cap = R;
+    w.slots_cap = S;
+  }
+  *out = &w;
+  return RB_OK;
+}
+
+// Launch chain of one group: route -> assemble | embbag -> layers -> head | seqpool | split.
+rb_status run_group(rb_sched* s, const Group& g, const rb_k_batch* d_batches, const rb_k_req* d_reqs,
+                    const float* dense, int64_t dense_len, const int32_t* lens, const int32_t* ids, float* out) {
+  rb_model* m = g.q->m;
+  const int64_t slots = g.slots;
+  const int64_t M = group_rows(m, g.q, slots);
+  Work* w = nullptr;
+  rb_status st = ensure_work(s, m, M, slots, &w);
+  if (st != RB_OK) return st;
+  if (std::find(m->used.begin(), m->used.end(), s->stream) == m->used.end()) m->used.push_back(s->stream);
+  void* hs = (void*)s->stream;
+  const float pad = s->opts.pad_value;
+  RB_LAUNCH(s, "route", rb_k_route(hs, m->kind, d_batches, (int)g.batches.size(), d_reqs, lens, m->d_in,
+                                   m->d_out, m->n_tables, w->rows, s->err_dev));
+  const bool bf16 = m->dtype == RB_DT_BF16;
+  const int Kp0 = m->layers[0].Kp;
+  if (m->kind == RB_MODEL_RANKING) {
+    RB_LAUNCH(s, "embbag", rb_k_embbag(hs, w->rows, (int)slots, lens, ids, (const void* const*)m->tables_dev,
+                                       m->n_tables, m->table_rows, m->emb_dim, dense, m->n_dense, w->X, Kp0, pad,
+                                       s->err_dev));
+  } else {
+    RB_LAUNCH(s, "assemble", rb_k_assemble(hs, w->rows, (int)M, m->kind == RB_MODEL_SEQPOOL ? g.q->bucket : 0,
+                                           dense, dense_len, m->d_in, w->X, Kp0, bf16 ? 1 : 0, pad, s->err_dev));
+  }
+  const size_t nL = m->layers.size() - (m->head_last ? 1 : 0);
+  void* h = w->X;
+  int ldh = Kp0;
+  for (size_t i = 0; i < nL; ++i) {
+    const DevLayer& L = m->layers[i];
+    const bool last = (i + 1 == nL) && !m->head_last;
+    void* y = last ? (void*)w->Y : (i % 2 == 0 ? w->A : w->B);
+    if (bf16) {
+      RB_LAUNCH(s, "gemm_bf16", rb_k_gemm_bf16(hs, h, ldh, L.w, L.Kp, L.b, y, L.Np, (int)M, L.Np, L.Kp, L.act,
+                                               last ? 1 : 0));
+    } else {
+      RB_LAUNCH(s, "gemm_f32", rb_k_gemm_f32(hs, (const float*)h, ldh, (const float*)L.w, L.Kp, L.b, (float*)y,
+                                             L.Np, (int)M, L.Np, L.Kp, L.act));
+    }
+    h = y;
+    ldh = L.Np;
+  }
+  if (m->head_last) {
+    const DevLayer& L = m->layers.back();
+    RB_LAUNCH(s, "head", rb_k_head(hs, w->rows, (int)slots, h, ldh, L.w, m->head_bias, L.K, L.act, out));
+  } else if (m->kind == RB_MODEL_SEQPOOL) {
+    RB_LAUNCH(s, "seqpool", rb_k_seqpool(hs, w->rows, (int)slots, g.q->bucket, (const float*)h, ldh, m->sp_in,
+                                         m->sp_w, m->sp_b, m->sp_out, m->sp_act, out));
+  } else {
+    RB_LAUNCH(s, "split", rb_k_split(hs, w->rows, (int)slots, w->Y, ldh, m->d_out, out));
+  }
+  return RB_OK;
+}
+
+// A slot whose work has finished: hand its serving outputs to their requests.
+void retire_slot(rb_sched* s, Slot& sl) {
+  for (int64_t id : sl.serving_reqs) {
+    HostReq& r = s->hreqs[(size_t)id];
+    const int64_t n = (int64_t)r.n_rows * r.q->m->d_out;
+    r.out.assign(sl.host_out + r.out_off, sl.host_out + r.out_off + n);
+    r.state = 2;
+    r.slot = -1;
+  }
+  sl.serving_reqs.clear();
+  sl.busy = false;
+}
+
+// Reuse a staging slot: wait for its previous work, retire it, and make room
+// for `bytes` of tables/payload and `out_bytes` of outputs.
+rb_status acquire_slot(rb_sched* s, size_t bytes, size_t out_bytes, Slot** out) {
+  Slot& sl = s->slots[s->next_slot];
+  s->next_slot = (s->next_slot + 1) % N_SLOTS;
+  if (sl.busy) {
+    if (!hip_ok(hipEventSynchronize(sl.ev))) return RB_EDEVICE;
+    retire_slot(s, sl);
+  }
+  if (bytes > sl.cap) {
+    const size_t cap = std::max(bytes, sl.cap * 2);
+    hipHostFree(sl.host);
+    hipFree(sl.dev);
+    sl.host = nullptr;
+    sl.dev = nullptr;
+    sl.cap = 0;
+    if (!hip_ok(hipHostMalloc((void**)&sl.host, cap, hipHostMallocDefault))) return RB_ENOMEM;
+    if (!hip_ok(hipMalloc((void**)&sl.dev, cap))) return RB_ENOMEM;
+    sl.cap = cap;
+  }
+  if (out_bytes > sl.out_cap) {
+    hipHostFree(sl.host_out);
+    sl.host_out = nullptr;
+    sl.out_cap = 0;
+    if (!hip_ok(hipHostMalloc((void**)&sl.host_out, out_bytes, hipHostMallocDefault))) return RB_ENOMEM;
+    sl.out_cap = out_bytes;
+  }
+  if (!sl.ev) hipEventCreateWithFlags(&sl.ev, hipEventDisableTiming);
+  *out = &sl;
+  return RB_OK;
+}
+
+// Flush the closed windows of a replay: one host->device copy of every
+// group's batch and request tables, then each group's launch chain.
+rb_status flush_chunk(rb_sched* s) {
+  if (s->chunk.empty()) return RB_OK;
+  size_t bytes = 0;
+  for (auto& win : s->chunk)
+    for (Group& g : win)
+      bytes += round_up((int64_t)(g.batches.size() * sizeof(rb_k_batch)), 256) +
+               round_up((int64_t)(g.reqs.size() * sizeof(rb_k_req)), 256);
+  Slot* sl = nullptr;
+  rb_status st = acquire_slot(s, bytes, 0, &sl);
+  if (st != RB_OK) return st;
+  size_t off = 0;
+  std::vector<std::pair<size_t, size_t>> offs;
+  for (auto& win : s->chunk)
+    for (Group& g : win) {
+      const size_t bb = g.batches.size() * sizeof(rb_k_batch), rr = g.reqs.size() * sizeof(rb_k_req);
+      std::memcpy(sl->host + off, g.batches.data(), bb);
+      const size_t o1 = off;
+      off += round_up((int64_t)bb, 256);
+      std::memcpy(sl->host + off, g.reqs.data(), rr);
+      offs.push_back({o1, off});
+      off += round_up((int64_t)rr, 256);
+    }
+  if (!hip_ok(hipMemcpyAsync(sl->dev, sl->host, off, hipMemcpyHostToDevice, s->stream))) return RB_EDEVICE;
+  size_t gi = 0;
+  for (auto& win : s->chunk)
+    for (Group& g : win) {
+      st = run_group(s, g, (const rb_k_batch*)(sl->dev + offs[gi].first), (const rb_k_req*)(sl->dev + offs[gi].second),
+                     s->a_dense, s->a_dense_len, s->a_lens, s->a_ids, s->a_out);
+      ++gi;
+      if (st != RB_OK) return st;
+    }
+  hipEventRecord(sl->ev, s->stream);
+  sl->busy = true;
+  s->chunk.clear();
+  return RB_OK;
+}
+
+void close_window(rb_sched* s) {
+  if (s->window.empty()) return;
+  s->chunk.push_back(std::move(s->window));
+  s->window.clear();
+  s->window_batches = 0;
+}
+
+// Add a dispatched batch (its requests already described) to the window.
+void window_add(rb_sched* s, rb_queue* q, const Batch& b, std::vector<rb_k_req>& reqs) {
+  Group* g = nullptr;
+  for (Group& x : s->window)
+    if (x.q == q) g = &x;
+  if (!g) {
+    s->window.push_back(Group{});
+    g = &s->window.back();
+    g->q = q;
+  }
+  rb_k_batch kb;
+  kb.req_begin = (int32_t)g->reqs.size();
+  kb.n_req = (int32_t)reqs.size();
+  kb.row_base = (int32_t)g->slots;
+  kb.padded = b.P;
+  kb.real = b.s;
+  kb.seq_T = q->m->kind == RB_MODEL_SEQPOOL ? q->bucket : 0;
+  g->batches.push_back(kb);
+  g->reqs.insert(g->reqs.end(), reqs.begin(), reqs.end());
+  g->slots += b.P;
+  s->window_batches++;
+}
+
+}  // namespace
+
+// ================================================================== C ABI
+
+extern "C" {
+
+const char* rb_status_str(rb_status s) {
+  switch (s) {
+    case RB_OK: return "ok";
+    case RB_EINVAL: return "invalid argument";
+    case RB_EBUSY: return "busy";
+    case RB_EAGAIN: return "not ready";
+    case RB_EEMPTY: return "nothing to run";
+    case RB_ESIZE: return "buffer too small";
+    case RB_ENOENT: return "no such request";
+    case RB_EDEVICE: return "device error";
+    case RB_ENOMEM: return "out of memory";
+    case RB_ERANGE: return "id or length out of range";
+    default: return "unknown status";
+  }
+}
+
+rb_status rb_ctx_create(int32_t hip_device, rb_ctx** out) {
+  if (!out) return RB_EINVAL;
+  rb_ctx* c = new (std::nothrow) rb_ctx();
+  if (!c) return RB_ENOMEM;
+  if (hip_device >= 0) {
+    int n = 0;
+    if (!hip_ok(hipGetDeviceCount(&n)) || hip_device >= n || !hip_ok(hipSetDevice(hip_device))) {
+      delete c;
+      return RB_EDEVICE;
+    }
+    c->device = hip_device;
+    c->deleter = std::thread(deleter_main, c);
+  }
+  *out = c;
+  return RB_OK;
+}
+
+rb_status rb_ctx_destroy(rb_ctx* c) {
+  if (!c) return RB_OK;
+  if (c->n_models || c->n_scheds) return RB_EBUSY;
+  if (c->deleter.joinable()) {
+    {
+      std::lock_guard<std::mutex> lk(c->mu);
+      c->stop = true;
+    }
+    c->cv.notify_all();
+    c->deleter.join();
+  }
+  delete c;
+  return RB_OK;
+}
+
+rb_status rb_model_create(rb_ctx* ctx, const rb_model_desc* d, rb_model** out) {
+  if (!ctx || !d || !out) return RB_EINVAL;
+  if (d->kind < RB_MODEL_MLP || d->kind > RB_MODEL_SEQPOOL) return RB_EINVAL;
+  if (d->dtype != RB_DT_F32 && d->dtype != RB_DT_BF16) return RB_EINVAL;
+  if (d->n_layers < 1 || !d->layers) return RB_EINVAL;
+  const bool dev = ctx->device >= 0;
+  for (int i = 0; i < d->n_layers; ++i) {
+    const rb_layer_desc& L = d->layers[i];
+    if (L.fan_in < 1 || L.fan_out < 1) return RB_EINVAL;
+    if (dev && (!L.w || !L.b)) return RB_EINVAL;
+    if (i + 1 < d->n_layers && L.fan_out != d->layers[i + 1].fan_in) return RB_EINVAL;
+    if (i + 1 < d->n_layers ? !valid_hidden_act(L.act) : !valid_last_act(L.act)) return RB_EINVAL;
+  }
+  const rb_layer_desc& last = d->layers[d->n_layers - 1];
+  if (d->kind == RB_MODEL_RANKING) {
+    if (d->dtype != RB_DT_BF16 || d->emb_dim != 64 || d->n_tables < 1 || d->n_tables > 64 || d->n_dense < 0 ||
+        d->table_rows < 1 || d->table_rows > INT32_MAX)
+      return RB_EINVAL;
+    if (d->layers[0].fan_in != d->n_tables * d->emb_dim + d->n_dense) return RB_EINVAL;
+    if (dev && !d->tables) return RB_EINVAL;
+  }
+  if (d->kind == RB_MODEL_SEQPOOL) {
+    if (d->dtype != RB_DT_F32) return RB_EINVAL;
+    if (d->head.fan_in != last.fan_out || d->head.fan_out < 1 || d->head.fan_out > 16 || d->head.fan_in > 1024)
+      return RB_EINVAL;
+    if (d->head.act != RB_ACT_SOFTMAX && d->head.act != RB_ACT_NONE) return RB_EINVAL;
+    if (dev && (!d->head.w || !d->head.b)) return RB_EINVAL;
+    if (last.act == RB_ACT_SIGMOID) return RB_EINVAL;
+  }
+  rb_model* m = new (std::nothrow) rb_model();
+  if (!m) return RB_ENOMEM;
+  m->ctx = ctx;
+  m->id = ctx->next_model_id++;
+  m->kind = d->kind;
+  m->dtype = d->dtype;
+  m->d_in = d->kind == RB_MODEL_RANKING ? d->n_dense : d->layers[0].fan_in;
+  m->d_out = d->kind == RB_MODEL_SEQPOOL ? d->head.fan_out : last.fan_out;
+  m->n_tables = d->kind == RB_MODEL_RANKING ? d->n_tables : 0;
+  m->emb_dim = d->emb_dim;
+  m->n_dense = d->n_dense;
+  m->table_rows = d->table_rows;
+  m->head_last = d->kind != RB_MODEL_SEQPOOL && d->dtype == RB_DT_BF16 && last.fan_out == 1 && d->n_layers >= 2 &&
+                 (last.act == RB_ACT_SIGMOID || last.act == RB_ACT_NONE);
+  if (dev) hipSetDevice(ctx->device);
+  m->layers.resize(d->n_layers);
+  rb_status st = RB_OK;
+  for (int i = 0; i < d->n_layers && st == RB_OK; ++i) {
+    const rb_layer_desc& L = d->layers[i];
+    if (i == d->n_layers - 1 && m->head_last) {
+      // fused head: one bf16 weight row, bias kept on the host
+      DevLayer& H = m->layers[i];
+      H.K = L.fan_in;
+      H.N = 1;
+      H.Kp = (int)round_up(L.fan_in, KPAD);
+      H.Np = 1;
+      H.act = L.act;
+      if (dev) {
+        std::vector<uint16_t> h(H.Kp, 0);
+        for (int k = 0; k < L.fan_in; ++k) h[k] = host_f2bf(L.w[k]);
+        st = dev_alloc(m, (size_t)H.Kp * 2, &H.w);
+        if (st == RB_OK && !hip_ok(hipMemcpy(H.w, h.data(), (size_t)H.Kp * 2, hipMemcpyHostToDevice))) st = RB_EDEVICE;
+        m->head_bias = L.b[0];
+      }
+    } else {
+      st = upload_layer(m, L, m->layers[i], d->dtype == RB_DT_BF16);
+    }
+  }
+  if (st == RB_OK && d->kind == RB_MODEL_RANKING && dev) {
+    const size_t per = (size_t)d->table_rows * d->emb_dim;
+    std::vector<uint16_t> h(per);
+    for (int t = 0; t < d->n_tables && st == RB_OK; ++t) {
+      if (!d->tables[t]) {
+        st = RB_EINVAL;
+        break;
+      }
+      for (size_t i = 0; i < per; ++i) h[i] = host_f2bf(d->tables[t][i]);
+      void* p = nullptr;
+      st = dev_alloc(m, per * 2, &p);
+      if (st == RB_OK && !hip_ok(hipMemcpy(p, h.data(), per * 2, hipMemcpyHostToDevice))) st = RB_EDEVICE;
+      m->tables.push_back(p);
+    }
+    if (st == RB_OK) {
+      void* p = nullptr;
+      st = dev_alloc(m, sizeof(void*) * d->n_tables, &p);
+      m->tables_dev = (void**)p;
+      if (st == RB_OK &&
+          !hip_ok(hipMemcpy(m->tables_dev, m->tables.data(), sizeof(void*) * d->n_tables, hipMemcpyHostToDevice)))
+        st = RB_EDEVICE;
+    }
+  }
+  if (st == RB_OK && d->kind == RB_MODEL_SEQPOOL) {
+    m->sp_in = d->head.fan_in;
+    m->sp_out = d->head.fan_out;
+    m->sp_act = d->head.act;
+    if (dev) {
+      void *pw = nullptr, *pb = nullptr;
+      const size_t nw = (size_t)m->sp_in * m->sp_out;
+      st = dev_alloc(m, nw * 4, &pw);
+      if (st == RB_OK) st = dev_alloc(m, (size_t)m->sp_out * 4, &pb);
+      if (st == RB_OK && (!hip_ok(hipMemcpy(pw, d->head.w, nw * 4, hipMemcpyHostToDevice)) ||
+                          !hip_ok(hipMemcpy(pb, d->head.b, (size_t)m->sp_out * 4, hipMemcpyHostToDevice))))
+        st = RB_EDEVICE;
+      m->sp_w = (float*)pw;
+      m->sp_b = (float*)pb;
+    }
+  }
+  if (st != RB_OK) {
+    free_model_now(m);
+    delete m;
+    return st;
+  }
+  ctx->n_models++;
+  ctx->models.push_back(m);
+  *out = m;
+  return RB_OK;
+}
+
+rb_status rb_model_info(const rb_model* m, int32_t* d_in, int32_t* d_out) {
+  if (!m || !d_in || !d_out) return RB_EINVAL;
+  *d_in = m->d_in;
+  *d_out = m->d_out;
+  return RB_OK;
+}
+
+rb_status rb_model_destroy(rb_model* m) {
+  if (!m) return RB_OK;
+  if (m->bound) return RB_EBUSY;
+  rb_ctx* c = m->ctx;
+  if (c->device >= 0 && !m->allocs.empty()) {
+    DevFree f;
+    f.ptrs = std::move(m->allocs);
+    for (hipStream_t st : m->used) {
+      hipEvent_t e = nullptr;
+      if (hip_ok(hipEventCreateWithFlags(&e, hipEventDisableTiming))) {
+        hipEventRecord(e, st);
+        f.events.push_back(e);
+      }
+    }
+    {
+      std::lock_guard<std::mutex> lk(c->mu);
+      c->pending.push_back(std::move(f));
+    }
+    c->cv.notify_all();
+  }
+  c->n_models--;
+  c->models.erase(std::remove(c->models.begin(), c->models.end(), m), c->models.end());
+  delete m;
+  return RB_OK;
+}
+
+rb_status rb_sched_create(rb_ctx* ctx, const rb_sched_opts* o, rb_sched** out) {
+  if (!ctx || !o || !out) return RB_EINVAL;
+  if (o->mode != RB_MODE_DEVICE && o->mode != RB_MODE_NO_DEVICE) return RB_EINVAL;
+  if (o->mode == RB_MODE_DEVICE && ctx->device < 0) return RB_EDEVICE;
+  if (o->window_batches < 1) return RB_EINVAL;
+  rb_sched* s = new (std::nothrow) rb_sched();
+  if (!s) return RB_ENOMEM;
+  s->ctx = ctx;
+  s->opts = *o;
+  if (o->mode == RB_MODE_DEVICE) {
+    hipSetDevice(ctx->device);
+    if (!hip_ok(hipStreamCreateWithFlags(&s->stream, hipStreamNonBlocking)) ||
+        !hip_ok(hipMalloc((void**)&s->err_dev, sizeof(int))) || !hip_ok(hipMemset(s->err_dev, 0, sizeof(int)))) {
+      if (s->stream) hipStreamDestroy(s->stream);
+      delete s;
+      return RB_EDEVICE;
+    }
+  }
+  ctx->n_scheds++;
+  *out = s;
+  return RB_OK;
+}
+
+rb_status rb_sched_destroy(rb_sched* s) {
+  if (!s) return RB_OK;
+  if (s->n_live_queues) return RB_EBUSY;
+  if (s->stream) {
+    hipStreamSynchronize(s->stream);
+    for (auto& kv : s->work) {
+      Work& w = kv.second;
+      hipFree(w.X);
+      hipFree(w.A);
+      hipFree(w.B);
+      hipFree(w.Y);
+      hipFree(w.rows);
+    }
+    for (Slot& sl : s->slots) {
+      hipHostFree(sl.host);
+      hipFree(sl.dev);
+      hipHostFree(sl.host_out);
+      if (sl.ev) hipEventDestroy(sl.ev);
+    }
+    for (Prof& p : s->prof_pending) {
+      hipEventDestroy(p.a);
+      hipEventDestroy(p.b);
+    }
+    for (hipEvent_t e : s->ev_pool) hipEventDestroy(e);
+    hipFree(s->err_dev);
+    // the stream is drained: models no longer need to wait on it
+    for (rb_model* m : s->ctx->models) m->used.erase(std::remove(m->used.begin(), m->used.end(), s->stream), m->used.end());
+    hipStreamDestroy(s->stream);
+  }
+  s->ctx->n_scheds--;
+  delete s;
+  return RB_OK;
+}
+
+rb_status rb_sync(rb_sched* s) {
+  if (!s) return RB_EINVAL;
+  if (!s->stream) return RB_OK;
+  if (!hip_ok(hipStreamSynchronize(s->stream))) return RB_EDEVICE;
+  for (Slot& sl : s->slots)
+    if (sl.busy) retire_slot(s, sl);
+  prof_collect(s);
+  int err = 0;
+  if (!hip_ok(hipMemcpy(&err, s->err_dev, sizeof(int), hipMemcpyDeviceToHost))) return RB_EDEVICE;
+  if (err) {
+    hipMemset(s->err_dev, 0, sizeof(int));
+    return RB_ERANGE;
+  }
+  return RB_OK;
+}
+
+rb_status rb_sched_kernel_stats(rb_sched* s, const char* kernel, int64_t* launches, double* total_ms) {
+  if (!s || !kernel || !launches || !total_ms) return RB_EINVAL;
+  auto it = s->prof.find(kernel);
+  *launches = it == s->prof.end() ? 0 : it->second.first;
+  *total_ms = it == s->prof.end() ? 0.0 : it->second.second;
+  return RB_OK;
+}
+
+rb_status rb_sched_stream(rb_sched* s, void** stream) {
+  if (!s || !stream) return RB_EINVAL;
+  *stream = (void*)s->stream;
+  return RB_OK;
+}
+
+rb_status rb_queue_create(rb_sched* s, rb_model* m, const rb_queue_opts* o, rb_queue** out) {
+  if (!s || !m || !o || !out || m->ctx != s->ctx) return RB_EINVAL;
+  if (o->max_batch_size < 1 || o->n_allowed < 0 || (o->n_allowed > 0 && !o->allowed_batch_sizes)) return RB_EINVAL;
+  if (o->batch_timeout_ns < 1) return RB_EINVAL;
+  for (int i = 0; i < o->n_allowed; ++i) {
+    const int a = o->allowed_batch_sizes[i];
+    if (a < 1 || (i > 0 && a <= o->allowed_batch_sizes[i - 1])) return RB_EINVAL;
+  }
+  if (o->n_allowed > 0 && o->allowed_batch_sizes[o->n_allowed - 1] != o->max_batch_size) return RB_EINVAL;
+  if (o->bucket_len < 0 || (m->kind == RB_MODEL_SEQPOOL) != (o->bucket_len > 0)) return RB_EINVAL;
+  if (o->service_ns && o->n_service != o->max_batch_size + 1) return RB_EINVAL;
+  if (o->service_ns)
+    for (int i = 0; i < o->n_service; ++i)
+      if (o->service_ns[i] < 0) return RB_EINVAL;
+  rb_queue* q = new (std::nothrow) rb_queue();
+  if (!q) return RB_ENOMEM;
+  q->s = s;
+  q->m = m;
+  q->id = (int)s->queues.size();
+  q->B = o->max_batch_size;
+  q->allowed.assign(o->allowed_batch_sizes, o->allowed_batch_sizes + o->n_allowed);
+  q->T = o->batch_timeout_ns;
+  q->bucket = o->bucket_len;
+  if (o->service_ns) q->svc.assign(o->service_ns, o->service_ns + o->n_service);
+  s->queues.push_back(q);
+  s->n_live_queues++;
+  m->bound++;
+  *out = q;
+  return RB_OK;
+}
+
+rb_status rb_queue_destroy(rb_queue* q) {
+  if (!q) return RB_OK;
+  if (q->undispatched) return RB_EBUSY;
+  rb_sched* s = q->s;
+  // a queue with batches still in the unflushed window keeps them: flush first
+  for (Group& g : s->window)
+    if (g.q == q) return RB_EBUSY;
+  s->queues[(size_t)q->id] = nullptr;
+  s->n_live_queues--;
+  q->m->bound--;
+  delete q;
+  return RB_OK;
+}
+
+rb_status rb_queue_id(const rb_queue* q, int32_t* id) {
+  if (!q || !id) return RB_EINVAL;
+  *id = q->id;
+  return RB_OK;
+}
+
+// ---------------------------------------------------------------- serving
+
+static rb_status validate_request(const rb_queue* q, const rb_request* r) {
+  const rb_model* m = q->m;
+  if (r->n_rows < 1 || r->n_rows > q->B) return RB_EINVAL;
+  const int64_t n = r->n_rows;
+  if (r->n_dense < 0 || r->n_lens < 0 || r->n_ids < 0) return RB_EINVAL;
+  if (r->n_dense > 0 && !r->dense) return RB_EINVAL;
+  if (r->n_lens > 0 && !r->lens) return RB_EINVAL;
+  if (r->n_ids > 0 && !r->ids) return RB_EINVAL;
+  if (m->kind == RB_MODEL_MLP) {
+    if (r->n_dense != n * m->d_in || r->n_lens || r->n_ids) return RB_EINVAL;
+  } else if (m->kind == RB_MODEL_RANKING) {
+    if (r->n_dense != n * m->n_dense || r->n_lens != n * m->n_tables) return RB_EINVAL;
+    int64_t tot = 0;
+    for (int64_t i = 0; i < r->n_lens; ++i) {
+      if (r->lens[i] < 0) return RB_EINVAL;
+      tot += r->lens[i];
+    }
+    if (tot != r->n_ids) return RB_EINVAL;
+    for (int64_t i = 0; i < r->n_ids; ++i)
+      if (r->ids[i] < 0 || r->ids[i] >= m->table_rows) return RB_EINVAL;
+  } else {
+    if (r->n_lens != n || r->n_ids) return RB_EINVAL;
+    int64_t tot = 0;
+    for (int64_t i = 0; i < n; ++i) {
+      if (r->lens[i] < 1 || r->lens[i] > q->bucket) return RB_EINVAL;
+      tot += r->lens[i];
+    }
+    if (r->n_dense != tot * m->d_in) return RB_EINVAL;
+  }
+  return RB_OK;
+}
+
+rb_status rb_submit(rb_queue* q, const rb_request* r, int64_t arrival_ns, uint64_t* out_req_id) {
+  if (!q || !r || !out_req_id) return RB_EINVAL;
+  rb_sched* s = q->s;
+  if (arrival_ns < s->now) return RB_EINVAL;
+  rb_status st = validate_request(q, r);
+  if (st != RB_OK) return st;
+  HostReq h;
+  h.q = q;
+  h.n_rows = r->n_rows;
+  try {
+    h.dense.assign(r->dense, r->dense + r->n_dense);
+    if (r->n_lens) h.lens.assign(r->lens, r->lens + r->n_lens);
+    if (r->n_ids) h.ids.assign(r->ids, r->ids + r->n_ids);
+    s->hreqs.push_back(std::move(h));
+  } catch (...) {
+    return RB_ENOMEM;
+  }
+  fire_timeouts_upto(s, arrival_ns);
+  s->now = arrival_ns;
+  const int64_t id = (int64_t)s->hreqs.size() - 1;
+  arrive(q, id, r->n_rows, arrival_ns);
+  *out_req_id = (uint64_t)id;
+  return RB_OK;
+}
+
+rb_status rb_advance(rb_sched* s, int64_t now_ns) {
+  if (!s || now_ns < s->now) return RB_EINVAL;
+  fire_timeouts_upto(s, now_ns);
+  s->now = now_ns;
+  return RB_OK;
+}
+
+rb_status rb_flush(rb_queue* q) {
+  if (!q) return RB_EINVAL;
+  if (q->open_s > 0) close_open(q, std::max<int64_t>(q->s->now, q->open_t));
+  return RB_OK;
+}
+
+// Serving-mode device run of one batch: stage its payloads, run the chain,
+// copy the outputs back into the slot's pinned output buffer.
+static rb_status run_serving_batch(rb_sched* s, rb_queue* q, const Batch& b) {
+  const rb_model* m = q->m;
+  int64_t nd = 0, nl = 0, ni = 0, no = 0;
+  for (int64_t id : b.reqs) {
+    const HostReq& h = s->hreqs[(size_t)id];
+    nd += (int64_t)h.dense.size();
+    nl += (int64_t)h.lens.size();
+    ni += (int64_t)h.ids.size();
+    no += (int64_t)h.n_rows * m->d_out;
+  }
+  const size_t o_batch = 0;
+  const size_t o_reqs = 256;
+  const size_t o_dense = o_reqs + round_up((int64_t)(b.reqs.size() * sizeof(rb_k_req)), 256);
+  const size_t o_lens = o_dense + round_up(nd * 4, 256);
+  const size_t o_ids = o_lens + round_up(nl * 4, 256);
+  const size_t o_out = o_ids + round_up(ni * 4, 256);
+  const size_t total = o_out + round_up(no * 4, 256);
+  Slot* sl = nullptr;
+  rb_status st = acquire_slot(s, total, (size_t)std::max<int64_t>(no, 1) * 4, &sl);
+  if (st != RB_OK) return st;
+  Group g;
+  g.q = q;
+  g.slots = b.P;
+  rb_k_batch kb{0, (int32_t)b.reqs.size(), 0, b.P, b.s, m->kind == RB_MODEL_SEQPOOL ? q->bucket : 0};
+  g.batches.push_back(kb);
+  int64_t cd = 0, cl = 0, ci = 0, co = 0;
+  for (int64_t id : b.reqs) {
+    HostReq& h = s->hreqs[(size_t)id];
+    rb_k_req kr{};
+    kr.dense_off = cd;
+    kr.dense_end = cd + (int64_t)h.dense.size();
+    kr.lens_off = cl;
+    kr.ids_off = ci;
+    kr.ids_end = ci + (int64_t)h.ids.size();
+    kr.out_off = co;
+    kr.n_rows = h.n_rows;
+    std::memcpy(sl->host + o_dense + cd * 4, h.dense.data(), h.dense.size() * 4);
+    if (!h.lens.empty()) std::memcpy(sl->host + o_lens + cl * 4, h.lens.data(), h.lens.size() * 4);
+    if (!h.ids.empty()) std::memcpy(sl->host + o_ids + ci * 4, h.ids.data(), h.ids.size() * 4);
+    h.out_off = co;
+    h.slot = (int)(sl - s->slots);
+    h.state = 1;
+    cd += (int64_t)h.dense.size();
+    cl += (int64_t)h.lens.size();
+    ci += (int64_t)h.ids.size();
+    co += (int64_t)h.n_rows * m->d_out;
+    g.reqs.push_back(kr);
+    sl->serving_reqs.push_back(id);
+  }
+  std::memcpy(sl->host + o_batch, &kb, sizeof(kb));
+  std::memcpy(sl->host + o_reqs, g.reqs.data(), g.reqs.size() * sizeof(rb_k_req));
+  if (!hip_ok(hipMemcpyAsync(sl->dev, sl->host, o_out, hipMemcpyHostToDevice, s->stream))) return RB_EDEVICE;
+  float* dout = (float*)(sl->dev + o_out);
+  st = run_group(s, g, (const rb_k_batch*)(sl->dev + o_batch), (const rb_k_req*)(sl->dev + o_reqs),
+                 (const float*)(sl->dev + o_dense), nd, (const int32_t*)(sl->dev + o_lens),
+                 (const int32_t*)(sl->dev + o_ids), dout);
+  if (st != RB_OK) return st;
+  if (!hip_ok(hipMemcpyAsync(sl->host_out, dout, (size_t)no * 4, hipMemcpyDeviceToHost, s->stream)))
+    return RB_EDEVICE;
+  hipEventRecord(sl->ev, s->stream);
+  sl->busy = true;
+  return RB_OK;
+}
+
+rb_status rb_run_next(rb_sched* s, rb_batch_info* out) {
+  if (!s || !out) return RB_EINVAL;
+  rb_queue* q = pick_round_robin(s);
+  if (!q) return RB_EEMPTY;
+  Batch b = std::move(q->closed.front());
+  q->closed.pop_front();
+  s->n_closed--;
+  q->undispatched -= (int64_t)b.reqs.size();
+  b.seq = s->batch_seq++;
+  b.dispatch_ns = std::max(s->now, s->device_free);
+  b.done_ns = b.dispatch_ns + service(q, b.P);
+  s->device_free = b.done_ns;
+  s->last_served = q->id;
+  if (s->stream) {
+    rb_status st = run_serving_batch(s, q, b);
+    if (st != RB_OK) return st;
+  } else {
+    for (int64_t id : b.reqs) s->hreqs[(size_t)id].state = 2;
+  }
+  s->last_batch_u64.assign(b.reqs.begin(), b.reqs.end());
+  out->batch_id = (uint64_t)b.seq;
+  out->queue = q->id;
+  out->real_rows = b.s;
+  out->padded_rows = b.P;
+  out->n_req = (int32_t)b.reqs.size();
+  out->close_ns = b.close_ns;
+  out->dispatch_ns = b.dispatch_ns;
+  out->done_ns = b.done_ns;
+  out->req_ids = s->last_batch_u64.data();
+  return RB_OK;
+}
+
+rb_status rb_collect(rb_sched* s, uint64_t req_id, float* dst, size_t dst_bytes, int32_t* out_rows) {
+  if (!s || !out_rows) return RB_EINVAL;
+  if (req_id >= s->hreqs.size()) return RB_ENOENT;
+  HostReq& h = s->hreqs[(size_t)req_id];
+  if (h.state == 3) return RB_ENOENT;
+  if (h.state == 0) return RB_EAGAIN;
+  if (!s->stream) return RB_EDEVICE;  // no outputs without a device
+  if (h.state == 1) {
+    Slot& sl = s->slots[h.slot];
+    const hipError_t e = hipEventQuery(sl.ev);
+    if (e == hipErrorNotReady) return RB_EAGAIN;
+    if (e != hipSuccess) return RB_EDEVICE;
+    retire_slot(s, sl);
+  }
+  const size_t need = h.out.size() * sizeof(float);
+  if (!dst || dst_bytes < need) return RB_ESIZE;
+  std::memcpy(dst, h.out.data(), need);
+  *out_rows = h.n_rows;
+  h.state = 3;
+  std::vector<float>().swap(h.out);
+  std::vector<float>().swap(h.dense);
+  std::vector<int32_t>().swap(h.lens);
+  std::vector<int32_t>().swap(h.ids);
+  return RB_OK;
+}
+
+// ---------------------------------------------------------------- replay
+
+rb_status rb_sim_run(rb_sched* s, const rb_servable* sv, int32_t n_sv, const rb_trace* tr, rb_log* log) {
+  if (!s || !sv || n_sv < 1 || !tr || !log) return RB_EINVAL;
+  const int64_t N = tr->n_requests;
+  if (N < 0 || (N > 0 && (!tr->servable || !tr->arrival_ns || !tr->n_rows))) return RB_EINVAL;
+  if (log->max_batches < N || (N > 0 && (!log->req_done_ns || !log->req_queue || !log->b_queue || !log->b_real ||
+                                         !log->b_padded || !log->b_close_ns || !log->b_dispatch_ns ||
+                                         !log->b_done_ns || !log->b_req_begin || !log->b_reqs)))
+    return log->max_batches < N ? RB_ESIZE : RB_EINVAL;
+  for (int32_t i = 0; i < n_sv; ++i) {
+    if (sv[i].n_queues < 1 || !sv[i].queues) return RB_EINVAL;
+    for (int32_t j = 0; j < sv[i].n_queues; ++j) {
+      rb_queue* q = sv[i].queues[j];
+      if (!q || q->s != s || q->undispatched || !q->closed.empty()) return RB_EINVAL;
+    }
+  }
+  const bool dev = s->stream != nullptr;
+  if (dev && N > 0 && (!tr->dense || !tr->dense_off || !tr->out || !tr->out_off)) return RB_EINVAL;
+  // route every request to its queue and validate it against that queue
+  std::vector<rb_queue*> rq((size_t)N);
+  for (int64_t r = 0; r < N; ++r) {
+    const int32_t si = tr->servable[r];
+    if (si < 0 || si >= n_sv) return RB_EINVAL;
+    const rb_servable& v = sv[si];
+    rb_queue* q = nullptr;
+    if (v.n_queues == 1 && v.queues[0]->bucket == 0) {
+      q = v.queues[0];
+    } else {
+      if (!tr->max_len) return RB_EINVAL;
+      const int L = tr->max_len[r];
+      for (int32_t j = 0; j < v.n_queues; ++j) {
+        rb_queue* c = v.queues[j];
+        if (c->bucket >= L && (!q || c->bucket < q->bucket)) q = c;
+      }
+      if (!q || L < 1) return RB_EINVAL;
+    }
+    if (tr->n_rows[r] < 1 || tr->n_rows[r] > q->B) return RB_EINVAL;
+    if (r > 0 && tr->arrival_ns[r] < tr->arrival_ns[r - 1]) return RB_EINVAL;
+    if (dev) {
+      const rb_model* m = q->m;
+      const int64_t n = tr->n_rows[r];
+      if (tr->out_off[r + 1] - tr->out_off[r] != n * m->d_out || tr->out_off[r] < 0) return RB_EINVAL;
+      if (tr->dense_off[r] < 0 || tr->dense_off[r + 1] < tr->dense_off[r]) return RB_EINVAL;
+      if (m->kind != RB_MODEL_SEQPOOL && tr->dense_off[r + 1] - tr->dense_off[r] != n * m->d_in) return RB_EINVAL;
+      if (m->kind != RB_MODEL_MLP) {
+        if (!tr->lens || !tr->lens_off) return RB_EINVAL;
+        const int64_t want = m->kind == RB_MODEL_RANKING ? n * m->n_tables : n;
+        if (tr->lens_off[r] < 0 || tr->lens_off[r + 1] - tr->lens_off[r] != want) return RB_EINVAL;
+      }
+      if (m->kind == RB_MODEL_RANKING) {
+        if (!tr->ids || !tr->ids_off || tr->ids_off[r] < 0 || tr->ids_off[r + 1] < tr->ids_off[r]) return RB_EINVAL;
+      }
+    }
+    rq[(size_t)r] = q;
+  }
+  if (dev) {
+    s->a_dense = tr->dense;
+    s->a_dense_len = N > 0 ? tr->dense_off[N] : 0;
+    s->a_lens = tr->lens;
+    s->a_ids = tr->ids;
+    s->a_out = tr->out;
+  }
+  // a replay runs on its own simulated clock, starting idle
+  s->now = INT64_MIN;
+  s->device_free = INT64_MIN;
+  s->last_served = -1;
+  // event loop
+  int64_t nb = 0, nreq_logged = 0;
+  const int64_t end_t = N > 0 ? tr->arrival_ns[N - 1] : 0;
+  bool flushed = N == 0;
+  int64_t nxt = 0;
+  std::vector<rb_k_req> kreqs;
+  rb_status st = RB_OK;
+  auto dispatch_at = [&](int64_t t) -> rb_status {
+    while (s->device_free <= t && s->n_closed > 0) {
+      rb_queue* q = pick_round_robin(s);
+      Batch b = std::move(q->closed.front());
+      q->closed.pop_front();
+      s->n_closed--;
+      q->undispatched -= (int64_t)b.reqs.size();
+      b.seq = s->batch_seq++;
+      b.dispatch_ns = t;
+      b.done_ns = t + service(q, b.P);
+      s->device_free = b.done_ns;
+      s->last_served = q->id;
+      log->b_queue[nb] = q->id;
+      log->b_real[nb] = b.s;
+      log->b_padded[nb] = b.P;
+      log->b_close_ns[nb] = b.close_ns;
+      log->b_dispatch_ns[nb] = b.dispatch_ns;
+      log->b_done_ns[nb] = b.done_ns;
+      log->b_req_begin[nb] = nreq_logged;
+      for (int64_t r : b.reqs) {
+        log->b_reqs[nreq_logged++] = (int32_t)r;
+        log->req_done_ns[r] = b.done_ns;
+        log->req_queue[r] = q->id;
+      }
+      ++nb;
+      if (dev) {
+        kreqs.clear();
+        for (int64_t r : b.reqs) {
+          rb_k_req k{};
+          k.dense_off = tr->dense_off[r];
+          k.dense_end = tr->dense_off[r + 1];
+          k.lens_off = tr->lens_off ? tr->lens_off[r] : 0;
+          k.ids_off = tr->ids_off ? tr->ids_off[r] : 0;
+          k.ids_end = tr->ids_off ? tr->ids_off[r + 1] : 0;
+          k.out_off = tr->out_off[r];
+          k.n_rows = tr->n_rows[r];
+          kreqs.push_back(k);
+        }
+        window_add(s, q, b, kreqs);
+        if (s->window_batches >= s->opts.window_batches) {
+          close_window(s);
+          if ((int)s->chunk.size() >= CHUNK_WINDOWS) {
+            rb_status e = flush_chunk(s);
+            if (e != RB_OK) return e;
+          }
+        }
+      }
+    }
+    return RB_OK;
+  };
+  for (;;) {
+    int64_t t = INT64_MAX;
+    if (nxt < N) t = std::min(t, tr->arrival_ns[nxt]);
+    t = std::min(t, next_timeout(s));
+    if (!flushed && nxt >= N) t = std::min(t, end_t);
+    if (s->n_closed > 0) t = std::min(t, s->device_free);
+    if (t == INT64_MAX) break;
+    fire_timeouts_at(s, t);
+    while (nxt < N && tr->arrival_ns[nxt] == t) {
+      arrive(rq[(size_t)nxt], nxt, tr->n_rows[nxt], t);
+      ++nxt;
+    }
+    if (!flushed && nxt >= N && t == end_t) {
+      for (rb_queue* q : s->queues)
+        if (q && q->T == NO_TIMEOUT && q->open_s > 0) close_open(q, t);
+      flushed = true;
+    }
+    s->now = std::max(s->now, t);
+    if ((st = dispatch_at(t)) != RB_OK) break;
+  }
+  if (st == RB_OK && dev) {
+    close_window(s);
+    st = flush_chunk(s);
+  }
+  log->n_batches = nb;
+  if (N > 0) log->b_req_begin[nb] = nreq_logged;
+  return st;
+}
+
+}  // extern "C"

@@ -1,0 +1,198 @@
+"""End-to-end GPU parity: every workload's trace (a prefix sized for the
+oracle) is replayed through the library on the GPU; the batch log must equal
+the oracle's bit for bit and every request's output rows must match the
+oracle's unbatched forward of that request within the tolerance of its
+precision (row-scaled: max_j |y_j - ref_j| <= rtol * max_j |ref_j|, rtol 1e-5
+for fp32 models, 2e-2 for bf16 weights with fp32 accumulation). Also: NaN
+padding never reaches an output, outputs do not depend on the launch window
+(bit for bit), and the serving API (submit / run_next / collect)."""
+import functools
+
+import numpy as np
+import pytest
+
+torch = pytest.importorskip("torch")
+
+import synth
+from oracle.models import OracleModel
+from paper_1712_06139_amd import rb
+from paper_1712_06139_amd.deploy import Deployment
+
+from helpers import lib_batches, oracle_batches, oracle_sim, service_table
+
+pytestmark = pytest.mark.gpu
+
+RTOL = {"f32": 1e-5, "bf16": 2e-2}
+
+PREFIX = {"small_mlp": 256, "ranking": 1200, "large_mlp": 72, "multi_tenant": 1500, "ragged_seq": 300}
+
+
+@pytest.fixture(scope="module")
+def ctx():
+    c = rb.Ctx(0)
+    yield c
+
+
+@functools.lru_cache(maxsize=None)
+def oracle_model(name, s):
+    w = synth.workload(name)
+    return OracleModel(w.models[s], synth.model_params(w, s))
+
+
+@functools.lru_cache(maxsize=None)
+def trace_and_arenas(name, n):
+    w = synth.workload(name)
+    t = synth.trace(w, n)
+    return t, synth.arenas(t)
+
+
+def row_scaled_err(y, ref):
+    scale = np.maximum(np.max(np.abs(ref), axis=1, keepdims=True), 1e-30)
+    return float(np.max(np.abs(y.astype(np.float64) - ref) / scale))
+
+
+def run(ctx, name, n, window=1, pad=0.0, profile=False):
+    w = synth.workload(name)
+    t, a = trace_and_arenas(name, n)
+    svc = service_table(w)
+    dep = Deployment(w, ctx, device=True, window_batches=window, pad_value=pad, service_ns=svc, profile=profile)
+    try:
+        dt = dep.upload(t, a)
+        log = dep.replay(dt)
+        dep.sched.sync()
+        out = dt.out.cpu().numpy()
+        return w, t, a, dep.qindex, log, out, dt.out_off
+    finally:
+        dep.destroy()
+
+
+def check_outputs(name, t, a, out, out_off, reqs):
+    w = synth.workload(name)
+    worst = 0.0
+    for r in reqs:
+        s = int(t.servable[r])
+        om = oracle_model(name, s)
+        ref = om.forward(a.payload(r))
+        y = out[out_off[r]:out_off[r + 1]].reshape(ref.shape)
+        assert np.isfinite(y).all(), r
+        e = row_scaled_err(y, ref.astype(np.float64))
+        worst = max(worst, e)
+        assert e <= RTOL[w.models[s].dtype], (name, r, e)
+    return worst
+
+
+@pytest.mark.parametrize("name", list(PREFIX))
+def test_workload_prefix_matches_oracle(ctx, name):
+    n = PREFIX[name]
+    w, t, a, qindex, log, out, out_off = run(ctx, name, n)
+    assert lib_batches(log, qindex) == oracle_batches(oracle_sim(w, t, service_table(w)))
+    worst = check_outputs(name, t, a, out, out_off, range(t.n))
+    print(f"{name}: {t.n} requests, worst row-scaled error {worst:.3g}")
+
+
+@pytest.mark.parametrize("name", ["small_mlp", "ranking", "ragged_seq"])
+def test_nan_padding_never_leaks(ctx, name):
+    n = min(PREFIX[name], 400)
+    *_, out0, _ = run(ctx, name, n, pad=0.0)
+    *_, out1, _ = run(ctx, name, n, pad=float("nan"))
+    assert np.isfinite(out1).all()
+    assert np.array_equal(out0, out1)
+
+
+@pytest.mark.parametrize("name", ["small_mlp", "ranking", "large_mlp", "ragged_seq"])
+def test_outputs_independent_of_launch_window(ctx, name):
+    n = min(PREFIX[name], 600)
+    *_, out1, _ = run(ctx, name, n, window=1)
+    *_, out8, _ = run(ctx, name, n, window=8)
+    assert np.array_equal(out1, out8)
+
+
+def test_serving_api_matches_oracle(ctx):
+    name = "small_mlp"
+    w = synth.workload(name)
+    t, a = trace_and_arenas(name, 256)
+    dep = Deployment(w, ctx, device=True, service_ns=service_table(w))
+    try:
+        q = dep.queues[0]
+        ids = []
+        for r in range(t.n):
+            p = a.payload(r)
+            ids.append(dep.sched.submit(q, int(t.n_rows[r]), p.dense, arrival_ns=int(t.arrival_ns[r])))
+            while dep.sched.run_next() is not None:
+                pass
+        rb.check(rb.lib().rb_flush(q.h), "rb_flush")
+        while dep.sched.run_next() is not None:
+            pass
+        dep.sched.sync()
+        om = oracle_model(name, 0)
+        for r in range(t.n):
+            y = dep.sched.collect(ids[r], int(t.n_rows[r]), 16)
+            ref = om.forward(a.payload(r))
+            assert row_scaled_err(y, ref.astype(np.float64)) <= RTOL["f32"]
+        with pytest.raises(rb.RBError) as e:
+            dep.sched.collect(ids[0], int(t.n_rows[0]), 16)
+        assert e.value.status == rb.RB_ENOENT
+    finally:
+        dep.destroy()
+
+
+def test_serving_api_ranking_and_seqpool(ctx):
+    for name, n in (("ranking", 120), ("ragged_seq", 60)):
+        w = synth.workload(name)
+        t, a = trace_and_arenas(name, n)
+        dep = Deployment(w, ctx, device=True)
+        try:
+            ids = []
+            maxlen = dep.max_len(t)
+            for r in range(t.n):
+                p = a.payload(r)
+                if name == "ragged_seq":
+                    q = min((q for q in dep.queues if w.queues[dep.qindex[q.id]].bucket_len >= maxlen[r]),
+                            key=lambda q: w.queues[dep.qindex[q.id]].bucket_len)
+                else:
+                    q = dep.queues[0]
+                ids.append(dep.sched.submit(q, int(t.n_rows[r]), p.dense, p.lens, p.ids, 0))
+            for q in dep.queues:
+                rb.check(rb.lib().rb_flush(q.h), "rb_flush")
+            while dep.sched.run_next() is not None:
+                pass
+            dep.sched.sync()
+            for r in range(t.n):
+                om = oracle_model(name, 0)
+                ref = om.forward(a.payload(r))
+                y = dep.sched.collect(ids[r], int(t.n_rows[r]), ref.shape[1])
+                assert row_scaled_err(y, ref.astype(np.float64)) <= RTOL[w.models[0].dtype]
+        finally:
+            dep.destroy()
+
+
+def test_device_bounds_errors_are_reported(ctx):
+    # an id outside its table and bag lengths that disagree with the ids are
+    # caught by the kernels' own bounds checks: nothing is read out of bounds
+    name = "ranking"
+    w = synth.workload(name)
+    t, a = trace_and_arenas(name, 40)
+    dep = Deployment(w, ctx, device=True)
+    try:
+        bad_ids = a.ids.copy()
+        bad_ids[5] = 100_000_000
+        a2 = synth.Arenas(a.dense, a.lens, bad_ids, a.dense_off, a.lens_off, a.ids_off)
+        dt = dep.upload(t, a2)
+        dep.replay(dt)
+        with pytest.raises(rb.RBError) as e:
+            dep.sched.sync()
+        assert e.value.status == rb.RB_ERANGE
+        bad_lens = a.lens.copy()
+        bad_lens[3] += 1
+        a3 = synth.Arenas(a.dense, bad_lens, a.ids, a.dense_off, a.lens_off, a.ids_off)
+        dt = dep.upload(t, a3)
+        dep.replay(dt)
+        with pytest.raises(rb.RBError) as e:
+            dep.sched.sync()
+        assert e.value.status == rb.RB_ERANGE
+        # the scheduler keeps serving afterwards
+        dt = dep.upload(t, a)
+        dep.replay(dt)
+        dep.sched.sync()
+    finally:
+        dep.destroy()

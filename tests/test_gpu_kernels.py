@@ -1,0 +1,331 @@
+"""GPU parity of each kernel of the batching path against the oracle, called
+through the C ABI (rb_k_*), on shapes that span several tiles, ragged tails
+and padding. Bit-exact for routing and copies; the floating-point kernels are
+held to the oracle's fp64 result within the stated tolerances."""
+import numpy as np
+import pytest
+
+torch = pytest.importorskip("torch")
+
+from oracle import batching as ob
+from oracle import numerics as nx
+from paper_1712_06139_amd import rb
+
+pytestmark = pytest.mark.gpu
+
+DEV = "cuda"
+
+
+def _stream():
+    return rb.torch_stream_ptr()
+
+
+def _dev(a):
+    return torch.from_numpy(np.ascontiguousarray(a)).to(DEV)
+
+
+def _err():
+    return torch.zeros(1, dtype=torch.int32, device=DEV)
+
+
+def _rows_np(t):
+    return t.cpu().numpy().view(np.uint8).view(rb.K_ROW_DTYPE)
+
+
+def _make_group(rng, kind, n_batches, B, allowed, d_in, d_out, n_tables=0, seq_T=0, max_n=None):
+    """Random batches of requests laid out like a trace arena."""
+    max_n = max_n or B
+    batches, reqs = [], []
+    dense, lens, ids = [], [], []
+    dense_off = lens_off = ids_off = out_off = 0
+    row_base = 0
+    for _ in range(n_batches):
+        s, nreq, begin = 0, 0, len(reqs)
+        while True:
+            n = int(rng.integers(1, max_n + 1))
+            if s + n > B or (nreq and rng.random() < 0.1):
+                break
+            if kind == rb.RB_MODEL_SEQPOOL:
+                L = rng.integers(1, seq_T + 1, size=n)
+                d = rng.standard_normal((int(L.sum()), d_in)).astype(np.float32)
+                ln = L.astype(np.int32)
+                ii = np.zeros(0, np.int32)
+            elif kind == rb.RB_MODEL_RANKING:
+                d = rng.standard_normal((n, d_in)).astype(np.float32)
+                ln = rng.integers(0, 21, size=(n, n_tables)).astype(np.int32)
+                ii = rng.integers(0, 1000, size=int(ln.sum())).astype(np.int32)
+            else:
+                d = rng.standard_normal((n, d_in)).astype(np.float32)
+                ln = np.zeros(0, np.int32)
+                ii = np.zeros(0, np.int32)
+            reqs.append((dense_off, dense_off + d.size, lens_off, ids_off, ids_off + ii.size, out_off, n))
+            dense.append(d.ravel()); lens.append(ln.ravel()); ids.append(ii)
+            dense_off += d.size; lens_off += ln.size; ids_off += ii.size; out_off += n * d_out
+            s += n
+            nreq += 1
+        P = ob.padded_size(s, allowed)
+        batches.append((begin, nreq, row_base, P, s, seq_T))
+        row_base += P
+    kb = np.array(batches, dtype=np.int32).view(rb.K_BATCH_DTYPE).ravel()
+    kr = np.zeros(len(reqs), dtype=rb.K_REQ_DTYPE)
+    for i, r in enumerate(reqs):
+        kr[i] = r + (0,)
+    arena = dict(dense=np.concatenate(dense), lens=np.concatenate(lens) if lens_off else np.zeros(1, np.int32),
+                 ids=np.concatenate(ids) if ids_off else np.zeros(1, np.int32), out_len=out_off)
+    return kb, kr, arena, row_base
+
+
+def _route(kind, kb, kr, arena, rows_total, d_in, d_out, n_tables=0):
+    rows = torch.empty(rows_total * 4, dtype=torch.int64, device=DEV)
+    err = _err()
+    # device tensors stay referenced until the kernel has run
+    lens = _dev(arena["lens"])
+    kb_d = _dev(kb.view(np.uint8))
+    kr_d = _dev(kr.view(np.uint8))
+    rb.check(rb.lib().rb_k_route(_stream(), kind, rb.dptr(kb_d), len(kb), rb.dptr(kr_d), rb.dptr(lens), d_in,
+                                 d_out, n_tables, rb.dptr(rows), rb.dptr(err)), "rb_k_route")
+    torch.cuda.synchronize()
+    return rows, err
+
+
+def _expected_rows(kind, kb, kr, arena, d_in, d_out, n_tables=0):
+    """Row map from the oracle's routing (exclusive prefix sums)."""
+    out = []
+    for b in kb:
+        rq = kr[b["req_begin"]:b["req_begin"] + b["n_req"]]
+        dst = ob.dst_rows(rq["n_rows"])
+        rows = [(-1, 0, -1, -1)] * int(b["padded"])
+        for q, d0 in zip(rq, dst):
+            n = int(q["n_rows"])
+            if kind == rb.RB_MODEL_SEQPOOL:
+                L = arena["lens"][q["lens_off"]:q["lens_off"] + n]
+                t0 = np.concatenate([[0], np.cumsum(L)[:-1]])
+                for e in range(n):
+                    rows[d0 + e] = (q["dense_off"] + t0[e] * d_in, int(L[e]), q["lens_off"] + e,
+                                    q["out_off"] + e * d_out)
+            else:
+                id0 = q["ids_off"]
+                for e in range(n):
+                    lo = q["lens_off"] + e * n_tables if kind == rb.RB_MODEL_RANKING else -1
+                    rows[d0 + e] = (q["dense_off"] + e * d_in, id0, lo, q["out_off"] + e * d_out)
+                    if kind == rb.RB_MODEL_RANKING:
+                        id0 += int(arena["lens"][lo:lo + n_tables].sum())
+        out.extend(rows)
+    return np.array(out, dtype=np.int64)
+
+
+@pytest.mark.parametrize("kind,B,allowed,d_in,d_out,nt,T", [
+    (rb.RB_MODEL_MLP, 32, (8, 16, 32), 64, 16, 0, 0),
+    (rb.RB_MODEL_MLP, 1024, (128, 256, 512, 1024), 40, 7, 0, 0),
+    (rb.RB_MODEL_RANKING, 512, (64, 128, 256, 512), 13, 1, 26, 0),
+    (rb.RB_MODEL_SEQPOOL, 64, (), 16, 2, 0, 64),
+])
+def test_route_bit_exact(kind, B, allowed, d_in, d_out, nt, T):
+    rng = np.random.default_rng(1)
+    kb, kr, arena, R = _make_group(rng, kind, 7, B, allowed, d_in, d_out, nt, T,
+                                   max_n=64 if kind == rb.RB_MODEL_RANKING else (4 if T else 32))
+    rows, err = _route(kind, kb, kr, arena, R, d_in, d_out, nt)
+    got = _rows_np(rows)
+    want = _expected_rows(kind, kb, kr, arena, d_in, d_out, nt)
+    assert int(err.item()) == 0
+    g = np.stack([got["src"], got["aux"], got["lens"], got["out"]], axis=1)
+    pad = want[:, 0] < 0
+    assert np.array_equal(g[~pad], want[~pad])
+    assert np.all(g[pad][:, 0] == -1) and np.all(g[pad][:, 3] == -1)
+
+
+@pytest.mark.parametrize("bf16", [0, 1])
+@pytest.mark.parametrize("d_in,ldx", [(64, 64), (4096, 4096), (13, 64), (40, 64)])
+def test_assemble_bit_exact(bf16, d_in, ldx):
+    rng = np.random.default_rng(2)
+    kb, kr, arena, R = _make_group(rng, rb.RB_MODEL_MLP, 5, 256, (64, 128, 256), d_in, 4, max_n=32)
+    rows, err = _route(rb.RB_MODEL_MLP, kb, kr, arena, R, d_in, 4)
+    dense = _dev(arena["dense"])
+    X = torch.empty((R, ldx), dtype=torch.int16 if bf16 else torch.float32, device=DEV)
+    rb.check(rb.lib().rb_k_assemble(_stream(), rb.dptr(rows), R, 0, rb.dptr(dense), dense.numel(), d_in,
+                                    rb.dptr(X), ldx, bf16, float("nan"), rb.dptr(err)), "rb_k_assemble")
+    torch.cuda.synchronize()
+    assert int(err.item()) == 0
+    got = X.cpu().numpy()
+    if bf16:
+        got = (got.astype(np.uint16).astype(np.uint32) << 16).view(np.float32)
+    for b in kb:
+        rq = kr[b["req_begin"]:b["req_begin"] + b["n_req"]]
+        pays = [synth_payload(arena["dense"][q["dense_off"]:q["dense_end"]].reshape(-1, d_in)) for q in rq]
+        ref = ob.assemble(_MlpShape(d_in), pays, int(b["padded"]), pad=np.nan).dense
+        if bf16:
+            ref = nx.round_bf16(ref)
+        blk = got[b["row_base"]:b["row_base"] + b["padded"]]
+        assert np.array_equal(blk[:, :d_in], ref, equal_nan=True)
+        assert np.all(blk[:, d_in:] == 0)
+
+
+class _MlpShape:
+    kind = "mlp"
+
+    def __init__(self, d_in):
+        self.d_in = d_in
+
+
+def synth_payload(d):
+    from synth import Payload
+    return Payload(d)
+
+
+def test_embbag_matches_oracle():
+    rng = np.random.default_rng(3)
+    nt, rows_t = 26, 1000
+    kb, kr, arena, R = _make_group(rng, rb.RB_MODEL_RANKING, 4, 512, (64, 128, 256, 512), 13, 1, nt, 0,
+                                   max_n=64)
+    rows, err = _route(rb.RB_MODEL_RANKING, kb, kr, arena, R, 13, 1, nt)
+    tables = [(rng.standard_normal((rows_t, 64)) / 8).astype(np.float32) for _ in range(nt)]
+    tb = [nx.round_bf16(t).astype(np.float32) for t in tables]
+    dev_t = [torch.from_numpy((t.view(np.uint32) >> 16).astype(np.uint16).view(np.int16)).to(DEV) for t in tb]
+    ptrs = _dev(np.array([t.data_ptr() for t in dev_t], dtype=np.uint64).view(np.int64))
+    ldx = 1728
+    X = torch.empty((R, ldx), dtype=torch.int16, device=DEV)
+    dense, lens, ids = _dev(arena["dense"]), _dev(arena["lens"]), _dev(arena["ids"])
+    rb.check(rb.lib().rb_k_embbag(_stream(), rb.dptr(rows), R, rb.dptr(lens), rb.dptr(ids), rb.dptr(ptrs), nt,
+                                  rows_t, 64, rb.dptr(dense), 13, rb.dptr(X), ldx, 0.0, rb.dptr(err)), "embbag")
+    torch.cuda.synchronize()
+    assert int(err.item()) == 0
+    got = (X.cpu().numpy().astype(np.uint16).astype(np.uint32) << 16).view(np.float32)
+    rmap = _rows_np(rows)
+    from oracle.models import OracleModel
+    from synth import Layer, Model, Params
+    m = Model(kind="ranking", dtype="bf16", seed_id=0, layers=(Layer(nt * 64 + 13, 1, "sigmoid"),),
+              n_tables=nt, table_rows=rows_t, emb_dim=64, n_dense=13)
+    om = OracleModel(m, Params([(np.zeros((1, nt * 64 + 13), np.float32), np.zeros(1, np.float32))], tables))
+    n_exact = n_tot = 0
+    for r in range(R):
+        rw = rmap[r]
+        if rw["src"] < 0:
+            assert np.all(got[r, :nt * 64 + 13] == 0) and np.all(got[r, nt * 64 + 13:] == 0)
+            continue
+        ln = arena["lens"][rw["lens"]:rw["lens"] + nt]
+        ii = arena["ids"][rw["aux"]:rw["aux"] + ln.sum()]
+        dn = arena["dense"][rw["src"]:rw["src"] + 13]
+        ref = om.ranking_input(dn[None, :], ln[None, :], ii)[0]
+        g = got[r, :nt * 64 + 13].astype(np.float64)
+        # fp32 accumulation vs fp64: at most one bf16 ulp apart after rounding
+        ulp = np.maximum(np.abs(ref), 2.0 ** -126) * 2.0 ** -7
+        assert np.all(np.abs(g - ref) <= ulp), r
+        assert np.all(got[r, nt * 64 + 13:] == 0)
+        n_exact += int(np.sum(g == ref))
+        n_tot += g.size
+    assert n_exact >= 0.99 * n_tot
+
+
+def _bf16_dev(a):
+    b = nx.round_bf16(a).astype(np.float32)
+    return torch.from_numpy((b.view(np.uint32) >> 16).astype(np.uint16).view(np.int16)).to(DEV), b
+
+
+def _row_scaled_err(y, ref):
+    scale = np.maximum(np.max(np.abs(ref), axis=1, keepdims=True), 1e-30)
+    return np.max(np.abs(y - ref) / scale)
+
+
+@pytest.mark.parametrize("M,N,K,act,out_f32", [
+    (1, 128, 64, rb.RB_ACT_NONE, 1), (200, 256, 1728, rb.RB_ACT_RELU, 0), (1024, 1024, 512, rb.RB_ACT_RELU, 0),
+    (333, 512, 1024, rb.RB_ACT_NONE, 1), (130, 128, 4096, rb.RB_ACT_SIGMOID, 1)])
+def test_gemm_bf16_matches_fp64(M, N, K, act, out_f32):
+    rng = np.random.default_rng(4)
+    Xd, X = _bf16_dev(rng.standard_normal((M, K)))
+    Wd, W = _bf16_dev(rng.standard_normal((N, K)) / np.sqrt(K))
+    b = rng.uniform(-0.5, 0.5, N).astype(np.float32)
+    bd = _dev(b)
+    Y = torch.empty((M, N), dtype=torch.float32 if out_f32 else torch.int16, device=DEV)
+    rb.check(rb.lib().rb_k_gemm_bf16(_stream(), rb.dptr(Xd), K, rb.dptr(Wd), K, rb.dptr(bd), rb.dptr(Y), N, M, N, K,
+                                     act, out_f32), "gemm_bf16")
+    torch.cuda.synchronize()
+    got = Y.cpu().numpy()
+    if not out_f32:
+        got = (got.astype(np.uint16).astype(np.uint32) << 16).view(np.float32)
+    name = {0: "none", 1: "relu", 2: "sigmoid"}[act]
+    ref = nx.dense(X, W, b, name)
+    # fp32 accumulation of exact bf16 products: far inside the 2e-2 bf16 bar
+    tol = 2e-2 if not out_f32 else 1e-4
+    assert _row_scaled_err(got, ref) <= tol
+    if not out_f32:
+        assert np.max(np.abs(got - ref) / np.maximum(np.abs(ref), 1e-3)) <= 2.0 ** -7
+
+
+@pytest.mark.parametrize("M,N,K,act", [(1, 64, 64, rb.RB_ACT_RELU), (257, 1024, 256, rb.RB_ACT_RELU),
+                                       (1000, 64, 1024, rb.RB_ACT_NONE), (64 * 64, 512, 256, rb.RB_ACT_RELU)])
+def test_gemm_f32_matches_fp64(M, N, K, act):
+    rng = np.random.default_rng(5)
+    X = rng.standard_normal((M, K)).astype(np.float32)
+    W = (rng.standard_normal((N, K)) / np.sqrt(K)).astype(np.float32)
+    b = rng.uniform(-0.5, 0.5, N).astype(np.float32)
+    Y = torch.empty((M, N), dtype=torch.float32, device=DEV)
+    Xd, Wd, bd = _dev(X), _dev(W), _dev(b)
+    rb.check(rb.lib().rb_k_gemm_f32(_stream(), rb.dptr(Xd), K, rb.dptr(Wd), K, rb.dptr(bd),
+                                    rb.dptr(Y), N, M, N, K, act), "gemm_f32")
+    torch.cuda.synchronize()
+    ref = nx.dense(X, W, b, "relu" if act == rb.RB_ACT_RELU else "none")
+    assert _row_scaled_err(Y.cpu().numpy(), ref) <= 1e-5
+
+
+def _rows_dev(src, aux, out):
+    a = np.zeros(len(src), dtype=rb.K_ROW_DTYPE)
+    a["src"], a["aux"], a["lens"], a["out"] = src, aux, -1, out
+    return _dev(a.view(np.uint8))
+
+
+def test_head_and_split():
+    rng = np.random.default_rng(6)
+    R, K = 300, 256
+    out_idx = np.where(rng.random(R) < 0.8, np.arange(R) * 3, -1)
+    rows = _rows_dev(np.zeros(R), np.zeros(R), out_idx)
+    Hd, H = _bf16_dev(rng.standard_normal((R, K)))
+    wd, w = _bf16_dev(rng.standard_normal(K) / 16)
+    out = torch.full((R * 3,), -7.0, device=DEV)
+    rb.check(rb.lib().rb_k_head(_stream(), rb.dptr(rows), R, rb.dptr(Hd), K, rb.dptr(wd), 0.25, K,
+                                rb.RB_ACT_SIGMOID, rb.dptr(out)), "head")
+    Y = rng.standard_normal((R, 64)).astype(np.float32)
+    out2 = torch.full((R * 3 * 10,), -7.0, device=DEV)
+    rows2 = _rows_dev(np.zeros(R), np.zeros(R), np.where(out_idx >= 0, out_idx * 10, -1))
+    Yd = _dev(Y)
+    rb.check(rb.lib().rb_k_split(_stream(), rb.dptr(rows2), R, rb.dptr(Yd), 64, 30, rb.dptr(out2)), "split")
+    torch.cuda.synchronize()
+    o = out.cpu().numpy()
+    o2 = out2.cpu().numpy()
+    ref = nx.sigmoid(H.astype(np.float64) @ w.astype(np.float64) + 0.25)
+    for r in range(R):
+        if out_idx[r] < 0:
+            continue
+        assert abs(o[out_idx[r]] - ref[r]) <= 1e-5 * abs(ref[r])
+        assert np.array_equal(o2[out_idx[r] * 10:out_idx[r] * 10 + 30], Y[r, :30])
+    keep = np.zeros(R * 3, bool)
+    keep[out_idx[out_idx >= 0]] = True
+    assert np.all(o[~keep] == -7.0)
+
+
+def test_seqpool_matches_oracle():
+    rng = np.random.default_rng(7)
+    S, T, D, n_out = 50, 64, 256, 2
+    L = rng.integers(1, T + 1, size=S)
+    L[:3] = [1, T, 2]
+    H = rng.standard_normal((S * T, D)).astype(np.float32)
+    Hn = H.copy()
+    for s in range(S):
+        Hn[s * T + L[s]:(s + 1) * T] = np.nan   # tokens past L must never be read
+    Wh = (rng.standard_normal((n_out, D)) / 16).astype(np.float32)
+    bh = rng.uniform(-0.5, 0.5, n_out).astype(np.float32)
+    out_idx = np.arange(S) * n_out
+    out_idx[5] = -1
+    rows = _rows_dev(np.zeros(S), L, out_idx)
+    out = torch.full((S * n_out,), -7.0, device=DEV)
+    Hd, Whd, bhd = _dev(Hn), _dev(Wh), _dev(bh)
+    rb.check(rb.lib().rb_k_seqpool(_stream(), rb.dptr(rows), S, T, rb.dptr(Hd), D, D, rb.dptr(Whd),
+                                   rb.dptr(bhd), n_out, rb.RB_ACT_SOFTMAX, rb.dptr(out)), "seqpool")
+    torch.cuda.synchronize()
+    o = out.cpu().numpy().reshape(S, n_out)
+    for s in range(S):
+        if out_idx[s] < 0:
+            assert np.all(o[s] == -7.0)
+            continue
+        pooled = nx.round_f32(np.sum(H[s * T:s * T + L[s]].astype(np.float64), axis=0) / L[s])
+        ref = nx.round_f32(nx.softmax(nx.round_f32(nx.dense(pooled[None], Wh, bh, "none"))))[0]
+        assert np.max(np.abs(o[s] - ref)) <= 1e-5 * np.max(np.abs(ref)), s
