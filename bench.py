@@ -1,0 +1,279 @@
+#!/usr/bin/env python
+"""Throughput and latency of batched inference on one MI355X.
+
+Workload (default): the ranking model - 26 sum-pooled embedding bags (ids
+Zipf(1.1) over 100k-row x 64 bf16 tables, 1..20 ids per bag) plus 13 dense
+features into an MLP 1677->1024->512->256->1 (ReLU, sigmoid out), bf16
+weights with fp32 accumulation; 100k requests of 1..64 examples, batches of
+at most 512 rows padded to {64,128,256,512}, formed by count in arrival order.
+
+One step replays the whole 100k-request trace through the library: batch
+formation, padded-size choice, round-robin dispatch on the simulated clock,
+and every batch's route -> embedding-bag -> 3 GEMMs -> head on the GPU, with
+the request payloads already resident in HBM and the outputs left there.
+
+Printed: one JSON line with examples/s, p50/p99 request latency on the
+simulated clock (service times measured on this GPU, Poisson arrivals at 90%
+of the measured capacity), the dominant kernel against its roofline (HIP
+events on the library's stream during a profiled replay), and the CPU oracle
+timed on a bounded sample of the same trace.
+"""
+import argparse
+import json
+import math
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "examples/sec per MI355X (batched MLP/embedding model); p50/p99 request latency"
+HBM_PEAK_GBS = 8000.0
+BF16_PEAK_TFLOPS = 2500.0
+F32_PEAK_TFLOPS = 157.3
+
+
+def log(msg):
+    print(f"[bench] {msg}", file=sys.stderr, flush=True)
+
+
+def nearest_rank(v, q):
+    v = np.sort(np.asarray(v))
+    return int(v[max(1, int(math.ceil(q * len(v)))) - 1])
+
+
+def algorithmic_work(w, t, a, logd):
+    """Algorithmic bytes / flops of one replay, per kernel (real model dims;
+    padded rows count as rows: they are computed as the method pads them)."""
+    m = w.models[0]
+    P = logd["b_padded"].astype(np.int64)
+    M = int(P.sum())
+    real = int(logd["b_real"].sum())
+    n_req = t.n
+    n_ids = int(a.ids.size)
+    row_desc = 32
+    work = {}
+    # route: request descriptors, batch descriptors, bag lengths of real rows, row map writes
+    work["route"] = {"bytes": n_req * 56 + len(P) * 24 + real * m.n_tables * 4 + M * row_desc}
+    # embedding bags: row map, lengths, ids, one 128 B table row per id, dense, X row write
+    ldx = m.n_tables * m.emb_dim + m.n_dense
+    work["embbag"] = {"bytes": M * row_desc + real * (m.n_tables * 4 + m.n_dense * 4) + n_ids * (4 + m.emb_dim * 2)
+                      + M * ldx * 2}
+    fl = 0
+    by = 0
+    for L in m.layers[:-1]:
+        fl += 2 * M * L.fan_in * L.fan_out
+        by += (M * L.fan_in + L.fan_in * L.fan_out + M * L.fan_out) * 2 + L.fan_out * 4
+    work["gemm_bf16"] = {"flops": fl, "bytes": by}
+    last = m.layers[-1]
+    work["head"] = {"bytes": M * row_desc + M * last.fan_in * 2 + last.fan_in * 2 + real * 4,
+                    "flops": 2 * M * last.fan_in}
+    return work
+
+
+def cpu_baseline(w, t, a, seconds):
+    """The oracle, as it stands, on the first requests of the trace for about
+    `seconds` of CPU time (setup excluded)."""
+    from oracle.models import OracleModel
+    import synth
+    try:
+        from threadpoolctl import threadpool_info
+        cores = max([d.get("num_threads", 1) for d in threadpool_info()] + [1])
+    except Exception:
+        cores = 1
+    om = OracleModel(w.models[0], synth.model_params(w, 0))
+    n = ex = 0
+    t0 = time.perf_counter()
+    while time.perf_counter() - t0 < seconds and n < t.n:
+        om.forward(a.payload(n))
+        ex += int(t.n_rows[n])
+        n += 1
+    el = time.perf_counter() - t0
+    return {"value": ex / el, "unit": "examples/s", "cores": int(cores), "kind": "oracle",
+            "sample": f"first {n} requests ({ex} examples) of the same trace, unbatched fp64 forward per request, "
+                      f"{el:.1f} s"}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=5)
+    ap.add_argument("--warmup", type=int, default=2)
+    ap.add_argument("--window", type=int, default=64, help="dispatched batches per launch window")
+    ap.add_argument("--cpu-seconds", type=float, default=15.0)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-latency", action="store_true")
+    ap.add_argument("--sweep-windows", default="", help="comma list: also time these windows (stderr)")
+    args = ap.parse_args()
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print("bench.py measures one MI355X only: batching serves independent requests, so more GPUs are "
+              "independent replicas (no collectives); run with --gpus 1", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    import synth
+    from paper_1712_06139_amd import rb
+    from paper_1712_06139_amd.deploy import Deployment
+
+    assert torch.cuda.is_available(), "needs a GPU"
+    w = synth.workload("ranking")
+    t = synth.trace(w)
+    log(f"generating {t.n} requests ({int(t.n_rows.sum())} examples)")
+    t0 = time.time()
+    a = synth.arenas(t)
+    log(f"payloads drawn in {time.time() - t0:.1f} s ({a.ids.size} ids); building model")
+    synth.model_params(w, 0)
+    ctx = rb.Ctx(0)
+    examples = int(t.n_rows.sum())
+
+    shared = {}
+
+    def make(window, profile=False):
+        d = Deployment(w, ctx, device=True, window_batches=window, profile=profile, models=shared.get("m"))
+        shared.setdefault("m", d.models)
+        return d
+
+    dep = make(args.window)
+    dt = dep.upload(t, a)
+    log("uploaded; warmup")
+    for _ in range(args.warmup):
+        dep.replay(dt)
+        dep.sched.sync()
+    stream = torch.cuda.ExternalStream(dep.sched.stream())
+    ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    ev0.record(stream)
+    for _ in range(args.steps):
+        logd = dep.replay(dt)
+    ev1.record(stream)
+    dep.sched.sync()
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    dev_ms = ev0.elapsed_time(ev1)
+    ms_per_step = wall * 1e3 / args.steps
+    value = examples * args.steps / wall
+    n_batches = int(logd["n_batches"])
+    log(f"timed {args.steps} steps: {ms_per_step:.2f} ms/step (device {dev_ms / args.steps:.2f} ms), "
+        f"{value / 1e6:.2f} M examples/s, {n_batches} batches/step")
+
+    # profiled replay: per-kernel durations from HIP events on the library's stream
+    pdep = make(args.window, profile=True)
+    pdep.replay(dt)
+    pdep.sched.sync()
+    kernels = {}
+    work = algorithmic_work(w, t, a, logd)
+    for k in ("route", "embbag", "gemm_bf16", "head"):
+        n, ms = pdep.sched.kernel_stats(k)
+        if n == 0:
+            continue
+        e = {"launches": n, "total_ms": round(ms, 4), "avg_us": round(ms * 1e3 / n, 3)}
+        wk = work.get(k, {})
+        if "bytes" in wk:
+            e["gbs"] = round(wk["bytes"] / (ms * 1e-3) / 1e9, 1)
+        if "flops" in wk:
+            e["tflops"] = round(wk["flops"] / (ms * 1e-3) / 1e12, 2)
+        kernels[k] = e
+    pdep.destroy()
+    dom = max(kernels, key=lambda k: kernels[k]["total_ms"])
+    dk = kernels[dom]
+    wk = work[dom]
+    if dom == "gemm_bf16":
+        ach = wk["flops"] / (dk["total_ms"] * 1e-3) / 1e12
+        roof = {"bound": "mfma", "achieved": round(ach, 2), "peak": BF16_PEAK_TFLOPS, "unit": "TFLOP/s",
+                "frac": round(ach / BF16_PEAK_TFLOPS, 4), "traffic": None, "kernel": dom}
+    else:
+        ach = wk["bytes"] / (dk["total_ms"] * 1e-3) / 1e9
+        roof = {"bound": "hbm", "achieved": round(ach, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                "frac": round(ach / HBM_PEAK_GBS, 4), "traffic": None, "kernel": dom}
+    roof["launches_per_step"] = dk["launches"]
+    roof["avg_launch_us"] = dk["avg_us"]
+    log(f"kernels: {json.dumps(kernels)}")
+
+    for sw in [int(x) for x in args.sweep_windows.split(",") if x]:
+        d2 = make(sw)
+        d2.replay(dt)
+        d2.sched.sync()
+        torch.cuda.synchronize()
+        s0 = time.perf_counter()
+        for _ in range(2):
+            d2.replay(dt)
+        d2.sched.sync()
+        el = (time.perf_counter() - s0) / 2
+        log(f"window {sw}: {el * 1e3:.2f} ms/step, {examples / el / 1e6:.2f} M examples/s")
+        d2.destroy()
+
+    latency = None
+    if not args.no_latency:
+        # service time per padded size P: a replay of a prefix of the trace
+        # through a queue whose every batch is padded to P (max batch P)
+        allowed = list(w.queues[0].allowed)
+        svc = np.zeros(w.queues[0].max_batch_size + 1, dtype=np.int64)
+        n_cal = 20_000
+        tcal = synth.trace(w, n_cal)
+        for P in allowed:
+            cw = synth.Workload(w.name, w.wid, w.models, (synth.Queue(0, P, (P,), None),), w.n_requests, w.rows,
+                                w.rate_per_s)
+            cdep = Deployment(cw, ctx, device=True, window_batches=args.window, models=dep.models)
+            out_off = cdep.out_offsets(tcal)
+            out = torch.empty(int(out_off[-1]), dtype=torch.float32, device="cuda")
+            kw = dict(dense=dt.dense, dense_off=a.dense_off[:n_cal + 1], lens=dt.lens,
+                      lens_off=a.lens_off[:n_cal + 1], ids=dt.ids, ids_off=a.ids_off[:n_cal + 1], out=out,
+                      out_off=out_off)
+            cdep.sched.sim_run(cdep.servables, tcal.servable, tcal.arrival_ns, tcal.n_rows, None, **kw)
+            cdep.sched.sync()
+            torch.cuda.synchronize()
+            s0 = time.perf_counter()
+            lg = cdep.sched.sim_run(cdep.servables, tcal.servable, tcal.arrival_ns, tcal.n_rows, None, **kw)
+            cdep.sched.sync()
+            el = time.perf_counter() - s0
+            svc[P] = int(el * 1e9 / lg["n_batches"])
+            cdep.destroy()
+        for s in range(len(svc)):
+            svc[s] = svc[min(p for p in allowed if p >= s)] if s <= allowed[-1] else svc[s]
+        cap = t.n / (ms_per_step * 1e-3)  # requests/s the GPU sustains on this trace
+        latency = {"clock": "simulated", "service_us_by_padded_size": {str(P): round(svc[P] / 1e3, 2) for P in allowed}}
+        for rho in (0.5, 0.9):
+            tr = synth.trace(w, rate_per_s=rho * cap)
+            lctx = rb.Ctx(-1)
+            ld = Deployment(w, lctx, device=False, service_ns=[svc.tolist()], with_params=False)
+            lg = ld.replay_meta(tr)
+            lat = lg["req_done_ns"] - tr.arrival_ns
+            latency[f"rho{rho}"] = {"arrival_rate_req_s": round(rho * cap, 1),
+                                    "p50_us": round(nearest_rank(lat, 0.5) / 1e3, 2),
+                                    "p99_us": round(nearest_rank(lat, 0.99) / 1e3, 2)}
+            ld.destroy()
+            lctx.destroy()
+        log(f"latency: {json.dumps(latency)}")
+
+    cpu = None
+    if not args.no_cpu_baseline:
+        log("timing the CPU oracle")
+        cpu = cpu_baseline(w, t, a, args.cpu_seconds)
+
+    out = {
+        "metric": METRIC, "value": round(value, 1), "unit": "examples/s", "n_gpus": 1, "steps": args.steps,
+        "warmup": args.warmup, "ms_per_step": round(ms_per_step, 3), "higher_is_better": True, "scaling": "weak",
+        "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
+        "config": {"workload": "ranking: 26 Zipf(1.1) embedding bags over 100k x 64 bf16 tables + 13 dense -> "
+                               "MLP 1677-1024-512-256-1 (ReLU, sigmoid), bf16 weights, fp32 accumulation; "
+                               "100k requests of 1-64 examples; max batch 512, allowed {64,128,256,512}",
+                   "requests_per_step": t.n, "examples_per_step": examples, "batches_per_step": n_batches,
+                   "window_batches": args.window, "parallelism": "single GPU"},
+        "latency": latency,
+        "p50_us": None if latency is None else latency["rho0.9"]["p50_us"],
+        "p99_us": None if latency is None else latency["rho0.9"]["p99_us"],
+        "device_ms_per_step": round(dev_ms / args.steps, 3),
+        "kernels": kernels,
+        "roofline": roof,
+        "cpu_baseline": cpu,
+    }
+    print(json.dumps(out), flush=True)
+    dep.destroy()
+
+
+if __name__ == "__main__":
+    main()

@@ -147,8 +147,10 @@ rb_status rb_sched_stream(rb_sched* s, void** stream);
 
 /* ---------------------------------------------------------------- queues */
 
+#define RB_MAX_BATCH_ROWS 4096
+
 typedef struct {
-  int32_t max_batch_size;            /* rows (sequences for seqpool) per batch, >= 1 */
+  int32_t max_batch_size;            /* rows (sequences for seqpool) per batch, 1..RB_MAX_BATCH_ROWS */
   const int32_t* allowed_batch_sizes;/* strictly ascending, last == max_batch_size */
   int32_t n_allowed;                 /* 0: batches run at their real size */
   int64_t batch_timeout_ns;          /* > 0; INT64_MAX: batches close by count only */
@@ -310,7 +312,7 @@ typedef struct {
 } rb_k_row;
 
 /* Row routing (exclusive prefix scans): fills rows[row_base .. row_base + P)
- * of every batch. kind = RB_MODEL_*; d_in floats per row (per token for
+ * of every batch (P <= RB_MAX_BATCH_ROWS; every request has >= 1 row). kind = RB_MODEL_*; d_in floats per row (per token for
  * seqpool); d_out floats per output row; n_tables bags per ranking row.
  * A request whose payload does not match its n_rows (dense length, bag
  * lengths vs ids, sequence lengths outside [1, seq_T]) sets *err = 1 and

@@ -61,104 +61,144 @@ __device__ __forceinline__ float wave_sum(float v) {
 
 // ---------------------------------------------------------------- route
 
-// One workgroup per batch. Phase 1: block-wide exclusive scan of the
-// requests' row counts (256 requests per pass, carried across passes) gives
-// each request's first row in the batch. Phase 2: the thread owning a request
-// validates its payload and writes its rows' entries (ranking: a running sum
-// of the rows' bag lengths gives each row's first id; seqpool: a running sum
-// of sequence lengths gives each sequence's first token). Phase 3: padding.
+constexpr int ROUTE_MAX_ROWS = 4096;  // rows (sequence slots) per batch
+
+// Block-wide exclusive scan of one value per thread (256 threads); returns
+// the exclusive prefix and writes the block total to *total.
+__device__ __forceinline__ int64_t block_exclusive_scan(int64_t v, int64_t* s_w, int64_t* total) {
+  const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6;
+  int64_t incl = v;
+  for (int o = 1; o < 64; o <<= 1) {
+    const int64_t u = __shfl_up(incl, o);
+    if (lane >= o) incl += u;
+  }
+  if (lane == 63) s_w[wid] = incl;
+  __syncthreads();
+  int64_t off = 0;
+  for (int w = 0; w < wid; ++w) off += s_w[w];
+  *total = s_w[0] + s_w[1] + s_w[2] + s_w[3];
+  __syncthreads();
+  return off + incl - v;
+}
+
+// One workgroup per batch, all steps parallel over requests or rows:
+//  1. exclusive scan of the requests' row counts -> each request's first row
+//     (the concatenation offsets), and a row -> request map in LDS;
+//  2. per real row, its id count (ranking: sum of its bag lengths) or token
+//     count (seqpool: its sequence length), loaded in parallel;
+//  3. exclusive scan of those counts over the batch's rows; a row's first id
+//     (token) is its request's base plus the scan difference to the request's
+//     first row; each request is checked against its payload extent;
+//  4. the row map entries, then padding rows.
 __global__ __launch_bounds__(256) void k_route(int kind, const rb_k_batch* __restrict__ batches,
                                                const rb_k_req* __restrict__ reqs,
                                                const int32_t* __restrict__ lens, int d_in, int d_out,
                                                int n_tables, rb_k_row* __restrict__ rows,
                                                int* __restrict__ err) {
   const rb_k_batch b = batches[blockIdx.x];
-  const int tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
-  __shared__ int s_wsum[4];
-  __shared__ int s_carry;
-  if (tid == 0) s_carry = 0;
+  const int tid = threadIdx.x;
+  __shared__ int s_first[ROUTE_MAX_ROWS + 1];   // first row of request i (batch-relative)
+  __shared__ int s_req[ROUTE_MAX_ROWS];         // request of row p
+  __shared__ int64_t s_ex[ROUTE_MAX_ROWS + 1];  // exclusive scan of per-row id/token counts
+  __shared__ unsigned char s_bad[ROUTE_MAX_ROWS];
+  __shared__ int64_t s_w[4];
+  if (b.padded > ROUTE_MAX_ROWS || b.n_req > b.padded || b.real > b.padded) {
+    if (tid == 0) *err = 1;
+    return;
+  }
+  // 1. request offsets
+  __shared__ int s_desc_bad;
+  if (tid == 0) s_desc_bad = 0;
   __syncthreads();
+  int64_t carry = 0;
   for (int base = 0; base < b.n_req; base += 256) {
     const int i = base + tid;
-    rb_k_req rq = {};
-    int n = 0;
+    const int n = i < b.n_req ? reqs[b.req_begin + i].n_rows : 0;
+    if (i < b.n_req && n < 1) s_desc_bad = 1;  // every request has >= 1 row
+    int64_t tot;
+    const int64_t ex = block_exclusive_scan(n, s_w, &tot);
     if (i < b.n_req) {
-      rq = reqs[b.req_begin + i];
-      n = rq.n_rows;
+      s_first[i] = (int)(carry + ex);
+      s_bad[i] = 0;
     }
-    int incl = n;
-    for (int o = 1; o < 64; o <<= 1) {
-      int v = __shfl_up(incl, o);
-      if (lane >= o) incl += v;
-    }
-    if (lane == 63) s_wsum[wid] = incl;
-    __syncthreads();
-    int wofs = 0;
-    for (int w = 0; w < wid; ++w) wofs += s_wsum[w];
-    const int carry = s_carry;
-    const int dst = carry + wofs + incl - n;
-    __syncthreads();
-    if (tid == 255) s_carry = carry + wofs + incl;
-    if (i < b.n_req) {
-      if (dst + n > b.padded) {
-        *err = 1;
-      } else if (kind == RB_MODEL_SEQPOOL) {
-        // rows are sequences; validate lengths against the bucket and the tokens
-        int64_t tok = 0;
-        bool ok = true;
-        for (int e = 0; e < n; ++e) {
-          int L = lens[rq.lens_off + e];
-          ok = ok && L >= 1 && L <= b.seq_T;
-          tok += L;
-        }
-        ok = ok && (tok * d_in == rq.dense_end - rq.dense_off);
-        if (!ok) *err = 1;
-        int64_t t0 = 0;
-        for (int e = 0; e < n; ++e) {
-          int L = lens[rq.lens_off + e];
-          rb_k_row rw;
-          rw.src = ok ? rq.dense_off + t0 * d_in : -1;
-          rw.aux = ok ? L : 0;
-          rw.lens = rq.lens_off + e;
-          rw.out = rq.out_off + (int64_t)e * d_out;
-          rows[b.row_base + dst + e] = rw;
-          t0 += ok ? L : 0;
+    carry += tot;
+  }
+  if (tid == 0) s_first[b.n_req] = (int)carry;
+  __syncthreads();
+  const int s = (int)carry;
+  if (s > b.padded || s_desc_bad) {
+    if (tid == 0) *err = 1;
+    return;
+  }
+  for (int i = tid; i < b.n_req; i += 256)
+    for (int p = s_first[i]; p < s_first[i + 1]; ++p) s_req[p] = i;
+  __syncthreads();
+  // 2 + 3. per-row counts and their scan
+  carry = 0;
+  for (int base = 0; base < s; base += 256) {
+    const int p = base + tid;
+    int64_t c = 0;
+    if (p < s && kind != RB_MODEL_MLP) {
+      const int i = s_req[p];
+      const rb_k_req& rq = reqs[b.req_begin + i];
+      const int e = p - s_first[i];
+      if (kind == RB_MODEL_RANKING) {
+        const int32_t* l = lens + rq.lens_off + (int64_t)e * n_tables;
+        for (int f = 0; f < n_tables; ++f) {
+          const int v = l[f];
+          if (v < 0) s_bad[i] = 1;
+          c += v;
         }
       } else {
-        bool ok = (int64_t)n * d_in == rq.dense_end - rq.dense_off;
-        bool ids_ok = true;
-        if (kind == RB_MODEL_RANKING) {
-          int64_t tot = 0;
-          for (int e = 0; e < n * n_tables; ++e) {
-            int L = lens[rq.lens_off + e];
-            ids_ok = ids_ok && L >= 0;
-            tot += L;
-          }
-          ids_ok = ids_ok && tot == rq.ids_end - rq.ids_off;
-        }
-        if (!ok || !ids_ok) *err = 1;
-        int64_t id0 = rq.ids_off;
-        for (int e = 0; e < n; ++e) {
-          rb_k_row rw;
-          rw.src = ok ? rq.dense_off + (int64_t)e * d_in : -1;
-          rw.aux = id0;
-          rw.lens = (kind == RB_MODEL_RANKING && ids_ok) ? rq.lens_off + (int64_t)e * n_tables : -1;
-          rw.out = rq.out_off + (int64_t)e * d_out;
-          if (kind == RB_MODEL_RANKING && ids_ok)
-            for (int f = 0; f < n_tables; ++f) id0 += lens[rq.lens_off + (int64_t)e * n_tables + f];
-          rows[b.row_base + dst + e] = rw;
-        }
+        const int v = lens[rq.lens_off + e];
+        if (v < 1 || v > b.seq_T) s_bad[i] = 1;
+        c = v;
       }
     }
-    __syncthreads();
+    int64_t tot;
+    const int64_t ex = block_exclusive_scan(c, s_w, &tot);
+    if (p < s) s_ex[p] = carry + ex;
+    carry += tot;
   }
-  const int s = s_carry;
-  for (int p = s + tid; p < b.padded; p += 256) {
+  if (tid == 0) s_ex[s] = carry;
+  __syncthreads();
+  for (int i = tid; i < b.n_req; i += 256) {
+    const rb_k_req& rq = reqs[b.req_begin + i];
+    const int n = s_first[i + 1] - s_first[i];
+    const int64_t cnt = s_ex[s_first[i + 1]] - s_ex[s_first[i]];
+    bool ok = !s_bad[i] && n == rq.n_rows;
+    if (kind == RB_MODEL_SEQPOOL) ok = ok && cnt * d_in == rq.dense_end - rq.dense_off;
+    else ok = ok && (int64_t)n * d_in == rq.dense_end - rq.dense_off;
+    if (kind == RB_MODEL_RANKING) ok = ok && cnt == rq.ids_end - rq.ids_off;
+    if (!ok) *err = 1;
+    s_bad[i] = ok ? 0 : 1;
+  }
+  __syncthreads();
+  // 4. row entries
+  for (int p = tid; p < b.padded; p += 256) {
     rb_k_row rw;
-    rw.src = -1;
-    rw.aux = 0;
-    rw.lens = -1;
-    rw.out = -1;
+    if (p < s) {
+      const int i = s_req[p];
+      const rb_k_req& rq = reqs[b.req_begin + i];
+      const int e = p - s_first[i];
+      const bool ok = !s_bad[i];
+      const int64_t within = s_ex[p] - s_ex[s_first[i]];
+      if (kind == RB_MODEL_SEQPOOL) {
+        rw.src = ok ? rq.dense_off + within * d_in : -1;
+        rw.aux = ok ? s_ex[p + 1] - s_ex[p] : 0;
+        rw.lens = rq.lens_off + e;
+      } else {
+        rw.src = ok ? rq.dense_off + (int64_t)e * d_in : -1;
+        rw.aux = rq.ids_off + within;
+        rw.lens = (kind == RB_MODEL_RANKING && ok) ? rq.lens_off + (int64_t)e * n_tables : -1;
+      }
+      rw.out = rq.out_off + (int64_t)e * d_out;
+    } else {
+      rw.src = -1;
+      rw.aux = 0;
+      rw.lens = -1;
+      rw.out = -1;
+    }
     rows[b.row_base + p] = rw;
   }
 }

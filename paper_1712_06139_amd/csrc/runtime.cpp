@@ -885,7 +885,9 @@ rb_status rb_sched_stream(rb_sched* s, void** stream) {
 
 rb_status rb_queue_create(rb_sched* s, rb_model* m, const rb_queue_opts* o, rb_queue** out) {
   if (!s || !m || !o || !out || m->ctx != s->ctx) return RB_EINVAL;
-  if (o->max_batch_size < 1 || o->n_allowed < 0 || (o->n_allowed > 0 && !o->allowed_batch_sizes)) return RB_EINVAL;
+  if (o->max_batch_size < 1 || o->max_batch_size > RB_MAX_BATCH_ROWS || o->n_allowed < 0 ||
+      (o->n_allowed > 0 && !o->allowed_batch_sizes))
+    return RB_EINVAL;
   if (o->batch_timeout_ns < 1) return RB_EINVAL;
   for (int i = 0; i < o->n_allowed; ++i) {
     const int a = o->allowed_batch_sizes[i];

@@ -38,12 +38,13 @@ class DeviceTrace:
 class Deployment:
     def __init__(self, w, ctx: rb.Ctx, device: bool = True, window_batches: int = 1, pad_value: float = 0.0,
                  profile: bool = False, service_ns: Optional[Sequence[Sequence[int]]] = None,
-                 with_params: bool = True):
+                 with_params: bool = True, models: Optional[List[rb.Model]] = None):
         import synth
         self.w = w
         self.ctx = ctx
-        self.models: List[rb.Model] = []
-        for si, m in enumerate(w.models):
+        self.owns_models = models is None
+        self.models: List[rb.Model] = [] if models is None else list(models)
+        for si, m in enumerate(w.models if models is None else ()):
             if with_params:
                 p = synth.model_params(w, si)
                 layers = [(W, b, L.act) for (W, b), L in zip(p.weights, m.layers)]
@@ -75,8 +76,9 @@ class Deployment:
         for q in self.queues:
             q.destroy()
         self.sched.destroy()
-        for m in self.models:
-            m.destroy()
+        if self.owns_models:
+            for m in self.models:
+                m.destroy()
 
     # -- traces ------------------------------------------------------------
 

@@ -357,23 +357,72 @@ class Payload:
     ids: Optional[np.ndarray] = None
 
 
-def _draw_request(w: Workload, t: Trace, r: int, rng: np.random.Generator) -> Payload:
-    m = w.models[int(t.servable[r])]
-    n = int(t.n_rows[r])
-    if m.kind == "mlp":
-        return Payload(rng.standard_normal((n, m.d_in), dtype=np.float32))
-    if m.kind == "seqpool":
-        L = t.seq_lens[t.seq_off[r]:t.seq_off[r + 1]]
-        toks = rng.standard_normal((int(L.sum()), m.d_in), dtype=np.float32)
-        return Payload(toks, lens=L.astype(np.int32).copy())
-    # ranking
-    dense = rng.standard_normal((n, m.n_dense), dtype=np.float32)
-    lens = rng.integers(m.bag_len[0], m.bag_len[1] + 1, size=(n, m.n_tables)).astype(np.int32)
-    total = int(lens.sum())
-    ranks0 = _zipf_alias(m.table_rows, m.zipf_s).sample(rng, total)
-    table_of = np.repeat(np.tile(np.arange(m.n_tables, dtype=np.int32), n), lens.ravel())
-    ids = _rank_to_row(w, m)[table_of, ranks0]
-    return Payload(dense, lens, ids.astype(np.int32))
+@dataclasses.dataclass
+class _Chunk:
+    """Payloads of CHUNK consecutive requests, concatenated in request order."""
+    dense: np.ndarray
+    lens: np.ndarray
+    ids: np.ndarray
+    n_dense: np.ndarray   # per request element counts
+    n_lens: np.ndarray
+    n_ids: np.ndarray
+
+
+def _draw_chunk(w: Workload, t: Trace, lo: int, hi: int, rng: np.random.Generator) -> _Chunk:
+    """Draw the payloads of requests [lo, hi): servable after servable (in
+    servable order), each tensor for all of that servable's requests at once,
+    then laid out in request order."""
+    n_req = hi - lo
+    srv = t.servable[lo:hi]
+    rows = t.n_rows[lo:hi].astype(np.int64)
+    parts = {}
+    for s in np.unique(srv):
+        m = w.models[int(s)]
+        sel = np.nonzero(srv == s)[0]
+        nr = rows[sel]
+        if m.kind == "mlp":
+            d = rng.standard_normal((int(nr.sum()), m.d_in), dtype=np.float32)
+            parts[int(s)] = (sel, d.reshape(-1), nr * m.d_in, None, np.zeros_like(nr), None, np.zeros_like(nr))
+        elif m.kind == "seqpool":
+            L = np.concatenate([t.seq_lens[t.seq_off[lo + i]:t.seq_off[lo + i + 1]] for i in sel])
+            tok_per_req = np.add.reduceat(L.astype(np.int64), np.concatenate([[0], np.cumsum(nr)[:-1]]))
+            d = rng.standard_normal((int(L.sum()), m.d_in), dtype=np.float32)
+            parts[int(s)] = (sel, d.reshape(-1), tok_per_req * m.d_in, L.astype(np.int32), nr, None,
+                             np.zeros_like(nr))
+        else:
+            tot_rows = int(nr.sum())
+            dense = rng.standard_normal((tot_rows, m.n_dense), dtype=np.float32)
+            lens = rng.integers(m.bag_len[0], m.bag_len[1] + 1, size=(tot_rows, m.n_tables)).astype(np.int32)
+            ranks0 = _zipf_alias(m.table_rows, m.zipf_s).sample(rng, int(lens.sum()))
+            table_of = np.repeat(np.tile(np.arange(m.n_tables, dtype=np.int64), tot_rows), lens.ravel())
+            ids = np.take(_rank_to_row(w, m).ravel(), table_of * m.table_rows + ranks0)
+            row_off = np.concatenate([[0], np.cumsum(nr)[:-1]])
+            ids_per_req = np.add.reduceat(lens.sum(axis=1, dtype=np.int64), row_off) if tot_rows else nr * 0
+            parts[int(s)] = (sel, dense.reshape(-1), nr * m.n_dense, lens.reshape(-1), nr * m.n_tables,
+                             ids.astype(np.int32), ids_per_req)
+    n_dense = np.zeros(n_req, np.int64)
+    n_lens = np.zeros(n_req, np.int64)
+    n_ids = np.zeros(n_req, np.int64)
+    for sel, _, nd, _, nl, _, ni in parts.values():
+        n_dense[sel], n_lens[sel], n_ids[sel] = nd, nl, ni
+    if len(parts) == 1:
+        (_, d, _, ln, _, ii, _), = parts.values()
+        return _Chunk(d, ln if ln is not None else np.zeros(0, np.int32),
+                      ii if ii is not None else np.zeros(0, np.int32), n_dense, n_lens, n_ids)
+    # several servables: scatter each servable's slices back into request order
+    def gather(idx_data, idx_cnt, counts, dtype):
+        out = np.empty(int(counts.sum()), dtype=dtype)
+        off = np.concatenate([[0], np.cumsum(counts)])
+        for sel, *rest in parts.values():
+            data, cnt = rest[idx_data - 1], rest[idx_cnt - 1]
+            if data is None:
+                continue
+            src = np.concatenate([[0], np.cumsum(cnt)])
+            for j, r in enumerate(sel):
+                out[off[r]:off[r + 1]] = data[src[j]:src[j + 1]]
+        return out
+    return _Chunk(gather(1, 2, n_dense, np.float32), gather(3, 4, n_lens, np.int32),
+                  gather(5, 6, n_ids, np.int32), n_dense, n_lens, n_ids)
 
 
 _full_cache: Dict[str, Trace] = {}
@@ -385,18 +434,30 @@ def _full_trace(w: Workload) -> Trace:
     return _full_cache[w.name]
 
 
-def _chunk_payloads(w: Workload, c: int) -> List[Payload]:
+def _chunk(w: Workload, c: int) -> _Chunk:
     # a chunk is always drawn in full from the full trace's metadata, so a
     # prefix trace sees exactly the payloads of the full one
     full = _full_trace(w)
     lo, hi = c * CHUNK, min((c + 1) * CHUNK, w.n_requests)
-    rng = _rng(w.wid, _S_PAYLOAD, c)
-    return [_draw_request(w, full, r, rng) for r in range(lo, hi)]
+    return _draw_chunk(w, full, lo, hi, _rng(w.wid, _S_PAYLOAD, c))
+
+
+def _slice(ch: _Chunk, i: int, w: Workload, t: Trace, r: int) -> Payload:
+    d0, l0, i0 = (int(x[:i].sum()) for x in (ch.n_dense, ch.n_lens, ch.n_ids))
+    m = w.models[int(t.servable[r])]
+    dense = ch.dense[d0:d0 + ch.n_dense[i]]
+    lens = ch.lens[l0:l0 + ch.n_lens[i]]
+    ids = ch.ids[i0:i0 + ch.n_ids[i]]
+    if m.kind == "mlp":
+        return Payload(dense.reshape(-1, m.d_in))
+    if m.kind == "seqpool":
+        return Payload(dense.reshape(-1, m.d_in), lens=lens)
+    return Payload(dense.reshape(-1, m.n_dense), lens.reshape(-1, m.n_tables), ids)
 
 
 def request_payload(t: Trace, r: int) -> Payload:
     w = t.workload
-    return _chunk_payloads(w, r // CHUNK)[r % CHUNK]
+    return _slice(_chunk(w, r // CHUNK), r % CHUNK, w, _full_trace(w), r)
 
 
 @dataclasses.dataclass
@@ -425,31 +486,25 @@ def arenas(t: Trace, threads: Optional[int] = None) -> Arenas:
     w = t.workload
     n_chunks = (t.n + CHUNK - 1) // CHUNK
     threads = threads or min(16, len(os.sched_getaffinity(0)))
+    _full_trace(w)
     with ThreadPoolExecutor(max_workers=threads) as ex:
-        chunks = list(ex.map(lambda c: _chunk_payloads(w, c), range(n_chunks)))
-    pays = [p for ch in chunks for p in ch][: t.n]
-    dense_n = np.array([p.dense.size for p in pays], dtype=np.int64)
-    lens_n = np.array([0 if p.lens is None else p.lens.size for p in pays], dtype=np.int64)
-    ids_n = np.array([0 if p.ids is None else p.ids.size for p in pays], dtype=np.int64)
+        chunks = list(ex.map(lambda c: _chunk(w, c), range(n_chunks)))
+    last = t.n - (n_chunks - 1) * CHUNK if n_chunks else 0
 
-    def offs(sz):
+    def cat(field, counts_field):
+        parts = []
+        for i, ch in enumerate(chunks):
+            a = getattr(ch, field)
+            if i == n_chunks - 1:
+                a = a[:int(getattr(ch, counts_field)[:last].sum())]
+            parts.append(a)
+        return np.concatenate(parts) if parts else np.zeros(0)
+
+    def offs(counts_field):
+        cnt = np.concatenate([getattr(ch, counts_field) for ch in chunks])[: t.n] if chunks else np.zeros(0, np.int64)
         o = np.zeros(t.n + 1, dtype=np.int64)
-        np.cumsum(sz, out=o[1:])
+        np.cumsum(cnt, out=o[1:])
         return o
 
-    dense_off, lens_off, ids_off = offs(dense_n), offs(lens_n), offs(ids_n)
-    dense = np.empty(int(dense_off[-1]), dtype=np.float32)
-    lens = np.empty(int(lens_off[-1]), dtype=np.int32)
-    ids = np.empty(int(ids_off[-1]), dtype=np.int32)
-
-    def fill(r):
-        p = pays[r]
-        dense[dense_off[r]:dense_off[r + 1]] = p.dense.ravel()
-        if p.lens is not None:
-            lens[lens_off[r]:lens_off[r + 1]] = p.lens.ravel()
-        if p.ids is not None:
-            ids[ids_off[r]:ids_off[r + 1]] = p.ids
-
-    for r in range(t.n):
-        fill(r)
-    return Arenas(dense, lens, ids, dense_off, lens_off, ids_off)
+    return Arenas(cat("dense", "n_dense").astype(np.float32, copy=False), cat("lens", "n_lens").astype(np.int32, copy=False),
+                  cat("ids", "n_ids").astype(np.int32, copy=False), offs("n_dense"), offs("n_lens"), offs("n_ids"))
