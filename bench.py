@@ -107,6 +107,9 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-latency", action="store_true")
     ap.add_argument("--sweep-windows", default="", help="comma list: also time these windows (stderr)")
+    ap.add_argument("--copy-probe-mb", type=int, default=0,
+                    help="first run one plain elementwise copy of this many MiB (fp32), a known-size kernel "
+                         "for scaling hardware byte counters")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py measures one MI355X only: batching serves independent requests, so more GPUs are "
@@ -119,6 +122,15 @@ def main():
     from paper_1712_06139_amd.deploy import Deployment
 
     assert torch.cuda.is_available(), "needs a GPU"
+    if args.copy_probe_mb:
+        n = args.copy_probe_mb * (1 << 20) // 4
+        src = torch.ones(n, dtype=torch.float32, device="cuda")
+        dst = torch.empty_like(src)
+        torch.cuda.synchronize()
+        torch.mul(src, 1.0, out=dst)
+        torch.cuda.synchronize()
+        log(f"copy probe: read {n * 4} B, wrote {n * 4} B")
+        del src, dst
     w = synth.workload("ranking")
     t = synth.trace(w)
     log(f"generating {t.n} requests ({int(t.n_rows.sum())} examples)")
@@ -234,15 +246,23 @@ def main():
             cdep.destroy()
         for s in range(len(svc)):
             svc[s] = svc[min(p for p in allowed if p >= s)] if s <= allowed[-1] else svc[s]
-        cap = t.n / (ms_per_step * 1e-3)  # requests/s the GPU sustains on this trace
-        latency = {"clock": "simulated", "service_us_by_padded_size": {str(P): round(svc[P] / 1e3, 2) for P in allowed}}
+        # capacity of the simulated device: requests / total service time of
+        # the trace's batches (composition is count-only, so arrival-free)
+        lctx = rb.Ctx(-1)
+        ld = Deployment(w, lctx, device=False, service_ns=[svc.tolist()], with_params=False)
+        busy_ns = int(svc[ld.replay_meta(t)["b_padded"]].sum())
+        ld.destroy()
+        lctx.destroy()
+        cap = t.n / (busy_ns * 1e-9)
+        latency = {"clock": "simulated", "capacity_req_s": round(cap, 1),
+                   "service_us_by_padded_size": {str(P): round(svc[P] / 1e3, 2) for P in allowed}}
         for rho in (0.5, 0.9):
             tr = synth.trace(w, rate_per_s=rho * cap)
             lctx = rb.Ctx(-1)
             ld = Deployment(w, lctx, device=False, service_ns=[svc.tolist()], with_params=False)
             lg = ld.replay_meta(tr)
             lat = lg["req_done_ns"] - tr.arrival_ns
-            latency[f"rho{rho}"] = {"arrival_rate_req_s": round(rho * cap, 1),
+            latency[f"rho{rho}"] = {"arrival_rate_req_s": round(rho * cap, 1), "utilization": rho,
                                     "p50_us": round(nearest_rank(lat, 0.5) / 1e3, 2),
                                     "p99_us": round(nearest_rank(lat, 0.99) / 1e3, 2)}
             ld.destroy()

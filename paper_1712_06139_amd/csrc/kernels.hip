@@ -23,6 +23,8 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include <type_traits>
+
 #include "../../include/rb.h"
 
 namespace {
@@ -52,6 +54,15 @@ __device__ __forceinline__ float act_fn(float z) {
   if (ACT == RB_ACT_RELU) return z > 0.f ? z : 0.f;
   if (ACT == RB_ACT_SIGMOID) return 1.f / (1.f + expf(-z));
   return z;
+}
+
+// Workgroups are handed to the 8 XCDs round-robin (block i runs on XCD i % 8)
+// and each XCD has its own L2. Remap so that XCD x gets a contiguous range of
+// tiles: with tiles ordered row-block-major, the tiles sharing an A row-block
+// then run on the same XCD and re-read it from that XCD's L2.
+__device__ __forceinline__ int xcd_tile(int bid, int nb) {
+  const int nb8 = nb & ~7;
+  return bid < nb8 ? (bid & 7) * (nb8 >> 3) + (bid >> 3) : bid;
 }
 
 __device__ __forceinline__ float wave_sum(float v) {
@@ -270,13 +281,15 @@ constexpr int EMB_DIM = 64;       // one table row = 128 bytes of bf16
 constexpr int MAX_TABLES = 64;
 constexpr int STAGE_IDS = 2048;   // ids of one row staged in LDS (more: read from global)
 
-// One workgroup (4 waves) per row. The row's bag lengths are scanned in LDS
-// and its ids staged in LDS with coalesced loads. Each wave then pools whole
-// bags: 8 lane groups of 8 lanes take every 8th id of the bag, each lane
-// loading 16 bytes (8 dims) of the table row; the 8 partial sums are combined
-// by a butterfly over the groups (fixed order: deterministic per row), rounded
-// to bf16 and stored as one 128-byte row segment. The dense features follow
-// the pooled bags; columns past them are zero.
+constexpr int EMB_UNROLL = 4;     // gathers in flight per lane
+
+// One workgroup (4 waves = 32 groups of 8 lanes) per row. The row's bag
+// lengths are scanned in LDS and its ids staged in LDS with coalesced loads.
+// Group g pools bags g, g + 32, ...: its 8 lanes each own 16 bytes (8 dims)
+// of the 128-byte table row and walk the bag's ids in order, EMB_UNROLL
+// gathers in flight at a time, summing in fp32 (a fixed order: deterministic
+// per row). The sum is rounded to bf16 and stored as one 128-byte segment.
+// The dense features follow the pooled bags; columns past them are zero.
 __global__ __launch_bounds__(256) void k_embbag(const rb_k_row* __restrict__ rows,
                                                 const int32_t* __restrict__ lens,
                                                 const int32_t* __restrict__ ids,
@@ -316,37 +329,40 @@ __global__ __launch_bounds__(256) void k_embbag(const rb_k_row* __restrict__ row
   if (staged)
     for (int i = tid; i < total; i += 256) s_ids[i] = ids[rw.aux + i];
   __syncthreads();
-  const int lane = tid & 63, wid = tid >> 6, g = lane >> 3, l8 = lane & 7;
-  for (int f = wid; f < n_tables; f += 4) {
+  const int g = tid >> 3, l8 = tid & 7;
+  for (int f = g; f < n_tables; f += 32) {
     float acc[8];
 #pragma unroll
     for (int k = 0; k < 8; ++k) acc[k] = 0.f;
-    const bf16_t* T = tables[f];
+    const bf16_t* T = tables[f] + l8 * 8;
     const int st = s_start[f], len = s_len[f];
-    for (int j = g; j < len; j += 8) {
-      const int id = staged ? s_ids[st + j] : ids[rw.aux + st + j];
-      if ((uint64_t)(int64_t)id >= (uint64_t)table_rows) {
-        *err = 1;
-        continue;
+    for (int j = 0; j < len; j += EMB_UNROLL) {
+      u32x4_t q[EMB_UNROLL];
+#pragma unroll
+      for (int u = 0; u < EMB_UNROLL; ++u) {
+        q[u] = (u32x4_t){0u, 0u, 0u, 0u};
+        if (j + u < len) {
+          const int id = staged ? s_ids[st + j + u] : ids[rw.aux + st + j + u];
+          if ((uint64_t)(int64_t)id < (uint64_t)table_rows)
+            q[u] = *(const u32x4_t*)(T + (int64_t)id * EMB_DIM);
+          else
+            *err = 1;
+        }
       }
-      const uint4 q = *(const uint4*)(T + (int64_t)id * EMB_DIM + l8 * 8);
-      acc[0] += bf2f(q.x & 0xffffu); acc[1] += bf2f(q.x >> 16);
-      acc[2] += bf2f(q.y & 0xffffu); acc[3] += bf2f(q.y >> 16);
-      acc[4] += bf2f(q.z & 0xffffu); acc[5] += bf2f(q.z >> 16);
-      acc[6] += bf2f(q.w & 0xffffu); acc[7] += bf2f(q.w >> 16);
-    }
 #pragma unroll
-    for (int o = 8; o < 64; o <<= 1)
-#pragma unroll
-      for (int k = 0; k < 8; ++k) acc[k] += __shfl_xor(acc[k], o);
-    if (g == 0) {
-      uint4 o;
-      o.x = pack2(acc[0], acc[1]);
-      o.y = pack2(acc[2], acc[3]);
-      o.z = pack2(acc[4], acc[5]);
-      o.w = pack2(acc[6], acc[7]);
-      *(uint4*)(xr + f * EMB_DIM + l8 * 8) = o;
+      for (int u = 0; u < EMB_UNROLL; ++u) {
+        acc[0] += bf2f(q[u].x & 0xffffu); acc[1] += bf2f(q[u].x >> 16);
+        acc[2] += bf2f(q[u].y & 0xffffu); acc[3] += bf2f(q[u].y >> 16);
+        acc[4] += bf2f(q[u].z & 0xffffu); acc[5] += bf2f(q[u].z >> 16);
+        acc[6] += bf2f(q[u].w & 0xffffu); acc[7] += bf2f(q[u].w >> 16);
+      }
     }
+    u32x4_t o;
+    o.x = pack2(acc[0], acc[1]);
+    o.y = pack2(acc[2], acc[3]);
+    o.z = pack2(acc[4], acc[5]);
+    o.w = pack2(acc[6], acc[7]);
+    *(u32x4_t*)(xr + f * EMB_DIM + l8 * 8) = o;
   }
   for (int c = demb + tid; c < ldx; c += 256)
     xr[c] = c < demb + n_dense ? f2bf(dense[rw.src + (c - demb)]) : (bf16_t)0;
@@ -354,107 +370,162 @@ __global__ __launch_bounds__(256) void k_embbag(const rb_k_row* __restrict__ row
 
 // ---------------------------------------------------------------- bf16 GEMM
 
-// Y = act(X W^T + b): X [M, K] and W [N, K] bf16, K contiguous. Workgroup tile
-// 128 x 128, k-step 64; four waves in a 2 x 2 grid, each owning 64 x 64 as
-// 2 x 2 v_mfma_f32_32x32x16_bf16 accumulators. LDS holds the A and B tiles
-// row-major with 16-byte chunks XOR-swizzled by row (bank-conflict-free
-// 16-byte reads), double-buffered so the next tile's global loads overlap the
-// current tile's MFMAs with one barrier per k-step.
-constexpr int G16_BM = 128, G16_BN = 128, G16_BK = 64;
+// s_waitcnt vmcnt(N) with the other counters unconstrained (gfx9 encoding:
+// vmcnt[3:0], expcnt[6:4], lgkmcnt[11:8], vmcnt[5:4] in bits 15:14).
+template <int N>
+__device__ __forceinline__ void wait_vmcnt() {
+  static_assert(N >= 0 && N < 64, "vmcnt range");
+  __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (7 << 4) | (15 << 8));
+}
 
-template <int ACT, bool OUT_F32>
-__global__ __launch_bounds__(256) void k_gemm_bf16(const bf16_t* __restrict__ X, int ldx,
-                                                   const bf16_t* __restrict__ W, int ldw,
-                                                   const float* __restrict__ bias, void* __restrict__ Y,
-                                                   int ldy, int M, int N, int K) {
-  __shared__ u32x4_t sA[2][G16_BM * G16_BK / 8];
-  __shared__ u32x4_t sB[2][G16_BN * G16_BK / 8];
+template <int I>
+using ic = std::integral_constant<int, I>;
+
+// Y = act(X W^T + b): X [M, K] and W [N, K] bf16, K contiguous; fp32
+// accumulation with v_mfma_f32_32x32x16_bf16.
+//
+// Workgroup tile BM x BN, k-step 32, NT/64 waves each owning a WM x WN
+// sub-tile ((WM/32) x (WN/32) accumulators). Operand tiles go from global
+// memory straight into LDS (global_load_lds_dwordx4: each wave instruction
+// fills 1 KB = 16 rows of 64 bytes, no register staging) through a ring of 4
+// LDS stages, so a k-step's loads are issued three steps before they are
+// read. Each stage is its own LDS array and the stage of every step is a
+// compile-time constant (the k loop is unrolled by 4), which lets the
+// compiler see that the loads in flight and the reads of the current stage
+// touch different arrays. Per step: wait for this wave's loads of the stage,
+// one barrier (all waves' loads landed; the stage refilled next was fully
+// read), issue the loads three steps ahead, then the MFMAs. The 16-byte chunk
+// c of row r sits at chunk c ^ ((r >> 2) & 3) of its 64-byte LDS row, so the
+// 16 lanes served per LDS cycle read 16 distinct bank groups.
+//
+// Every tile shape accumulates each output element in the same k order with
+// the same instruction, so results do not depend on the tile shape nor on
+// which rows share a tile.
+constexpr int G16_BK = 32, G16_STAGES = 4;
+
+template <int BM, int BN, int WM, int WN, int NT, int ACT, bool OUT_F32, int ORDER = 1>
+__global__ __launch_bounds__(NT) void k_gemm_bf16(const bf16_t* __restrict__ X, int ldx,
+                                                  const bf16_t* __restrict__ W, int ldw,
+                                                  const float* __restrict__ bias, void* __restrict__ Y,
+                                                  int ldy, int M, int N, int K) {
+  constexpr int NW = NT / 64;
+  static_assert((BM / WM) * (BN / WN) == NW, "one wave per sub-tile");
+  constexpr int TM = WM / 32, TN = WN / 32;
+  constexpr int SA = BM / 16 / NW, SB = BN / 16 / NW;  // 16-row slabs per wave per stage
+  static_assert(SA * NW * 16 == BM && SB * NW * 16 == BN, "slabs cover the tile");
+  constexpr int OPS = SA + SB;                         // load instructions per wave per stage
+  __shared__ u32x4_t sA0[BM * 4], sA1[BM * 4], sA2[BM * 4], sA3[BM * 4];
+  __shared__ u32x4_t sB0[BN * 4], sB1[BN * 4], sB2[BN * 4], sB3[BN * 4];
+  u32x4_t* const sA[G16_STAGES] = {sA0, sA1, sA2, sA3};
+  u32x4_t* const sB[G16_STAGES] = {sB0, sB1, sB2, sB3};
+
   const int tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
-  const int wm = wid >> 1, wn = wid & 1;
-  const int tiles_n = N / G16_BN;
-  const int bm = blockIdx.x / tiles_n, bn = blockIdx.x - bm * tiles_n;
-  const int m0 = bm * G16_BM, n0 = bn * G16_BN;
+  const int wm = wid / (BN / WN), wn = wid % (BN / WN);
+  const int tiles_n = N / BN;
+  const int tile = ORDER ? xcd_tile(blockIdx.x, gridDim.x) : (int)blockIdx.x;
+  const int bm = tile / tiles_n, bn = tile - bm * tiles_n;
+  const int m0 = bm * BM, n0 = bn * BN;
 
-  const int lrow = tid >> 3, lch = tid & 7;
-  const bf16_t* ag[4];
-  const bf16_t* bg[4];
+  // lane l of a load instruction fills LDS row l/4, chunk l%4 of its slab
+  const int lr = lane >> 2, lc = lane & 3;
+  const bf16_t* ga[SA];
+  const bf16_t* gb[SB];
 #pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    int ra = m0 + lrow + 32 * i;
+  for (int i = 0; i < SA; ++i) {
+    const int row = (wid * SA + i) * 16 + lr;
+    int ra = m0 + row;
     ra = ra < M ? ra : M - 1;  // rows past M are computed on a copy and never stored
-    ag[i] = X + (int64_t)ra * ldx + lch * 8;
-    bg[i] = W + (int64_t)(n0 + lrow + 32 * i) * ldw + lch * 8;
+    ga[i] = X + (int64_t)ra * ldx + (lc ^ ((row >> 2) & 3)) * 8;
   }
-  u32x4_t ra_[4], rb_[4];
-  floatx16_t acc[2][2];
 #pragma unroll
-  for (int i = 0; i < 2; ++i)
+  for (int i = 0; i < SB; ++i) {
+    const int row = (wid * SB + i) * 16 + lr;
+    gb[i] = W + (int64_t)(n0 + row) * ldw + (lc ^ ((row >> 2) & 3)) * 8;
+  }
+
+  floatx16_t acc[TM][TN];
 #pragma unroll
-    for (int j = 0; j < 2; ++j)
+  for (int i = 0; i < TM; ++i)
+#pragma unroll
+    for (int j = 0; j < TN; ++j)
 #pragma unroll
       for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
 
-  const int nk = K / G16_BK;
+  auto issue = [&](int kt, auto stc) {
+    constexpr int st = decltype(stc)::value;
+    const int k0 = kt * G16_BK;
 #pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    ra_[i] = *(const u32x4_t*)(ag[i]);
-    rb_[i] = *(const u32x4_t*)(bg[i]);
-  }
+    for (int i = 0; i < SA; ++i)
+      __builtin_amdgcn_global_load_lds((const void*)(ga[i] + k0), (__shared__ void*)(sA[st] + (wid * SA + i) * 64),
+                                       16, 0, 0);
 #pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    const int r = lrow + 32 * i;
-    sA[0][r * 8 + (lch ^ (r & 7))] = ra_[i];
-    sB[0][r * 8 + (lch ^ (r & 7))] = rb_[i];
-  }
-  __syncthreads();
-  for (int kt = 0; kt < nk; ++kt) {
-    const int buf = kt & 1;
-    if (kt + 1 < nk) {
-      const int k0 = (kt + 1) * G16_BK;
+    for (int i = 0; i < SB; ++i)
+      __builtin_amdgcn_global_load_lds((const void*)(gb[i] + k0), (__shared__ void*)(sB[st] + (wid * SB + i) * 64),
+                                       16, 0, 0);
+  };
+  auto compute = [&](auto stc) {
+    constexpr int st = decltype(stc)::value;
+    const u32x4_t* A_ = sA[st];
+    const u32x4_t* B_ = sB[st];
 #pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        ra_[i] = *(const u32x4_t*)(ag[i] + k0);
-        rb_[i] = *(const u32x4_t*)(bg[i] + k0);
-      }
-    }
-#pragma unroll
-    for (int kk = 0; kk < 4; ++kk) {
-      bf16x8_t a[2], bv[2];
+    for (int kk = 0; kk < 2; ++kk) {
+      bf16x8_t a[TM], bv[TN];
       const int ch = kk * 2 + (lane >> 5);
 #pragma unroll
-      for (int i = 0; i < 2; ++i) {
-        const int rA = wm * 64 + i * 32 + (lane & 31);
-        const int rB = wn * 64 + i * 32 + (lane & 31);
-        a[i] = __builtin_bit_cast(bf16x8_t, sA[buf][rA * 8 + (ch ^ (rA & 7))]);
-        bv[i] = __builtin_bit_cast(bf16x8_t, sB[buf][rB * 8 + (ch ^ (rB & 7))]);
+      for (int i = 0; i < TM; ++i) {
+        const int r = wm * WM + i * 32 + (lane & 31);
+        a[i] = __builtin_bit_cast(bf16x8_t, A_[r * 4 + (ch ^ ((r >> 2) & 3))]);
       }
 #pragma unroll
-      for (int i = 0; i < 2; ++i)
+      for (int j = 0; j < TN; ++j) {
+        const int r = wn * WN + j * 32 + (lane & 31);
+        bv[j] = __builtin_bit_cast(bf16x8_t, B_[r * 4 + (ch ^ ((r >> 2) & 3))]);
+      }
 #pragma unroll
-        for (int j = 0; j < 2; ++j)
+      for (int i = 0; i < TM; ++i)
+#pragma unroll
+        for (int j = 0; j < TN; ++j)
           acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[i], bv[j], acc[i][j], 0, 0, 0);
     }
-    if (kt + 1 < nk) {
-#pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const int r = lrow + 32 * i;
-        sA[buf ^ 1][r * 8 + (lch ^ (r & 7))] = ra_[i];
-        sB[buf ^ 1][r * 8 + (lch ^ (r & 7))] = rb_[i];
-      }
-    }
-    __syncthreads();
+  };
+  const int nk = K / G16_BK;
+  auto step = [&](int kt, auto stc, auto nxt) {
+    const int ahead = nk - 1 - kt;  // stages whose loads were issued after this one's
+    if (ahead >= 2)
+      wait_vmcnt<2 * OPS>();
+    else if (ahead == 1)
+      wait_vmcnt<OPS>();
+    else
+      wait_vmcnt<0>();
+    __builtin_amdgcn_s_barrier();
+    if (kt + 3 < nk) issue(kt + 3, nxt);
+    compute(stc);
+  };
+  if (0 < nk) issue(0, ic<0>{});
+  if (1 < nk) issue(1, ic<1>{});
+  if (2 < nk) issue(2, ic<2>{});
+  int kt = 0;
+  for (; kt + 4 <= nk; kt += 4) {
+    step(kt, ic<0>{}, ic<3>{});
+    step(kt + 1, ic<1>{}, ic<0>{});
+    step(kt + 2, ic<2>{}, ic<1>{});
+    step(kt + 3, ic<3>{}, ic<2>{});
   }
+  if (kt < nk) step(kt, ic<0>{}, ic<3>{});
+  if (kt + 1 < nk) step(kt + 1, ic<1>{}, ic<0>{});
+  if (kt + 2 < nk) step(kt + 2, ic<2>{}, ic<1>{});
+
   // accumulator (i, j) register r of lane l holds row 8*(r/4) + 4*(l/32) + r%4,
-  // column l%32 of the 32 x 32 block
+  // column l%32 of its 32 x 32 block
 #pragma unroll
-  for (int i = 0; i < 2; ++i)
+  for (int j = 0; j < TN; ++j) {
+    const int col = n0 + wn * WN + j * 32 + (lane & 31);
+    const float bb = bias[col];
 #pragma unroll
-    for (int j = 0; j < 2; ++j) {
-      const int col = n0 + wn * 64 + j * 32 + (lane & 31);
-      const float bb = bias[col];
+    for (int i = 0; i < TM; ++i)
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
-        const int row = m0 + wm * 64 + i * 32 + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
+        const int row = m0 + wm * WM + i * 32 + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
         if (row < M) {
           const float v = act_fn<ACT>(acc[i][j][r] + bb);
           if (OUT_F32)
@@ -463,7 +534,7 @@ __global__ __launch_bounds__(256) void k_gemm_bf16(const bf16_t* __restrict__ X,
             ((bf16_t*)Y)[(int64_t)row * ldy + col] = f2bf(v);
         }
       }
-    }
+  }
 }
 
 // ---------------------------------------------------------------- fp32 GEMM
@@ -484,7 +555,8 @@ __global__ __launch_bounds__(256) void k_gemm_f32(const float* __restrict__ X, i
   const int tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
   const int wm = wid >> 1, wn = wid & 1;
   const int tiles_n = N / G32_BN;
-  const int bm = blockIdx.x / tiles_n, bn = blockIdx.x - bm * tiles_n;
+  const int tile = xcd_tile(blockIdx.x, gridDim.x);
+  const int bm = tile / tiles_n, bn = tile - bm * tiles_n;
   const int m0 = bm * G32_BM, n0 = bn * G32_BN;
   const int lrow = tid >> 3, lk = (tid & 7) * 4;
   const float* ag[2];
@@ -640,6 +712,28 @@ inline unsigned blocks_for(int64_t threads) { return (unsigned)((threads + 255) 
 
 }  // namespace
 
+namespace {
+
+template <int BM, int BN, int WM, int WN, int NT, int ORDER = 1>
+void launch_gemm_bf16(hipStream_t s, const bf16_t* x, int ldx, const bf16_t* w, int ldw, const float* b,
+                             void* Y, int ldy, int M, int N, int K, int act, int out_f32) {
+  const unsigned g = (unsigned)(((M + BM - 1) / BM) * (N / BN));
+#define RB_G16(A, F) \
+  hipLaunchKernelGGL((k_gemm_bf16<BM, BN, WM, WN, NT, A, F, ORDER>), dim3(g), dim3(NT), 0, s, x, ldx, w, ldw, b, Y, ldy, M, N, K)
+  if (out_f32) {
+    if (act == RB_ACT_RELU) RB_G16(RB_ACT_RELU, true);
+    else if (act == RB_ACT_SIGMOID) RB_G16(RB_ACT_SIGMOID, true);
+    else RB_G16(RB_ACT_NONE, true);
+  } else {
+    if (act == RB_ACT_RELU) RB_G16(RB_ACT_RELU, false);
+    else if (act == RB_ACT_SIGMOID) RB_G16(RB_ACT_SIGMOID, false);
+    else RB_G16(RB_ACT_NONE, false);
+  }
+#undef RB_G16
+}
+
+}  // namespace
+
 // ---------------------------------------------------------------- kernel ABI
 
 extern "C" {
@@ -690,25 +784,28 @@ rb_status rb_k_embbag(void* stream, const rb_k_row* rows, int32_t n_rows_total, 
 
 rb_status rb_k_gemm_bf16(void* stream, const void* X, int32_t ldx, const void* W, int32_t ldw, const float* b,
                          void* Y, int32_t ldy, int32_t M, int32_t N, int32_t K, int32_t act, int32_t out_f32) {
-  if (M < 0 || N <= 0 || K <= 0 || (N % G16_BN) || (K % G16_BK) || ldx < K || ldw < K || ldy < N) return RB_EINVAL;
+  if (M < 0 || N <= 0 || K <= 0 || (N % 128) || (K % G16_BK) || ldx < K || ldw < K || ldy < N) return RB_EINVAL;
   if ((ldx & 7) || (ldw & 7) || !X || !W || !b || !Y) return RB_EINVAL;
   if (act != RB_ACT_NONE && act != RB_ACT_RELU && act != RB_ACT_SIGMOID) return RB_EINVAL;
   if (M == 0) return RB_OK;
-  const unsigned g = (unsigned)(((M + G16_BM - 1) / G16_BM) * (N / G16_BN));
   hipStream_t s = (hipStream_t)stream;
   const bf16_t* x = (const bf16_t*)X;
   const bf16_t* w = (const bf16_t*)W;
-#define RB_G16(A, F) hipLaunchKernelGGL((k_gemm_bf16<A, F>), dim3(g), dim3(256), 0, s, x, ldx, w, ldw, b, Y, ldy, M, N, K)
-  if (out_f32) {
-    if (act == RB_ACT_RELU) RB_G16(RB_ACT_RELU, true);
-    else if (act == RB_ACT_SIGMOID) RB_G16(RB_ACT_SIGMOID, true);
-    else RB_G16(RB_ACT_NONE, true);
+  // Tile shape and tile order only change speed: every choice accumulates
+  // each output in the same k order with the same instruction (identical
+  // bits). 256 x 256 tiles when there are enough of them to give every CU two,
+  // else 128 x 128. XCD-contiguous tile order when all of W fits in one XCD's
+  // L2 (then each XCD keeps its A row-blocks and W in its own L2); plain order
+  // otherwise (contiguous ranges would stream all of W through every XCD).
+  const bool big = N % 256 == 0 && (int64_t)((M + 255) / 256) * (N / 256) >= 512;
+  const bool xcd = (int64_t)N * K * 2 <= (4 << 20);
+  if (big) {
+    if (xcd) launch_gemm_bf16<256, 256, 64, 128, 512, 1>(s, x, ldx, w, ldw, b, Y, ldy, M, N, K, act, out_f32);
+    else launch_gemm_bf16<256, 256, 64, 128, 512, 0>(s, x, ldx, w, ldw, b, Y, ldy, M, N, K, act, out_f32);
   } else {
-    if (act == RB_ACT_RELU) RB_G16(RB_ACT_RELU, false);
-    else if (act == RB_ACT_SIGMOID) RB_G16(RB_ACT_SIGMOID, false);
-    else RB_G16(RB_ACT_NONE, false);
+    if (xcd) launch_gemm_bf16<128, 128, 64, 32, 512, 1>(s, x, ldx, w, ldw, b, Y, ldy, M, N, K, act, out_f32);
+    else launch_gemm_bf16<128, 128, 64, 32, 512, 0>(s, x, ldx, w, ldw, b, Y, ldy, M, N, K, act, out_f32);
   }
-#undef RB_G16
   return launch_status();
 }
 
