@@ -74,6 +74,20 @@ def algorithmic_work(w, t, a, logd):
     return work
 
 
+def recorded_traffic(kernel):
+    """HBM bytes per launch from the committed counter passes, if the kernel
+    source is still the one they were taken with (else None)."""
+    import hashlib
+    try:
+        rec = json.load(open(os.path.join(ROOT, "profiles", "traffic.json")))
+        src = open(os.path.join(ROOT, rec["source"]), "rb").read()
+    except (OSError, ValueError, KeyError):
+        return None
+    if hashlib.sha256(src).hexdigest() != rec.get("sha256"):
+        return None
+    return rec.get("bytes_per_launch", {}).get(kernel)
+
+
 def cpu_baseline(w, t, a, seconds):
     """The oracle, as it stands, on the first requests of the trace for about
     `seconds` of CPU time (setup excluded)."""
@@ -203,6 +217,10 @@ def main():
                 "frac": round(ach / HBM_PEAK_GBS, 4), "traffic": None, "kernel": dom}
     roof["launches_per_step"] = dk["launches"]
     roof["avg_launch_us"] = dk["avg_us"]
+    roof["algorithmic_bytes_per_launch" if dom != "gemm_bf16" else "algorithmic_flops_per_launch"] = \
+        round((wk["bytes"] if dom != "gemm_bf16" else wk["flops"]) / dk["launches"])
+    roof["traffic"] = recorded_traffic(dom)
+    roof["traffic_unit"] = "HBM bytes per launch (rocprofv3 FETCH_SIZE + WRITE_SIZE, copy-probe scaled)"
     log(f"kernels: {json.dumps(kernels)}")
 
     for sw in [int(x) for x in args.sweep_windows.split(",") if x]:

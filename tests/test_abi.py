@@ -1,0 +1,176 @@
+"""The C ABI without a GPU: the library loads and exports every entry point
+include/rb.h declares; status codes and ownership rules on the host paths
+(host-only context, no-device scheduler); the serving API's batch formation
+against the oracle."""
+import os
+import re
+
+import numpy as np
+import pytest
+
+from oracle import batching as ob
+from paper_1712_06139_amd import rb
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def declared_functions():
+    src = open(os.path.join(ROOT, "include", "rb.h")).read()
+    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+    return sorted(set(re.findall(r"^(?:rb_status|const char\*)\s+(rb_[a-z0-9_]+)\s*\(", src, flags=re.M)))
+
+
+def test_every_declared_symbol_is_exported_and_bound():
+    names = declared_functions()
+    assert len(names) >= 28
+    lib = rb.lib()
+    for n in names:
+        assert hasattr(lib, n), n
+    assert sorted(rb.EXPORTS) == names
+
+
+def test_status_strings():
+    for code in (rb.RB_OK, rb.RB_EINVAL, rb.RB_EBUSY, rb.RB_EAGAIN, rb.RB_EEMPTY, rb.RB_ESIZE, rb.RB_ENOENT,
+                 rb.RB_EDEVICE, rb.RB_ENOMEM, rb.RB_ERANGE):
+        assert rb.lib().rb_status_str(code)
+    assert rb.lib().rb_status_str(-1234) == b"unknown status"
+
+
+@pytest.fixture
+def ctx():
+    c = rb.Ctx(-1)
+    yield c
+
+
+def mlp(ctx, d_in=4, d_out=3):
+    return rb.Model(ctx, "mlp", "f32", [(None, None, "relu"), (None, None, "none")],
+                    shapes=[(8, d_in), (d_out, 8)])
+
+
+def status(fn):
+    try:
+        fn()
+    except rb.RBError as e:
+        return e.status
+    return rb.RB_OK
+
+
+def test_model_validation(ctx):
+    # layer chain mismatch
+    assert status(lambda: rb.Model(ctx, "mlp", "f32", [(None, None, "relu"), (None, None, "none")],
+                                   shapes=[(8, 4), (3, 9)])) == rb.RB_EINVAL
+    # softmax is not a layer activation
+    assert status(lambda: rb.Model(ctx, "mlp", "f32", [(None, None, "softmax")], shapes=[(3, 4)])) == rb.RB_EINVAL
+    # ranking: first layer must take n_tables * 64 + n_dense inputs
+    assert status(lambda: rb.Model(ctx, "ranking", "bf16", [(None, None, "sigmoid")], n_dense=13,
+                                   shapes=[(1, 26 * 64 + 12), (26, 0)], table_rows=10)) == rb.RB_EINVAL
+    # a device context needs weights
+    m = mlp(ctx)
+    assert (m.d_in, m.d_out) == (4, 3)
+    m.destroy()
+
+
+def test_queue_validation(ctx):
+    s = rb.Sched(ctx, device=False)
+    m = mlp(ctx)
+    bad = [dict(max_batch_size=0), dict(max_batch_size=8, allowed=(4, 2, 8)), dict(max_batch_size=8, allowed=(2, 4)),
+           dict(max_batch_size=8, allowed=(2, 2, 8)), dict(max_batch_size=8, timeout_ns=0),
+           dict(max_batch_size=5000), dict(max_batch_size=8, bucket_len=64),
+           dict(max_batch_size=8, service_ns=[1, 2, 3])]
+    for kw in bad:
+        kw = dict(kw)
+        B = kw.pop("max_batch_size")
+        assert status(lambda: rb.Queue(s, m, B, **kw)) == rb.RB_EINVAL, kw
+    q = rb.Queue(s, m, 8, (2, 4, 8), None, 0, list(range(9)))
+    q.destroy()
+    s.destroy()
+    m.destroy()
+
+
+def test_device_mode_needs_a_device(ctx):
+    assert status(lambda: rb.Sched(ctx, device=True)) == rb.RB_EDEVICE
+
+
+def test_ownership_and_busy_rules(ctx):
+    s = rb.Sched(ctx, device=False)
+    m = mlp(ctx)
+    q = rb.Queue(s, m, 8, (), None)
+    x = np.zeros((2, 4), np.float32)
+    # oversize request, wrong payload size, time going backwards
+    assert status(lambda: s.submit(q, 9, np.zeros((9, 4), np.float32), arrival_ns=0)) == rb.RB_EINVAL
+    assert status(lambda: s.submit(q, 2, np.zeros(7, np.float32), arrival_ns=0)) == rb.RB_EINVAL
+    rid = s.submit(q, 2, x, arrival_ns=100)
+    assert status(lambda: s.submit(q, 2, x, arrival_ns=50)) == rb.RB_EINVAL
+    assert status(lambda: s.advance(10)) == rb.RB_EINVAL
+    # pending work keeps queue, model, scheduler and context alive
+    assert status(q.destroy) == rb.RB_EBUSY
+    assert status(m.destroy) == rb.RB_EBUSY
+    assert status(s.destroy) == rb.RB_EBUSY
+    assert status(ctx.destroy) == rb.RB_EBUSY
+    # not run yet -> not ready; unknown -> no entry
+    assert status(lambda: s.collect(rid, 2, 3)) == rb.RB_EAGAIN
+    assert status(lambda: s.collect(rid + 10, 2, 3)) == rb.RB_ENOENT
+    assert s.run_next() is None          # the open batch is not closed yet
+    rb.check(rb.lib().rb_flush(q.h), "rb_flush")
+    b = s.run_next()
+    assert b["reqs"] == [rid] and b["real"] == 2 and b["padded"] == 2
+    assert s.run_next() is None
+    # no device: there are no outputs to collect
+    assert status(lambda: s.collect(rid, 2, 3)) == rb.RB_EDEVICE
+    q.destroy()
+    m.destroy()
+    s.destroy()
+
+
+def test_sim_run_argument_checks(ctx):
+    s = rb.Sched(ctx, device=False)
+    m = mlp(ctx)
+    q = rb.Queue(s, m, 8, (), None)
+    n_rows = np.array([1, 2, 3])
+    arr = np.array([0, 5, 3])
+    assert status(lambda: s.sim_run([[q]], np.zeros(3), arr, n_rows)) == rb.RB_EINVAL   # time goes back
+    assert status(lambda: s.sim_run([[q]], np.array([0, 1, 0]), np.sort(arr), n_rows)) == rb.RB_EINVAL
+    assert status(lambda: s.sim_run([[q]], np.zeros(3), np.sort(arr), np.array([1, 9, 1]))) == rb.RB_EINVAL
+    # a queue that still holds requests cannot take part in a replay
+    s.submit(q, 1, np.zeros((1, 4), np.float32), arrival_ns=0)
+    assert status(lambda: s.sim_run([[q]], np.zeros(3), np.sort(arr), n_rows)) == rb.RB_EINVAL
+    rb.check(rb.lib().rb_flush(q.h), "rb_flush")
+    s.run_next()
+    log = s.sim_run([[q]], np.zeros(3), np.sort(arr), n_rows)
+    assert log["n_batches"] == 1 and log["b_real"].tolist() == [6]
+    q.destroy()
+    m.destroy()
+    s.destroy()
+
+
+@pytest.mark.parametrize("seed", range(8))
+def test_serving_api_formation_matches_oracle(ctx, seed):
+    # submit/advance/run_next with timeouts: the batches (composition, close
+    # times) equal the oracle's formation on the same arrivals
+    rng = np.random.default_rng(seed)
+    B, T = int(rng.integers(2, 20)), int(rng.integers(5, 100))
+    N = 300
+    arrival = np.cumsum(rng.integers(0, 20, size=N))
+    n = rng.integers(1, B + 1, size=N)
+    s = rb.Sched(ctx, device=False)
+    m = mlp(ctx)
+    q = rb.Queue(s, m, B, (), T)
+    got = []
+    for r in range(N):
+        s.submit(q, int(n[r]), np.zeros((int(n[r]), 4), np.float32), arrival_ns=int(arrival[r]))
+        while True:
+            b = s.run_next()
+            if b is None:
+                break
+            got.append((b["reqs"], b["close_ns"]))
+    s.advance(int(arrival[-1]) + T)
+    while True:
+        b = s.run_next()
+        if b is None:
+            break
+        got.append((b["reqs"], b["close_ns"]))
+    ref = ob.simulate([ob.QueueCfg(B, (), T)], [0] * N, arrival.tolist(), n.tolist(), [[0] * (B + 1)])
+    assert got == [(list(b.reqs), b.close_ns) for b in ref.batches]
+    q.destroy()
+    m.destroy()
+    s.destroy()
