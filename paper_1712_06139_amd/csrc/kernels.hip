@@ -381,66 +381,81 @@ __device__ __forceinline__ void wait_vmcnt() {
 template <int I>
 using ic = std::integral_constant<int, I>;
 
+// LDS byte address of a __shared__ object.
+__device__ __forceinline__ uint32_t lds_addr(const void* p) {
+  return (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) void*)p;
+}
+
+// One 16-byte-per-lane global -> LDS load (global_load_lds_dwordx4): lane l's
+// 16 bytes land at LDS byte lds + 16 l. Issued as inline assembly so that the
+// compiler does not add its own conservative waits for it: the kernel waits
+// with explicit vmcnt counts and a barrier before the data is read.
+__device__ __forceinline__ void load_to_lds(const void* g, uint32_t lds) {
+  asm volatile("s_mov_b32 m0, %0\n\tglobal_load_lds_dwordx4 %1, off" ::"s"(lds), "v"(g) : "memory", "m0");
+}
+
+__device__ __forceinline__ void lds_barrier() { asm volatile("s_barrier" ::: "memory"); }
+
 // Y = act(X W^T + b): X [M, K] and W [N, K] bf16, K contiguous; fp32
 // accumulation with v_mfma_f32_32x32x16_bf16.
 //
-// Workgroup tile BM x BN, k-step 32, NT/64 waves each owning a WM x WN
-// sub-tile ((WM/32) x (WN/32) accumulators). Operand tiles go from global
-// memory straight into LDS (global_load_lds_dwordx4: each wave instruction
-// fills 1 KB = 16 rows of 64 bytes, no register staging) through a ring of 4
-// LDS stages, so a k-step's loads are issued three steps before they are
-// read. Each stage is its own LDS array and the stage of every step is a
-// compile-time constant (the k loop is unrolled by 4), which lets the
-// compiler see that the loads in flight and the reads of the current stage
-// touch different arrays. Per step: wait for this wave's loads of the stage,
-// one barrier (all waves' loads landed; the stage refilled next was fully
-// read), issue the loads three steps ahead, then the MFMAs. The 16-byte chunk
-// c of row r sits at chunk c ^ ((r >> 2) & 3) of its 64-byte LDS row, so the
-// 16 lanes served per LDS cycle read 16 distinct bank groups.
+// Workgroup tile BM x BN, k-step 64, NT/64 waves each owning a WM x WN
+// sub-tile ((WM/32) x (WN/32) accumulators). Operand tiles go straight from
+// global memory into a ring of S LDS stages (each wave load instruction fills
+// 1 KB = 8 rows of 128 bytes; no register staging), issued S-1 k-steps before
+// they are read. Per k-step: wait for this wave's loads of the stage, one
+// barrier (all waves' loads landed; the stage refilled next has been read by
+// everyone), read the first fragments, issue the loads S-1 steps ahead, then
+// the MFMAs with the next sub-step's LDS reads interleaved between them. The
+// 16-byte chunk c of row r sits at chunk c ^ ((r >> 1) & 7) of its LDS row, so
+// the 16 lanes served per LDS cycle hit 16 distinct bank groups (64 banks).
 //
-// Every tile shape accumulates each output element in the same k order with
-// the same instruction, so results do not depend on the tile shape nor on
-// which rows share a tile.
-constexpr int G16_BK = 32, G16_STAGES = 4;
+// Every tile shape, stage count and tile order accumulates each output
+// element in the same k order with the same instruction, so results do not
+// depend on them, nor on which rows share a tile.
+constexpr int G16_BK = 64;
+constexpr int G16_CPR = G16_BK / 8;   // 16-byte chunks per LDS row
+constexpr int G16_RPI = 64 / G16_CPR; // rows filled per wave load instruction
 
-template <int BM, int BN, int WM, int WN, int NT, int ACT, bool OUT_F32, int ORDER = 1>
+template <int BM, int BN, int WM, int WN, int NT, int S, int ORDER, int ACT, bool OUT_F32>
 __global__ __launch_bounds__(NT) void k_gemm_bf16(const bf16_t* __restrict__ X, int ldx,
                                                   const bf16_t* __restrict__ W, int ldw,
                                                   const float* __restrict__ bias, void* __restrict__ Y,
                                                   int ldy, int M, int N, int K) {
   constexpr int NW = NT / 64;
   static_assert((BM / WM) * (BN / WN) == NW, "one wave per sub-tile");
+  static_assert(S >= 2 && S <= 4, "2..4 stages");
   constexpr int TM = WM / 32, TN = WN / 32;
-  constexpr int SA = BM / 16 / NW, SB = BN / 16 / NW;  // 16-row slabs per wave per stage
-  static_assert(SA * NW * 16 == BM && SB * NW * 16 == BN, "slabs cover the tile");
-  constexpr int OPS = SA + SB;                         // load instructions per wave per stage
-  __shared__ u32x4_t sA0[BM * 4], sA1[BM * 4], sA2[BM * 4], sA3[BM * 4];
-  __shared__ u32x4_t sB0[BN * 4], sB1[BN * 4], sB2[BN * 4], sB3[BN * 4];
-  u32x4_t* const sA[G16_STAGES] = {sA0, sA1, sA2, sA3};
-  u32x4_t* const sB[G16_STAGES] = {sB0, sB1, sB2, sB3};
+  constexpr int SA = BM / G16_RPI / NW, SB = BN / G16_RPI / NW;  // load instructions per wave per stage
+  static_assert(SA * NW * G16_RPI == BM && SB * NW * G16_RPI == BN, "loads cover the tile");
+  constexpr int OPS = SA + SB;
+  constexpr int KK = G16_BK / 16;
+  __shared__ u32x4_t sA[S][BM * G16_CPR];
+  __shared__ u32x4_t sB[S][BN * G16_CPR];
 
-  const int tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wid = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int wm = wid / (BN / WN), wn = wid % (BN / WN);
   const int tiles_n = N / BN;
   const int tile = ORDER ? xcd_tile(blockIdx.x, gridDim.x) : (int)blockIdx.x;
   const int bm = tile / tiles_n, bn = tile - bm * tiles_n;
   const int m0 = bm * BM, n0 = bn * BN;
 
-  // lane l of a load instruction fills LDS row l/4, chunk l%4 of its slab
-  const int lr = lane >> 2, lc = lane & 3;
+  // lane l of a load instruction fills LDS row l / 8 (of its 8), chunk l % 8
+  const int lr = lane / G16_CPR, lc = lane % G16_CPR;
   const bf16_t* ga[SA];
   const bf16_t* gb[SB];
 #pragma unroll
   for (int i = 0; i < SA; ++i) {
-    const int row = (wid * SA + i) * 16 + lr;
+    const int row = (wid * SA + i) * G16_RPI + lr;
     int ra = m0 + row;
     ra = ra < M ? ra : M - 1;  // rows past M are computed on a copy and never stored
-    ga[i] = X + (int64_t)ra * ldx + (lc ^ ((row >> 2) & 3)) * 8;
+    ga[i] = X + (int64_t)ra * ldx + (lc ^ ((row >> 1) & 7)) * 8;
   }
 #pragma unroll
   for (int i = 0; i < SB; ++i) {
-    const int row = (wid * SB + i) * 16 + lr;
-    gb[i] = W + (int64_t)(n0 + row) * ldw + (lc ^ ((row >> 2) & 3)) * 8;
+    const int row = (wid * SB + i) * G16_RPI + lr;
+    gb[i] = W + (int64_t)(n0 + row) * ldw + (lc ^ ((row >> 1) & 7)) * 8;
   }
 
   floatx16_t acc[TM][TN];
@@ -455,65 +470,68 @@ __global__ __launch_bounds__(NT) void k_gemm_bf16(const bf16_t* __restrict__ X, 
     constexpr int st = decltype(stc)::value;
     const int k0 = kt * G16_BK;
 #pragma unroll
-    for (int i = 0; i < SA; ++i)
-      __builtin_amdgcn_global_load_lds((const void*)(ga[i] + k0), (__shared__ void*)(sA[st] + (wid * SA + i) * 64),
-                                       16, 0, 0);
+    for (int i = 0; i < SA; ++i) load_to_lds(ga[i] + k0, lds_addr(&sA[st][0]) + (wid * SA + i) * 1024);
 #pragma unroll
-    for (int i = 0; i < SB; ++i)
-      __builtin_amdgcn_global_load_lds((const void*)(gb[i] + k0), (__shared__ void*)(sB[st] + (wid * SB + i) * 64),
-                                       16, 0, 0);
+    for (int i = 0; i < SB; ++i) load_to_lds(gb[i] + k0, lds_addr(&sB[st][0]) + (wid * SB + i) * 1024);
   };
-  auto compute = [&](auto stc) {
+  auto read_frags = [&](auto stc, int kk, bf16x8_t* a, bf16x8_t* bv) {
     constexpr int st = decltype(stc)::value;
-    const u32x4_t* A_ = sA[st];
-    const u32x4_t* B_ = sB[st];
+    const int ch = kk * 2 + (lane >> 5);
 #pragma unroll
-    for (int kk = 0; kk < 2; ++kk) {
-      bf16x8_t a[TM], bv[TN];
-      const int ch = kk * 2 + (lane >> 5);
+    for (int i = 0; i < TM; ++i) {
+      const int r = wm * WM + i * 32 + (lane & 31);
+      a[i] = __builtin_bit_cast(bf16x8_t, sA[st][r * G16_CPR + (ch ^ ((r >> 1) & 7))]);
+    }
 #pragma unroll
-      for (int i = 0; i < TM; ++i) {
-        const int r = wm * WM + i * 32 + (lane & 31);
-        a[i] = __builtin_bit_cast(bf16x8_t, A_[r * 4 + (ch ^ ((r >> 2) & 3))]);
-      }
-#pragma unroll
-      for (int j = 0; j < TN; ++j) {
-        const int r = wn * WN + j * 32 + (lane & 31);
-        bv[j] = __builtin_bit_cast(bf16x8_t, B_[r * 4 + (ch ^ ((r >> 2) & 3))]);
-      }
-#pragma unroll
-      for (int i = 0; i < TM; ++i)
-#pragma unroll
-        for (int j = 0; j < TN; ++j)
-          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[i], bv[j], acc[i][j], 0, 0, 0);
+    for (int j = 0; j < TN; ++j) {
+      const int r = wn * WN + j * 32 + (lane & 31);
+      bv[j] = __builtin_bit_cast(bf16x8_t, sB[st][r * G16_CPR + (ch ^ ((r >> 1) & 7))]);
     }
   };
   const int nk = K / G16_BK;
   auto step = [&](int kt, auto stc, auto nxt) {
-    const int ahead = nk - 1 - kt;  // stages whose loads were issued after this one's
+    const int ahead = min(nk - 1 - kt, S - 2);  // stages whose loads were issued after this one's
     if (ahead >= 2)
       wait_vmcnt<2 * OPS>();
     else if (ahead == 1)
       wait_vmcnt<OPS>();
     else
       wait_vmcnt<0>();
-    __builtin_amdgcn_s_barrier();
-    if (kt + 3 < nk) issue(kt + 3, nxt);
-    compute(stc);
+    lds_barrier();
+    bf16x8_t fa[2][TM], fb[2][TN];
+    read_frags(stc, 0, fa[0], fb[0]);
+    if (kt + S - 1 < nk) issue(kt + S - 1, nxt);
+#pragma unroll
+    for (int kk = 0; kk < KK; ++kk) {
+      if (kk + 1 < KK) read_frags(stc, kk + 1, fa[(kk + 1) & 1], fb[(kk + 1) & 1]);
+#pragma unroll
+      for (int i = 0; i < TM; ++i)
+#pragma unroll
+        for (int j = 0; j < TN; ++j)
+          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[kk & 1][i], fb[kk & 1][j], acc[i][j], 0, 0, 0);
+      if (kk + 1 < KK) {
+        // one LDS read between consecutive MFMAs
+#pragma unroll
+        for (int q = 0; q < TM + TN; ++q) {
+          __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+          __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+        }
+      }
+    }
   };
-  if (0 < nk) issue(0, ic<0>{});
-  if (1 < nk) issue(1, ic<1>{});
-  if (2 < nk) issue(2, ic<2>{});
+  issue(0, ic<0>{});
+  if (S > 2 && 1 < nk) issue(1, ic<1 % S>{});
+  if (S > 3 && 2 < nk) issue(2, ic<2 % S>{});
   int kt = 0;
-  for (; kt + 4 <= nk; kt += 4) {
-    step(kt, ic<0>{}, ic<3>{});
-    step(kt + 1, ic<1>{}, ic<0>{});
-    step(kt + 2, ic<2>{}, ic<1>{});
-    step(kt + 3, ic<3>{}, ic<2>{});
+  for (; kt + S <= nk; kt += S) {
+    step(kt, ic<0>{}, ic<(S - 1) % S>{});
+    step(kt + 1, ic<1 % S>{}, ic<S % S>{});
+    if (S > 2) step(kt + 2, ic<2 % S>{}, ic<(S + 1) % S>{});
+    if (S > 3) step(kt + 3, ic<3 % S>{}, ic<(S + 2) % S>{});
   }
-  if (kt < nk) step(kt, ic<0>{}, ic<3>{});
-  if (kt + 1 < nk) step(kt + 1, ic<1>{}, ic<0>{});
-  if (kt + 2 < nk) step(kt + 2, ic<2>{}, ic<1>{});
+  if (kt < nk) step(kt, ic<0>{}, ic<(S - 1) % S>{});
+  if (S > 2 && kt + 1 < nk) step(kt + 1, ic<1 % S>{}, ic<S % S>{});
+  if (S > 3 && kt + 2 < nk) step(kt + 2, ic<2 % S>{}, ic<(S + 1) % S>{});
 
   // accumulator (i, j) register r of lane l holds row 8*(r/4) + 4*(l/32) + r%4,
   // column l%32 of its 32 x 32 block
@@ -714,12 +732,13 @@ inline unsigned blocks_for(int64_t threads) { return (unsigned)((threads + 255) 
 
 namespace {
 
-template <int BM, int BN, int WM, int WN, int NT, int ORDER = 1>
+template <int BM, int BN, int WM, int WN, int NT, int S, int ORDER>
 void launch_gemm_bf16(hipStream_t s, const bf16_t* x, int ldx, const bf16_t* w, int ldw, const float* b,
                              void* Y, int ldy, int M, int N, int K, int act, int out_f32) {
   const unsigned g = (unsigned)(((M + BM - 1) / BM) * (N / BN));
 #define RB_G16(A, F) \
-  hipLaunchKernelGGL((k_gemm_bf16<BM, BN, WM, WN, NT, A, F, ORDER>), dim3(g), dim3(NT), 0, s, x, ldx, w, ldw, b, Y, ldy, M, N, K)
+  hipLaunchKernelGGL((k_gemm_bf16<BM, BN, WM, WN, NT, S, ORDER, A, F>), dim3(g), dim3(NT), 0, s, x, ldx, w, ldw, b, Y, \
+                     ldy, M, N, K)
   if (out_f32) {
     if (act == RB_ACT_RELU) RB_G16(RB_ACT_RELU, true);
     else if (act == RB_ACT_SIGMOID) RB_G16(RB_ACT_SIGMOID, true);
@@ -791,21 +810,28 @@ rb_status rb_k_gemm_bf16(void* stream, const void* X, int32_t ldx, const void* W
   hipStream_t s = (hipStream_t)stream;
   const bf16_t* x = (const bf16_t*)X;
   const bf16_t* w = (const bf16_t*)W;
-  // Tile shape and tile order only change speed: every choice accumulates
-  // each output in the same k order with the same instruction (identical
-  // bits). 256 x 256 tiles when there are enough of them to give every CU two,
-  // else 128 x 128. XCD-contiguous tile order when all of W fits in one XCD's
-  // L2 (then each XCD keeps its A row-blocks and W in its own L2); plain order
-  // otherwise (contiguous ranges would stream all of W through every XCD).
-  const bool big = N % 256 == 0 && (int64_t)((M + 255) / 256) * (N / 256) >= 512;
+  // Tile shape, stage count and tile order only change speed: every choice
+  // accumulates each output in the same k order with the same instruction
+  // (identical bits). The largest tile that still gives every CU a tile:
+  // 256 x 256 (2 stages, 128 KB LDS), else 256 x 128 (3 stages, 144 KB), else
+  // 128 x 128 (4 stages, 128 KB). XCD-contiguous tile order when all of W fits
+  // in one XCD's L2 (each XCD then keeps its A row-blocks and W in its own
+  // L2); plain order otherwise (contiguous ranges would stream all of W
+  // through every XCD).
+  const int64_t rows256 = (M + 255) / 256;
   const bool xcd = (int64_t)N * K * 2 <= (4 << 20);
-  if (big) {
-    if (xcd) launch_gemm_bf16<256, 256, 64, 128, 512, 1>(s, x, ldx, w, ldw, b, Y, ldy, M, N, K, act, out_f32);
-    else launch_gemm_bf16<256, 256, 64, 128, 512, 0>(s, x, ldx, w, ldw, b, Y, ldy, M, N, K, act, out_f32);
-  } else {
-    if (xcd) launch_gemm_bf16<128, 128, 64, 32, 512, 1>(s, x, ldx, w, ldw, b, Y, ldy, M, N, K, act, out_f32);
-    else launch_gemm_bf16<128, 128, 64, 32, 512, 0>(s, x, ldx, w, ldw, b, Y, ldy, M, N, K, act, out_f32);
-  }
+#define RB_PICK(BM, BN, WM, WN, S)                                                                        \
+  do {                                                                                                    \
+    if (xcd) launch_gemm_bf16<BM, BN, WM, WN, 512, S, 1>(s, x, ldx, w, ldw, b, Y, ldy, M, N, K, act, out_f32); \
+    else launch_gemm_bf16<BM, BN, WM, WN, 512, S, 0>(s, x, ldx, w, ldw, b, Y, ldy, M, N, K, act, out_f32);     \
+  } while (0)
+  if (N % 256 == 0 && rows256 * (N / 256) >= 256)
+    RB_PICK(256, 256, 64, 128, 2);
+  else if (rows256 * (N / 128) >= 256)
+    RB_PICK(256, 128, 64, 64, 3);
+  else
+    RB_PICK(128, 128, 64, 32, 4);
+#undef RB_PICK
   return launch_status();
 }
 
