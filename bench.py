@@ -1,24 +1,28 @@
 #!/usr/bin/env python
 """Throughput and latency of batched inference on one MI355X.
 
-Workload (default): the ranking model - 26 sum-pooled embedding bags (ids
+Default workload: the ranking model - 26 sum-pooled embedding bags (ids
 Zipf(1.1) over 100k-row x 64 bf16 tables, 1..20 ids per bag) plus 13 dense
 features into an MLP 1677->1024->512->256->1 (ReLU, sigmoid out), bf16
 weights with fp32 accumulation; 100k requests of 1..64 examples, batches of
 at most 512 rows padded to {64,128,256,512}, formed by count in arrival order.
+`--workload` selects one of the other synthetic workloads instead.
 
-One step replays the whole 100k-request trace through the library: batch
+One step replays the whole request trace through the library: batch
 formation, padded-size choice, round-robin dispatch on the simulated clock,
-and every batch's route -> embedding-bag -> 3 GEMMs -> head on the GPU, with
-the request payloads already resident in HBM and the outputs left there.
+and every batch's device work (route -> assemble or embedding-bag -> dense
+layers -> head / pooling / split), with the request payloads already resident
+in HBM and the outputs left there.
 
 Printed: one JSON line with examples/s, p50/p99 request latency on the
-simulated clock (service times measured on this GPU, Poisson arrivals at 90%
-of the measured capacity), the dominant kernel against its roofline (HIP
-events on the library's stream during a profiled replay), and the CPU oracle
-timed on a bounded sample of the same trace.
+simulated clock (ranking: service times measured on this GPU, Poisson
+arrivals at 90% of the simulated device's capacity), the dominant kernel
+against its roofline (HIP events on the library's stream during a profiled
+replay), every kernel's figures, and the CPU oracle timed on a bounded sample
+of the same trace.
 """
 import argparse
+import collections
 import json
 import math
 import os
@@ -34,6 +38,20 @@ METRIC = "examples/sec per MI355X (batched MLP/embedding model); p50/p99 request
 HBM_PEAK_GBS = 8000.0
 BF16_PEAK_TFLOPS = 2500.0
 F32_PEAK_TFLOPS = 157.3
+KERNELS = ("route", "assemble", "embbag", "gemm_bf16", "gemm_f32", "head", "seqpool", "split")
+
+DESCRIPTION = {
+    "ranking": "ranking: 26 Zipf(1.1) embedding bags over 100k x 64 bf16 tables + 13 dense -> MLP "
+               "1677-1024-512-256-1 (ReLU, sigmoid), bf16 weights, fp32 accumulation; 100k requests of 1-64 "
+               "examples; max batch 512, allowed {64,128,256,512}",
+    "small_mlp": "small MLP: fp32 64-128(ReLU)-16; 256 requests of 1-8 rows; max batch 32, allowed {8,16,32}",
+    "large_mlp": "large MLP: bf16 4096-8192-8192-4096 (ReLU hidden), fp32 accumulation; 20k requests of 1-32 rows; "
+                 "max batch 1024, allowed {128,256,512,1024}",
+    "multi_tenant": "multi-tenant: 4 fp32 MLPs 256-1024-1024-32 + 4 ranking models on one GPU; 50k requests, "
+                    "Poisson 50k/s, servable Zipf(1.0); max batch 256, no padding, 2 ms timeout",
+    "ragged_seq": "ragged sequences: fp32 per-token 256-512(ReLU)-256, masked mean-pool, 256-2 softmax; 50k requests "
+                  "of 1-4 sequences of 1-512 tokens; length buckets {64,128,256,512}, max 64 sequences per batch",
+}
 
 
 def log(msg):
@@ -45,38 +63,60 @@ def nearest_rank(v, q):
     return int(v[max(1, int(math.ceil(q * len(v)))) - 1])
 
 
-def algorithmic_work(w, t, a, logd):
-    """Algorithmic bytes / flops of one replay, per kernel (real model dims;
-    padded rows count as rows: they are computed as the method pads them)."""
-    m = w.models[0]
-    P = logd["b_padded"].astype(np.int64)
-    M = int(P.sum())
-    real = int(logd["b_real"].sum())
-    n_req = t.n
-    n_ids = int(a.ids.size)
+def algorithmic_work(w, t, a, logd, qindex):
+    """Algorithmic bytes / flops of one replay, per kernel. Real model
+    dimensions; padded rows (and padded tokens) count as rows, since the
+    method pads them and computes them."""
+    work = collections.defaultdict(lambda: {"bytes": 0, "flops": 0})
+    nb = logd["n_batches"]
+    beg = logd["b_req_begin"][:nb + 1]
+    reqs = logd["b_reqs"][:beg[-1]].astype(np.int64)
+
+    def per_batch(v):  # per-request values summed over each batch
+        return np.add.reduceat(v[reqs], beg[:-1]) if nb else np.zeros(0)
+
+    n_req = np.diff(beg)
+    n_dense = per_batch(np.diff(a.dense_off))
+    n_ids = per_batch(np.diff(a.ids_off))
     row_desc = 32
-    work = {}
-    # route: request descriptors, batch descriptors, bag lengths of real rows, row map writes
-    work["route"] = {"bytes": n_req * 56 + len(P) * 24 + real * m.n_tables * 4 + M * row_desc}
-    # embedding bags: row map, lengths, ids, one 128 B table row per id, dense, X row write
-    ldx = m.n_tables * m.emb_dim + m.n_dense
-    work["embbag"] = {"bytes": M * row_desc + real * (m.n_tables * 4 + m.n_dense * 4) + n_ids * (4 + m.emb_dim * 2)
-                      + M * ldx * 2}
-    fl = 0
-    by = 0
-    for L in m.layers[:-1]:
-        fl += 2 * M * L.fan_in * L.fan_out
-        by += (M * L.fan_in + L.fan_in * L.fan_out + M * L.fan_out) * 2 + L.fan_out * 4
-    work["gemm_bf16"] = {"flops": fl, "bytes": by}
-    last = m.layers[-1]
-    work["head"] = {"bytes": M * row_desc + M * last.fan_in * 2 + last.fan_in * 2 + real * 4,
-                    "flops": 2 * M * last.fan_in}
+    for b in range(nb):
+        q = w.queues[qindex[int(logd["b_queue"][b])]]
+        m = w.models[q.servable]
+        P, s = int(logd["b_padded"][b]), int(logd["b_real"][b])
+        T = q.bucket_len or 1
+        M = P * T
+        bf16 = m.dtype == "bf16"
+        lens_bytes = s * m.n_tables * 4 if m.kind == "ranking" else (s * 4 if m.kind == "seqpool" else 0)
+        work["route"]["bytes"] += int(n_req[b]) * 56 + 24 + lens_bytes + P * row_desc
+        if m.kind == "ranking":
+            d = m.n_tables * m.emb_dim + m.n_dense
+            work["embbag"]["bytes"] += (P * row_desc + s * (m.n_tables * 4 + m.n_dense * 4)
+                                        + int(n_ids[b]) * (4 + m.emb_dim * 2) + P * d * 2)
+        else:
+            # real inputs read once; every padded row (token) written
+            work["assemble"]["bytes"] += (int(n_dense[b]) * 4 + M * m.d_in * (2 if bf16 else 4)
+                                          + (P if m.kind == "seqpool" else M) * row_desc)
+        layers = m.layers[:-1] if (m.kind == "ranking" and bf16 and m.layers[-1].fan_out == 1) else m.layers
+        key = "gemm_bf16" if bf16 else "gemm_f32"
+        for L in layers:
+            work[key]["flops"] += 2 * M * L.fan_in * L.fan_out
+            work[key]["bytes"] += (M * L.fan_in + L.fan_in * L.fan_out + M * L.fan_out) * (2 if bf16 else 4)
+        if m.kind == "ranking" and len(layers) < len(m.layers):
+            last = m.layers[-1]
+            work["head"]["bytes"] += P * row_desc + P * last.fan_in * 2 + last.fan_in * 2 + s * 4
+            work["head"]["flops"] += 2 * P * last.fan_in
+        elif m.kind == "seqpool":
+            D = m.head.fan_in
+            work["seqpool"]["bytes"] += (int(n_dense[b]) // m.d_in) * D * 4 + P * row_desc + s * m.d_out * 4
+            work["seqpool"]["flops"] += (int(n_dense[b]) // m.d_in) * D + 2 * s * D * m.d_out
+        else:
+            work["split"]["bytes"] += P * row_desc + s * m.d_out * 8
     return work
 
 
-def recorded_traffic(kernel):
-    """HBM bytes per launch from the committed counter passes, if the kernel
-    source is still the one they were taken with (else None)."""
+def recorded_traffic(workload, kernel):
+    """HBM bytes per launch from the committed counter passes, if they were
+    taken on this workload with the current kernel source (else None)."""
     import hashlib
     try:
         rec = json.load(open(os.path.join(ROOT, "profiles", "traffic.json")))
@@ -85,12 +125,12 @@ def recorded_traffic(kernel):
         return None
     if hashlib.sha256(src).hexdigest() != rec.get("sha256"):
         return None
-    return rec.get("bytes_per_launch", {}).get(kernel)
+    return rec.get("workloads", {}).get(workload, {}).get(kernel)
 
 
 def cpu_baseline(w, t, a, seconds):
     """The oracle, as it stands, on the first requests of the trace for about
-    `seconds` of CPU time (setup excluded)."""
+    `seconds` of CPU time (model setup excluded)."""
     from oracle.models import OracleModel
     import synth
     try:
@@ -98,17 +138,71 @@ def cpu_baseline(w, t, a, seconds):
         cores = max([d.get("num_threads", 1) for d in threadpool_info()] + [1])
     except Exception:
         cores = 1
-    om = OracleModel(w.models[0], synth.model_params(w, 0))
+    oms = {}
     n = ex = 0
-    t0 = time.perf_counter()
-    while time.perf_counter() - t0 < seconds and n < t.n:
-        om.forward(a.payload(n))
+    el = 0.0
+    while el < seconds and n < t.n:
+        s = int(t.servable[n])
+        if s not in oms:
+            oms[s] = OracleModel(w.models[s], synth.model_params(w, s))
+        t0 = time.perf_counter()
+        oms[s].forward(a.payload(n))
+        el += time.perf_counter() - t0
         ex += int(t.n_rows[n])
         n += 1
-    el = time.perf_counter() - t0
     return {"value": ex / el, "unit": "examples/s", "cores": int(cores), "kind": "oracle",
             "sample": f"first {n} requests ({ex} examples) of the same trace, unbatched fp64 forward per request, "
                       f"{el:.1f} s"}
+
+
+def calibrate_latency(w, t, a, dt, ctx, dep, window):
+    """Service time per padded size measured on this GPU (a replay of a prefix
+    of the trace through a queue whose every batch is padded to P), then
+    Poisson arrivals at rho x the simulated device's capacity through the
+    no-device scheduler: nearest-rank p50 / p99 per request."""
+    import synth
+    import torch
+    from paper_1712_06139_amd import rb
+    from paper_1712_06139_amd.deploy import Deployment
+    allowed = list(w.queues[0].allowed)
+    svc = np.zeros(w.queues[0].max_batch_size + 1, dtype=np.int64)
+    n_cal = min(20_000, t.n)
+    tcal = synth.trace(w, n_cal)
+    for P in allowed:
+        cw = synth.Workload(w.name, w.wid, w.models, (synth.Queue(0, P, (P,), None),), w.n_requests, w.rows,
+                            w.rate_per_s)
+        cdep = Deployment(cw, ctx, device=True, window_batches=window, models=dep.models)
+        out_off = cdep.out_offsets(tcal)
+        out = torch.empty(int(out_off[-1]), dtype=torch.float32, device="cuda")
+        kw = dict(dense=dt.dense, dense_off=a.dense_off[:n_cal + 1], lens=dt.lens,
+                  lens_off=None if a.lens.size == 0 else a.lens_off[:n_cal + 1], ids=dt.ids,
+                  ids_off=None if a.ids.size == 0 else a.ids_off[:n_cal + 1], out=out, out_off=out_off)
+        cdep.sched.sim_run(cdep.servables, tcal.servable, tcal.arrival_ns, tcal.n_rows, None, **kw)
+        cdep.sched.sync()
+        torch.cuda.synchronize()
+        s0 = time.perf_counter()
+        lg = cdep.sched.sim_run(cdep.servables, tcal.servable, tcal.arrival_ns, tcal.n_rows, None, **kw)
+        cdep.sched.sync()
+        svc[P] = int((time.perf_counter() - s0) * 1e9 / lg["n_batches"])
+        cdep.destroy()
+    for s in range(len(svc)):
+        svc[s] = svc[min(p for p in allowed if p >= s)]
+    lctx = rb.Ctx(-1)
+    ld = Deployment(w, lctx, device=False, service_ns=[svc.tolist()], with_params=False)
+    busy_ns = int(svc[ld.replay_meta(t)["b_padded"]].sum())
+    cap = t.n / (busy_ns * 1e-9)
+    lat = {"clock": "simulated", "capacity_req_s": round(cap, 1),
+           "service_us_by_padded_size": {str(P): round(svc[P] / 1e3, 2) for P in allowed}}
+    for rho in (0.5, 0.9):
+        tr = synth.trace(w, rate_per_s=rho * cap)
+        lg = ld.replay_meta(tr)
+        v = lg["req_done_ns"] - tr.arrival_ns
+        lat[f"rho{rho}"] = {"arrival_rate_req_s": round(rho * cap, 1), "utilization": rho,
+                            "p50_us": round(nearest_rank(v, 0.5) / 1e3, 2),
+                            "p99_us": round(nearest_rank(v, 0.99) / 1e3, 2)}
+    ld.destroy()
+    lctx.destroy()
+    return lat
 
 
 def main():
@@ -116,6 +210,7 @@ def main():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=5)
     ap.add_argument("--warmup", type=int, default=2)
+    ap.add_argument("--workload", default="ranking", choices=sorted(DESCRIPTION))
     ap.add_argument("--window", type=int, default=64, help="dispatched batches per launch window")
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -145,16 +240,14 @@ def main():
         torch.cuda.synchronize()
         log(f"copy probe: read {n * 4} B, wrote {n * 4} B")
         del src, dst
-    w = synth.workload("ranking")
+    w = synth.workload(args.workload)
     t = synth.trace(w)
-    log(f"generating {t.n} requests ({int(t.n_rows.sum())} examples)")
+    examples = int(t.n_rows.sum())
+    log(f"{w.name}: generating {t.n} requests ({examples} rows)")
     t0 = time.time()
     a = synth.arenas(t)
-    log(f"payloads drawn in {time.time() - t0:.1f} s ({a.ids.size} ids); building model")
-    synth.model_params(w, 0)
+    log(f"payloads drawn in {time.time() - t0:.1f} s; building models")
     ctx = rb.Ctx(0)
-    examples = int(t.n_rows.sum())
-
     shared = {}
 
     def make(window, profile=False):
@@ -184,43 +277,44 @@ def main():
     value = examples * args.steps / wall
     n_batches = int(logd["n_batches"])
     log(f"timed {args.steps} steps: {ms_per_step:.2f} ms/step (device {dev_ms / args.steps:.2f} ms), "
-        f"{value / 1e6:.2f} M examples/s, {n_batches} batches/step")
+        f"{value / 1e6:.2f} M rows/s, {n_batches} batches/step")
 
     # profiled replay: per-kernel durations from HIP events on the library's stream
     pdep = make(args.window, profile=True)
     pdep.replay(dt)
     pdep.sched.sync()
+    work = algorithmic_work(w, t, a, logd, dep.qindex)
     kernels = {}
-    work = algorithmic_work(w, t, a, logd)
-    for k in ("route", "embbag", "gemm_bf16", "head"):
+    for k in KERNELS:
         n, ms = pdep.sched.kernel_stats(k)
         if n == 0:
             continue
         e = {"launches": n, "total_ms": round(ms, 4), "avg_us": round(ms * 1e3 / n, 3)}
         wk = work.get(k, {})
-        if "bytes" in wk:
+        if wk.get("bytes"):
             e["gbs"] = round(wk["bytes"] / (ms * 1e-3) / 1e9, 1)
-        if "flops" in wk:
+        if wk.get("flops"):
             e["tflops"] = round(wk["flops"] / (ms * 1e-3) / 1e12, 2)
         kernels[k] = e
     pdep.destroy()
     dom = max(kernels, key=lambda k: kernels[k]["total_ms"])
-    dk = kernels[dom]
-    wk = work[dom]
-    if dom == "gemm_bf16":
+    dk, wk = kernels[dom], work[dom]
+    if dom.startswith("gemm"):
+        peak = BF16_PEAK_TFLOPS if dom == "gemm_bf16" else F32_PEAK_TFLOPS
         ach = wk["flops"] / (dk["total_ms"] * 1e-3) / 1e12
-        roof = {"bound": "mfma", "achieved": round(ach, 2), "peak": BF16_PEAK_TFLOPS, "unit": "TFLOP/s",
-                "frac": round(ach / BF16_PEAK_TFLOPS, 4), "traffic": None, "kernel": dom}
+        roof = {"bound": "mfma", "achieved": round(ach, 2), "peak": peak, "unit": "TFLOP/s",
+                "frac": round(ach / peak, 4)}
+        roof["algorithmic_flops_per_launch"] = round(wk["flops"] / dk["launches"])
     else:
         ach = wk["bytes"] / (dk["total_ms"] * 1e-3) / 1e9
         roof = {"bound": "hbm", "achieved": round(ach, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                "frac": round(ach / HBM_PEAK_GBS, 4), "traffic": None, "kernel": dom}
+                "frac": round(ach / HBM_PEAK_GBS, 4)}
+        roof["algorithmic_bytes_per_launch"] = round(wk["bytes"] / dk["launches"])
+    roof["traffic"] = recorded_traffic(w.name, dom)
+    roof["traffic_unit"] = "HBM bytes per launch (rocprofv3 FETCH_SIZE + WRITE_SIZE, copy-probe scaled)"
+    roof["kernel"] = dom
     roof["launches_per_step"] = dk["launches"]
     roof["avg_launch_us"] = dk["avg_us"]
-    roof["algorithmic_bytes_per_launch" if dom != "gemm_bf16" else "algorithmic_flops_per_launch"] = \
-        round((wk["bytes"] if dom != "gemm_bf16" else wk["flops"]) / dk["launches"])
-    roof["traffic"] = recorded_traffic(dom)
-    roof["traffic_unit"] = "HBM bytes per launch (rocprofv3 FETCH_SIZE + WRITE_SIZE, copy-probe scaled)"
     log(f"kernels: {json.dumps(kernels)}")
 
     for sw in [int(x) for x in args.sweep_windows.split(",") if x]:
@@ -233,58 +327,12 @@ def main():
             d2.replay(dt)
         d2.sched.sync()
         el = (time.perf_counter() - s0) / 2
-        log(f"window {sw}: {el * 1e3:.2f} ms/step, {examples / el / 1e6:.2f} M examples/s")
+        log(f"window {sw}: {el * 1e3:.2f} ms/step, {examples / el / 1e6:.2f} M rows/s")
         d2.destroy()
 
     latency = None
-    if not args.no_latency:
-        # service time per padded size P: a replay of a prefix of the trace
-        # through a queue whose every batch is padded to P (max batch P)
-        allowed = list(w.queues[0].allowed)
-        svc = np.zeros(w.queues[0].max_batch_size + 1, dtype=np.int64)
-        n_cal = 20_000
-        tcal = synth.trace(w, n_cal)
-        for P in allowed:
-            cw = synth.Workload(w.name, w.wid, w.models, (synth.Queue(0, P, (P,), None),), w.n_requests, w.rows,
-                                w.rate_per_s)
-            cdep = Deployment(cw, ctx, device=True, window_batches=args.window, models=dep.models)
-            out_off = cdep.out_offsets(tcal)
-            out = torch.empty(int(out_off[-1]), dtype=torch.float32, device="cuda")
-            kw = dict(dense=dt.dense, dense_off=a.dense_off[:n_cal + 1], lens=dt.lens,
-                      lens_off=a.lens_off[:n_cal + 1], ids=dt.ids, ids_off=a.ids_off[:n_cal + 1], out=out,
-                      out_off=out_off)
-            cdep.sched.sim_run(cdep.servables, tcal.servable, tcal.arrival_ns, tcal.n_rows, None, **kw)
-            cdep.sched.sync()
-            torch.cuda.synchronize()
-            s0 = time.perf_counter()
-            lg = cdep.sched.sim_run(cdep.servables, tcal.servable, tcal.arrival_ns, tcal.n_rows, None, **kw)
-            cdep.sched.sync()
-            el = time.perf_counter() - s0
-            svc[P] = int(el * 1e9 / lg["n_batches"])
-            cdep.destroy()
-        for s in range(len(svc)):
-            svc[s] = svc[min(p for p in allowed if p >= s)] if s <= allowed[-1] else svc[s]
-        # capacity of the simulated device: requests / total service time of
-        # the trace's batches (composition is count-only, so arrival-free)
-        lctx = rb.Ctx(-1)
-        ld = Deployment(w, lctx, device=False, service_ns=[svc.tolist()], with_params=False)
-        busy_ns = int(svc[ld.replay_meta(t)["b_padded"]].sum())
-        ld.destroy()
-        lctx.destroy()
-        cap = t.n / (busy_ns * 1e-9)
-        latency = {"clock": "simulated", "capacity_req_s": round(cap, 1),
-                   "service_us_by_padded_size": {str(P): round(svc[P] / 1e3, 2) for P in allowed}}
-        for rho in (0.5, 0.9):
-            tr = synth.trace(w, rate_per_s=rho * cap)
-            lctx = rb.Ctx(-1)
-            ld = Deployment(w, lctx, device=False, service_ns=[svc.tolist()], with_params=False)
-            lg = ld.replay_meta(tr)
-            lat = lg["req_done_ns"] - tr.arrival_ns
-            latency[f"rho{rho}"] = {"arrival_rate_req_s": round(rho * cap, 1), "utilization": rho,
-                                    "p50_us": round(nearest_rank(lat, 0.5) / 1e3, 2),
-                                    "p99_us": round(nearest_rank(lat, 0.99) / 1e3, 2)}
-            ld.destroy()
-            lctx.destroy()
+    if not args.no_latency and len(w.queues) == 1 and w.queues[0].allowed:
+        latency = calibrate_latency(w, t, a, dt, ctx, dep, args.window)
         log(f"latency: {json.dumps(latency)}")
 
     cpu = None
@@ -292,15 +340,13 @@ def main():
         log("timing the CPU oracle")
         cpu = cpu_baseline(w, t, a, args.cpu_seconds)
 
+    dtypes = {m.dtype for m in w.models}
     out = {
         "metric": METRIC, "value": round(value, 1), "unit": "examples/s", "n_gpus": 1, "steps": args.steps,
         "warmup": args.warmup, "ms_per_step": round(ms_per_step, 3), "higher_is_better": True, "scaling": "weak",
-        "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
-        "config": {"workload": "ranking: 26 Zipf(1.1) embedding bags over 100k x 64 bf16 tables + 13 dense -> "
-                               "MLP 1677-1024-512-256-1 (ReLU, sigmoid), bf16 weights, fp32 accumulation; "
-                               "100k requests of 1-64 examples; max batch 512, allowed {64,128,256,512}",
-                   "requests_per_step": t.n, "examples_per_step": examples, "batches_per_step": n_batches,
-                   "window_batches": args.window, "parallelism": "single GPU"},
+        "vs_baseline": None, "dtype": dtypes.pop() if len(dtypes) == 1 else "bf16+f32", "data": "synthetic",
+        "config": {"workload": DESCRIPTION[w.name], "requests_per_step": t.n, "examples_per_step": examples,
+                   "batches_per_step": n_batches, "window_batches": args.window, "parallelism": "single GPU"},
         "latency": latency,
         "p50_us": None if latency is None else latency["rho0.9"]["p50_us"],
         "p99_us": None if latency is None else latency["rho0.9"]["p99_us"],

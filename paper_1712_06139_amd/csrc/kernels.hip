@@ -710,16 +710,26 @@ __global__ __launch_bounds__(256) void k_seqpool(const rb_k_row* __restrict__ ro
   }
 }
 
-__global__ __launch_bounds__(256) void k_split(const rb_k_row* __restrict__ rows, int n,
+// Split: TPR threads per row, 256 / TPR rows per workgroup. With V = 4 a row
+// whose output offset is a multiple of 4 floats is copied with 16-byte loads
+// and stores (Y rows always are; output rows of a mixed-width arena may not
+// be, and those take the scalar path).
+template <int V>
+__global__ __launch_bounds__(256) void k_split(const rb_k_row* __restrict__ rows, int n, int tpr,
                                                const float* __restrict__ Y, int ldy, int d_out,
                                                float* __restrict__ out) {
-  const int64_t gid = (int64_t)blockIdx.x * 256 + threadIdx.x;
-  const int64_t r = gid / d_out;
+  const int rpb = 256 / tpr;
+  const int r = blockIdx.x * rpb + threadIdx.x / tpr;
   if (r >= n) return;
-  const int c = (int)(gid - r * d_out);
   const int64_t o = rows[r].out;
   if (o < 0) return;
-  out[o + c] = Y[r * ldy + c];
+  const float* y = Y + (int64_t)r * ldy;
+  const int t = threadIdx.x % tpr;
+  if (V == 4 && (o & 3) == 0) {
+    for (int c = t * 4; c < d_out; c += tpr * 4) *(float4*)(out + o + c) = *(const float4*)(y + c);
+  } else {
+    for (int c = t; c < d_out; c += tpr) out[o + c] = y[c];
+  }
 }
 
 inline rb_status launch_status() {
@@ -884,8 +894,18 @@ rb_status rb_k_split(void* stream, const rb_k_row* rows, int32_t n_rows_total, c
                      int32_t d_out, float* out) {
   if (n_rows_total < 0 || d_out < 1 || ldy < d_out || !rows || !Y || !out) return RB_EINVAL;
   if (n_rows_total == 0) return RB_OK;
-  hipLaunchKernelGGL(k_split, dim3(blocks_for((int64_t)n_rows_total * d_out)), dim3(256), 0, (hipStream_t)stream,
-                     rows, n_rows_total, Y, ldy, d_out, out);
+  // 16-byte path: width, row stride and both bases multiples of 4 floats
+  const bool v4 = (d_out % 4) == 0 && (ldy % 4) == 0 && ((uintptr_t)Y % 16) == 0 && ((uintptr_t)out % 16) == 0;
+  const int per = v4 ? d_out / 4 : d_out;
+  int tpr = 1;
+  while (tpr < per && tpr < 256) tpr <<= 1;
+  const unsigned g = (unsigned)((n_rows_total + 256 / tpr - 1) / (256 / tpr));
+  if (v4)
+    hipLaunchKernelGGL(k_split<4>, dim3(g), dim3(256), 0, (hipStream_t)stream, rows, n_rows_total, tpr, Y, ldy,
+                       d_out, out);
+  else
+    hipLaunchKernelGGL(k_split<1>, dim3(g), dim3(256), 0, (hipStream_t)stream, rows, n_rows_total, tpr, Y, ldy,
+                       d_out, out);
   return launch_status();
 }
 

@@ -400,6 +400,10 @@ int64_t group_rows(const rb_model* m, const rb_queue* q, int64_t slots) {
 rb_status ensure_work(rb_sched* s, rb_model* m, int64_t rows, int64_t slots, Work** out) {
   Work& w = s->work[m->id];
   if (rows > w.rows_cap || slots > w.slots_cap) {
+    // capacities only grow (both at once), so groups of different shapes
+    // never make the buffers shrink and grow back
+    const int64_t R = std::max<int64_t>({rows, w.rows_cap, 64});
+    const int64_t S = std::max<int64_t>({slots, w.slots_cap, 64});
     hipStreamSynchronize(s->stream);
     hipFree(w.X);
     hipFree(w.A);
@@ -407,8 +411,6 @@ rb_status ensure_work(rb_sched* s, rb_model* m, int64_t rows, int64_t slots, Wor
     hipFree(w.Y);
     hipFree(w.rows);
     w = Work{};
-    const int64_t R = std::max<int64_t>(rows, 64);
-    const int64_t S = std::max<int64_t>(slots, 64);
     const size_t elt = m->dtype == RB_DT_BF16 ? 2 : 4;
     int maxN = 0;
     for (const DevLayer& L : m->layers) maxN = std::max(maxN, L.Np);

@@ -329,3 +329,25 @@ def test_seqpool_matches_oracle():
         pooled = nx.round_f32(np.sum(H[s * T:s * T + L[s]].astype(np.float64), axis=0) / L[s])
         ref = nx.round_f32(nx.softmax(nx.round_f32(nx.dense(pooled[None], Wh, bh, "none"))))[0]
         assert np.max(np.abs(o[s] - ref)) <= 1e-5 * np.max(np.abs(ref)), s
+
+
+@pytest.mark.parametrize("d_out,ldy", [(64, 64), (4096, 4096), (32, 64), (7, 8)])
+def test_split_vector_and_scalar_paths(d_out, ldy):
+    # output offsets mix multiples of 4 floats (16-byte path) and others
+    rng = np.random.default_rng(8)
+    R = 257
+    gaps = rng.integers(0, 3, size=R)
+    off = np.cumsum(np.concatenate([[0], (d_out + gaps)[:-1]]))
+    out_idx = np.where(rng.random(R) < 0.9, off, -1)
+    rows = _rows_dev(np.zeros(R), np.zeros(R), out_idx)
+    Y = rng.standard_normal((R, ldy)).astype(np.float32)
+    Yd = _dev(Y)
+    out = torch.full((int(off[-1]) + d_out + 8,), -7.0, device=DEV)
+    rb.check(rb.lib().rb_k_split(_stream(), rb.dptr(rows), R, rb.dptr(Yd), ldy, d_out, rb.dptr(out)), "split")
+    torch.cuda.synchronize()
+    o = out.cpu().numpy()
+    want = np.full_like(o, -7.0)
+    for r in range(R):
+        if out_idx[r] >= 0:
+            want[out_idx[r]:out_idx[r] + d_out] = Y[r, :d_out]
+    assert np.array_equal(o, want)
