@@ -328,11 +328,13 @@ rb_status rb_k_assemble(void* stream, const rb_k_row* rows, int32_t n_rows_total
                         int32_t out_bf16, float pad, int32_t* err);
 /* Ranking input: X[r] = [bf16(sum of bag f of row r from table f), f = 0..n_tables-1 |
  * bf16(dense) | 0 ...] with row stride ldx; tables: n_tables device pointers
- * (in a device array) to [table_rows, emb_dim] bf16. emb_dim must be 64. */
+ * (in a device array) to [table_rows, emb_dim] bf16. emb_dim must be 64,
+ * n_dense <= 256. ids_len is the length of the ids arena (reads stay below it).
+ * An id outside its table sets *err = 1 and contributes nothing. */
 rb_status rb_k_embbag(void* stream, const rb_k_row* rows, int32_t n_rows_total, const int32_t* lens,
-                      const int32_t* ids, const void* const* tables, int32_t n_tables, int64_t table_rows,
-                      int32_t emb_dim, const float* dense, int32_t n_dense, void* X, int32_t ldx,
-                      float pad, int32_t* err);
+                      const int32_t* ids, int64_t ids_len, const void* const* tables, int32_t n_tables,
+                      int64_t table_rows, int32_t emb_dim, const float* dense, int32_t n_dense, void* X,
+                      int32_t ldx, float pad, int32_t* err);
 /* Y[M, N] = act(X[M, K] W[N, K]^T + b), bf16 X and W (row strides ldx, ldw),
  * fp32 accumulation; Y bf16 (out_f32 == 0) or fp32, row stride ldy. K % 64 == 0,
  * N % 64 == 0. act: RB_ACT_NONE or RB_ACT_RELU. */

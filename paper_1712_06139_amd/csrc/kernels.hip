@@ -279,20 +279,29 @@ __global__ __launch_bounds__(256) void k_assemble(const rb_k_row* __restrict__ r
 
 constexpr int EMB_DIM = 64;       // one table row = 128 bytes of bf16
 constexpr int MAX_TABLES = 64;
-constexpr int STAGE_IDS = 2048;   // ids of one row staged in LDS (more: read from global)
+constexpr int STAGE_IDS = 384;    // ids of one row staged in LDS (more: read from global)
 
 constexpr int EMB_UNROLL = 4;     // gathers in flight per lane
+constexpr int EMB_GROUPS = 32;    // 8-lane groups per workgroup
 
-// One workgroup (4 waves = 32 groups of 8 lanes) per row. The row's bag
-// lengths are scanned in LDS and its ids staged in LDS with coalesced loads.
-// Group g pools bags g, g + 32, ...: its 8 lanes each own 16 bytes (8 dims)
-// of the 128-byte table row and walk the bag's ids in order, EMB_UNROLL
-// gathers in flight at a time, summing in fp32 (a fixed order: deterministic
-// per row). The sum is rounded to bf16 and stored as one 128-byte segment.
-// The dense features follow the pooled bags; columns past them are zero.
+// One workgroup (4 waves = 32 groups of 8 lanes) per row.
+//  1. One round trip: the bag lengths (scanned in LDS), the dense features and,
+//     speculatively, the first STAGE_IDS ids from the row's first id onwards
+//     (clamped to the ids arena) into LDS.
+//  2. The row's ids, flattened bag after bag, are cut into 32 equal segments,
+//     one per group (so a long bag no longer holds the row back). Group g walks
+//     its segment EMB_UNROLL gathers at a time, its 8 lanes each owning 16
+//     bytes (8 dims) of the 128-byte table row, and keeps an fp32 running sum
+//     that it writes to LDS slot (bag + g) whenever the segment leaves a bag
+//     (a bag + segment pair is a piece; pieces in flat order have distinct
+//     slots because bag and group both grow along the flat order).
+//  3. Group f adds bag f's pieces in group order (a fixed order: the result
+//     is deterministic and depends on this row only), rounds to bf16 and
+//     stores one 128-byte segment. The dense features follow; columns past
+//     them are zero.
 __global__ __launch_bounds__(256) void k_embbag(const rb_k_row* __restrict__ rows,
                                                 const int32_t* __restrict__ lens,
-                                                const int32_t* __restrict__ ids,
+                                                const int32_t* __restrict__ ids, int64_t ids_len,
                                                 const bf16_t* const* __restrict__ tables, int n_tables,
                                                 int64_t table_rows, const float* __restrict__ dense,
                                                 int n_dense, bf16_t* __restrict__ X, int ldx, float pad,
@@ -307,54 +316,98 @@ __global__ __launch_bounds__(256) void k_embbag(const rb_k_row* __restrict__ row
     for (int c = tid; c < ldx; c += 256) xr[c] = c < demb + n_dense ? p : (bf16_t)0;
     return;
   }
-  __shared__ int s_len[MAX_TABLES];
-  __shared__ int s_start[MAX_TABLES + 1];
   __shared__ int s_ids[STAGE_IDS];
-  if (tid < n_tables) s_len[tid] = rw.lens >= 0 ? lens[rw.lens + tid] : 0;
-  __syncthreads();
+  __shared__ int s_incl[MAX_TABLES];                  // inclusive prefix of bag lengths
+  __shared__ const bf16_t* s_tab[MAX_TABLES];
+  extern __shared__ float s_part[];                   // [n_tables + EMB_GROUPS][64] piece sums
+  // 1. lengths, dense, speculative id stage
   if (tid < 64) {
-    // wave-level exclusive scan of the bag lengths
-    int v = tid < n_tables ? s_len[tid] : 0;
+    const int v = (tid < n_tables && rw.lens >= 0) ? lens[rw.lens + tid] : 0;
     int incl = v;
     for (int o = 1; o < 64; o <<= 1) {
-      int u = __shfl_up(incl, o);
+      const int u = __shfl_up(incl, o);
       if (tid >= o) incl += u;
     }
-    if (tid < n_tables) s_start[tid] = incl - v;
-    if (tid == 63) s_start[n_tables] = incl;
+    if (tid < n_tables) s_incl[tid] = incl;
   }
+  if (tid >= 64 && tid - 64 < n_tables) s_tab[tid - 64] = tables[tid - 64];
+  const int64_t stage_n = min((int64_t)STAGE_IDS, ids_len - rw.aux);
+  for (int i = tid; i < stage_n; i += 256) s_ids[i] = ids[rw.aux + i];
+  float dv = 0.f;
+  if (tid < n_dense) dv = dense[rw.src + tid];
   __syncthreads();
-  const int total = s_start[n_tables];
-  const bool staged = total <= STAGE_IDS;
-  if (staged)
-    for (int i = tid; i < total; i += 256) s_ids[i] = ids[rw.aux + i];
-  __syncthreads();
+  const int total = s_incl[n_tables - 1];
   const int g = tid >> 3, l8 = tid & 7;
-  for (int f = g; f < n_tables; f += 32) {
+  // 2. balanced segments of the flat id list. The bag of the next position
+  // only needs an LDS read when the segment crosses a bag end, so the ids and
+  // table pointers of one round come from LDS together and its gathers issue
+  // back to back.
+  const int a = (int)((int64_t)total * g / EMB_GROUPS), b = (int)((int64_t)total * (g + 1) / EMB_GROUPS);
+  if (a < b) {
+    int f = 0;
+    while (s_incl[f] <= a) ++f;  // bag holding flat position a
+    int f_end = s_incl[f];       // flat end of bag f
+    int cur = f;                 // bag of the piece held in acc
     float acc[8];
 #pragma unroll
     for (int k = 0; k < 8; ++k) acc[k] = 0.f;
-    const bf16_t* T = tables[f] + l8 * 8;
-    const int st = s_start[f], len = s_len[f];
-    for (int j = 0; j < len; j += EMB_UNROLL) {
+    for (int p = a; p < b; p += EMB_UNROLL) {
       u32x4_t q[EMB_UNROLL];
+      int fb[EMB_UNROLL];
 #pragma unroll
       for (int u = 0; u < EMB_UNROLL; ++u) {
+        const int k = p + u;
         q[u] = (u32x4_t){0u, 0u, 0u, 0u};
-        if (j + u < len) {
-          const int id = staged ? s_ids[st + j + u] : ids[rw.aux + st + j + u];
+        fb[u] = f;
+        if (k < b) {
+          while (k >= f_end) f_end = s_incl[++f];  // ends because k < total
+          fb[u] = f;
+          const int id = k < stage_n ? s_ids[k] : ids[rw.aux + k];
           if ((uint64_t)(int64_t)id < (uint64_t)table_rows)
-            q[u] = *(const u32x4_t*)(T + (int64_t)id * EMB_DIM);
+            q[u] = *(const u32x4_t*)(s_tab[f] + l8 * 8 + (int64_t)id * EMB_DIM);
           else
             *err = 1;
         }
       }
 #pragma unroll
       for (int u = 0; u < EMB_UNROLL; ++u) {
-        acc[0] += bf2f(q[u].x & 0xffffu); acc[1] += bf2f(q[u].x >> 16);
-        acc[2] += bf2f(q[u].y & 0xffffu); acc[3] += bf2f(q[u].y >> 16);
-        acc[4] += bf2f(q[u].z & 0xffffu); acc[5] += bf2f(q[u].z >> 16);
-        acc[6] += bf2f(q[u].w & 0xffffu); acc[7] += bf2f(q[u].w >> 16);
+        if (p + u < b) {
+          if (fb[u] != cur) {  // the segment left bag cur: store its piece
+            float* dst = s_part + (cur + g) * 64 + l8 * 8;
+#pragma unroll
+            for (int k = 0; k < 8; ++k) {
+              dst[k] = acc[k];
+              acc[k] = 0.f;
+            }
+            cur = fb[u];
+          }
+          acc[0] += bf2f(q[u].x & 0xffffu); acc[1] += bf2f(q[u].x >> 16);
+          acc[2] += bf2f(q[u].y & 0xffffu); acc[3] += bf2f(q[u].y >> 16);
+          acc[4] += bf2f(q[u].z & 0xffffu); acc[5] += bf2f(q[u].z >> 16);
+          acc[6] += bf2f(q[u].w & 0xffffu); acc[7] += bf2f(q[u].w >> 16);
+        }
+      }
+    }
+    float* dst = s_part + (cur + g) * 64 + l8 * 8;
+#pragma unroll
+    for (int k = 0; k < 8; ++k) dst[k] = acc[k];
+  }
+  __syncthreads();
+  // 3. bag f = pieces of groups seg(start) .. seg(end - 1), in group order
+  for (int f = g; f < n_tables; f += EMB_GROUPS) {
+    const int end = s_incl[f], start = f ? s_incl[f - 1] : 0;
+    float acc[8];
+#pragma unroll
+    for (int k = 0; k < 8; ++k) acc[k] = 0.f;
+    if (end > start) {
+      const int g0 = (int)(((int64_t)(start + 1) * EMB_GROUPS - 1) / total);
+      const int g1 = (int)(((int64_t)end * EMB_GROUPS - 1) / total);
+      for (int h = g0; h <= g1; ++h) {
+        // groups with an empty segment (rows with fewer than 32 ids) wrote nothing
+        if ((int64_t)total * h / EMB_GROUPS == (int64_t)total * (h + 1) / EMB_GROUPS) continue;
+        const float* src = s_part + (f + h) * 64 + l8 * 8;
+#pragma unroll
+        for (int k = 0; k < 8; ++k) acc[k] += src[k];
       }
     }
     u32x4_t o;
@@ -364,8 +417,8 @@ __global__ __launch_bounds__(256) void k_embbag(const rb_k_row* __restrict__ row
     o.w = pack2(acc[6], acc[7]);
     *(u32x4_t*)(xr + f * EMB_DIM + l8 * 8) = o;
   }
-  for (int c = demb + tid; c < ldx; c += 256)
-    xr[c] = c < demb + n_dense ? f2bf(dense[rw.src + (c - demb)]) : (bf16_t)0;
+  if (tid < n_dense) xr[demb + tid] = f2bf(dv);
+  for (int c = demb + n_dense + tid; c < ldx; c += 256) xr[c] = (bf16_t)0;
 }
 
 // ---------------------------------------------------------------- bf16 GEMM
@@ -797,15 +850,17 @@ rb_status rb_k_assemble(void* stream, const rb_k_row* rows, int32_t n_rows_total
 }
 
 rb_status rb_k_embbag(void* stream, const rb_k_row* rows, int32_t n_rows_total, const int32_t* lens,
-                      const int32_t* ids, const void* const* tables, int32_t n_tables, int64_t table_rows,
-                      int32_t emb_dim, const float* dense, int32_t n_dense, void* X, int32_t ldx, float pad,
-                      int32_t* err) {
-  if (emb_dim != EMB_DIM || n_tables < 1 || n_tables > MAX_TABLES || n_dense < 0 || table_rows < 1)
+                      const int32_t* ids, int64_t ids_len, const void* const* tables, int32_t n_tables,
+                      int64_t table_rows, int32_t emb_dim, const float* dense, int32_t n_dense, void* X, int32_t ldx,
+                      float pad, int32_t* err) {
+  if (emb_dim != EMB_DIM || n_tables < 1 || n_tables > MAX_TABLES || n_dense < 0 || n_dense > 256 ||
+      table_rows < 1 || ids_len < 0)
     return RB_EINVAL;
   if (n_rows_total < 0 || ldx < n_tables * EMB_DIM + n_dense || (ldx & 7) || !rows || !X || !err || !tables)
     return RB_EINVAL;
   if (n_rows_total == 0) return RB_OK;
-  hipLaunchKernelGGL(k_embbag, dim3(n_rows_total), dim3(256), 0, (hipStream_t)stream, rows, lens, ids,
+  const size_t part_bytes = (size_t)(n_tables + EMB_GROUPS) * 64 * sizeof(float);
+  hipLaunchKernelGGL(k_embbag, dim3(n_rows_total), dim3(256), part_bytes, (hipStream_t)stream, rows, lens, ids, ids_len,
                      (const bf16_t* const*)tables, n_tables, table_rows, dense, n_dense, (bf16_t*)X, ldx, pad,
                      err);
   return launch_status();

@@ -207,6 +207,7 @@ struct rb_sched {
   int64_t a_dense_len = 0;
   const int32_t* a_lens = nullptr;
   const int32_t* a_ids = nullptr;
+  int64_t a_ids_len = 0;
   float* a_out = nullptr;
   // profiling
   std::vector<Prof> prof_pending;
@@ -429,7 +430,8 @@ rb_status ensure_work(rb_sched* s, rb_model* m, int64_t rows, int64_t slots, Wor
 
 // Launch chain of one group: route -> assemble | embbag -> layers -> head | seqpool | split.
 rb_status run_group(rb_sched* s, const Group& g, const rb_k_batch* d_batches, const rb_k_req* d_reqs,
-                    const float* dense, int64_t dense_len, const int32_t* lens, const int32_t* ids, float* out) {
+                    const float* dense, int64_t dense_len, const int32_t* lens, const int32_t* ids, int64_t ids_len,
+                    float* out) {
   rb_model* m = g.q->m;
   const int64_t slots = g.slots;
   const int64_t M = group_rows(m, g.q, slots);
@@ -444,7 +446,7 @@ rb_status run_group(rb_sched* s, const Group& g, const rb_k_batch* d_batches, co
   const bool bf16 = m->dtype == RB_DT_BF16;
   const int Kp0 = m->layers[0].Kp;
   if (m->kind == RB_MODEL_RANKING) {
-    RB_LAUNCH(s, "embbag", rb_k_embbag(hs, w->rows, (int)slots, lens, ids, (const void* const*)m->tables_dev,
+    RB_LAUNCH(s, "embbag", rb_k_embbag(hs, w->rows, (int)slots, lens, ids, ids_len, (const void* const*)m->tables_dev,
                                        m->n_tables, m->table_rows, m->emb_dim, dense, m->n_dense, w->X, Kp0, pad,
                                        s->err_dev));
   } else {
@@ -554,7 +556,7 @@ rb_status flush_chunk(rb_sched* s) {
   for (auto& win : s->chunk)
     for (Group& g : win) {
       st = run_group(s, g, (const rb_k_batch*)(sl->dev + offs[gi].first), (const rb_k_req*)(sl->dev + offs[gi].second),
-                     s->a_dense, s->a_dense_len, s->a_lens, s->a_ids, s->a_out);
+                     s->a_dense, s->a_dense_len, s->a_lens, s->a_ids, s->a_ids_len, s->a_out);
       ++gi;
       if (st != RB_OK) return st;
     }
@@ -1067,7 +1069,7 @@ static rb_status run_serving_batch(rb_sched* s, rb_queue* q, const Batch& b) {
   float* dout = (float*)(sl->dev + o_out);
   st = run_group(s, g, (const rb_k_batch*)(sl->dev + o_batch), (const rb_k_req*)(sl->dev + o_reqs),
                  (const float*)(sl->dev + o_dense), nd, (const int32_t*)(sl->dev + o_lens),
-                 (const int32_t*)(sl->dev + o_ids), dout);
+                 (const int32_t*)(sl->dev + o_ids), ni, dout);
   if (st != RB_OK) return st;
   if (!hip_ok(hipMemcpyAsync(sl->host_out, dout, (size_t)no * 4, hipMemcpyDeviceToHost, s->stream)))
     return RB_EDEVICE;
@@ -1195,6 +1197,7 @@ rb_status rb_sim_run(rb_sched* s, const rb_servable* sv, int32_t n_sv, const rb_
     s->a_dense_len = N > 0 ? tr->dense_off[N] : 0;
     s->a_lens = tr->lens;
     s->a_ids = tr->ids;
+    s->a_ids_len = (N > 0 && tr->ids_off) ? tr->ids_off[N] : 0;
     s->a_out = tr->out;
   }
   // a replay runs on its own simulated clock, starting idle

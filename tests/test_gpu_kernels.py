@@ -32,8 +32,9 @@ def _rows_np(t):
     return t.cpu().numpy().view(np.uint8).view(rb.K_ROW_DTYPE)
 
 
-def _make_group(rng, kind, n_batches, B, allowed, d_in, d_out, n_tables=0, seq_T=0, max_n=None):
-    """Random batches of requests laid out like a trace arena."""
+def _make_group(rng, kind, n_batches, B, allowed, d_in, d_out, n_tables=0, seq_T=0, max_n=None, lens_gen=None):
+    """Random batches of requests laid out like a trace arena. lens_gen(rng,
+    n, n_tables) draws the bag lengths of ranking requests (default 0..20)."""
     max_n = max_n or B
     batches, reqs = [], []
     dense, lens, ids = [], [], []
@@ -52,7 +53,7 @@ def _make_group(rng, kind, n_batches, B, allowed, d_in, d_out, n_tables=0, seq_T
                 ii = np.zeros(0, np.int32)
             elif kind == rb.RB_MODEL_RANKING:
                 d = rng.standard_normal((n, d_in)).astype(np.float32)
-                ln = rng.integers(0, 21, size=(n, n_tables)).astype(np.int32)
+                ln = (lens_gen(rng, n, n_tables) if lens_gen else rng.integers(0, 21, size=(n, n_tables))).astype(np.int32)
                 ii = rng.integers(0, 1000, size=int(ln.sum())).astype(np.int32)
             else:
                 d = rng.standard_normal((n, d_in)).astype(np.float32)
@@ -172,11 +173,28 @@ def synth_payload(d):
     return Payload(d)
 
 
-def test_embbag_matches_oracle():
+def _lens_skewed(rng, n, nt):
+    # mostly empty bags, now and then one long bag (past the ids staged in LDS)
+    ln = rng.integers(0, 2, size=(n, nt)) * (rng.random((n, nt)) < 0.2)
+    long = rng.random(n) < 0.3
+    ln[long, rng.integers(0, nt, size=int(long.sum()))] = rng.integers(30, 700, size=int(long.sum()))
+    return ln
+
+
+_LENS = {
+    "uniform": None,                                            # 0..20 per bag
+    "tiny": lambda rng, n, nt: rng.integers(0, 2, size=(n, nt)),  # rows with fewer ids than lane groups
+    "skewed": _lens_skewed,
+    "all_empty": lambda rng, n, nt: np.zeros((n, nt), np.int64),
+}
+
+
+@pytest.mark.parametrize("lens", list(_LENS))
+def test_embbag_matches_oracle(lens):
     rng = np.random.default_rng(3)
     nt, rows_t = 26, 1000
     kb, kr, arena, R = _make_group(rng, rb.RB_MODEL_RANKING, 4, 512, (64, 128, 256, 512), 13, 1, nt, 0,
-                                   max_n=64)
+                                   max_n=64, lens_gen=_LENS[lens])
     rows, err = _route(rb.RB_MODEL_RANKING, kb, kr, arena, R, 13, 1, nt)
     tables = [(rng.standard_normal((rows_t, 64)) / 8).astype(np.float32) for _ in range(nt)]
     tb = [nx.round_bf16(t).astype(np.float32) for t in tables]
@@ -185,7 +203,7 @@ def test_embbag_matches_oracle():
     ldx = 1728
     X = torch.empty((R, ldx), dtype=torch.int16, device=DEV)
     dense, lens, ids = _dev(arena["dense"]), _dev(arena["lens"]), _dev(arena["ids"])
-    rb.check(rb.lib().rb_k_embbag(_stream(), rb.dptr(rows), R, rb.dptr(lens), rb.dptr(ids), rb.dptr(ptrs), nt,
+    rb.check(rb.lib().rb_k_embbag(_stream(), rb.dptr(rows), R, rb.dptr(lens), rb.dptr(ids), ids.numel(), rb.dptr(ptrs), nt,
                                   rows_t, 64, rb.dptr(dense), 13, rb.dptr(X), ldx, 0.0, rb.dptr(err)), "embbag")
     torch.cuda.synchronize()
     assert int(err.item()) == 0
@@ -196,6 +214,8 @@ def test_embbag_matches_oracle():
     m = Model(kind="ranking", dtype="bf16", seed_id=0, layers=(Layer(nt * 64 + 13, 1, "sigmoid"),),
               n_tables=nt, table_rows=rows_t, emb_dim=64, n_dense=13)
     om = OracleModel(m, Params([(np.zeros((1, nt * 64 + 13), np.float32), np.zeros(1, np.float32))], tables))
+    om_abs = OracleModel(m, Params([(np.zeros((1, nt * 64 + 13), np.float32), np.zeros(1, np.float32))],
+                                   [np.abs(t) for t in tb]))
     n_exact = n_tot = 0
     for r in range(R):
         rw = rmap[r]
@@ -207,9 +227,12 @@ def test_embbag_matches_oracle():
         dn = arena["dense"][rw["src"]:rw["src"] + 13]
         ref = om.ranking_input(dn[None, :], ln[None, :], ii)[0]
         g = got[r, :nt * 64 + 13].astype(np.float64)
-        # fp32 accumulation vs fp64: at most one bf16 ulp apart after rounding
+        # fp32 summation of n terms is within (n - 1) 2^-24 sum|x| of the exact
+        # sum (any order); bf16 rounding then adds at most one bf16 ulp
+        sabs = om_abs.ranking_input(dn[None, :], ln[None, :], ii)[0]
+        nterm = np.concatenate([np.repeat(np.maximum(ln - 1, 0), 64), np.zeros(13)])
         ulp = np.maximum(np.abs(ref), 2.0 ** -126) * 2.0 ** -7
-        assert np.all(np.abs(g - ref) <= ulp), r
+        assert np.all(np.abs(g - ref) <= ulp + 2.0 * nterm * 2.0 ** -24 * sabs), r
         assert np.all(got[r, nt * 64 + 13:] == 0)
         n_exact += int(np.sum(g == ref))
         n_tot += g.size
