@@ -34,6 +34,7 @@ typedef __attribute__((__vector_size__(8 * sizeof(short)))) short bf16x8_t;
 typedef __attribute__((__vector_size__(4 * sizeof(float)))) float floatx4_t;
 typedef __attribute__((__vector_size__(16 * sizeof(float)))) float floatx16_t;
 typedef unsigned int u32x4_t __attribute__((ext_vector_type(4)));
+typedef int i32x4_t __attribute__((ext_vector_type(4)));
 
 __device__ __forceinline__ bf16_t f2bf(float f) {
   // round to nearest even on the 16 dropped bits; NaN stays a (quiet) NaN
@@ -423,68 +424,112 @@ __global__ __launch_bounds__(256) void k_embbag(const rb_k_row* __restrict__ row
 
 // ---------------------------------------------------------------- bf16 GEMM
 
-// s_waitcnt vmcnt(N) with the other counters unconstrained (gfx9 encoding:
-// vmcnt[3:0], expcnt[6:4], lgkmcnt[11:8], vmcnt[5:4] in bits 15:14).
+// s_waitcnt vmcnt(N) lgkmcnt(0) (gfx9 encoding: vmcnt[3:0], expcnt[6:4],
+// lgkmcnt[11:8], vmcnt[5:4] in bits 15:14): at most N vector memory
+// operations of this wave in flight and every LDS read of it returned.
 template <int N>
-__device__ __forceinline__ void wait_vmcnt() {
+__device__ __forceinline__ void wait_vmcnt_lds() {
   static_assert(N >= 0 && N < 64, "vmcnt range");
-  __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (7 << 4) | (15 << 8));
+  __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (7 << 4));
 }
 
 template <int I>
 using ic = std::integral_constant<int, I>;
+
+// f(ic<0>{}), f(ic<1>{}), ..., f(ic<N - 1>{}), unrolled at compile time
+template <int... I, class F>
+__device__ __forceinline__ void for_each_ic(std::integer_sequence<int, I...>, F&& f) {
+  (f(ic<I>{}), ...);
+}
+template <int N, class F>
+__device__ __forceinline__ void static_for(F&& f) {
+  for_each_ic(std::make_integer_sequence<int, N>{}, f);
+}
 
 // LDS byte address of a __shared__ object.
 __device__ __forceinline__ uint32_t lds_addr(const void* p) {
   return (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) void*)p;
 }
 
-// One 16-byte-per-lane global -> LDS load (global_load_lds_dwordx4): lane l's
-// 16 bytes land at LDS byte lds + 16 l. Issued as inline assembly so that the
-// compiler does not add its own conservative waits for it: the kernel waits
-// with explicit vmcnt counts and a barrier before the data is read.
-__device__ __forceinline__ void load_to_lds(const void* g, uint32_t lds) {
-  asm volatile("s_mov_b32 m0, %0\n\tglobal_load_lds_dwordx4 %1, off" ::"s"(lds), "v"(g) : "memory", "m0");
+__device__ __forceinline__ void lds_barrier() { asm volatile("s_barrier" ::: "memory"); }
+
+// Buffer resource (gfx9 layout: base address, stride 0, no range limit) for
+// a wave-uniform base address.
+__device__ __forceinline__ i32x4_t buffer_rsrc(const void* base) {
+  const uint64_t p = (uint64_t)(uintptr_t)base;
+  i32x4_t r;
+  r.x = __builtin_amdgcn_readfirstlane((int)(uint32_t)p);
+  r.y = __builtin_amdgcn_readfirstlane((int)((uint32_t)(p >> 32) & 0xffffu));
+  r.z = -1;
+  r.w = 0x00020000;
+  return r;
 }
 
-__device__ __forceinline__ void lds_barrier() { asm volatile("s_barrier" ::: "memory"); }
+// One 16-byte-per-lane buffer -> LDS load (buffer_load_dwordx4 ... lds) of the
+// bytes at base + voff + soff: lane l's 16 bytes land at LDS byte lds + 16 l.
+// Issued as inline assembly so that the compiler does not add its own
+// conservative waits for it: the kernel waits with explicit vmcnt counts and
+// a barrier before the data is read.
+__device__ __forceinline__ void buffer_to_lds(i32x4_t rsrc, uint32_t voff, uint32_t soff, uint32_t lds) {
+  asm volatile("s_mov_b32 m0, %0\n\tbuffer_load_dwordx4 %1, %2, %3 offen lds" ::"s"(lds), "v"(voff), "s"(rsrc),
+               "s"(soff)
+               : "memory", "m0");
+}
 
 // Y = act(X W^T + b): X [M, K] and W [N, K] bf16, K contiguous; fp32
 // accumulation with v_mfma_f32_32x32x16_bf16.
 //
-// Workgroup tile BM x BN, k-step 64, NT/64 waves each owning a WM x WN
-// sub-tile ((WM/32) x (WN/32) accumulators). Operand tiles go straight from
-// global memory into a ring of S LDS stages (each wave load instruction fills
-// 1 KB = 8 rows of 128 bytes; no register staging), issued S-1 k-steps before
-// they are read. Per k-step: wait for this wave's loads of the stage, one
-// barrier (all waves' loads landed; the stage refilled next has been read by
-// everyone), read the first fragments, issue the loads S-1 steps ahead, then
-// the MFMAs with the next sub-step's LDS reads interleaved between them. The
-// 16-byte chunk c of row r sits at chunk c ^ ((r >> 1) & 7) of its LDS row, so
-// the 16 lanes served per LDS cycle hit 16 distinct bank groups (64 banks).
+// Workgroup tile BM x BN, k-step BK (32 or 64), NT/64 waves each owning a
+// WM x WN sub-tile ((WM/32) x (WN/32) accumulators). Operand tiles go straight
+// from global memory into a ring of S >= 3 LDS stages (global_load_lds: each
+// wave load instruction fills 1 KB of consecutive LDS rows of BK bf16; no
+// register staging). K-step kt reads stage kt % S while the stage of k-step
+// kt - 1 is refilled with k-step kt - 1 + S, its loads spread one every few
+// MFMAs over the step: issued back to back they stall the wave on the texture
+// path with no MFMA in flight. Each 16-deep sub-step's MFMAs have the next
+// sub-step's fragment reads between them. In the last sub-step, after half of
+// its MFMAs, the wave waits for its loads of the next k-step and for its LDS
+// reads, and all waves meet at one barrier: the next stage has landed and
+// nobody reads the current one again. The other half then runs with the next
+// k-step's first fragment reads between the MFMAs. The order of MFMAs, LDS
+// reads and loads within a step is fixed with scheduling barriers.
 //
-// Every tile shape, stage count and tile order accumulates each output
+// LDS rows hold BK/8 16-byte chunks; chunk c of row r sits at chunk
+// c ^ ((r / (16 / (BK/8))) % (BK/8)), so the 16 rows one fragment read serves
+// per LDS cycle hit 16 distinct bank groups (64 banks).
+//
+// Every tile shape, k-step, stage count and tile order accumulates each output
 // element in the same k order with the same instruction, so results do not
 // depend on them, nor on which rows share a tile.
-constexpr int G16_BK = 64;
-constexpr int G16_CPR = G16_BK / 8;   // 16-byte chunks per LDS row
-constexpr int G16_RPI = 64 / G16_CPR; // rows filled per wave load instruction
+constexpr int G16_KALIGN = 64;  // K multiple the entry point accepts
 
-template <int BM, int BN, int WM, int WN, int NT, int S, int ORDER, int ACT, bool OUT_F32>
+template <int BM, int BN, int WM, int WN, int NT, int MI, int BK, int S, int ORDER, int ACT, bool OUT_F32>
 __global__ __launch_bounds__(NT) void k_gemm_bf16(const bf16_t* __restrict__ X, int ldx,
                                                   const bf16_t* __restrict__ W, int ldw,
                                                   const float* __restrict__ bias, void* __restrict__ Y,
                                                   int ldy, int M, int N, int K) {
   constexpr int NW = NT / 64;
   static_assert((BM / WM) * (BN / WN) == NW, "one wave per sub-tile");
-  static_assert(S >= 2 && S <= 4, "2..4 stages");
-  constexpr int TM = WM / 32, TN = WN / 32;
-  constexpr int SA = BM / G16_RPI / NW, SB = BN / G16_RPI / NW;  // load instructions per wave per stage
-  static_assert(SA * NW * G16_RPI == BM && SB * NW * G16_RPI == BN, "loads cover the tile");
+  static_assert(BK == 32 || BK == 64, "k-step 32 or 64");
+  static_assert(S >= 3 && S <= 4, "3..4 stages");
+  constexpr int CPR = BK / 8;    // 16-byte chunks per LDS row
+  constexpr int RPI = 64 / CPR;  // rows filled per wave load instruction
+  constexpr int SWZ = 16 / CPR;  // rows sharing one swizzle pattern
+  static_assert(MI == 32 || MI == 16, "32x32x16 or 16x16x32 MFMA");
+  constexpr int KS = MI == 32 ? 16 : 32;  // k depth of one MFMA
+  constexpr int NREG = MI == 32 ? 16 : 4;  // accumulator registers per MFMA tile
+  using acc_t = std::conditional_t<MI == 32, floatx16_t, floatx4_t>;
+  constexpr int TM = WM / MI, TN = WN / MI;
+  static_assert(TM % 2 == 0, "the last sub-step splits the A fragments in halves");
+  constexpr int SA = BM / RPI / NW, SB = BN / RPI / NW;  // load instructions per wave per stage
+  static_assert(SA * NW * RPI == BM && SB * NW * RPI == BN, "loads cover the tile");
   constexpr int OPS = SA + SB;
-  constexpr int KK = G16_BK / 16;
-  __shared__ u32x4_t sA[S][BM * G16_CPR];
-  __shared__ u32x4_t sB[S][BN * G16_CPR];
+  constexpr int KK = BK / KS;    // MFMA sub-steps per k-step
+  constexpr int NM = TM * TN;    // MFMAs per sub-step
+  constexpr int NR = TM + TN;    // fragment reads per sub-step
+  constexpr int PRE = (KK - 1) * NM + NM / 2;  // MFMAs of a step before its barrier
+  __shared__ u32x4_t sA[S][BM * CPR];
+  __shared__ u32x4_t sB[S][BN * CPR];
 
   const int tid = threadIdx.x, lane = tid & 63;
   const int wid = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -494,109 +539,123 @@ __global__ __launch_bounds__(NT) void k_gemm_bf16(const bf16_t* __restrict__ X, 
   const int bm = tile / tiles_n, bn = tile - bm * tiles_n;
   const int m0 = bm * BM, n0 = bn * BN;
 
-  // lane l of a load instruction fills LDS row l / 8 (of its 8), chunk l % 8
-  const int lr = lane / G16_CPR, lc = lane % G16_CPR;
-  const bf16_t* ga[SA];
-  const bf16_t* gb[SB];
+  // lane l of a load instruction fills LDS row l / CPR (of its RPI), chunk l % CPR
+  const int lr = lane / CPR, lc = lane % CPR;
+  // byte offsets from the tile's first row (buffer resources based there; the
+  // k-step's byte offset goes in the scalar offset)
+  const i32x4_t rA = buffer_rsrc(X + (int64_t)m0 * ldx), rB = buffer_rsrc(W + (int64_t)n0 * ldw);
+  uint32_t va[SA], vb[SB];
 #pragma unroll
   for (int i = 0; i < SA; ++i) {
-    const int row = (wid * SA + i) * G16_RPI + lr;
-    int ra = m0 + row;
-    ra = ra < M ? ra : M - 1;  // rows past M are computed on a copy and never stored
-    ga[i] = X + (int64_t)ra * ldx + (lc ^ ((row >> 1) & 7)) * 8;
+    const int row = (wid * SA + i) * RPI + lr;
+    const int ra = min(row, M - 1 - m0);  // rows past M are computed on a copy and never stored
+    va[i] = (uint32_t)(ra * ldx + (lc ^ ((row / SWZ) % CPR)) * 8) * 2u;
   }
 #pragma unroll
   for (int i = 0; i < SB; ++i) {
-    const int row = (wid * SB + i) * G16_RPI + lr;
-    gb[i] = W + (int64_t)(n0 + row) * ldw + (lc ^ ((row >> 1) & 7)) * 8;
+    const int row = (wid * SB + i) * RPI + lr;
+    vb[i] = (uint32_t)(row * ldw + (lc ^ ((row / SWZ) % CPR)) * 8) * 2u;
   }
 
-  floatx16_t acc[TM][TN];
+  acc_t acc[TM][TN];
 #pragma unroll
   for (int i = 0; i < TM; ++i)
 #pragma unroll
     for (int j = 0; j < TN; ++j)
 #pragma unroll
-      for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
+      for (int r = 0; r < NREG; ++r) acc[i][j][r] = 0.f;
 
-  auto issue = [&](int kt, auto stc) {
-    constexpr int st = decltype(stc)::value;
-    const int k0 = kt * G16_BK;
-#pragma unroll
-    for (int i = 0; i < SA; ++i) load_to_lds(ga[i] + k0, lds_addr(&sA[st][0]) + (wid * SA + i) * 1024);
-#pragma unroll
-    for (int i = 0; i < SB; ++i) load_to_lds(gb[i] + k0, lds_addr(&sB[st][0]) + (wid * SB + i) * 1024);
-  };
-  auto read_frags = [&](auto stc, int kk, bf16x8_t* a, bf16x8_t* bv) {
-    constexpr int st = decltype(stc)::value;
-    const int ch = kk * 2 + (lane >> 5);
-#pragma unroll
-    for (int i = 0; i < TM; ++i) {
-      const int r = wm * WM + i * 32 + (lane & 31);
-      a[i] = __builtin_bit_cast(bf16x8_t, sA[st][r * G16_CPR + (ch ^ ((r >> 1) & 7))]);
-    }
-#pragma unroll
-    for (int j = 0; j < TN; ++j) {
-      const int r = wn * WN + j * 32 + (lane & 31);
-      bv[j] = __builtin_bit_cast(bf16x8_t, sB[st][r * G16_CPR + (ch ^ ((r >> 1) & 7))]);
-    }
-  };
-  const int nk = K / G16_BK;
-  auto step = [&](int kt, auto stc, auto nxt) {
-    const int ahead = min(nk - 1 - kt, S - 2);  // stages whose loads were issued after this one's
-    if (ahead >= 2)
-      wait_vmcnt<2 * OPS>();
-    else if (ahead == 1)
-      wait_vmcnt<OPS>();
+  const int nk = K / BK;
+  // load instruction o (A rows for o < SA, then B rows) of k-step kt into
+  // stage st. K-steps past the end reload the last one into a stage that is
+  // never read again, so every step runs the same branch-free code.
+  auto issue_one = [&](int kt, auto stc, auto oc) {
+    constexpr int st = decltype(stc)::value, o = decltype(oc)::value;
+    const uint32_t kb = (uint32_t)(min(kt, nk - 1) * BK) * 2u;
+    if constexpr (o < SA)
+      buffer_to_lds(rA, va[o], kb, lds_addr(&sA[st][0]) + (wid * SA + o) * 1024);
     else
-      wait_vmcnt<0>();
-    lds_barrier();
-    bf16x8_t fa[2][TM], fb[2][TN];
-    read_frags(stc, 0, fa[0], fb[0]);
-    if (kt + S - 1 < nk) issue(kt + S - 1, nxt);
-#pragma unroll
-    for (int kk = 0; kk < KK; ++kk) {
-      if (kk + 1 < KK) read_frags(stc, kk + 1, fa[(kk + 1) & 1], fb[(kk + 1) & 1]);
-#pragma unroll
-      for (int i = 0; i < TM; ++i)
-#pragma unroll
-        for (int j = 0; j < TN; ++j)
-          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[kk & 1][i], fb[kk & 1][j], acc[i][j], 0, 0, 0);
-      if (kk + 1 < KK) {
-        // one LDS read between consecutive MFMAs
-#pragma unroll
-        for (int q = 0; q < TM + TN; ++q) {
-          __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
-          __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
-        }
-      }
+      buffer_to_lds(rB, vb[o - SA], kb, lds_addr(&sB[st][0]) + (wid * SB + o - SA) * 1024);
+  };
+  bf16x8_t fa[2][TM], fb[2][TN];
+  // fragment read q (A fragment q for q < TM, then B) of sub-step kk of stage st
+  auto read_one = [&](auto stc, int kk, auto qc, auto bufc) {
+    constexpr int st = decltype(stc)::value, q = decltype(qc)::value, bf = decltype(bufc)::value;
+    // MFMA operand layout: lane l holds row l % MI, k = 8 (l / MI) .. + 7 of the sub-step
+    const int ch = kk * (KS / 8) + lane / MI;
+    if constexpr (q < TM) {
+      const int r = wm * WM + q * MI + lane % MI;
+      fa[bf][q] = __builtin_bit_cast(bf16x8_t, sA[st][r * CPR + (ch ^ ((r / SWZ) % CPR))]);
+    } else {
+      const int r = wn * WN + (q - TM) * MI + lane % MI;
+      fb[bf][q - TM] = __builtin_bit_cast(bf16x8_t, sB[st][r * CPR + (ch ^ ((r / SWZ) % CPR))]);
     }
   };
-  issue(0, ic<0>{});
-  if (S > 2 && 1 < nk) issue(1, ic<1 % S>{});
-  if (S > 3 && 2 < nk) issue(2, ic<2 % S>{});
+  // k-step kt: stage stc, next stage nstc, refilled stage rstc (k-step kt - 1's)
+  auto step = [&](int kt, auto stc, auto nstc, auto rstc) {
+    static_for<KK>([&](auto kkc) {
+      constexpr int kk = decltype(kkc)::value;
+      constexpr bool last = kk == KK - 1;
+      constexpr int cur = kk & 1, nxt = (kk + 1) & 1;
+      static_for<NM>([&](auto mc) {
+        constexpr int m = decltype(mc)::value;
+        if constexpr (last && m == NM / 2) {
+          wait_vmcnt_lds<(S - 2) * OPS>();
+          lds_barrier();
+        }
+        if constexpr (MI == 32)
+          acc[m / TN][m % TN] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[cur][m / TN], fb[cur][m % TN],
+                                                                        acc[m / TN][m % TN], 0, 0, 0);
+        else
+          acc[m / TN][m % TN] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(fa[cur][m / TN], fb[cur][m % TN],
+                                                                        acc[m / TN][m % TN], 0, 0, 0);
+        __builtin_amdgcn_sched_barrier(0);
+        static_for<NR>([&](auto qc) {
+          constexpr int q = decltype(qc)::value;
+          if constexpr (!last) {
+            if constexpr (q * NM / NR == m) read_one(stc, kk + 1, qc, ic<nxt>{});
+          } else if constexpr (m >= NM / 2) {
+            if constexpr (NM / 2 + q * (NM / 2) / NR == m) read_one(nstc, 0, qc, ic<0>{});
+          }
+        });
+        constexpr int pos = kk * NM + m;
+        static_for<OPS>([&](auto oc) {
+          constexpr int o = decltype(oc)::value;
+          if constexpr (o * PRE / OPS == pos) issue_one(kt - 1 + S, rstc, oc);
+        });
+        __builtin_amdgcn_sched_barrier(0);
+      });
+    });
+  };
+  static_for<S - 1>([&](auto sc) { static_for<OPS>([&](auto oc) { issue_one(decltype(sc)::value, sc, oc); }); });
+  wait_vmcnt_lds<(S - 2) * OPS>();
+  lds_barrier();
+  static_for<NR>([&](auto qc) { read_one(ic<0>{}, 0, qc, ic<0>{}); });
   int kt = 0;
   for (; kt + S <= nk; kt += S) {
-    step(kt, ic<0>{}, ic<(S - 1) % S>{});
-    step(kt + 1, ic<1 % S>{}, ic<S % S>{});
-    if (S > 2) step(kt + 2, ic<2 % S>{}, ic<(S + 1) % S>{});
-    if (S > 3) step(kt + 3, ic<3 % S>{}, ic<(S + 2) % S>{});
+    step(kt, ic<0>{}, ic<1>{}, ic<S - 1>{});
+    step(kt + 1, ic<1>{}, ic<2 % S>{}, ic<0>{});
+    step(kt + 2, ic<2>{}, ic<3 % S>{}, ic<1>{});
+    if constexpr (S > 3) step(kt + 3, ic<3>{}, ic<0>{}, ic<2>{});
   }
-  if (kt < nk) step(kt, ic<0>{}, ic<(S - 1) % S>{});
-  if (S > 2 && kt + 1 < nk) step(kt + 1, ic<1 % S>{}, ic<S % S>{});
-  if (S > 3 && kt + 2 < nk) step(kt + 2, ic<2 % S>{}, ic<(S + 1) % S>{});
+  if (kt < nk) step(kt, ic<0>{}, ic<1>{}, ic<S - 1>{});
+  if (kt + 1 < nk) step(kt + 1, ic<1>{}, ic<2 % S>{}, ic<0>{});
+  if (S > 3 && kt + 2 < nk) step(kt + 2, ic<2>{}, ic<3 % S>{}, ic<1>{});
+  // no load into LDS may still be in flight when the wave ends
+  wait_vmcnt_lds<0>();
 
-  // accumulator (i, j) register r of lane l holds row 8*(r/4) + 4*(l/32) + r%4,
-  // column l%32 of its 32 x 32 block
+  // accumulator (i, j) register r of lane l holds column l % MI of its MI x MI
+  // block and row 8*(r/4) + 4*(l/32) + r%4 (32x32x16) or 4*(l/16) + r (16x16x32)
 #pragma unroll
   for (int j = 0; j < TN; ++j) {
-    const int col = n0 + wn * WN + j * 32 + (lane & 31);
+    const int col = n0 + wn * WN + j * MI + lane % MI;
     const float bb = bias[col];
 #pragma unroll
     for (int i = 0; i < TM; ++i)
 #pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const int row = m0 + wm * WM + i * 32 + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
+      for (int r = 0; r < NREG; ++r) {
+        const int rr = MI == 32 ? 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3) : 4 * (lane >> 4) + r;
+        const int row = m0 + wm * WM + i * MI + rr;
         if (row < M) {
           const float v = act_fn<ACT>(acc[i][j][r] + bb);
           if (OUT_F32)
@@ -795,13 +854,13 @@ inline unsigned blocks_for(int64_t threads) { return (unsigned)((threads + 255) 
 
 namespace {
 
-template <int BM, int BN, int WM, int WN, int NT, int S, int ORDER>
+template <int BM, int BN, int WM, int WN, int NT, int MI, int BK, int S, int ORDER>
 void launch_gemm_bf16(hipStream_t s, const bf16_t* x, int ldx, const bf16_t* w, int ldw, const float* b,
                              void* Y, int ldy, int M, int N, int K, int act, int out_f32) {
   const unsigned g = (unsigned)(((M + BM - 1) / BM) * (N / BN));
-#define RB_G16(A, F) \
-  hipLaunchKernelGGL((k_gemm_bf16<BM, BN, WM, WN, NT, S, ORDER, A, F>), dim3(g), dim3(NT), 0, s, x, ldx, w, ldw, b, Y, \
-                     ldy, M, N, K)
+#define RB_G16(A, F)                                                                                            \
+  hipLaunchKernelGGL((k_gemm_bf16<BM, BN, WM, WN, NT, MI, BK, S, ORDER, A, F>), dim3(g), dim3(NT), 0, s, x, ldx, w, \
+                     ldw, b, Y, ldy, M, N, K)
   if (out_f32) {
     if (act == RB_ACT_RELU) RB_G16(RB_ACT_RELU, true);
     else if (act == RB_ACT_SIGMOID) RB_G16(RB_ACT_SIGMOID, true);
@@ -868,34 +927,37 @@ rb_status rb_k_embbag(void* stream, const rb_k_row* rows, int32_t n_rows_total, 
 
 rb_status rb_k_gemm_bf16(void* stream, const void* X, int32_t ldx, const void* W, int32_t ldw, const float* b,
                          void* Y, int32_t ldy, int32_t M, int32_t N, int32_t K, int32_t act, int32_t out_f32) {
-  if (M < 0 || N <= 0 || K <= 0 || (N % 128) || (K % G16_BK) || ldx < K || ldw < K || ldy < N) return RB_EINVAL;
+  if (M < 0 || N <= 0 || K <= 0 || (N % 128) || (K % G16_KALIGN) || ldx < K || ldw < K || ldy < N) return RB_EINVAL;
   if ((ldx & 7) || (ldw & 7) || !X || !W || !b || !Y) return RB_EINVAL;
+  // operand byte offsets within a 256-row tile are 32-bit
+  if ((int64_t)ldx * 512 >= ((int64_t)1 << 31) || (int64_t)ldw * 512 >= ((int64_t)1 << 31)) return RB_EINVAL;
   if (act != RB_ACT_NONE && act != RB_ACT_RELU && act != RB_ACT_SIGMOID) return RB_EINVAL;
   if (M == 0) return RB_OK;
   hipStream_t s = (hipStream_t)stream;
   const bf16_t* x = (const bf16_t*)X;
   const bf16_t* w = (const bf16_t*)W;
-  // Tile shape, stage count and tile order only change speed: every choice
-  // accumulates each output in the same k order with the same instruction
-  // (identical bits). The largest tile that still gives every CU a tile:
-  // 256 x 256 (2 stages, 128 KB LDS), else 256 x 128 (3 stages, 144 KB), else
-  // 128 x 128 (4 stages, 128 KB). XCD-contiguous tile order when all of W fits
-  // in one XCD's L2 (each XCD then keeps its A row-blocks and W in its own
-  // L2); plain order otherwise (contiguous ranges would stream all of W
-  // through every XCD).
+  // Tile shape, k-step, stage count and tile order only change speed: every
+  // choice accumulates each output in the same k order with the same
+  // instruction (identical bits). The largest tile that still gives every CU a
+  // tile: 256 x 256 (8 waves of 64 x 128, k-step 32, 4 stages, 128 KB LDS),
+  // else 256 x 128 (8 waves of 64 x 64, k-step 64, 3 stages, 144 KB), else
+  // 128 x 128 (8 waves of 64 x 32, k-step 64, 4 stages, 128 KB). XCD-contiguous
+  // tile order when all of W fits in one XCD's L2 (each XCD then keeps its A
+  // row-blocks and W in its own L2); plain order otherwise (contiguous ranges
+  // would stream all of W through every XCD).
   const int64_t rows256 = (M + 255) / 256;
   const bool xcd = (int64_t)N * K * 2 <= (4 << 20);
-#define RB_PICK(BM, BN, WM, WN, S)                                                                        \
-  do {                                                                                                    \
-    if (xcd) launch_gemm_bf16<BM, BN, WM, WN, 512, S, 1>(s, x, ldx, w, ldw, b, Y, ldy, M, N, K, act, out_f32); \
-    else launch_gemm_bf16<BM, BN, WM, WN, 512, S, 0>(s, x, ldx, w, ldw, b, Y, ldy, M, N, K, act, out_f32);     \
+#define RB_PICK(BM, BN, WM, WN, NT, BK, S)                                                                        \
+  do {                                                                                                            \
+    if (xcd) launch_gemm_bf16<BM, BN, WM, WN, NT, 32, BK, S, 1>(s, x, ldx, w, ldw, b, Y, ldy, M, N, K, act, out_f32); \
+    else launch_gemm_bf16<BM, BN, WM, WN, NT, 32, BK, S, 0>(s, x, ldx, w, ldw, b, Y, ldy, M, N, K, act, out_f32);     \
   } while (0)
   if (N % 256 == 0 && rows256 * (N / 256) >= 256)
-    RB_PICK(256, 256, 64, 128, 2);
+    RB_PICK(256, 256, 64, 128, 512, 32, 4);
   else if (rows256 * (N / 128) >= 256)
-    RB_PICK(256, 128, 64, 64, 3);
+    RB_PICK(256, 128, 64, 64, 512, 64, 3);
   else
-    RB_PICK(128, 128, 64, 32, 4);
+    RB_PICK(128, 128, 64, 32, 512, 64, 4);
 #undef RB_PICK
   return launch_status();
 }
