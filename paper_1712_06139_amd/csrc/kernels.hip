@@ -503,7 +503,7 @@ __device__ __forceinline__ void buffer_to_lds(i32x4_t rsrc, uint32_t voff, uint3
 // depend on them, nor on which rows share a tile.
 constexpr int G16_KALIGN = 64;  // K multiple the entry point accepts
 
-template <int BM, int BN, int WM, int WN, int NT, int MI, int BK, int S, int ORDER, int ACT, bool OUT_F32>
+template <int BM, int BN, int WM, int WN, int NT, int BK, int S, int ORDER, int ACT, bool OUT_F32>
 __global__ __launch_bounds__(NT) void k_gemm_bf16(const bf16_t* __restrict__ X, int ldx,
                                                   const bf16_t* __restrict__ W, int ldw,
                                                   const float* __restrict__ bias, void* __restrict__ Y,
@@ -515,16 +515,12 @@ __global__ __launch_bounds__(NT) void k_gemm_bf16(const bf16_t* __restrict__ X, 
   constexpr int CPR = BK / 8;    // 16-byte chunks per LDS row
   constexpr int RPI = 64 / CPR;  // rows filled per wave load instruction
   constexpr int SWZ = 16 / CPR;  // rows sharing one swizzle pattern
-  static_assert(MI == 32 || MI == 16, "32x32x16 or 16x16x32 MFMA");
-  constexpr int KS = MI == 32 ? 16 : 32;  // k depth of one MFMA
-  constexpr int NREG = MI == 32 ? 16 : 4;  // accumulator registers per MFMA tile
-  using acc_t = std::conditional_t<MI == 32, floatx16_t, floatx4_t>;
-  constexpr int TM = WM / MI, TN = WN / MI;
+  constexpr int TM = WM / 32, TN = WN / 32;
   static_assert(TM % 2 == 0, "the last sub-step splits the A fragments in halves");
   constexpr int SA = BM / RPI / NW, SB = BN / RPI / NW;  // load instructions per wave per stage
   static_assert(SA * NW * RPI == BM && SB * NW * RPI == BN, "loads cover the tile");
   constexpr int OPS = SA + SB;
-  constexpr int KK = BK / KS;    // MFMA sub-steps per k-step
+  constexpr int KK = BK / 16;    // MFMA sub-steps per k-step
   constexpr int NM = TM * TN;    // MFMAs per sub-step
   constexpr int NR = TM + TN;    // fragment reads per sub-step
   constexpr int PRE = (KK - 1) * NM + NM / 2;  // MFMAs of a step before its barrier
@@ -557,13 +553,13 @@ __global__ __launch_bounds__(NT) void k_gemm_bf16(const bf16_t* __restrict__ X, 
     vb[i] = (uint32_t)(row * ldw + (lc ^ ((row / SWZ) % CPR)) * 8) * 2u;
   }
 
-  acc_t acc[TM][TN];
+  floatx16_t acc[TM][TN];
 #pragma unroll
   for (int i = 0; i < TM; ++i)
 #pragma unroll
     for (int j = 0; j < TN; ++j)
 #pragma unroll
-      for (int r = 0; r < NREG; ++r) acc[i][j][r] = 0.f;
+      for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
 
   const int nk = K / BK;
   // load instruction o (A rows for o < SA, then B rows) of k-step kt into
@@ -581,13 +577,13 @@ __global__ __launch_bounds__(NT) void k_gemm_bf16(const bf16_t* __restrict__ X, 
   // fragment read q (A fragment q for q < TM, then B) of sub-step kk of stage st
   auto read_one = [&](auto stc, int kk, auto qc, auto bufc) {
     constexpr int st = decltype(stc)::value, q = decltype(qc)::value, bf = decltype(bufc)::value;
-    // MFMA operand layout: lane l holds row l % MI, k = 8 (l / MI) .. + 7 of the sub-step
-    const int ch = kk * (KS / 8) + lane / MI;
+    // MFMA operand layout: lane l holds row l % 32, k = 8 (l / 32) .. + 7 of the sub-step
+    const int ch = kk * 2 + (lane >> 5);
     if constexpr (q < TM) {
-      const int r = wm * WM + q * MI + lane % MI;
+      const int r = wm * WM + q * 32 + (lane & 31);
       fa[bf][q] = __builtin_bit_cast(bf16x8_t, sA[st][r * CPR + (ch ^ ((r / SWZ) % CPR))]);
     } else {
-      const int r = wn * WN + (q - TM) * MI + lane % MI;
+      const int r = wn * WN + (q - TM) * 32 + (lane & 31);
       fb[bf][q - TM] = __builtin_bit_cast(bf16x8_t, sB[st][r * CPR + (ch ^ ((r / SWZ) % CPR))]);
     }
   };
@@ -603,12 +599,8 @@ __global__ __launch_bounds__(NT) void k_gemm_bf16(const bf16_t* __restrict__ X, 
           wait_vmcnt_lds<(S - 2) * OPS>();
           lds_barrier();
         }
-        if constexpr (MI == 32)
-          acc[m / TN][m % TN] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[cur][m / TN], fb[cur][m % TN],
-                                                                        acc[m / TN][m % TN], 0, 0, 0);
-        else
-          acc[m / TN][m % TN] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(fa[cur][m / TN], fb[cur][m % TN],
-                                                                        acc[m / TN][m % TN], 0, 0, 0);
+        acc[m / TN][m % TN] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[cur][m / TN], fb[cur][m % TN],
+                                                                      acc[m / TN][m % TN], 0, 0, 0);
         __builtin_amdgcn_sched_barrier(0);
         static_for<NR>([&](auto qc) {
           constexpr int q = decltype(qc)::value;
@@ -644,18 +636,17 @@ __global__ __launch_bounds__(NT) void k_gemm_bf16(const bf16_t* __restrict__ X, 
   // no load into LDS may still be in flight when the wave ends
   wait_vmcnt_lds<0>();
 
-  // accumulator (i, j) register r of lane l holds column l % MI of its MI x MI
-  // block and row 8*(r/4) + 4*(l/32) + r%4 (32x32x16) or 4*(l/16) + r (16x16x32)
+  // accumulator (i, j) register r of lane l holds row 8*(r/4) + 4*(l/32) + r%4,
+  // column l%32 of its 32 x 32 block
 #pragma unroll
   for (int j = 0; j < TN; ++j) {
-    const int col = n0 + wn * WN + j * MI + lane % MI;
+    const int col = n0 + wn * WN + j * 32 + (lane & 31);
     const float bb = bias[col];
 #pragma unroll
     for (int i = 0; i < TM; ++i)
 #pragma unroll
-      for (int r = 0; r < NREG; ++r) {
-        const int rr = MI == 32 ? 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3) : 4 * (lane >> 4) + r;
-        const int row = m0 + wm * WM + i * MI + rr;
+      for (int r = 0; r < 16; ++r) {
+        const int row = m0 + wm * WM + i * 32 + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
         if (row < M) {
           const float v = act_fn<ACT>(acc[i][j][r] + bb);
           if (OUT_F32)
@@ -854,12 +845,12 @@ inline unsigned blocks_for(int64_t threads) { return (unsigned)((threads + 255) 
 
 namespace {
 
-template <int BM, int BN, int WM, int WN, int NT, int MI, int BK, int S, int ORDER>
+template <int BM, int BN, int WM, int WN, int NT, int BK, int S, int ORDER>
 void launch_gemm_bf16(hipStream_t s, const bf16_t* x, int ldx, const bf16_t* w, int ldw, const float* b,
                              void* Y, int ldy, int M, int N, int K, int act, int out_f32) {
   const unsigned g = (unsigned)(((M + BM - 1) / BM) * (N / BN));
 #define RB_G16(A, F)                                                                                            \
-  hipLaunchKernelGGL((k_gemm_bf16<BM, BN, WM, WN, NT, MI, BK, S, ORDER, A, F>), dim3(g), dim3(NT), 0, s, x, ldx, w, \
+  hipLaunchKernelGGL((k_gemm_bf16<BM, BN, WM, WN, NT, BK, S, ORDER, A, F>), dim3(g), dim3(NT), 0, s, x, ldx, w, \
                      ldw, b, Y, ldy, M, N, K)
   if (out_f32) {
     if (act == RB_ACT_RELU) RB_G16(RB_ACT_RELU, true);
@@ -949,8 +940,8 @@ rb_status rb_k_gemm_bf16(void* stream, const void* X, int32_t ldx, const void* W
   const bool xcd = (int64_t)N * K * 2 <= (4 << 20);
 #define RB_PICK(BM, BN, WM, WN, NT, BK, S)                                                                        \
   do {                                                                                                            \
-    if (xcd) launch_gemm_bf16<BM, BN, WM, WN, NT, 32, BK, S, 1>(s, x, ldx, w, ldw, b, Y, ldy, M, N, K, act, out_f32); \
-    else launch_gemm_bf16<BM, BN, WM, WN, NT, 32, BK, S, 0>(s, x, ldx, w, ldw, b, Y, ldy, M, N, K, act, out_f32);     \
+    if (xcd) launch_gemm_bf16<BM, BN, WM, WN, NT, BK, S, 1>(s, x, ldx, w, ldw, b, Y, ldy, M, N, K, act, out_f32); \
+    else launch_gemm_bf16<BM, BN, WM, WN, NT, BK, S, 0>(s, x, ldx, w, ldw, b, Y, ldy, M, N, K, act, out_f32);     \
   } while (0)
   if (N % 256 == 0 && rows256 * (N / 256) >= 256)
     RB_PICK(256, 256, 64, 128, 512, 32, 4);
