@@ -65,8 +65,10 @@ def nearest_rank(v, q):
 
 def algorithmic_work(w, t, a, logd, qindex):
     """Algorithmic bytes / flops of one replay, per kernel. Real model
-    dimensions; padded rows (and padded tokens) count as rows, since the
-    method pads them and computes them."""
+    dimensions; padded rows count as rows, since the method pads them and
+    computes them. Sequence groups: padding tokens are not written by the
+    assembler and 64-token blocks of them are not computed by the GEMMs (the
+    pooling never reads them), so both count real tokens only."""
     work = collections.defaultdict(lambda: {"bytes": 0, "flops": 0})
     nb = logd["n_batches"]
     beg = logd["b_req_begin"][:nb + 1]
@@ -93,14 +95,17 @@ def algorithmic_work(w, t, a, logd, qindex):
             work["embbag"]["bytes"] += (P * row_desc + s * (m.n_tables * 4 + m.n_dense * 4)
                                         + int(n_ids[b]) * (4 + m.emb_dim * 2) + P * d * 2)
         else:
-            # real inputs read once; every padded row (token) written
-            work["assemble"]["bytes"] += (int(n_dense[b]) * 4 + M * m.d_in * (2 if bf16 else 4)
+            # real inputs read once; every padded row written (for sequences
+            # in 64-token buckets, the real tokens only)
+            Mw = int(n_dense[b]) // m.d_in if (m.kind == "seqpool" and T % 64 == 0) else M
+            work["assemble"]["bytes"] += (int(n_dense[b]) * 4 + Mw * m.d_in * (2 if bf16 else 4)
                                           + (P if m.kind == "seqpool" else M) * row_desc)
         layers = m.layers[:-1] if (m.kind == "ranking" and bf16 and m.layers[-1].fan_out == 1) else m.layers
         key = "gemm_bf16" if bf16 else "gemm_f32"
+        Mg = int(n_dense[b]) // m.d_in if m.kind == "seqpool" else M  # rows the layers must compute
         for L in layers:
-            work[key]["flops"] += 2 * M * L.fan_in * L.fan_out
-            work[key]["bytes"] += (M * L.fan_in + L.fan_in * L.fan_out + M * L.fan_out) * (2 if bf16 else 4)
+            work[key]["flops"] += 2 * Mg * L.fan_in * L.fan_out
+            work[key]["bytes"] += (Mg * L.fan_in + L.fan_in * L.fan_out + Mg * L.fan_out) * (2 if bf16 else 4)
         if m.kind == "ranking" and len(layers) < len(m.layers):
             last = m.layers[-1]
             work["head"]["bytes"] += P * row_desc + P * last.fan_in * 2 + last.fan_in * 2 + s * 4

@@ -322,10 +322,14 @@ rb_status rb_k_route(void* stream, int32_t kind, const rb_k_batch* batches, int3
                      int32_t n_tables, rb_k_row* rows, int32_t* err);
 /* Gather rows into X [n_rows_total, ldx] (ldx >= d_in, columns [d_in, ldx)
  * zeroed), padding rows set to pad; out_bf16 != 0 writes bf16 (RNE), else fp32.
- * Seqpool (seq_T > 0): row r*T + t is token t of sequence slot r (pad past L). */
+ * Seqpool (seq_T > 0): row r*T + t is token t of sequence slot r (pad past L).
+ * seq_real_only != 0 (seqpool, fp32 out, n_rows_total a multiple of seq_T):
+ * rows t >= L and every row of a padding slot are not written and keep
+ * whatever X held; every layer maps row i to row i alone and the pooling reads
+ * t < L only, so no value there reaches an output. */
 rb_status rb_k_assemble(void* stream, const rb_k_row* rows, int32_t n_rows_total, int32_t seq_T,
-                        const float* dense, int64_t dense_len, int32_t d_in, void* X, int32_t ldx,
-                        int32_t out_bf16, float pad, int32_t* err);
+                        int32_t seq_real_only, const float* dense, int64_t dense_len, int32_t d_in, void* X,
+                        int32_t ldx, int32_t out_bf16, float pad, int32_t* err);
 /* Ranking input: X[r] = [bf16(sum of bag f of row r from table f), f = 0..n_tables-1 |
  * bf16(dense) | 0 ...] with row stride ldx; tables: n_tables device pointers
  * (in a device array) to [table_rows, emb_dim] bf16. emb_dim must be 64,
@@ -335,22 +339,29 @@ rb_status rb_k_embbag(void* stream, const rb_k_row* rows, int32_t n_rows_total, 
                       const int32_t* ids, int64_t ids_len, const void* const* tables, int32_t n_tables,
                       int64_t table_rows, int32_t emb_dim, const float* dense, int32_t n_dense, void* X,
                       int32_t ldx, float pad, int32_t* err);
-/* Y[M, N] = act(X[M, K] W[N, K]^T + b), bf16 X and W (row strides ldx, ldw),
- * fp32 accumulation; Y bf16 (out_f32 == 0) or fp32, row stride ldy. K % 64 == 0,
- * N % 64 == 0. act: RB_ACT_NONE or RB_ACT_RELU. */
+/* Y[M, N] = act(X[M, K] W[N, K]^T + b), bf16 X and W (row strides ldx, ldw,
+ * ldx and ldw < 2^22), fp32 accumulation; Y bf16 (out_f32 == 0) or fp32, row
+ * stride ldy. K % 64 == 0, N % 128 == 0. act: RB_ACT_NONE, RB_ACT_RELU or
+ * RB_ACT_SIGMOID. */
 rb_status rb_k_gemm_bf16(void* stream, const void* X, int32_t ldx, const void* W, int32_t ldw,
                          const float* b, void* Y, int32_t ldy, int32_t M, int32_t N, int32_t K,
                          int32_t act, int32_t out_f32);
-/* fp32 variant (fp32 MFMA); same layout rules. */
+/* fp32 variant (fp32 MFMA): K % 32 == 0, N % 64 == 0. Optional tile skip for
+ * sequence groups: with skip_rows (the per-slot row map, aux = sequence length)
+ * X holds skip_T rows per slot (token t of slot e at row e*skip_T + t) and a
+ * 64-row block starting at token t of slot e is neither computed nor stored
+ * when t >= L_e or slot e is padding: it holds only padding tokens, which the
+ * pooling never reads. skip_T % 64 == 0; skip_rows NULL computes every row. */
 rb_status rb_k_gemm_f32(void* stream, const float* X, int32_t ldx, const float* W, int32_t ldw,
-                        const float* b, float* Y, int32_t ldy, int32_t M, int32_t N, int32_t K, int32_t act);
+                        const float* b, float* Y, int32_t ldy, int32_t M, int32_t N, int32_t K, int32_t act,
+                        const rb_k_row* skip_rows, int32_t skip_T);
 /* Narrow last layer fused with the split: out[rows[r].out] = act(H[r, :K] . w + b)
  * for real rows (act RB_ACT_SIGMOID or RB_ACT_NONE); H bf16 [n_rows_total, ldh],
  * w bf16 [K]. */
 rb_status rb_k_head(void* stream, const rb_k_row* rows, int32_t n_rows_total, const void* H, int32_t ldh,
                     const void* w, float b, int32_t K, int32_t act, float* out);
 /* Seqpool head fused with the split: per sequence slot r with L = rows[r].aux
- * real tokens, pooled = mean of H[r*T + t, :D] over t < L (fp32; tokens past L
+ * real tokens (clamped to [0, seq_T]), pooled = mean of H[r*T + t, :D] over t < L (fp32; tokens past L
  * are never read), then out[rows[r].out + j] = act(Wh pooled + bh)[j], j < n_out
  * (act RB_ACT_SOFTMAX or RB_ACT_NONE; D <= 1024, n_out <= 16). */
 rb_status rb_k_seqpool(void* stream, const rb_k_row* rows, int32_t n_seqs, int32_t seq_T, const float* H,

@@ -221,58 +221,132 @@ __global__ __launch_bounds__(256) void k_route(int kind, const rb_k_batch* __res
 // padded batch tensor. Padding rows (and padding tokens) get `pad` in their
 // d_in input columns; columns past d_in are always zero so that they add
 // nothing in the next contraction.
-template <bool BF16>
+// Real tokens only (sequence slots): workgroup (e, j) copies tokens
+// [16 j, 16 j + 16) of slot e that lie below its length L (8 columns per thread
+// and chunk, two chunks in flight, columns past d_in zeroed); blocks past L,
+// rows t >= L and padding slots are not written (8..64-token blocks and 1..4
+// chunks in flight measured no faster). lg_c = log2(ldx / 8) when that is a power of two,
+// else -1.
+constexpr int SEQ_TOK = 16, SEQ_U = 2;
+__global__ __launch_bounds__(256) void k_assemble_seq(const rb_k_row* __restrict__ rows, int T,
+                                                      const float* __restrict__ dense, int64_t dense_len, int d_in,
+                                                      float* __restrict__ X, int ldx, int* __restrict__ err,
+                                                      int lg_c) {
+  const rb_k_row rw = rows[blockIdx.x];
+  const int t0 = blockIdx.y * SEQ_TOK;
+  if (rw.src < 0 || t0 >= rw.aux) return;
+  const int64_t L = rw.aux;
+  if (L > T || rw.src + L * d_in > dense_len) {
+    if (threadIdx.x == 0) *err = 1;
+    return;
+  }
+  const int cpr = ldx >> 3;
+  const int n_tok = (int)min((int64_t)SEQ_TOK, L - t0);
+  const int total = n_tok * cpr;
+  const float* src = dense + rw.src + (int64_t)t0 * d_in;
+  float* xb = X + ((int64_t)blockIdx.x * T + t0) * ldx;
+  const bool vec = (d_in & 3) == 0 && (rw.src & 3) == 0;
+  // SEQ_U chunks per thread and step: all loads issued before the stores
+  for (int base = threadIdx.x; base < total; base += 256 * SEQ_U) {
+    float v[SEQ_U][8];
+#pragma unroll
+    for (int u = 0; u < SEQ_U; ++u) {
+      const int i = base + 256 * u;
+      if (i >= total) break;
+      const int t = lg_c >= 0 ? i >> lg_c : i / cpr;
+      const int c0 = (i - t * cpr) * 8;
+      const float* sr = src + (int64_t)t * d_in;
+      if (vec) {
+#pragma unroll
+        for (int h = 0; h < 8; h += 4) {
+          if (c0 + h < d_in) {
+            const float4 a = *(const float4*)(sr + c0 + h);
+            v[u][h] = a.x; v[u][h + 1] = a.y; v[u][h + 2] = a.z; v[u][h + 3] = a.w;
+          } else {
+            v[u][h] = v[u][h + 1] = v[u][h + 2] = v[u][h + 3] = 0.f;
+          }
+        }
+      } else {
+#pragma unroll
+        for (int j = 0; j < 8; ++j) v[u][j] = (c0 + j < d_in) ? sr[c0 + j] : 0.f;
+      }
+    }
+#pragma unroll
+    for (int u = 0; u < SEQ_U; ++u) {
+      const int i = base + 256 * u;
+      if (i >= total) break;
+      const int t = lg_c >= 0 ? i >> lg_c : i / cpr;
+      const int c0 = (i - t * cpr) * 8;
+      float* y = xb + (int64_t)t * ldx + c0;
+      *(float4*)y = make_float4(v[u][0], v[u][1], v[u][2], v[u][3]);
+      *(float4*)(y + 4) = make_float4(v[u][4], v[u][5], v[u][6], v[u][7]);
+    }
+  }
+}
+
+// One thread per 8 consecutive columns of one row (one 16-byte bf16 store or
+// two fp32 ones; 4 or 16 columns measured slower). POW2: ldx / 8 and seq_T
+// (when non-zero) are powers of two and the thread count fits 31 bits, so the
+// row, chunk and slot indices come from shifts (lg_c = log2(ldx / 8), lg_t =
+// log2(seq_T)); otherwise 64-bit division.
+template <bool BF16, bool POW2>
 __global__ __launch_bounds__(256) void k_assemble(const rb_k_row* __restrict__ rows, int n_rows_total,
                                                   int seq_T, const float* __restrict__ dense,
                                                   int64_t dense_len, int d_in, void* __restrict__ X,
-                                                  int ldx, float pad, int* __restrict__ err) {
-  const int chunks = ldx >> 3;
-  const int64_t gid = (int64_t)blockIdx.x * 256 + threadIdx.x;
-  const int64_t r = gid / chunks;
+                                                  int ldx, float pad, int* __restrict__ err, int lg_c, int lg_t) {
+  constexpr int E = 8;
+  const int chunks = ldx / E;
+  int64_t r;
+  int c0;
+  if (POW2) {
+    const uint32_t gid = blockIdx.x * 256u + threadIdx.x;
+    r = (int64_t)(gid >> lg_c);
+    c0 = (int)(gid & (uint32_t)(chunks - 1)) * E;
+  } else {
+    const int64_t gid = (int64_t)blockIdx.x * 256 + threadIdx.x;
+    r = gid / chunks;
+    c0 = (int)(gid - r * chunks) * E;
+  }
   if (r >= n_rows_total) return;
-  const int c0 = (int)(gid - r * chunks) * 8;
   int64_t src;
   if (seq_T > 0) {
-    const int64_t slot = r / seq_T;
+    const int64_t slot = POW2 ? (int64_t)((uint32_t)r >> lg_t) : r / seq_T;
     const int t = (int)(r - slot * seq_T);
     const rb_k_row rw = rows[slot];
     src = (rw.src >= 0 && t < rw.aux) ? rw.src + (int64_t)t * d_in : -1;
   } else {
     src = rows[r].src;
   }
-  float v[8];
+  float v[E];
   if (src < 0) {
 #pragma unroll
-    for (int j = 0; j < 8; ++j) v[j] = (c0 + j < d_in) ? pad : 0.f;
+    for (int j = 0; j < E; ++j) v[j] = (c0 + j < d_in) ? pad : 0.f;
   } else if (src + d_in > dense_len) {
     *err = 1;
 #pragma unroll
-    for (int j = 0; j < 8; ++j) v[j] = 0.f;
-  } else if ((d_in & 7) == 0 && (src & 3) == 0) {
-    if (c0 < d_in) {
-      const float4 a = *(const float4*)(dense + src + c0);
-      const float4 c = *(const float4*)(dense + src + c0 + 4);
-      v[0] = a.x; v[1] = a.y; v[2] = a.z; v[3] = a.w;
-      v[4] = c.x; v[5] = c.y; v[6] = c.z; v[7] = c.w;
-    } else {
+    for (int j = 0; j < E; ++j) v[j] = 0.f;
+  } else if ((d_in & 3) == 0 && (src & 3) == 0) {
 #pragma unroll
-      for (int j = 0; j < 8; ++j) v[j] = 0.f;
+    for (int h = 0; h < E; h += 4) {
+      if (c0 + h < d_in) {  // d_in % 4 == 0: all 4 columns are inputs
+        const float4 a = *(const float4*)(dense + src + c0 + h);
+        v[h + 0] = a.x; v[h + 1] = a.y; v[h + 2] = a.z; v[h + 3] = a.w;
+      } else {
+#pragma unroll
+        for (int j = 0; j < 4; ++j) v[h + j] = 0.f;
+      }
     }
   } else {
 #pragma unroll
-    for (int j = 0; j < 8; ++j) v[j] = (c0 + j < d_in) ? dense[src + c0 + j] : 0.f;
+    for (int j = 0; j < E; ++j) v[j] = (c0 + j < d_in) ? dense[src + c0 + j] : 0.f;
   }
   if (BF16) {
-    uint4 o;
-    o.x = pack2(v[0], v[1]);
-    o.y = pack2(v[2], v[3]);
-    o.z = pack2(v[4], v[5]);
-    o.w = pack2(v[6], v[7]);
-    *(uint4*)((bf16_t*)X + r * ldx + c0) = o;
+    bf16_t* y = (bf16_t*)X + r * ldx + c0;
+    *(uint4*)y = make_uint4(pack2(v[0], v[1]), pack2(v[2], v[3]), pack2(v[4], v[5]), pack2(v[6], v[7]));
   } else {
     float* y = (float*)X + r * ldx + c0;
-    *(float4*)y = make_float4(v[0], v[1], v[2], v[3]);
-    *(float4*)(y + 4) = make_float4(v[4], v[5], v[6], v[7]);
+#pragma unroll
+    for (int h = 0; h < E; h += 4) *(float4*)(y + h) = make_float4(v[h], v[h + 1], v[h + 2], v[h + 3]);
   }
 }
 
@@ -670,7 +744,8 @@ template <int ACT>
 __global__ __launch_bounds__(256) void k_gemm_f32(const float* __restrict__ X, int ldx,
                                                   const float* __restrict__ W, int ldw,
                                                   const float* __restrict__ bias, float* __restrict__ Y,
-                                                  int ldy, int M, int N, int K) {
+                                                  int ldy, int M, int N, int K,
+                                                  const rb_k_row* __restrict__ skip_rows, int skip_T) {
   __shared__ float sA[2][G32_BK][G32_BM + G32_PAD];
   __shared__ float sB[2][G32_BK][G32_BN + G32_PAD];
   const int tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
@@ -679,6 +754,11 @@ __global__ __launch_bounds__(256) void k_gemm_f32(const float* __restrict__ X, i
   const int tile = xcd_tile(blockIdx.x, gridDim.x);
   const int bm = tile / tiles_n, bn = tile - bm * tiles_n;
   const int m0 = bm * G32_BM, n0 = bn * G32_BN;
+  if (skip_rows) {  // a block of padding tokens only (uniform per workgroup)
+    const int e = m0 / skip_T;
+    const rb_k_row rw = skip_rows[e];
+    if (rw.src < 0 || m0 - e * skip_T >= rw.aux) return;
+  }
   const int lrow = tid >> 3, lk = (tid & 7) * 4;
   const float* ag[2];
   const float* bg[2];
@@ -762,11 +842,14 @@ __global__ __launch_bounds__(256) void k_head(const rb_k_row* __restrict__ rows,
 
 constexpr int POOL_MAX_D = 1024, POOL_MAX_OUT = 16;
 
-// One workgroup per sequence slot: each thread sums one feature over the
-// sequence's L real tokens (coalesced token rows; tokens past L are never
-// read, so padding cannot reach the mean), divides by L, then the block
-// computes the head logits with fixed-order reductions and thread 0 applies
-// the softmax and writes the request's output row.
+// One workgroup per sequence slot. Wave w sums the slot's real tokens
+// [w L / 4, (w + 1) L / 4) (tokens past L are never read, so padding cannot
+// reach the mean), each lane owning float4 columns and keeping four token
+// loads in flight while adding them in token order; the four partial sums are
+// added in wave order and divided by L (a fixed order, so the result depends
+// on the sequence only). The block then computes the head logits with
+// fixed-order reductions and thread 0 applies the softmax and writes the
+// request's output row.
 __global__ __launch_bounds__(256) void k_seqpool(const rb_k_row* __restrict__ rows, int n_seqs, int T,
                                                  const float* __restrict__ H, int ldh, int D,
                                                  const float* __restrict__ Wh,
@@ -775,16 +858,42 @@ __global__ __launch_bounds__(256) void k_seqpool(const rb_k_row* __restrict__ ro
   const int r = blockIdx.x;
   const rb_k_row rw = rows[r];
   if (rw.out < 0) return;
-  const int L = (int)rw.aux;
+  const int L = (int)min(max(rw.aux, (int64_t)0), (int64_t)T);  // reads stay inside the slot
   const int tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
+  __shared__ float psum[4][POOL_MAX_D];
   __shared__ float pooled[POOL_MAX_D];
   __shared__ float part[4][POOL_MAX_OUT];
   const float* h = H + (int64_t)r * T * ldh;
-  for (int c = tid; c < D; c += 256) {
-    float s = 0.f;
-    for (int t = 0; t < L; ++t) s += h[(int64_t)t * ldh + c];
-    pooled[c] = s / (float)L;
+  const int t0 = (int)((int64_t)L * wid / 4), t1 = (int)((int64_t)L * (wid + 1) / 4);
+  if ((D & 3) == 0 && (ldh & 3) == 0) {
+    for (int c = lane * 4; c < D; c += 256) {
+      float4 s = make_float4(0.f, 0.f, 0.f, 0.f);
+      int t = t0;
+      for (; t + 4 <= t1; t += 4) {
+        float4 v[4];
+#pragma unroll
+        for (int u = 0; u < 4; ++u) v[u] = *(const float4*)(h + (int64_t)(t + u) * ldh + c);
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+          s.x += v[u].x; s.y += v[u].y; s.z += v[u].z; s.w += v[u].w;
+        }
+      }
+      for (; t < t1; ++t) {
+        const float4 v = *(const float4*)(h + (int64_t)t * ldh + c);
+        s.x += v.x; s.y += v.y; s.z += v.z; s.w += v.w;
+      }
+      *(float4*)&psum[wid][c] = s;
+    }
+  } else {
+    for (int c = lane; c < D; c += 64) {
+      float s = 0.f;
+      for (int t = t0; t < t1; ++t) s += h[(int64_t)t * ldh + c];
+      psum[wid][c] = s;
+    }
   }
+  __syncthreads();
+  const float inv = 1.f / (float)max(L, 1);
+  for (int c = tid; c < D; c += 256) pooled[c] = (((psum[0][c] + psum[1][c]) + psum[2][c]) + psum[3][c]) * inv;
   __syncthreads();
   for (int j = 0; j < n_out; ++j) {
     float s = 0.f;
@@ -884,18 +993,35 @@ rb_status rb_k_route(void* stream, int32_t kind, const rb_k_batch* batches, int3
 }
 
 rb_status rb_k_assemble(void* stream, const rb_k_row* rows, int32_t n_rows_total, int32_t seq_T,
-                        const float* dense, int64_t dense_len, int32_t d_in, void* X, int32_t ldx,
-                        int32_t out_bf16, float pad, int32_t* err) {
+                        int32_t seq_real_only, const float* dense, int64_t dense_len, int32_t d_in, void* X,
+                        int32_t ldx, int32_t out_bf16, float pad, int32_t* err) {
   if (n_rows_total < 0 || seq_T < 0 || d_in < 1 || ldx < d_in || (ldx & 7) || !rows || !X || !err)
     return RB_EINVAL;
+  if (seq_real_only && (seq_T == 0 || n_rows_total % seq_T || out_bf16)) return RB_EINVAL;
   if (n_rows_total == 0) return RB_OK;
-  const unsigned g = blocks_for((int64_t)n_rows_total * (ldx / 8));
-  if (out_bf16)
-    hipLaunchKernelGGL(k_assemble<true>, dim3(g), dim3(256), 0, (hipStream_t)stream, rows, n_rows_total, seq_T,
-                       dense, dense_len, d_in, X, ldx, pad, err);
-  else
-    hipLaunchKernelGGL(k_assemble<false>, dim3(g), dim3(256), 0, (hipStream_t)stream, rows, n_rows_total, seq_T,
-                       dense, dense_len, d_in, X, ldx, pad, err);
+  auto lg2 = [](int v) { int l = 0; while ((1 << l) < v) ++l; return (1 << l) == v ? l : -1; };
+  if (seq_real_only) {
+    const dim3 grid(n_rows_total / seq_T, (seq_T + SEQ_TOK - 1) / SEQ_TOK);
+    hipLaunchKernelGGL(k_assemble_seq, grid, dim3(256), 0, (hipStream_t)stream, rows, seq_T, dense, dense_len, d_in,
+                       (float*)X, ldx, err, lg2(ldx / 8));
+    return launch_status();
+  }
+  const int64_t threads = (int64_t)n_rows_total * (ldx / 8);
+  const unsigned g = blocks_for(threads);
+  const int lg_c = lg2(ldx / 8), lg_t = seq_T > 0 ? lg2(seq_T) : 0;
+  const bool pow2 = lg_c >= 0 && lg_t >= 0 && (int64_t)g * 256 < ((int64_t)1 << 31);
+  hipStream_t hs = (hipStream_t)stream;
+#define RB_ASM(B, P)                                                                                         \
+  hipLaunchKernelGGL((k_assemble<B, P>), dim3(g), dim3(256), 0, hs, rows, n_rows_total, seq_T, dense, dense_len, \
+                     d_in, X, ldx, pad, err, lg_c, lg_t)
+  if (out_bf16) {
+    if (pow2) RB_ASM(true, true);
+    else RB_ASM(true, false);
+  } else {
+    if (pow2) RB_ASM(false, true);
+    else RB_ASM(false, false);
+  }
+#undef RB_ASM
   return launch_status();
 }
 
@@ -954,19 +1080,24 @@ rb_status rb_k_gemm_bf16(void* stream, const void* X, int32_t ldx, const void* W
 }
 
 rb_status rb_k_gemm_f32(void* stream, const float* X, int32_t ldx, const float* W, int32_t ldw, const float* b,
-                        float* Y, int32_t ldy, int32_t M, int32_t N, int32_t K, int32_t act) {
+                        float* Y, int32_t ldy, int32_t M, int32_t N, int32_t K, int32_t act,
+                        const rb_k_row* skip_rows, int32_t skip_T) {
   if (M < 0 || N <= 0 || K <= 0 || (N % G32_BN) || (K % G32_BK) || ldx < K || ldw < K || ldy < N) return RB_EINVAL;
   if ((ldx & 3) || (ldw & 3) || !X || !W || !b || !Y) return RB_EINVAL;
   if (act != RB_ACT_NONE && act != RB_ACT_RELU && act != RB_ACT_SIGMOID) return RB_EINVAL;
+  if (skip_rows && (skip_T <= 0 || skip_T % G32_BM)) return RB_EINVAL;
   if (M == 0) return RB_OK;
   const unsigned g = (unsigned)(((M + G32_BM - 1) / G32_BM) * (N / G32_BN));
   hipStream_t s = (hipStream_t)stream;
   if (act == RB_ACT_RELU)
-    hipLaunchKernelGGL(k_gemm_f32<RB_ACT_RELU>, dim3(g), dim3(256), 0, s, X, ldx, W, ldw, b, Y, ldy, M, N, K);
+    hipLaunchKernelGGL(k_gemm_f32<RB_ACT_RELU>, dim3(g), dim3(256), 0, s, X, ldx, W, ldw, b, Y, ldy, M, N, K,
+                       skip_rows, skip_T);
   else if (act == RB_ACT_SIGMOID)
-    hipLaunchKernelGGL(k_gemm_f32<RB_ACT_SIGMOID>, dim3(g), dim3(256), 0, s, X, ldx, W, ldw, b, Y, ldy, M, N, K);
+    hipLaunchKernelGGL(k_gemm_f32<RB_ACT_SIGMOID>, dim3(g), dim3(256), 0, s, X, ldx, W, ldw, b, Y, ldy, M, N, K,
+                       skip_rows, skip_T);
   else
-    hipLaunchKernelGGL(k_gemm_f32<RB_ACT_NONE>, dim3(g), dim3(256), 0, s, X, ldx, W, ldw, b, Y, ldy, M, N, K);
+    hipLaunchKernelGGL(k_gemm_f32<RB_ACT_NONE>, dim3(g), dim3(256), 0, s, X, ldx, W, ldw, b, Y, ldy, M, N, K,
+                       skip_rows, skip_T);
   return launch_status();
 }
 

@@ -445,13 +445,18 @@ rb_status run_group(rb_sched* s, const Group& g, const rb_k_batch* d_batches, co
                                    m->d_out, m->n_tables, w->rows, s->err_dev));
   const bool bf16 = m->dtype == RB_DT_BF16;
   const int Kp0 = m->layers[0].Kp;
+  // sequence groups: padding tokens are not assembled and 64-token blocks of
+  // them are not computed (every layer is row-wise and the pooling reads
+  // tokens t < L only)
+  const bool seq_skip = m->kind == RB_MODEL_SEQPOOL && g.q->bucket % 64 == 0;
   if (m->kind == RB_MODEL_RANKING) {
     RB_LAUNCH(s, "embbag", rb_k_embbag(hs, w->rows, (int)slots, lens, ids, ids_len, (const void* const*)m->tables_dev,
                                        m->n_tables, m->table_rows, m->emb_dim, dense, m->n_dense, w->X, Kp0, pad,
                                        s->err_dev));
   } else {
     RB_LAUNCH(s, "assemble", rb_k_assemble(hs, w->rows, (int)M, m->kind == RB_MODEL_SEQPOOL ? g.q->bucket : 0,
-                                           dense, dense_len, m->d_in, w->X, Kp0, bf16 ? 1 : 0, pad, s->err_dev));
+                                           seq_skip ? 1 : 0, dense, dense_len, m->d_in, w->X, Kp0, bf16 ? 1 : 0,
+                                           pad, s->err_dev));
   }
   const size_t nL = m->layers.size() - (m->head_last ? 1 : 0);
   void* h = w->X;
@@ -465,7 +470,8 @@ rb_status run_group(rb_sched* s, const Group& g, const rb_k_batch* d_batches, co
                                                last ? 1 : 0));
     } else {
       RB_LAUNCH(s, "gemm_f32", rb_k_gemm_f32(hs, (const float*)h, ldh, (const float*)L.w, L.Kp, L.b, (float*)y,
-                                             L.Np, (int)M, L.Np, L.Kp, L.act));
+                                             L.Np, (int)M, L.Np, L.Kp, L.act, seq_skip ? w->rows : nullptr,
+                                             seq_skip ? g.q->bucket : 0));
     }
     h = y;
     ldh = L.Np;

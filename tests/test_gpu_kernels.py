@@ -136,14 +136,14 @@ def test_route_bit_exact(kind, B, allowed, d_in, d_out, nt, T):
 
 
 @pytest.mark.parametrize("bf16", [0, 1])
-@pytest.mark.parametrize("d_in,ldx", [(64, 64), (4096, 4096), (13, 64), (40, 64)])
+@pytest.mark.parametrize("d_in,ldx", [(64, 64), (4096, 4096), (13, 64), (40, 64), (40, 72), (100, 200)])
 def test_assemble_bit_exact(bf16, d_in, ldx):
     rng = np.random.default_rng(2)
     kb, kr, arena, R = _make_group(rng, rb.RB_MODEL_MLP, 5, 256, (64, 128, 256), d_in, 4, max_n=32)
     rows, err = _route(rb.RB_MODEL_MLP, kb, kr, arena, R, d_in, 4)
     dense = _dev(arena["dense"])
     X = torch.empty((R, ldx), dtype=torch.int16 if bf16 else torch.float32, device=DEV)
-    rb.check(rb.lib().rb_k_assemble(_stream(), rb.dptr(rows), R, 0, rb.dptr(dense), dense.numel(), d_in,
+    rb.check(rb.lib().rb_k_assemble(_stream(), rb.dptr(rows), R, 0, 0, rb.dptr(dense), dense.numel(), d_in,
                                     rb.dptr(X), ldx, bf16, float("nan"), rb.dptr(err)), "rb_k_assemble")
     torch.cuda.synchronize()
     assert int(err.item()) == 0
@@ -159,6 +159,53 @@ def test_assemble_bit_exact(bf16, d_in, ldx):
         blk = got[b["row_base"]:b["row_base"] + b["padded"]]
         assert np.array_equal(blk[:, :d_in], ref, equal_nan=True)
         assert np.all(blk[:, d_in:] == 0)
+
+
+@pytest.mark.parametrize("T,ldx,skip", [(64, 16, 0), (48, 16, 0), (64, 24, 0), (128, 16, 0), (128, 16, 1),
+                                         (192, 24, 1)])
+def test_assemble_seq_bit_exact(T, ldx, skip):
+    # sequences padded along time to T: token t < L of slot e at row e*T + t,
+    # pad value elsewhere (power-of-two and general index paths); with
+    # real-only, rows t >= L and padding slots stay untouched
+    rng = np.random.default_rng(5)
+    d_in = 16
+    kb, kr, arena, R = _make_group(rng, rb.RB_MODEL_SEQPOOL, 5, 16, (8, 16), d_in, 2, 0, T, max_n=4)
+    rows, err = _route(rb.RB_MODEL_SEQPOOL, kb, kr, arena, R, d_in, 2)
+    dense = _dev(arena["dense"])
+    M = R * T
+    X = torch.full((M, ldx), -3.0, dtype=torch.float32, device=DEV)
+    rb.check(rb.lib().rb_k_assemble(_stream(), rb.dptr(rows), M, T, skip, rb.dptr(dense), dense.numel(), d_in,
+                                    rb.dptr(X), ldx, 0, float("nan"), rb.dptr(err)), "rb_k_assemble")
+    torch.cuda.synchronize()
+    assert int(err.item()) == 0
+    got = X.cpu().numpy().reshape(R, T, ldx)
+    from synth import Payload
+    for b in kb:
+        rq = kr[b["req_begin"]:b["req_begin"] + b["n_req"]]
+        pays = [Payload(arena["dense"][q["dense_off"]:q["dense_end"]],
+                        arena["lens"][q["lens_off"]:q["lens_off"] + q["n_rows"]]) for q in rq]
+        asm = ob.assemble(_SeqShape(d_in), pays, int(b["padded"]), pad=np.nan, bucket_len=T)
+        ref = asm.tokens
+        blk = got[b["row_base"]:b["row_base"] + b["padded"]]
+        if skip:
+            live = np.arange(T)[None, :] < asm.seq_len[:, None]  # pad slots have L = 0
+            assert np.array_equal(blk[live][:, :d_in], ref[live], equal_nan=True)
+            assert np.all(blk[live][:, d_in:] == 0)
+            assert np.all(blk[~live] == -3.0)
+            assert (~live).any()
+        else:
+            assert np.array_equal(blk[:, :, :d_in], ref, equal_nan=True)
+            assert np.all(blk[:, :, d_in:] == 0)
+    # real-only needs a sequence layout
+    assert rb.lib().rb_k_assemble(_stream(), rb.dptr(rows), M, 0, 1, rb.dptr(dense), dense.numel(),
+                                  d_in, rb.dptr(X), ldx, 0, 0.0, rb.dptr(err)) == rb.RB_EINVAL
+
+
+class _SeqShape:
+    kind = "seqpool"
+
+    def __init__(self, d_in):
+        self.d_in = d_in
 
 
 class _MlpShape:
@@ -284,10 +331,42 @@ def test_gemm_f32_matches_fp64(M, N, K, act):
     Y = torch.empty((M, N), dtype=torch.float32, device=DEV)
     Xd, Wd, bd = _dev(X), _dev(W), _dev(b)
     rb.check(rb.lib().rb_k_gemm_f32(_stream(), rb.dptr(Xd), K, rb.dptr(Wd), K, rb.dptr(bd),
-                                    rb.dptr(Y), N, M, N, K, act), "gemm_f32")
+                                    rb.dptr(Y), N, M, N, K, act, None, 0), "gemm_f32")
     torch.cuda.synchronize()
     ref = nx.dense(X, W, b, "relu" if act == rb.RB_ACT_RELU else "none")
     assert _row_scaled_err(Y.cpu().numpy(), ref) <= 1e-5
+
+
+@pytest.mark.parametrize("T", [64, 128, 256])
+def test_gemm_f32_skips_padding_token_blocks(T):
+    # sequence layout: slot e owns rows [e*T, (e+1)*T); 64-row blocks at or past
+    # the slot's length (and every block of a pad slot) are neither computed
+    # nor stored; every block holding a real token matches fp64 in full
+    rng = np.random.default_rng(7)
+    n_slots, N, K = 9, 128, 64
+    L = rng.integers(1, T + 1, size=n_slots)
+    L[2] = T
+    src = np.where(np.arange(n_slots) == 5, -1, 0)  # slot 5 is padding
+    rows = _rows_dev(src, L, np.arange(n_slots))
+    M = n_slots * T
+    X = rng.standard_normal((M, K)).astype(np.float32)
+    W = (rng.standard_normal((N, K)) / np.sqrt(K)).astype(np.float32)
+    b = rng.uniform(-0.5, 0.5, N).astype(np.float32)
+    Y = torch.full((M, N), -7.0, dtype=torch.float32, device=DEV)
+    Xd, Wd, bd = _dev(X), _dev(W), _dev(b)
+    rb.check(rb.lib().rb_k_gemm_f32(_stream(), rb.dptr(Xd), K, rb.dptr(Wd), K, rb.dptr(bd), rb.dptr(Y), N, M, N,
+                                    K, rb.RB_ACT_RELU, rb.dptr(rows), T), "gemm_f32")
+    torch.cuda.synchronize()
+    got = Y.cpu().numpy()
+    ref = nx.dense(X, W, b, "relu")
+    t = np.arange(M) % T
+    e = np.arange(M) // T
+    live = (src[e] >= 0) & ((t // 64) * 64 < L[e])
+    assert _row_scaled_err(got[live], ref[live]) <= 1e-5
+    assert np.all(got[~live] == -7.0)
+    # bad skip_T is rejected
+    assert rb.lib().rb_k_gemm_f32(_stream(), rb.dptr(Xd), K, rb.dptr(Wd), K, rb.dptr(bd), rb.dptr(Y), N, M, N, K,
+                                  rb.RB_ACT_RELU, rb.dptr(rows), 48) == rb.RB_EINVAL
 
 
 def _rows_dev(src, aux, out):
@@ -325,9 +404,11 @@ def test_head_and_split():
     assert np.all(o[~keep] == -7.0)
 
 
-def test_seqpool_matches_oracle():
+@pytest.mark.parametrize("S,T,D", [(50, 64, 256), (20, 512, 256), (30, 64, 100), (10, 128, 1000)])
+def test_seqpool_matches_oracle(S, T, D):
+    # float4 path (D % 4 == 0), scalar path, long sequences split over waves
     rng = np.random.default_rng(7)
-    S, T, D, n_out = 50, 64, 256, 2
+    n_out = 2
     L = rng.integers(1, T + 1, size=S)
     L[:3] = [1, T, 2]
     H = rng.standard_normal((S * T, D)).astype(np.float32)
