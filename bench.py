@@ -217,6 +217,8 @@ def main():
     ap.add_argument("--warmup", type=int, default=2)
     ap.add_argument("--workload", default="ranking", choices=sorted(DESCRIPTION))
     ap.add_argument("--window", type=int, default=64, help="dispatched batches per launch window")
+    ap.add_argument("--streams", type=int, default=8,
+                    help="HIP streams for concurrent launch chains of different models")
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-latency", action="store_true")
@@ -255,12 +257,13 @@ def main():
     ctx = rb.Ctx(0)
     shared = {}
 
-    def make(window, profile=False):
-        d = Deployment(w, ctx, device=True, window_batches=window, profile=profile, models=shared.get("m"))
+    def make(window, profile=False, n_streams=1):
+        d = Deployment(w, ctx, device=True, window_batches=window, profile=profile, models=shared.get("m"),
+                       n_streams=n_streams)
         shared.setdefault("m", d.models)
         return d
 
-    dep = make(args.window)
+    dep = make(args.window, n_streams=args.streams)
     dt = dep.upload(t, a)
     log("uploaded; warmup")
     for _ in range(args.warmup):
@@ -284,7 +287,8 @@ def main():
     log(f"timed {args.steps} steps: {ms_per_step:.2f} ms/step (device {dev_ms / args.steps:.2f} ms), "
         f"{value / 1e6:.2f} M rows/s, {n_batches} batches/step")
 
-    # profiled replay: per-kernel durations from HIP events on the library's stream
+    # profiled replay: per-kernel durations from HIP events around each launch,
+    # on one stream so that no other chain shares the device meanwhile
     pdep = make(args.window, profile=True)
     pdep.replay(dt)
     pdep.sched.sync()
@@ -351,7 +355,8 @@ def main():
         "warmup": args.warmup, "ms_per_step": round(ms_per_step, 3), "higher_is_better": True, "scaling": "weak",
         "vs_baseline": None, "dtype": dtypes.pop() if len(dtypes) == 1 else "bf16+f32", "data": "synthetic",
         "config": {"workload": DESCRIPTION[w.name], "requests_per_step": t.n, "examples_per_step": examples,
-                   "batches_per_step": n_batches, "window_batches": args.window, "parallelism": "single GPU"},
+                   "batches_per_step": n_batches, "window_batches": args.window, "streams": args.streams,
+                   "parallelism": "single GPU"},
         "latency": latency,
         "p50_us": None if latency is None else latency["rho0.9"]["p50_us"],
         "p99_us": None if latency is None else latency["rho0.9"]["p99_us"],

@@ -127,10 +127,16 @@ typedef struct {
   float pad_value;
   /* Nonzero: time every kernel launch with HIP events (rb_sched_kernel_stats). */
   int32_t profile;
+  /* Device mode: the launch chains of different models in a replay run on up
+   * to n_streams HIP streams of their own (0 or 1: the scheduler's stream).
+   * Each model keeps one stream, assigned in order of first use, so its
+   * chains stay in order; outputs do not depend on this setting. */
+  int32_t n_streams;
 } rb_sched_opts;
 
-/* One scheduler owns one HIP stream of the context's device (device mode) and
- * round-robins its queues onto it. */
+/* One scheduler owns one HIP stream of the context's device (device mode),
+ * plus opts->n_streams streams for concurrent launch chains in replays, and
+ * round-robins its queues onto the device. */
 rb_status rb_sched_create(rb_ctx* ctx, const rb_sched_opts* opts, rb_sched** out);
 /* RB_EBUSY while queues exist. Waits for the scheduler's device work. */
 rb_status rb_sched_destroy(rb_sched* s);
@@ -148,6 +154,7 @@ rb_status rb_sched_stream(rb_sched* s, void** stream);
 /* ---------------------------------------------------------------- queues */
 
 #define RB_MAX_BATCH_ROWS 4096
+#define RB_MAX_STREAMS 16  /* rb_sched_opts.n_streams */
 
 typedef struct {
   int32_t max_batch_size;            /* rows (sequences for seqpool) per batch, 1..RB_MAX_BATCH_ROWS */

@@ -183,6 +183,11 @@ struct rb_sched {
   rb_ctx* ctx = nullptr;
   rb_sched_opts opts{};
   hipStream_t stream = nullptr;
+  // replay launch chains: one stream per model (lanes), or the main stream
+  std::vector<hipStream_t> lanes;
+  std::vector<hipEvent_t> lane_done;
+  hipEvent_t ev_copy = nullptr;
+  std::map<int64_t, int> lane_of;  // model id -> lane, in order of first use
   std::vector<rb_queue*> queues;  // by id; null once destroyed
   int n_live_queues = 0;
   int64_t now = INT64_MIN;
@@ -358,16 +363,16 @@ hipEvent_t ev_get(rb_sched* s) {
   return e;
 }
 
-void prof_begin(rb_sched* s, hipEvent_t* a) {
+void prof_begin(rb_sched* s, hipStream_t st, hipEvent_t* a) {
   if (!s->opts.profile) return;
   *a = ev_get(s);
-  hipEventRecord(*a, s->stream);
+  hipEventRecord(*a, st);
 }
 
-void prof_end(rb_sched* s, const char* name, hipEvent_t a) {
+void prof_end(rb_sched* s, hipStream_t st, const char* name, hipEvent_t a) {
   if (!s->opts.profile) return;
   hipEvent_t b = ev_get(s);
-  hipEventRecord(b, s->stream);
+  hipEventRecord(b, st);
   s->prof_pending.push_back(Prof{name, a, b});
 }
 
@@ -385,17 +390,31 @@ void prof_collect(rb_sched* s) {
   s->prof_pending.clear();
 }
 
-#define RB_LAUNCH(s, name, call)           \
-  do {                                     \
-    hipEvent_t ev_a_ = nullptr;            \
-    prof_begin(s, &ev_a_);                 \
-    rb_status st_ = (call);                \
-    prof_end(s, name, ev_a_);              \
-    if (st_ != RB_OK) return st_;          \
+#define RB_LAUNCH(s, strm, name, call) \
+  do {                                 \
+    hipEvent_t ev_a_ = nullptr;        \
+    prof_begin(s, strm, &ev_a_);       \
+    rb_status st_ = (call);            \
+    prof_end(s, strm, name, ev_a_);    \
+    if (st_ != RB_OK) return st_;      \
   } while (0)
 
 int64_t group_rows(const rb_model* m, const rb_queue* q, int64_t slots) {
   return m->kind == RB_MODEL_SEQPOOL ? slots * q->bucket : slots;
+}
+
+// Drain every stream of the scheduler (main and lanes).
+void sync_all(rb_sched* s) {
+  hipStreamSynchronize(s->stream);
+  for (hipStream_t l : s->lanes) hipStreamSynchronize(l);
+}
+
+// Stream of a model's launch chains in a replay.
+hipStream_t lane_for(rb_sched* s, const rb_model* m) {
+  if (s->lanes.empty()) return s->stream;
+  auto it = s->lane_of.find(m->id);
+  if (it == s->lane_of.end()) it = s->lane_of.emplace(m->id, (int)(s->lane_of.size() % s->lanes.size())).first;
+  return s->lanes[(size_t)it->second];
 }
 
 rb_status ensure_work(rb_sched* s, rb_model* m, int64_t rows, int64_t slots, Work** out) {
@@ -405,7 +424,7 @@ rb_status ensure_work(rb_sched* s, rb_model* m, int64_t rows, int64_t slots, Wor
     // never make the buffers shrink and grow back
     const int64_t R = std::max<int64_t>({rows, w.rows_cap, 64});
     const int64_t S = std::max<int64_t>({slots, w.slots_cap, 64});
-    hipStreamSynchronize(s->stream);
+    sync_all(s);
     hipFree(w.X);
     hipFree(w.A);
     hipFree(w.B);
@@ -428,20 +447,21 @@ rb_status ensure_work(rb_sched* s, rb_model* m, int64_t rows, int64_t slots, Wor
   return RB_OK;
 }
 
-// Launch chain of one group: route -> assemble | embbag -> layers -> head | seqpool | split.
-rb_status run_group(rb_sched* s, const Group& g, const rb_k_batch* d_batches, const rb_k_req* d_reqs,
-                    const float* dense, int64_t dense_len, const int32_t* lens, const int32_t* ids, int64_t ids_len,
-                    float* out) {
+// Launch chain of one group on stream st_h: route -> assemble | embbag ->
+// layers -> head | seqpool | split.
+rb_status run_group(rb_sched* s, hipStream_t st_h, const Group& g, const rb_k_batch* d_batches,
+                    const rb_k_req* d_reqs, const float* dense, int64_t dense_len, const int32_t* lens,
+                    const int32_t* ids, int64_t ids_len, float* out) {
   rb_model* m = g.q->m;
   const int64_t slots = g.slots;
   const int64_t M = group_rows(m, g.q, slots);
   Work* w = nullptr;
   rb_status st = ensure_work(s, m, M, slots, &w);
   if (st != RB_OK) return st;
-  if (std::find(m->used.begin(), m->used.end(), s->stream) == m->used.end()) m->used.push_back(s->stream);
-  void* hs = (void*)s->stream;
+  if (std::find(m->used.begin(), m->used.end(), st_h) == m->used.end()) m->used.push_back(st_h);
+  void* hs = (void*)st_h;
   const float pad = s->opts.pad_value;
-  RB_LAUNCH(s, "route", rb_k_route(hs, m->kind, d_batches, (int)g.batches.size(), d_reqs, lens, m->d_in,
+  RB_LAUNCH(s, st_h, "route", rb_k_route(hs, m->kind, d_batches, (int)g.batches.size(), d_reqs, lens, m->d_in,
                                    m->d_out, m->n_tables, w->rows, s->err_dev));
   const bool bf16 = m->dtype == RB_DT_BF16;
   const int Kp0 = m->layers[0].Kp;
@@ -450,11 +470,11 @@ rb_status run_group(rb_sched* s, const Group& g, const rb_k_batch* d_batches, co
   // tokens t < L only)
   const bool seq_skip = m->kind == RB_MODEL_SEQPOOL && g.q->bucket % 64 == 0;
   if (m->kind == RB_MODEL_RANKING) {
-    RB_LAUNCH(s, "embbag", rb_k_embbag(hs, w->rows, (int)slots, lens, ids, ids_len, (const void* const*)m->tables_dev,
+    RB_LAUNCH(s, st_h, "embbag", rb_k_embbag(hs, w->rows, (int)slots, lens, ids, ids_len, (const void* const*)m->tables_dev,
                                        m->n_tables, m->table_rows, m->emb_dim, dense, m->n_dense, w->X, Kp0, pad,
                                        s->err_dev));
   } else {
-    RB_LAUNCH(s, "assemble", rb_k_assemble(hs, w->rows, (int)M, m->kind == RB_MODEL_SEQPOOL ? g.q->bucket : 0,
+    RB_LAUNCH(s, st_h, "assemble", rb_k_assemble(hs, w->rows, (int)M, m->kind == RB_MODEL_SEQPOOL ? g.q->bucket : 0,
                                            seq_skip ? 1 : 0, dense, dense_len, m->d_in, w->X, Kp0, bf16 ? 1 : 0,
                                            pad, s->err_dev));
   }
@@ -466,10 +486,10 @@ rb_status run_group(rb_sched* s, const Group& g, const rb_k_batch* d_batches, co
     const bool last = (i + 1 == nL) && !m->head_last;
     void* y = last ? (void*)w->Y : (i % 2 == 0 ? w->A : w->B);
     if (bf16) {
-      RB_LAUNCH(s, "gemm_bf16", rb_k_gemm_bf16(hs, h, ldh, L.w, L.Kp, L.b, y, L.Np, (int)M, L.Np, L.Kp, L.act,
+      RB_LAUNCH(s, st_h, "gemm_bf16", rb_k_gemm_bf16(hs, h, ldh, L.w, L.Kp, L.b, y, L.Np, (int)M, L.Np, L.Kp, L.act,
                                                last ? 1 : 0));
     } else {
-      RB_LAUNCH(s, "gemm_f32", rb_k_gemm_f32(hs, (const float*)h, ldh, (const float*)L.w, L.Kp, L.b, (float*)y,
+      RB_LAUNCH(s, st_h, "gemm_f32", rb_k_gemm_f32(hs, (const float*)h, ldh, (const float*)L.w, L.Kp, L.b, (float*)y,
                                              L.Np, (int)M, L.Np, L.Kp, L.act, seq_skip ? w->rows : nullptr,
                                              seq_skip ? g.q->bucket : 0));
     }
@@ -478,12 +498,12 @@ rb_status run_group(rb_sched* s, const Group& g, const rb_k_batch* d_batches, co
   }
   if (m->head_last) {
     const DevLayer& L = m->layers.back();
-    RB_LAUNCH(s, "head", rb_k_head(hs, w->rows, (int)slots, h, ldh, L.w, m->head_bias, L.K, L.act, out));
+    RB_LAUNCH(s, st_h, "head", rb_k_head(hs, w->rows, (int)slots, h, ldh, L.w, m->head_bias, L.K, L.act, out));
   } else if (m->kind == RB_MODEL_SEQPOOL) {
-    RB_LAUNCH(s, "seqpool", rb_k_seqpool(hs, w->rows, (int)slots, g.q->bucket, (const float*)h, ldh, m->sp_in,
+    RB_LAUNCH(s, st_h, "seqpool", rb_k_seqpool(hs, w->rows, (int)slots, g.q->bucket, (const float*)h, ldh, m->sp_in,
                                          m->sp_w, m->sp_b, m->sp_out, m->sp_act, out));
   } else {
-    RB_LAUNCH(s, "split", rb_k_split(hs, w->rows, (int)slots, w->Y, ldh, m->d_out, out));
+    RB_LAUNCH(s, st_h, "split", rb_k_split(hs, w->rows, (int)slots, w->Y, ldh, m->d_out, out));
   }
   return RB_OK;
 }
@@ -558,14 +578,25 @@ rb_status flush_chunk(rb_sched* s) {
       off += round_up((int64_t)rr, 256);
     }
   if (!hip_ok(hipMemcpyAsync(sl->dev, sl->host, off, hipMemcpyHostToDevice, s->stream))) return RB_EDEVICE;
+  // lanes start after the copy; the main stream (and the slot's event) after
+  // every lane's chains
+  if (!s->lanes.empty()) {
+    hipEventRecord(s->ev_copy, s->stream);
+    for (hipStream_t l : s->lanes) hipStreamWaitEvent(l, s->ev_copy, 0);
+  }
   size_t gi = 0;
   for (auto& win : s->chunk)
     for (Group& g : win) {
-      st = run_group(s, g, (const rb_k_batch*)(sl->dev + offs[gi].first), (const rb_k_req*)(sl->dev + offs[gi].second),
-                     s->a_dense, s->a_dense_len, s->a_lens, s->a_ids, s->a_ids_len, s->a_out);
+      st = run_group(s, lane_for(s, g.q->m), g, (const rb_k_batch*)(sl->dev + offs[gi].first),
+                     (const rb_k_req*)(sl->dev + offs[gi].second), s->a_dense, s->a_dense_len, s->a_lens, s->a_ids,
+                     s->a_ids_len, s->a_out);
       ++gi;
       if (st != RB_OK) return st;
     }
+  for (size_t i = 0; i < s->lanes.size(); ++i) {
+    hipEventRecord(s->lane_done[i], s->lanes[i]);
+    hipStreamWaitEvent(s->stream, s->lane_done[i], 0);
+  }
   hipEventRecord(sl->ev, s->stream);
   sl->busy = true;
   s->chunk.clear();
@@ -810,7 +841,7 @@ rb_status rb_sched_create(rb_ctx* ctx, const rb_sched_opts* o, rb_sched** out) {
   if (!ctx || !o || !out) return RB_EINVAL;
   if (o->mode != RB_MODE_DEVICE && o->mode != RB_MODE_NO_DEVICE) return RB_EINVAL;
   if (o->mode == RB_MODE_DEVICE && ctx->device < 0) return RB_EDEVICE;
-  if (o->window_batches < 1) return RB_EINVAL;
+  if (o->window_batches < 1 || o->n_streams < 0 || o->n_streams > RB_MAX_STREAMS) return RB_EINVAL;
   rb_sched* s = new (std::nothrow) rb_sched();
   if (!s) return RB_ENOMEM;
   s->ctx = ctx;
@@ -820,6 +851,27 @@ rb_status rb_sched_create(rb_ctx* ctx, const rb_sched_opts* o, rb_sched** out) {
     if (!hip_ok(hipStreamCreateWithFlags(&s->stream, hipStreamNonBlocking)) ||
         !hip_ok(hipMalloc((void**)&s->err_dev, sizeof(int))) || !hip_ok(hipMemset(s->err_dev, 0, sizeof(int)))) {
       if (s->stream) hipStreamDestroy(s->stream);
+      delete s;
+      return RB_EDEVICE;
+    }
+    bool ok = true;
+    if (o->n_streams > 1) {
+      ok = hip_ok(hipEventCreateWithFlags(&s->ev_copy, hipEventDisableTiming));
+      for (int i = 0; ok && i < o->n_streams; ++i) {
+        hipStream_t l = nullptr;
+        hipEvent_t e = nullptr;
+        ok = hip_ok(hipStreamCreateWithFlags(&l, hipStreamNonBlocking));
+        if (ok) s->lanes.push_back(l);
+        ok = ok && hip_ok(hipEventCreateWithFlags(&e, hipEventDisableTiming));
+        if (ok) s->lane_done.push_back(e);
+      }
+    }
+    if (!ok) {
+      for (hipStream_t l : s->lanes) hipStreamDestroy(l);
+      for (hipEvent_t e : s->lane_done) hipEventDestroy(e);
+      if (s->ev_copy) hipEventDestroy(s->ev_copy);
+      hipFree(s->err_dev);
+      hipStreamDestroy(s->stream);
       delete s;
       return RB_EDEVICE;
     }
@@ -833,7 +885,7 @@ rb_status rb_sched_destroy(rb_sched* s) {
   if (!s) return RB_OK;
   if (s->n_live_queues) return RB_EBUSY;
   if (s->stream) {
-    hipStreamSynchronize(s->stream);
+    sync_all(s);
     for (auto& kv : s->work) {
       Work& w = kv.second;
       hipFree(w.X);
@@ -854,8 +906,14 @@ rb_status rb_sched_destroy(rb_sched* s) {
     }
     for (hipEvent_t e : s->ev_pool) hipEventDestroy(e);
     hipFree(s->err_dev);
-    // the stream is drained: models no longer need to wait on it
-    for (rb_model* m : s->ctx->models) m->used.erase(std::remove(m->used.begin(), m->used.end(), s->stream), m->used.end());
+    // the streams are drained: models no longer need to wait on them
+    std::vector<hipStream_t> mine = s->lanes;
+    mine.push_back(s->stream);
+    for (rb_model* m : s->ctx->models)
+      for (hipStream_t st : mine) m->used.erase(std::remove(m->used.begin(), m->used.end(), st), m->used.end());
+    for (hipStream_t l : s->lanes) hipStreamDestroy(l);
+    for (hipEvent_t e : s->lane_done) hipEventDestroy(e);
+    if (s->ev_copy) hipEventDestroy(s->ev_copy);
     hipStreamDestroy(s->stream);
   }
   s->ctx->n_scheds--;
@@ -867,6 +925,8 @@ rb_status rb_sync(rb_sched* s) {
   if (!s) return RB_EINVAL;
   if (!s->stream) return RB_OK;
   if (!hip_ok(hipStreamSynchronize(s->stream))) return RB_EDEVICE;
+  for (hipStream_t l : s->lanes)
+    if (!hip_ok(hipStreamSynchronize(l))) return RB_EDEVICE;
   for (Slot& sl : s->slots)
     if (sl.busy) retire_slot(s, sl);
   prof_collect(s);
@@ -1073,7 +1133,7 @@ static rb_status run_serving_batch(rb_sched* s, rb_queue* q, const Batch& b) {
   std::memcpy(sl->host + o_reqs, g.reqs.data(), g.reqs.size() * sizeof(rb_k_req));
   if (!hip_ok(hipMemcpyAsync(sl->dev, sl->host, o_out, hipMemcpyHostToDevice, s->stream))) return RB_EDEVICE;
   float* dout = (float*)(sl->dev + o_out);
-  st = run_group(s, g, (const rb_k_batch*)(sl->dev + o_batch), (const rb_k_req*)(sl->dev + o_reqs),
+  st = run_group(s, s->stream, g, (const rb_k_batch*)(sl->dev + o_batch), (const rb_k_req*)(sl->dev + o_reqs),
                  (const float*)(sl->dev + o_dense), nd, (const int32_t*)(sl->dev + o_lens),
                  (const int32_t*)(sl->dev + o_ids), ni, dout);
   if (st != RB_OK) return st;

@@ -51,7 +51,7 @@ class rb_model_desc(C.Structure):
 
 class rb_sched_opts(C.Structure):
     _fields_ = [("mode", C.c_int32), ("window_batches", C.c_int32), ("pad_value", C.c_float),
-                ("profile", C.c_int32)]
+                ("profile", C.c_int32), ("n_streams", C.c_int32)]
 
 
 class rb_queue_opts(C.Structure):
@@ -294,9 +294,9 @@ class Queue:
 
 class Sched:
     def __init__(self, ctx: Ctx, device: bool = True, window_batches: int = 1, pad_value: float = 0.0,
-                 profile: bool = False):
+                 profile: bool = False, n_streams: int = 1):
         o = rb_sched_opts(RB_MODE_DEVICE if device else RB_MODE_NO_DEVICE, window_batches, pad_value,
-                          1 if profile else 0)
+                          1 if profile else 0, n_streams)
         h = C.c_void_p()
         check(_lib().rb_sched_create(ctx.h, C.byref(o), C.byref(h)), "rb_sched_create")
         self.h = h

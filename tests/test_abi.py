@@ -91,6 +91,12 @@ def test_device_mode_needs_a_device(ctx):
     assert status(lambda: rb.Sched(ctx, device=True)) == rb.RB_EDEVICE
 
 
+def test_stream_count_bounds(ctx):
+    assert status(lambda: rb.Sched(ctx, device=False, n_streams=-1)) == rb.RB_EINVAL
+    assert status(lambda: rb.Sched(ctx, device=False, n_streams=17)) == rb.RB_EINVAL
+    rb.Sched(ctx, device=False, n_streams=16).destroy()
+
+
 def test_ownership_and_busy_rules(ctx):
     s = rb.Sched(ctx, device=False)
     m = mlp(ctx)

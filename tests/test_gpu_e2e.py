@@ -51,11 +51,12 @@ def row_scaled_err(y, ref):
     return float(np.max(np.abs(y.astype(np.float64) - ref) / scale))
 
 
-def run(ctx, name, n, window=1, pad=0.0, profile=False):
+def run(ctx, name, n, window=1, pad=0.0, profile=False, n_streams=1):
     w = synth.workload(name)
     t, a = trace_and_arenas(name, n)
     svc = service_table(w)
-    dep = Deployment(w, ctx, device=True, window_batches=window, pad_value=pad, service_ns=svc, profile=profile)
+    dep = Deployment(w, ctx, device=True, window_batches=window, pad_value=pad, service_ns=svc, profile=profile,
+                     n_streams=n_streams)
     try:
         dt = dep.upload(t, a)
         log = dep.replay(dt)
@@ -105,6 +106,18 @@ def test_outputs_independent_of_launch_window(ctx, name):
     *_, out1, _ = run(ctx, name, n, window=1)
     *_, out8, _ = run(ctx, name, n, window=8)
     assert np.array_equal(out1, out8)
+
+
+@pytest.mark.parametrize("name,n_streams", [("multi_tenant", 4), ("multi_tenant", 3), ("ragged_seq", 4)])
+def test_outputs_independent_of_stream_count(ctx, name, n_streams):
+    # concurrent launch chains of different models (ragged_seq: one model over
+    # four bucket queues, so its chains share one stream) change nothing
+    n = min(PREFIX[name], 1500)
+    w, t, a, qindex, log1, out1, _ = run(ctx, name, n, window=16)
+    _, _, _, _, logk, outk, out_off = run(ctx, name, n, window=16, n_streams=n_streams)
+    assert lib_batches(log1, qindex) == lib_batches(logk, qindex)
+    assert np.array_equal(out1, outk)
+    check_outputs(name, t, a, outk, out_off, range(0, t.n, 7))
 
 
 def test_serving_api_matches_oracle(ctx):
