@@ -160,6 +160,50 @@ def cpu_baseline(w, t, a, seconds):
                       f"{el:.1f} s"}
 
 
+def serving_rate(w, t, a, ctx, models, n):
+    """The serving API with host payloads: the first n requests submitted in
+    arrival order from host memory (rb_submit copies them), every batch run
+    as soon as it closes (rb_run_next: one launch chain per batch, payload
+    staged to HBM and outputs copied back over PCIe), the rest flushed, and
+    every request's rows collected on the host (rb_collect). Wall time from
+    the first submit to the last collect, Python call overhead included."""
+    import torch
+    from paper_1712_06139_amd import rb
+    from paper_1712_06139_amd.deploy import Deployment
+    n = min(n, t.n)
+    dep = Deployment(w, ctx, device=True, models=models)
+    try:
+        payloads = [a.payload(r) for r in range(n)]
+        qs = [dep.queue_for(t, r) for r in range(n)]
+        d_out = [dep.models[int(t.servable[r])].d_out for r in range(n)]
+        sched = dep.sched
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        ids = []
+        for r in range(n):
+            p = payloads[r]
+            ids.append(sched.submit(qs[r], int(t.n_rows[r]), p.dense, p.lens, p.ids, arrival_ns=int(t.arrival_ns[r])))
+            while sched.run_next() is not None:
+                pass
+        for q in dep.queues:
+            rb.check(rb.lib().rb_flush(q.h), "rb_flush")
+        while sched.run_next() is not None:
+            pass
+        sched.sync()
+        rows = 0
+        for r in range(n):
+            rows += sched.collect(ids[r], int(t.n_rows[r]), d_out[r]).shape[0]
+        el = time.perf_counter() - t0
+    finally:
+        dep.destroy()
+    ex = int(t.n_rows[:n].sum())
+    assert rows == ex
+    return {"value": round(ex / el, 1), "unit": "examples/s", "requests": n, "examples": ex,
+            "seconds": round(el, 3),
+            "path": "host payloads: rb_submit -> rb_run_next (one batch per launch chain, PCIe in and out) "
+                    "-> rb_collect"}
+
+
 def calibrate_latency(w, t, a, dt, ctx, dep, window):
     """Service time per padded size measured on this GPU (a replay of a prefix
     of the trace through a queue whose every batch is padded to P), then
@@ -222,6 +266,8 @@ def main():
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-latency", action="store_true")
+    ap.add_argument("--serving-requests", type=int, default=20000,
+                    help="also time the serving API with host payloads on this many requests (0: skip)")
     ap.add_argument("--sweep-windows", default="", help="comma list: also time these windows (stderr)")
     ap.add_argument("--copy-probe-mb", type=int, default=0,
                     help="first run one plain elementwise copy of this many MiB (fp32), a known-size kernel "
@@ -344,6 +390,12 @@ def main():
         latency = calibrate_latency(w, t, a, dt, ctx, dep, args.window)
         log(f"latency: {json.dumps(latency)}")
 
+    serving = None
+    if args.serving_requests > 0:
+        log(f"serving API with host payloads ({args.serving_requests} requests)")
+        serving = serving_rate(w, t, a, ctx, shared["m"], args.serving_requests)
+        log(f"serving: {json.dumps(serving)}")
+
     cpu = None
     if not args.no_cpu_baseline:
         log("timing the CPU oracle")
@@ -364,6 +416,7 @@ def main():
         "kernels": kernels,
         "roofline": roof,
         "cpu_baseline": cpu,
+        "serving_pcie": serving,
     }
     print(json.dumps(out), flush=True)
     dep.destroy()

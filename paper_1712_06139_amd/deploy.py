@@ -72,6 +72,16 @@ class Deployment:
                           for s in range(len(w.models))]
         self.qindex = {q.id: i for i, q in enumerate(self.queues)}
 
+    def queue_for(self, t, r: int) -> rb.Queue:
+        """The queue request r of trace t is submitted to: its servable's
+        queue, or for bucketed sequence queues the smallest bucket that holds
+        the request's longest sequence (the replay's rule)."""
+        qs = self.servables[int(t.servable[r])]
+        if len(qs) == 1 or t.seq_lens is None:
+            return qs[0]
+        L = int(t.seq_lens[t.seq_off[r]:t.seq_off[r + 1]].max())
+        return min((q for q in qs if q.bucket_len >= L), key=lambda q: q.bucket_len)
+
     def destroy(self):
         for q in self.queues:
             q.destroy()

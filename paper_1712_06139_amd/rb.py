@@ -282,6 +282,7 @@ class Queue:
         check(_lib().rb_queue_create(sched.h, model.h, C.byref(o), C.byref(h)), "rb_queue_create")
         self.h = h
         self.model = model
+        self.bucket_len = bucket_len
         qid = C.c_int32()
         check(_lib().rb_queue_id(h, C.byref(qid)), "rb_queue_id")
         self.id = qid.value
