@@ -133,31 +133,55 @@ def recorded_traffic(workload, kernel):
     return rec.get("workloads", {}).get(workload, {}).get(kernel)
 
 
+def cpu_model():
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
 def cpu_baseline(w, t, a, seconds):
     """The oracle, as it stands, on the first requests of the trace for about
-    `seconds` of CPU time (model setup excluded)."""
+    `seconds` of CPU time (model setup excluded), with the BLAS threads it
+    runs on by default; then the same requests again on one thread (a
+    bounded second pass, at most a quarter of the time)."""
     from oracle.models import OracleModel
     import synth
     try:
-        from threadpoolctl import threadpool_info
+        from threadpoolctl import threadpool_info, threadpool_limits
         cores = max([d.get("num_threads", 1) for d in threadpool_info()] + [1])
     except Exception:
+        threadpool_limits = None
         cores = 1
     oms = {}
-    n = ex = 0
-    el = 0.0
-    while el < seconds and n < t.n:
-        s = int(t.servable[n])
-        if s not in oms:
-            oms[s] = OracleModel(w.models[s], synth.model_params(w, s))
-        t0 = time.perf_counter()
-        oms[s].forward(a.payload(n))
-        el += time.perf_counter() - t0
-        ex += int(t.n_rows[n])
-        n += 1
+
+    def run(limit_s, max_n):
+        n = ex = 0
+        el = 0.0
+        while el < limit_s and n < max_n:
+            s = int(t.servable[n])
+            if s not in oms:
+                oms[s] = OracleModel(w.models[s], synth.model_params(w, s))
+            t0 = time.perf_counter()
+            oms[s].forward(a.payload(n))
+            el += time.perf_counter() - t0
+            ex += int(t.n_rows[n])
+            n += 1
+        return n, ex, el
+
+    n, ex, el = run(seconds, t.n)
+    one = None
+    if threadpool_limits is not None:
+        with threadpool_limits(limits=1):
+            n1, ex1, el1 = run(seconds / 4, n)
+        one = {"value": ex1 / el1, "cores": 1, "sample": f"first {n1} requests ({ex1} examples), {el1:.1f} s"}
     return {"value": ex / el, "unit": "examples/s", "cores": int(cores), "kind": "oracle",
             "sample": f"first {n} requests ({ex} examples) of the same trace, unbatched fp64 forward per request, "
-                      f"{el:.1f} s"}
+                      f"{el:.1f} s",
+            "cpu_model": cpu_model(), "one_thread": one}
 
 
 def serving_rate(w, t, a, ctx, models, n):
@@ -204,53 +228,124 @@ def serving_rate(w, t, a, ctx, models, n):
                     "-> rb_collect"}
 
 
+def _subset(t, a, idx):
+    """Requests idx (ascending) of trace t as a trace and arenas of their own
+    (slices copied so that each request's slice stays contiguous)."""
+    import synth
+
+    def cat(arr, off):
+        parts = [arr[off[r]:off[r + 1]] for r in idx]
+        o = np.zeros(len(idx) + 1, dtype=np.int64)
+        np.cumsum([len(x) for x in parts], out=o[1:])
+        return (np.concatenate(parts) if parts else arr[:0]), o
+
+    dense, doff = cat(a.dense, a.dense_off)
+    lens, loff = cat(a.lens, a.lens_off)
+    ids, ioff = cat(a.ids, a.ids_off)
+    seq_lens = seq_off = None
+    if t.seq_lens is not None:
+        seq_lens, seq_off = cat(t.seq_lens, t.seq_off)
+    st = synth.Trace(t.workload, np.zeros(len(idx), dtype=t.servable.dtype), t.arrival_ns[idx], t.n_rows[idx],
+                     seq_lens, seq_off)
+    return st, synth.Arenas(dense, lens, ids, doff, loff, ioff)
+
+
 def calibrate_latency(w, t, a, dt, ctx, dep, window):
-    """Service time per padded size measured on this GPU (a replay of a prefix
-    of the trace through a queue whose every batch is padded to P), then
-    Poisson arrivals at rho x the simulated device's capacity through the
-    no-device scheduler: nearest-rank p50 / p99 per request."""
+    """Per-request latency on the simulated clock (nearest-rank p50 / p99).
+    Each queue's service time per batch size is measured on this GPU: the
+    queue's first requests of the trace replayed through a queue whose every
+    batch is padded to P, for its allowed sizes (or B/8, B/4, B/2 and B,
+    interpolated linearly in between when the queue does not pad). The
+    no-device scheduler then replays arrivals with those service tables:
+    Poisson arrivals at rho x the simulated device's capacity for count-only
+    workloads, the trace's own arrivals for workloads with batch timeouts."""
     import synth
     import torch
     from paper_1712_06139_amd import rb
     from paper_1712_06139_amd.deploy import Deployment
-    allowed = list(w.queues[0].allowed)
-    svc = np.zeros(w.queues[0].max_batch_size + 1, dtype=np.int64)
-    n_cal = min(20_000, t.n)
-    tcal = synth.trace(w, n_cal)
-    for P in allowed:
-        cw = synth.Workload(w.name, w.wid, w.models, (synth.Queue(0, P, (P,), None),), w.n_requests, w.rows,
-                            w.rate_per_s)
-        cdep = Deployment(cw, ctx, device=True, window_batches=window, models=dep.models)
-        out_off = cdep.out_offsets(tcal)
-        out = torch.empty(int(out_off[-1]), dtype=torch.float32, device="cuda")
-        kw = dict(dense=dt.dense, dense_off=a.dense_off[:n_cal + 1], lens=dt.lens,
-                  lens_off=None if a.lens.size == 0 else a.lens_off[:n_cal + 1], ids=dt.ids,
-                  ids_off=None if a.ids.size == 0 else a.ids_off[:n_cal + 1], out=out, out_off=out_off)
-        cdep.sched.sim_run(cdep.servables, tcal.servable, tcal.arrival_ns, tcal.n_rows, None, **kw)
-        cdep.sched.sync()
-        torch.cuda.synchronize()
-        s0 = time.perf_counter()
-        lg = cdep.sched.sim_run(cdep.servables, tcal.servable, tcal.arrival_ns, tcal.n_rows, None, **kw)
-        cdep.sched.sync()
-        svc[P] = int((time.perf_counter() - s0) * 1e9 / lg["n_batches"])
-        cdep.destroy()
-    for s in range(len(svc)):
-        svc[s] = svc[min(p for p in allowed if p >= s)]
+    qsel = np.array([dep.qindex[dep.queue_for(t, r).id] for r in range(t.n)])
+    tables, measured = [], {}
+    for qi, q in enumerate(w.queues):
+        m_idx = q.servable
+        mine = np.nonzero(qsel == qi)[0]
+        sizes = sorted(set(q.allowed)) if q.allowed else sorted(
+            {max(q.max_batch_size // 8, 1), q.max_batch_size // 4, q.max_batch_size // 2, q.max_batch_size})
+        sizes = [P for P in sizes if P >= int(t.n_rows[mine].max(initial=1))]
+        if len(w.queues) == 1:
+            idx = mine[:20_000]  # a prefix of the trace, already in device memory
+        else:
+            # a copied subset: up to 3000 requests and about 256 MB of payload
+            cum = np.cumsum(np.diff(a.dense_off)[mine])
+            idx = mine[:max(1, min(3000, int(np.searchsorted(cum, 64 << 20))))]
+        prefix = bool(len(idx)) and idx[-1] == len(idx) - 1
+        if prefix:
+            st = synth.trace(w, len(idx))
+            sa = None
+        else:
+            st, sa = _subset(t, a, idx)
+        svc_at = {}
+        for P in sizes:
+            cw = synth.Workload(w.name, w.wid, (w.models[m_idx],),
+                                (synth.Queue(0, P, (P,), None, q.bucket_len),), len(idx), w.rows, w.rate_per_s)
+            cdep = Deployment(cw, ctx, device=True, window_batches=window, models=[dep.models[m_idx]])
+            try:
+                if prefix:
+                    out_off = cdep.out_offsets(st)
+                    out = torch.empty(int(out_off[-1]), dtype=torch.float32, device="cuda")
+                    kw = dict(dense=dt.dense, dense_off=a.dense_off[:len(idx) + 1], lens=dt.lens,
+                              lens_off=None if a.lens.size == 0 else a.lens_off[:len(idx) + 1], ids=dt.ids,
+                              ids_off=None if a.ids.size == 0 else a.ids_off[:len(idx) + 1], out=out,
+                              out_off=out_off)
+                    run = lambda: cdep.sched.sim_run(cdep.servables, np.zeros(len(idx), np.int32), st.arrival_ns,
+                                                     st.n_rows, cdep.max_len(st), **kw)
+                else:
+                    sdt = cdep.upload(st, sa)
+                    run = lambda: cdep.replay(sdt)
+                run()
+                cdep.sched.sync()
+                torch.cuda.synchronize()
+                s0 = time.perf_counter()
+                lg = run()
+                cdep.sched.sync()
+                svc_at[P] = int((time.perf_counter() - s0) * 1e9 / lg["n_batches"])
+            finally:
+                cdep.destroy()
+        ps = sorted(svc_at)
+        svc = np.zeros(q.max_batch_size + 1, dtype=np.int64)
+        for s_ in range(1, q.max_batch_size + 1):
+            if q.allowed:
+                svc[s_] = svc_at[min(P for P in ps if P >= s_)]
+            else:
+                svc[s_] = int(np.interp(s_, ps, [svc_at[P] for P in ps]))
+        svc[0] = svc[1]
+        tables.append(svc.tolist())
+        measured[f"queue{qi}"] = {str(P): round(svc_at[P] / 1e3, 2) for P in ps}
     lctx = rb.Ctx(-1)
-    ld = Deployment(w, lctx, device=False, service_ns=[svc.tolist()], with_params=False)
-    busy_ns = int(svc[ld.replay_meta(t)["b_padded"]].sum())
-    cap = t.n / (busy_ns * 1e-9)
-    lat = {"clock": "simulated", "capacity_req_s": round(cap, 1),
-           "service_us_by_padded_size": {str(P): round(svc[P] / 1e3, 2) for P in allowed}}
-    for rho in (0.5, 0.9):
-        tr = synth.trace(w, rate_per_s=rho * cap)
-        lg = ld.replay_meta(tr)
-        v = lg["req_done_ns"] - tr.arrival_ns
-        lat[f"rho{rho}"] = {"arrival_rate_req_s": round(rho * cap, 1), "utilization": rho,
-                            "p50_us": round(nearest_rank(v, 0.5) / 1e3, 2),
-                            "p99_us": round(nearest_rank(v, 0.99) / 1e3, 2)}
-    ld.destroy()
-    lctx.destroy()
+    ld = Deployment(w, lctx, device=False, service_ns=tables, with_params=False)
+    lat = {"clock": "simulated", "service_us_by_batch_size": measured}
+    try:
+        timed = any(q.timeout_ns is not None for q in w.queues)
+        lg0 = ld.replay_meta(t)
+        busy = sum(tables[ld.qindex[int(qid)]][int(P)] for qid, P in zip(lg0["b_queue"], lg0["b_padded"]))
+        if timed:
+            v = lg0["req_done_ns"] - t.arrival_ns
+            span = int(lg0["req_done_ns"].max() - t.arrival_ns.min())
+            lat["trace_arrivals"] = {"arrival_rate_req_s": w.rate_per_s, "utilization": round(busy / span, 3),
+                                     "p50_us": round(nearest_rank(v, 0.5) / 1e3, 2),
+                                     "p99_us": round(nearest_rank(v, 0.99) / 1e3, 2)}
+        else:
+            cap = t.n / (busy * 1e-9)
+            lat["capacity_req_s"] = round(cap, 1)
+            for rho in (0.5, 0.9):
+                tr = synth.trace(w, rate_per_s=rho * cap)
+                lg = ld.replay_meta(tr)
+                v = lg["req_done_ns"] - tr.arrival_ns
+                lat[f"rho{rho}"] = {"arrival_rate_req_s": round(rho * cap, 1), "utilization": rho,
+                                    "p50_us": round(nearest_rank(v, 0.5) / 1e3, 2),
+                                    "p99_us": round(nearest_rank(v, 0.99) / 1e3, 2)}
+    finally:
+        ld.destroy()
+        lctx.destroy()
     return lat
 
 
@@ -386,7 +481,7 @@ def main():
         d2.destroy()
 
     latency = None
-    if not args.no_latency and len(w.queues) == 1 and w.queues[0].allowed:
+    if not args.no_latency:
         latency = calibrate_latency(w, t, a, dt, ctx, dep, args.window)
         log(f"latency: {json.dumps(latency)}")
 
@@ -410,8 +505,8 @@ def main():
                    "batches_per_step": n_batches, "window_batches": args.window, "streams": args.streams,
                    "parallelism": "single GPU"},
         "latency": latency,
-        "p50_us": None if latency is None else latency["rho0.9"]["p50_us"],
-        "p99_us": None if latency is None else latency["rho0.9"]["p99_us"],
+        "p50_us": None if latency is None else latency.get("rho0.9", latency.get("trace_arrivals"))["p50_us"],
+        "p99_us": None if latency is None else latency.get("rho0.9", latency.get("trace_arrivals"))["p99_us"],
         "device_ms_per_step": round(dev_ms / args.steps, 3),
         "kernels": kernels,
         "roofline": roof,
