@@ -125,7 +125,10 @@ typedef struct {
   /* Value written into padding rows (and padding tokens) before the forward
    * pass. 0 in production; NaN shows that padding never reaches an output. */
   float pad_value;
-  /* Nonzero: time every kernel launch with HIP events (rb_sched_kernel_stats). */
+  /* 1: time every kernel launch with HIP events (rb_sched_kernel_stats);
+   * 2: the same with cold caches: before each timed launch the scheduler
+   * reads a 512 MB buffer on the launch stream (outside the timed events),
+   * evicting L2 and the Infinity Cache; 0: no timing. */
   int32_t profile;
   /* Device mode: the launch chains of different models in a replay run on up
    * to n_streams HIP streams of their own (0 or 1: the scheduler's stream).

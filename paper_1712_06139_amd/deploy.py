@@ -37,7 +37,7 @@ class DeviceTrace:
 
 class Deployment:
     def __init__(self, w, ctx: rb.Ctx, device: bool = True, window_batches: int = 1, pad_value: float = 0.0,
-                 profile: bool = False, service_ns: Optional[Sequence[Sequence[int]]] = None,
+                 profile: int = 0, service_ns: Optional[Sequence[Sequence[int]]] = None,
                  with_params: bool = True, models: Optional[List[rb.Model]] = None, n_streams: int = 1):
         import synth
         self.w = w

@@ -295,9 +295,9 @@ class Queue:
 
 class Sched:
     def __init__(self, ctx: Ctx, device: bool = True, window_batches: int = 1, pad_value: float = 0.0,
-                 profile: bool = False, n_streams: int = 1):
+                 profile: int = 0, n_streams: int = 1):
         o = rb_sched_opts(RB_MODE_DEVICE if device else RB_MODE_NO_DEVICE, window_batches, pad_value,
-                          1 if profile else 0, n_streams)
+                          int(profile), n_streams)
         h = C.c_void_p()
         check(_lib().rb_sched_create(ctx.h, C.byref(o), C.byref(h)), "rb_sched_create")
         self.h = h
