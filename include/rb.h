@@ -351,8 +351,8 @@ rb_status rb_k_embbag(void* stream, const rb_k_row* rows, int32_t n_rows_total, 
                       int32_t ldx, float pad, int32_t* err);
 /* Y[M, N] = act(X[M, K] W[N, K]^T + b), bf16 X and W (row strides ldx, ldw,
  * ldx and ldw < 2^22), fp32 accumulation; Y bf16 (out_f32 == 0) or fp32, row
- * stride ldy. K % 64 == 0, N % 128 == 0. act: RB_ACT_NONE, RB_ACT_RELU or
- * RB_ACT_SIGMOID. */
+ * stride ldy (a multiple of 8; Y 16-byte aligned). K % 64 == 0, N % 128 == 0.
+ * act: RB_ACT_NONE, RB_ACT_RELU or RB_ACT_SIGMOID. */
 rb_status rb_k_gemm_bf16(void* stream, const void* X, int32_t ldx, const void* W, int32_t ldw,
                          const float* b, void* Y, int32_t ldy, int32_t M, int32_t N, int32_t K,
                          int32_t act, int32_t out_f32);

@@ -498,6 +498,34 @@ __global__ __launch_bounds__(256) void k_embbag(const rb_k_row* __restrict__ row
 
 // ---------------------------------------------------------------- bf16 GEMM
 
+// 4 x 4 transpose across the four lanes of a quad: lane 4q + i holding x[k] =
+// element (k, i) ends up holding x[j] = element (i, j), where element (k, c)
+// is the value lane 4q + c held in x[k]. Two exchange rounds (lane xor 2, then
+// lane xor 1).
+__device__ __forceinline__ void quad_transpose4(float (&x)[4], int lane) {
+  const bool b1 = lane & 2, b0 = lane & 1;
+  float s0 = b1 ? x[0] : x[2], s1 = b1 ? x[1] : x[3];
+  float r0 = __shfl_xor(s0, 2), r1 = __shfl_xor(s1, 2);
+  if (b1) {
+    x[0] = r0;
+    x[1] = r1;
+  } else {
+    x[2] = r0;
+    x[3] = r1;
+  }
+  s0 = b0 ? x[0] : x[1];
+  s1 = b0 ? x[2] : x[3];
+  r0 = __shfl_xor(s0, 1);
+  r1 = __shfl_xor(s1, 1);
+  if (b0) {
+    x[0] = r0;
+    x[2] = r1;
+  } else {
+    x[1] = r0;
+    x[3] = r1;
+  }
+}
+
 // s_waitcnt vmcnt(N) lgkmcnt(0) (gfx9 encoding: vmcnt[3:0], expcnt[6:4],
 // lgkmcnt[11:8], vmcnt[5:4] in bits 15:14): at most N vector memory
 // operations of this wave in flight and every LDS read of it returned.
@@ -711,22 +739,30 @@ __global__ __launch_bounds__(NT) void k_gemm_bf16(const bf16_t* __restrict__ X, 
   wait_vmcnt_lds<0>();
 
   // accumulator (i, j) register r of lane l holds row 8*(r/4) + 4*(l/32) + r%4,
-  // column l%32 of its 32 x 32 block
+  // column l%32 of its 32 x 32 block. Bias and activation are applied per
+  // column; then each group of four registers (four consecutive rows) is
+  // transposed across the four lanes of a quad, so that a lane holds four
+  // consecutive columns of one row and stores them at once (8 bytes bf16, 16
+  // bytes fp32) instead of four single elements.
 #pragma unroll
   for (int j = 0; j < TN; ++j) {
-    const int col = n0 + wn * WN + j * 32 + (lane & 31);
-    const float bb = bias[col];
+    const float bb = bias[n0 + wn * WN + j * 32 + (lane & 31)];
+    const int colq = n0 + wn * WN + j * 32 + (lane & 28);  // first column of this lane's quad
 #pragma unroll
     for (int i = 0; i < TM; ++i)
 #pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const int row = m0 + wm * WM + i * 32 + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
+      for (int g = 0; g < 4; ++g) {
+        float v[4];
+#pragma unroll
+        for (int k = 0; k < 4; ++k) v[k] = act_fn<ACT>(acc[i][j][4 * g + k] + bb);
+        quad_transpose4(v, lane);
+        const int row = m0 + wm * WM + i * 32 + 8 * g + 4 * (lane >> 5) + (lane & 3);
         if (row < M) {
-          const float v = act_fn<ACT>(acc[i][j][r] + bb);
-          if (OUT_F32)
-            ((float*)Y)[(int64_t)row * ldy + col] = v;
-          else
-            ((bf16_t*)Y)[(int64_t)row * ldy + col] = f2bf(v);
+          if (OUT_F32) {
+            *(float4*)((float*)Y + (int64_t)row * ldy + colq) = make_float4(v[0], v[1], v[2], v[3]);
+          } else {
+            *(uint2*)((bf16_t*)Y + (int64_t)row * ldy + colq) = make_uint2(pack2(v[0], v[1]), pack2(v[2], v[3]));
+          }
         }
       }
   }
@@ -1063,7 +1099,7 @@ rb_status rb_k_embbag(void* stream, const rb_k_row* rows, int32_t n_rows_total, 
 rb_status rb_k_gemm_bf16(void* stream, const void* X, int32_t ldx, const void* W, int32_t ldw, const float* b,
                          void* Y, int32_t ldy, int32_t M, int32_t N, int32_t K, int32_t act, int32_t out_f32) {
   if (M < 0 || N <= 0 || K <= 0 || (N % 128) || (K % G16_KALIGN) || ldx < K || ldw < K || ldy < N) return RB_EINVAL;
-  if ((ldx & 7) || (ldw & 7) || !X || !W || !b || !Y) return RB_EINVAL;
+  if ((ldx & 7) || (ldw & 7) || (ldy & 7) || ((uintptr_t)Y & 15) || !X || !W || !b || !Y) return RB_EINVAL;
   // operand byte offsets within a 256-row tile are 32-bit
   if ((int64_t)ldx * 512 >= ((int64_t)1 << 31) || (int64_t)ldw * 512 >= ((int64_t)1 << 31)) return RB_EINVAL;
   if (act != RB_ACT_NONE && act != RB_ACT_RELU && act != RB_ACT_SIGMOID) return RB_EINVAL;

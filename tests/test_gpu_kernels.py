@@ -296,20 +296,25 @@ def _row_scaled_err(y, ref):
     return np.max(np.abs(y - ref) / scale)
 
 
-@pytest.mark.parametrize("M,N,K,act,out_f32", [
-    (1, 128, 64, rb.RB_ACT_NONE, 1), (200, 256, 1728, rb.RB_ACT_RELU, 0), (1024, 1024, 512, rb.RB_ACT_RELU, 0),
-    (333, 512, 1024, rb.RB_ACT_NONE, 1), (130, 128, 4096, rb.RB_ACT_SIGMOID, 1)])
-def test_gemm_bf16_matches_fp64(M, N, K, act, out_f32):
+@pytest.mark.parametrize("M,N,K,act,out_f32,pad_y", [
+    (1, 128, 64, rb.RB_ACT_NONE, 1, 0), (200, 256, 1728, rb.RB_ACT_RELU, 0, 0), (1024, 1024, 512, rb.RB_ACT_RELU, 0, 0),
+    (333, 512, 1024, rb.RB_ACT_NONE, 1, 0), (130, 128, 4096, rb.RB_ACT_SIGMOID, 1, 0),
+    (77, 256, 128, rb.RB_ACT_RELU, 0, 8), (300, 384, 256, rb.RB_ACT_NONE, 1, 24)])
+def test_gemm_bf16_matches_fp64(M, N, K, act, out_f32, pad_y):
     rng = np.random.default_rng(4)
     Xd, X = _bf16_dev(rng.standard_normal((M, K)))
     Wd, W = _bf16_dev(rng.standard_normal((N, K)) / np.sqrt(K))
     b = rng.uniform(-0.5, 0.5, N).astype(np.float32)
     bd = _dev(b)
-    Y = torch.empty((M, N), dtype=torch.float32 if out_f32 else torch.int16, device=DEV)
-    rb.check(rb.lib().rb_k_gemm_bf16(_stream(), rb.dptr(Xd), K, rb.dptr(Wd), K, rb.dptr(bd), rb.dptr(Y), N, M, N, K,
-                                     act, out_f32), "gemm_bf16")
+    ldy = N + pad_y  # padded output rows: columns past N must stay untouched
+    Y = torch.full((M, ldy), -7.0 if out_f32 else 0x5a5a, dtype=torch.float32 if out_f32 else torch.int16,
+                   device=DEV)
+    rb.check(rb.lib().rb_k_gemm_bf16(_stream(), rb.dptr(Xd), K, rb.dptr(Wd), K, rb.dptr(bd), rb.dptr(Y), ldy, M, N,
+                                     K, act, out_f32), "gemm_bf16")
     torch.cuda.synchronize()
-    got = Y.cpu().numpy()
+    full = Y.cpu().numpy()
+    assert np.all(full[:, N:] == (-7.0 if out_f32 else 0x5a5a))
+    got = full[:, :N]
     if not out_f32:
         got = (got.astype(np.uint16).astype(np.uint32) << 16).view(np.float32)
     name = {0: "none", 1: "relu", 2: "sigmoid"}[act]
@@ -319,6 +324,9 @@ def test_gemm_bf16_matches_fp64(M, N, K, act, out_f32):
     assert _row_scaled_err(got, ref) <= tol
     if not out_f32:
         assert np.max(np.abs(got - ref) / np.maximum(np.abs(ref), 1e-3)) <= 2.0 ** -7
+    # the output stride must keep 16-byte row alignment
+    assert rb.lib().rb_k_gemm_bf16(_stream(), rb.dptr(Xd), K, rb.dptr(Wd), K, rb.dptr(bd), rb.dptr(Y), N + 4, M,
+                                   N, K, act, out_f32) == rb.RB_EINVAL
 
 
 @pytest.mark.parametrize("M,N,K,act", [(1, 64, 64, rb.RB_ACT_RELU), (257, 1024, 256, rb.RB_ACT_RELU),
