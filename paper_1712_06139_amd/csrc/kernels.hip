@@ -847,12 +847,18 @@ __global__ __launch_bounds__(256) void k_gemm_f32(const float* __restrict__ X, i
     if (kt + 1 < nk) stage(buf ^ 1);
     __syncthreads();
   }
-  const int col = n0 + wn * 32 + (lane & 31);
-  const float bb = bias[col];
+  // as in the bf16 GEMM: per-column bias and activation, then a quad
+  // transpose so each lane stores four consecutive columns of one row
+  const float bb = bias[n0 + wn * 32 + (lane & 31)];
+  const int colq = n0 + wn * 32 + (lane & 28);
 #pragma unroll
-  for (int r = 0; r < 16; ++r) {
-    const int row = m0 + wm * 32 + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
-    if (row < M) Y[(int64_t)row * ldy + col] = act_fn<ACT>(acc[r] + bb);
+  for (int g = 0; g < 4; ++g) {
+    float v[4];
+#pragma unroll
+    for (int k = 0; k < 4; ++k) v[k] = act_fn<ACT>(acc[4 * g + k] + bb);
+    quad_transpose4(v, lane);
+    const int row = m0 + wm * 32 + 8 * g + 4 * (lane >> 5) + (lane & 3);
+    if (row < M) *(float4*)(Y + (int64_t)row * ldy + colq) = make_float4(v[0], v[1], v[2], v[3]);
   }
 }
 
@@ -1137,7 +1143,7 @@ rb_status rb_k_gemm_f32(void* stream, const float* X, int32_t ldx, const float* 
                         float* Y, int32_t ldy, int32_t M, int32_t N, int32_t K, int32_t act,
                         const rb_k_row* skip_rows, int32_t skip_T) {
   if (M < 0 || N <= 0 || K <= 0 || (N % G32_BN) || (K % G32_BK) || ldx < K || ldw < K || ldy < N) return RB_EINVAL;
-  if ((ldx & 3) || (ldw & 3) || !X || !W || !b || !Y) return RB_EINVAL;
+  if ((ldx & 3) || (ldw & 3) || (ldy & 3) || ((uintptr_t)Y & 15) || !X || !W || !b || !Y) return RB_EINVAL;
   if (act != RB_ACT_NONE && act != RB_ACT_RELU && act != RB_ACT_SIGMOID) return RB_EINVAL;
   if (skip_rows && (skip_T <= 0 || skip_T % G32_BM)) return RB_EINVAL;
   if (M == 0) return RB_OK;
