@@ -356,8 +356,9 @@ rb_status rb_k_embbag(void* stream, const rb_k_row* rows, int32_t n_rows_total, 
 rb_status rb_k_gemm_bf16(void* stream, const void* X, int32_t ldx, const void* W, int32_t ldw,
                          const float* b, void* Y, int32_t ldy, int32_t M, int32_t N, int32_t K,
                          int32_t act, int32_t out_f32);
-/* fp32 variant (fp32 MFMA): K % 32 == 0, N % 64 == 0, ldy % 4 == 0 (Y 16-byte
- * aligned). Optional tile skip for
+/* fp32 variant (fp32 MFMA, same k order for every M): K % 32 == 0, N % 64 == 0;
+ * ldx, ldw and ldy multiples of 4 with X, W and Y 16-byte aligned; ldx and
+ * ldw < 2^23. Optional tile skip for
  * sequence groups: with skip_rows (the per-slot row map, aux = sequence length)
  * X holds skip_T rows per slot (token t of slot e at row e*skip_T + t) and a
  * 64-row block starting at token t of slot e is neither computed nor stored

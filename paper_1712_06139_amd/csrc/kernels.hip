@@ -496,7 +496,7 @@ __global__ __launch_bounds__(256) void k_embbag(const rb_k_row* __restrict__ row
   for (int c = demb + n_dense + tid; c < ldx; c += 256) xr[c] = (bf16_t)0;
 }
 
-// ---------------------------------------------------------------- bf16 GEMM
+// ---------------------------------------------------------------- GEMM (bf16 and fp32)
 
 // 4 x 4 transpose across the four lanes of a quad: lane 4q + i holding x[k] =
 // element (k, i) ends up holding x[j] = element (i, j), where element (k, c)
@@ -578,54 +578,77 @@ __device__ __forceinline__ void buffer_to_lds(i32x4_t rsrc, uint32_t voff, uint3
                : "memory", "m0");
 }
 
-// Y = act(X W^T + b): X [M, K] and W [N, K] bf16, K contiguous; fp32
-// accumulation with v_mfma_f32_32x32x16_bf16.
+// Y = act(X W^T + b): X [M, K] and W [N, K] of element type TI (bf16 or
+// fp32), K contiguous; fp32 accumulation with v_mfma_f32_32x32x16_bf16 or
+// v_mfma_f32_32x32x2f32.
 //
-// Workgroup tile BM x BN, k-step BK (32 or 64), NT/64 waves each owning a
-// WM x WN sub-tile ((WM/32) x (WN/32) accumulators). Operand tiles go straight
-// from global memory into a ring of S >= 3 LDS stages (global_load_lds: each
-// wave load instruction fills 1 KB of consecutive LDS rows of BK bf16; no
-// register staging). K-step kt reads stage kt % S while the stage of k-step
-// kt - 1 is refilled with k-step kt - 1 + S, its loads spread one every few
-// MFMAs over the step: issued back to back they stall the wave on the texture
-// path with no MFMA in flight. Each 16-deep sub-step's MFMAs have the next
-// sub-step's fragment reads between them. In the last sub-step, after half of
-// its MFMAs, the wave waits for its loads of the next k-step and for its LDS
-// reads, and all waves meet at one barrier: the next stage has landed and
-// nobody reads the current one again. The other half then runs with the next
-// k-step's first fragment reads between the MFMAs. The order of MFMAs, LDS
-// reads and loads within a step is fixed with scheduling barriers.
+// Workgroup tile BM x BN, k-step of RB bytes per row (64 or 128: 32 or 64
+// bf16, 16 or 32 fp32), NT/64 waves each owning a WM x WN sub-tile
+// ((WM/32) x (WN/32) accumulators). Operand tiles go straight from global
+// memory into a ring of S >= 3 LDS stages (global_load_lds: each wave load
+// instruction fills 1 KB of consecutive LDS rows; no register staging).
+// K-step kt reads stage kt % S while the stage of k-step kt - 1 is refilled
+// with k-step kt - 1 + S, its loads spread one every few MFMAs over the step:
+// issued back to back they stall the wave on the texture path with no MFMA in
+// flight. A sub-step covers 32 bytes of every row (16 bf16 or 8 fp32 k values)
+// and its MFMAs have the next sub-step's fragment reads between them. In the
+// last sub-step, after half of its MFMAs, the wave waits for its loads of the
+// next k-step and for its LDS reads, and all waves meet at one barrier: the
+// next stage has landed and nobody reads the current one again. The other
+// half then runs with the next k-step's first fragment reads between the
+// MFMAs. The order of MFMAs, LDS reads and loads within a step is fixed with
+// scheduling barriers.
 //
-// LDS rows hold BK/8 16-byte chunks; chunk c of row r sits at chunk
-// c ^ ((r / (16 / (BK/8))) % (BK/8)), so the 16 rows one fragment read serves
-// per LDS cycle hit 16 distinct bank groups (64 banks).
+// A fragment is 16 bytes of one row: lane l holds row l % 32 and chunk
+// 2 kk + l / 32 of sub-step kk. bf16: one 32x32x16 MFMA per accumulator and
+// sub-step. fp32: chunk c holds k = 4c .. 4c + 3, and MFMA t (t = 0..3) of the
+// sub-step takes dword t, so it adds the products of k = 8 kk + t (lanes
+// 0..31) and k = 8 kk + 4 + t (lanes 32..63); the MFMAs of a sub-step run
+// t-major over the accumulators, so two MFMAs into one accumulator are NM
+// instructions apart.
+//
+// LDS rows hold RB/16 16-byte chunks; chunk c of row r sits at chunk
+// c ^ ((r / (16 / (RB/16))) % (RB/16)), so the 16 rows one fragment read
+// serves per LDS cycle hit 16 distinct bank groups (64 banks).
 //
 // Every tile shape, k-step, stage count and tile order accumulates each output
-// element in the same k order with the same instruction, so results do not
+// element in the same k order with the same instructions, so results do not
 // depend on them, nor on which rows share a tile.
-constexpr int G16_KALIGN = 64;  // K multiple the entry point accepts
+//
+// skip_rows (sequence layout, slot e owning rows [e skip_T, (e + 1) skip_T),
+// skip_T a multiple of BM): a workgroup whose rows are all padding tokens
+// (at or past its slot's length, or in a padding slot) returns at once.
+constexpr int G16_KALIGN = 64;  // K multiple the bf16 entry point accepts
+constexpr int G32_KALIGN = 32;  // K multiple the fp32 entry point accepts
+constexpr int G32_BM = 64;      // fp32 tile height (the padding-token skip granularity)
 
-template <int BM, int BN, int WM, int WN, int NT, int BK, int S, int ORDER, int ACT, bool OUT_F32>
-__global__ __launch_bounds__(NT) void k_gemm_bf16(const bf16_t* __restrict__ X, int ldx,
-                                                  const bf16_t* __restrict__ W, int ldw,
-                                                  const float* __restrict__ bias, void* __restrict__ Y,
-                                                  int ldy, int M, int N, int K) {
+template <typename TI, int BM, int BN, int WM, int WN, int NT, int RB, int S, int ORDER, int ACT, bool OUT_F32>
+__global__ __launch_bounds__(NT) void k_gemm_mfma(const TI* __restrict__ X, int ldx, const TI* __restrict__ W,
+                                                  int ldw, const float* __restrict__ bias, void* __restrict__ Y,
+                                                  int ldy, int M, int N, int K,
+                                                  const rb_k_row* __restrict__ skip_rows, int skip_T) {
+  constexpr bool F32 = sizeof(TI) == 4;
+  constexpr int ES = sizeof(TI);  // bytes per element
+  constexpr int BK = RB / ES;     // k values per k-step
   constexpr int NW = NT / 64;
   static_assert((BM / WM) * (BN / WN) == NW, "one wave per sub-tile");
-  static_assert(BK == 32 || BK == 64, "k-step 32 or 64");
+  static_assert(RB == 64 || RB == 128, "k-step of 64 or 128 bytes per row");
   static_assert(S >= 3 && S <= 4, "3..4 stages");
-  constexpr int CPR = BK / 8;    // 16-byte chunks per LDS row
+  constexpr int CPR = RB / 16;   // 16-byte chunks per LDS row
   constexpr int RPI = 64 / CPR;  // rows filled per wave load instruction
   constexpr int SWZ = 16 / CPR;  // rows sharing one swizzle pattern
+  constexpr int EPC = 16 / ES;   // elements per chunk
   constexpr int TM = WM / 32, TN = WN / 32;
-  static_assert(TM % 2 == 0, "the last sub-step splits the A fragments in halves");
+  static_assert(TM % 2 == 0 || F32, "the last sub-step splits the A fragments in halves");
   constexpr int SA = BM / RPI / NW, SB = BN / RPI / NW;  // load instructions per wave per stage
   static_assert(SA * NW * RPI == BM && SB * NW * RPI == BN, "loads cover the tile");
   constexpr int OPS = SA + SB;
-  constexpr int KK = BK / 16;    // MFMA sub-steps per k-step
-  constexpr int NM = TM * TN;    // MFMAs per sub-step
+  constexpr int KK = RB / 32;    // MFMA sub-steps per k-step
+  constexpr int NM = TM * TN;    // accumulators
+  constexpr int MPF = F32 ? 4 : 1;  // MFMAs per accumulator and sub-step
+  constexpr int NU = NM * MPF;   // MFMAs per sub-step
   constexpr int NR = TM + TN;    // fragment reads per sub-step
-  constexpr int PRE = (KK - 1) * NM + NM / 2;  // MFMAs of a step before its barrier
+  constexpr int PRE = (KK - 1) * NU + NU / 2;  // MFMAs of a step before its barrier
   __shared__ u32x4_t sA[S][BM * CPR];
   __shared__ u32x4_t sB[S][BN * CPR];
 
@@ -636,6 +659,11 @@ __global__ __launch_bounds__(NT) void k_gemm_bf16(const bf16_t* __restrict__ X, 
   const int tile = ORDER ? xcd_tile(blockIdx.x, gridDim.x) : (int)blockIdx.x;
   const int bm = tile / tiles_n, bn = tile - bm * tiles_n;
   const int m0 = bm * BM, n0 = bn * BN;
+  if (skip_rows) {  // uniform per workgroup
+    const int e = m0 / skip_T;
+    const rb_k_row rw = skip_rows[e];
+    if (rw.src < 0 || m0 - e * skip_T >= rw.aux) return;
+  }
 
   // lane l of a load instruction fills LDS row l / CPR (of its RPI), chunk l % CPR
   const int lr = lane / CPR, lc = lane % CPR;
@@ -647,12 +675,12 @@ __global__ __launch_bounds__(NT) void k_gemm_bf16(const bf16_t* __restrict__ X, 
   for (int i = 0; i < SA; ++i) {
     const int row = (wid * SA + i) * RPI + lr;
     const int ra = min(row, M - 1 - m0);  // rows past M are computed on a copy and never stored
-    va[i] = (uint32_t)(ra * ldx + (lc ^ ((row / SWZ) % CPR)) * 8) * 2u;
+    va[i] = (uint32_t)(ra * ldx + (lc ^ ((row / SWZ) % CPR)) * EPC) * (uint32_t)ES;
   }
 #pragma unroll
   for (int i = 0; i < SB; ++i) {
     const int row = (wid * SB + i) * RPI + lr;
-    vb[i] = (uint32_t)(row * ldw + (lc ^ ((row / SWZ) % CPR)) * 8) * 2u;
+    vb[i] = (uint32_t)(row * ldw + (lc ^ ((row / SWZ) % CPR)) * EPC) * (uint32_t)ES;
   }
 
   floatx16_t acc[TM][TN];
@@ -669,24 +697,24 @@ __global__ __launch_bounds__(NT) void k_gemm_bf16(const bf16_t* __restrict__ X, 
   // never read again, so every step runs the same branch-free code.
   auto issue_one = [&](int kt, auto stc, auto oc) {
     constexpr int st = decltype(stc)::value, o = decltype(oc)::value;
-    const uint32_t kb = (uint32_t)(min(kt, nk - 1) * BK) * 2u;
+    const uint32_t kb = (uint32_t)(min(kt, nk - 1) * RB);
     if constexpr (o < SA)
       buffer_to_lds(rA, va[o], kb, lds_addr(&sA[st][0]) + (wid * SA + o) * 1024);
     else
       buffer_to_lds(rB, vb[o - SA], kb, lds_addr(&sB[st][0]) + (wid * SB + o - SA) * 1024);
   };
-  bf16x8_t fa[2][TM], fb[2][TN];
+  u32x4_t fa[2][TM], fb[2][TN];
   // fragment read q (A fragment q for q < TM, then B) of sub-step kk of stage st
   auto read_one = [&](auto stc, int kk, auto qc, auto bufc) {
     constexpr int st = decltype(stc)::value, q = decltype(qc)::value, bf = decltype(bufc)::value;
-    // MFMA operand layout: lane l holds row l % 32, k = 8 (l / 32) .. + 7 of the sub-step
+    // lane l holds row l % 32, chunk 2 kk + l / 32
     const int ch = kk * 2 + (lane >> 5);
     if constexpr (q < TM) {
       const int r = wm * WM + q * 32 + (lane & 31);
-      fa[bf][q] = __builtin_bit_cast(bf16x8_t, sA[st][r * CPR + (ch ^ ((r / SWZ) % CPR))]);
+      fa[bf][q] = sA[st][r * CPR + (ch ^ ((r / SWZ) % CPR))];
     } else {
       const int r = wn * WN + (q - TM) * 32 + (lane & 31);
-      fb[bf][q - TM] = __builtin_bit_cast(bf16x8_t, sB[st][r * CPR + (ch ^ ((r / SWZ) % CPR))]);
+      fb[bf][q - TM] = sB[st][r * CPR + (ch ^ ((r / SWZ) % CPR))];
     }
   };
   // k-step kt: stage stc, next stage nstc, refilled stage rstc (k-step kt - 1's)
@@ -695,24 +723,30 @@ __global__ __launch_bounds__(NT) void k_gemm_bf16(const bf16_t* __restrict__ X, 
       constexpr int kk = decltype(kkc)::value;
       constexpr bool last = kk == KK - 1;
       constexpr int cur = kk & 1, nxt = (kk + 1) & 1;
-      static_for<NM>([&](auto mc) {
-        constexpr int m = decltype(mc)::value;
-        if constexpr (last && m == NM / 2) {
+      static_for<NU>([&](auto uc) {
+        constexpr int u = decltype(uc)::value;
+        constexpr int m = u % NM, t = u / NM;
+        if constexpr (last && u == NU / 2) {
           wait_vmcnt_lds<(S - 2) * OPS>();
           lds_barrier();
         }
-        acc[m / TN][m % TN] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[cur][m / TN], fb[cur][m % TN],
-                                                                      acc[m / TN][m % TN], 0, 0, 0);
+        if constexpr (F32)
+          acc[m / TN][m % TN] = __builtin_amdgcn_mfma_f32_32x32x2f32(
+              __uint_as_float(fa[cur][m / TN][t]), __uint_as_float(fb[cur][m % TN][t]), acc[m / TN][m % TN], 0, 0, 0);
+        else
+          acc[m / TN][m % TN] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
+              __builtin_bit_cast(bf16x8_t, fa[cur][m / TN]), __builtin_bit_cast(bf16x8_t, fb[cur][m % TN]),
+              acc[m / TN][m % TN], 0, 0, 0);
         __builtin_amdgcn_sched_barrier(0);
         static_for<NR>([&](auto qc) {
           constexpr int q = decltype(qc)::value;
           if constexpr (!last) {
-            if constexpr (q * NM / NR == m) read_one(stc, kk + 1, qc, ic<nxt>{});
-          } else if constexpr (m >= NM / 2) {
-            if constexpr (NM / 2 + q * (NM / 2) / NR == m) read_one(nstc, 0, qc, ic<0>{});
+            if constexpr (q * NU / NR == u) read_one(stc, kk + 1, qc, ic<nxt>{});
+          } else if constexpr (u >= NU / 2) {
+            if constexpr (NU / 2 + q * (NU / 2) / NR == u) read_one(nstc, 0, qc, ic<0>{});
           }
         });
-        constexpr int pos = kk * NM + m;
+        constexpr int pos = kk * NU + u;
         static_for<OPS>([&](auto oc) {
           constexpr int o = decltype(oc)::value;
           if constexpr (o * PRE / OPS == pos) issue_one(kt - 1 + S, rstc, oc);
@@ -765,100 +799,6 @@ __global__ __launch_bounds__(NT) void k_gemm_bf16(const bf16_t* __restrict__ X, 
           }
         }
       }
-  }
-}
-
-// ---------------------------------------------------------------- fp32 GEMM
-
-// fp32 X [M, K], W [N, K]. Workgroup tile 64 x 64, k-step 32; 2 x 2 waves each
-// owning 32 x 32 with v_mfma_f32_32x32x2f32 (one k pair per instruction).
-// Tiles are kept k-major in LDS so that the 32 lanes reading one k read 32
-// consecutive floats.
-constexpr int G32_BM = 64, G32_BN = 64, G32_BK = 32, G32_PAD = 4;
-
-template <int ACT>
-__global__ __launch_bounds__(256) void k_gemm_f32(const float* __restrict__ X, int ldx,
-                                                  const float* __restrict__ W, int ldw,
-                                                  const float* __restrict__ bias, float* __restrict__ Y,
-                                                  int ldy, int M, int N, int K,
-                                                  const rb_k_row* __restrict__ skip_rows, int skip_T) {
-  __shared__ float sA[2][G32_BK][G32_BM + G32_PAD];
-  __shared__ float sB[2][G32_BK][G32_BN + G32_PAD];
-  const int tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
-  const int wm = wid >> 1, wn = wid & 1;
-  const int tiles_n = N / G32_BN;
-  const int tile = xcd_tile(blockIdx.x, gridDim.x);
-  const int bm = tile / tiles_n, bn = tile - bm * tiles_n;
-  const int m0 = bm * G32_BM, n0 = bn * G32_BN;
-  if (skip_rows) {  // a block of padding tokens only (uniform per workgroup)
-    const int e = m0 / skip_T;
-    const rb_k_row rw = skip_rows[e];
-    if (rw.src < 0 || m0 - e * skip_T >= rw.aux) return;
-  }
-  const int lrow = tid >> 3, lk = (tid & 7) * 4;
-  const float* ag[2];
-  const float* bg[2];
-#pragma unroll
-  for (int i = 0; i < 2; ++i) {
-    int ra = m0 + lrow + 32 * i;
-    ra = ra < M ? ra : M - 1;
-    ag[i] = X + (int64_t)ra * ldx + lk;
-    bg[i] = W + (int64_t)(n0 + lrow + 32 * i) * ldw + lk;
-  }
-  float4 ra_[2], rb_[2];
-  floatx16_t acc;
-#pragma unroll
-  for (int r = 0; r < 16; ++r) acc[r] = 0.f;
-  const int nk = K / G32_BK;
-  auto stage = [&](int buf) {
-#pragma unroll
-    for (int i = 0; i < 2; ++i) {
-      const int r = lrow + 32 * i;
-      sA[buf][lk + 0][r] = ra_[i].x; sA[buf][lk + 1][r] = ra_[i].y;
-      sA[buf][lk + 2][r] = ra_[i].z; sA[buf][lk + 3][r] = ra_[i].w;
-      sB[buf][lk + 0][r] = rb_[i].x; sB[buf][lk + 1][r] = rb_[i].y;
-      sB[buf][lk + 2][r] = rb_[i].z; sB[buf][lk + 3][r] = rb_[i].w;
-    }
-  };
-#pragma unroll
-  for (int i = 0; i < 2; ++i) {
-    ra_[i] = *(const float4*)(ag[i]);
-    rb_[i] = *(const float4*)(bg[i]);
-  }
-  stage(0);
-  __syncthreads();
-  for (int kt = 0; kt < nk; ++kt) {
-    const int buf = kt & 1;
-    if (kt + 1 < nk) {
-      const int k0 = (kt + 1) * G32_BK;
-#pragma unroll
-      for (int i = 0; i < 2; ++i) {
-        ra_[i] = *(const float4*)(ag[i] + k0);
-        rb_[i] = *(const float4*)(bg[i] + k0);
-      }
-    }
-#pragma unroll
-    for (int kk = 0; kk < G32_BK / 2; ++kk) {
-      const int k = kk * 2 + (lane >> 5);
-      const float a = sA[buf][k][wm * 32 + (lane & 31)];
-      const float bv = sB[buf][k][wn * 32 + (lane & 31)];
-      acc = __builtin_amdgcn_mfma_f32_32x32x2f32(a, bv, acc, 0, 0, 0);
-    }
-    if (kt + 1 < nk) stage(buf ^ 1);
-    __syncthreads();
-  }
-  // as in the bf16 GEMM: per-column bias and activation, then a quad
-  // transpose so each lane stores four consecutive columns of one row
-  const float bb = bias[n0 + wn * 32 + (lane & 31)];
-  const int colq = n0 + wn * 32 + (lane & 28);
-#pragma unroll
-  for (int g = 0; g < 4; ++g) {
-    float v[4];
-#pragma unroll
-    for (int k = 0; k < 4; ++k) v[k] = act_fn<ACT>(acc[4 * g + k] + bb);
-    quad_transpose4(v, lane);
-    const int row = m0 + wm * 32 + 8 * g + 4 * (lane >> 5) + (lane & 3);
-    if (row < M) *(float4*)(Y + (int64_t)row * ldy + colq) = make_float4(v[0], v[1], v[2], v[3]);
   }
 }
 
@@ -996,23 +936,31 @@ inline unsigned blocks_for(int64_t threads) { return (unsigned)((threads + 255) 
 
 namespace {
 
-template <int BM, int BN, int WM, int WN, int NT, int BK, int S, int ORDER>
-void launch_gemm_bf16(hipStream_t s, const bf16_t* x, int ldx, const bf16_t* w, int ldw, const float* b,
-                             void* Y, int ldy, int M, int N, int K, int act, int out_f32) {
+template <typename TI, int BM, int BN, int WM, int WN, int NT, int RB, int S, int ORDER>
+void launch_gemm(hipStream_t s, const TI* x, int ldx, const TI* w, int ldw, const float* b, void* Y, int ldy,
+                 int M, int N, int K, int act, bool out_f32, const rb_k_row* skip_rows, int skip_T) {
   const unsigned g = (unsigned)(((M + BM - 1) / BM) * (N / BN));
-#define RB_G16(A, F)                                                                                            \
-  hipLaunchKernelGGL((k_gemm_bf16<BM, BN, WM, WN, NT, BK, S, ORDER, A, F>), dim3(g), dim3(NT), 0, s, x, ldx, w, \
-                     ldw, b, Y, ldy, M, N, K)
-  if (out_f32) {
-    if (act == RB_ACT_RELU) RB_G16(RB_ACT_RELU, true);
-    else if (act == RB_ACT_SIGMOID) RB_G16(RB_ACT_SIGMOID, true);
-    else RB_G16(RB_ACT_NONE, true);
-  } else {
-    if (act == RB_ACT_RELU) RB_G16(RB_ACT_RELU, false);
-    else if (act == RB_ACT_SIGMOID) RB_G16(RB_ACT_SIGMOID, false);
-    else RB_G16(RB_ACT_NONE, false);
+#define RB_G(A, F)                                                                                              \
+  hipLaunchKernelGGL((k_gemm_mfma<TI, BM, BN, WM, WN, NT, RB, S, ORDER, A, F>), dim3(g), dim3(NT), 0, s, x, ldx, \
+                     w, ldw, b, Y, ldy, M, N, K, skip_rows, skip_T)
+  if (out_f32 || sizeof(TI) == 4) {
+    if (act == RB_ACT_RELU) RB_G(RB_ACT_RELU, true);
+    else if (act == RB_ACT_SIGMOID) RB_G(RB_ACT_SIGMOID, true);
+    else RB_G(RB_ACT_NONE, true);
+  } else if constexpr (sizeof(TI) == 2) {
+    if (act == RB_ACT_RELU) RB_G(RB_ACT_RELU, false);
+    else if (act == RB_ACT_SIGMOID) RB_G(RB_ACT_SIGMOID, false);
+    else RB_G(RB_ACT_NONE, false);
   }
-#undef RB_G16
+#undef RB_G
+}
+
+// bf16 operands, k-step BK bf16 values
+template <int BM, int BN, int WM, int WN, int NT, int BK, int S, int ORDER>
+void launch_gemm_bf16(hipStream_t s, const bf16_t* x, int ldx, const bf16_t* w, int ldw, const float* b, void* Y,
+                      int ldy, int M, int N, int K, int act, int out_f32) {
+  launch_gemm<bf16_t, BM, BN, WM, WN, NT, BK * 2, S, ORDER>(s, x, ldx, w, ldw, b, Y, ldy, M, N, K, act, out_f32 != 0,
+                                                           nullptr, 0);
 }
 
 }  // namespace
@@ -1142,22 +1090,29 @@ rb_status rb_k_gemm_bf16(void* stream, const void* X, int32_t ldx, const void* W
 rb_status rb_k_gemm_f32(void* stream, const float* X, int32_t ldx, const float* W, int32_t ldw, const float* b,
                         float* Y, int32_t ldy, int32_t M, int32_t N, int32_t K, int32_t act,
                         const rb_k_row* skip_rows, int32_t skip_T) {
-  if (M < 0 || N <= 0 || K <= 0 || (N % G32_BN) || (K % G32_BK) || ldx < K || ldw < K || ldy < N) return RB_EINVAL;
-  if ((ldx & 3) || (ldw & 3) || (ldy & 3) || ((uintptr_t)Y & 15) || !X || !W || !b || !Y) return RB_EINVAL;
+  if (M < 0 || N <= 0 || K <= 0 || (N % 64) || (K % G32_KALIGN) || ldx < K || ldw < K || ldy < N) return RB_EINVAL;
+  if ((ldx & 3) || (ldw & 3) || (ldy & 3) || !X || !W || !b || !Y) return RB_EINVAL;
+  if (((uintptr_t)X & 15) || ((uintptr_t)W & 15) || ((uintptr_t)Y & 15)) return RB_EINVAL;
+  // operand byte offsets within a 64-row tile are 32-bit
+  if ((int64_t)ldx * 4 * G32_BM >= ((int64_t)1 << 31) || (int64_t)ldw * 4 * 64 >= ((int64_t)1 << 31)) return RB_EINVAL;
   if (act != RB_ACT_NONE && act != RB_ACT_RELU && act != RB_ACT_SIGMOID) return RB_EINVAL;
   if (skip_rows && (skip_T <= 0 || skip_T % G32_BM)) return RB_EINVAL;
   if (M == 0) return RB_OK;
-  const unsigned g = (unsigned)(((M + G32_BM - 1) / G32_BM) * (N / G32_BN));
   hipStream_t s = (hipStream_t)stream;
-  if (act == RB_ACT_RELU)
-    hipLaunchKernelGGL(k_gemm_f32<RB_ACT_RELU>, dim3(g), dim3(256), 0, s, X, ldx, W, ldw, b, Y, ldy, M, N, K,
-                       skip_rows, skip_T);
-  else if (act == RB_ACT_SIGMOID)
-    hipLaunchKernelGGL(k_gemm_f32<RB_ACT_SIGMOID>, dim3(g), dim3(256), 0, s, X, ldx, W, ldw, b, Y, ldy, M, N, K,
-                       skip_rows, skip_T);
+  // 64 x 64 tiles (64 rows: the padding-token skip granularity), 4 waves of
+  // 32 x 32, k-step 16, 3 stages (24 KB LDS, six workgroups per CU). Small
+  // wave tiles keep the work per wave small, so the CUs stay evenly loaded when
+  // padding-token blocks leave holes in the grid (64 x 64 wave tiles measured
+  // up to 1.5x slower there). XCD-contiguous tile order when W fits in one
+  // XCD's L2 (each XCD then reads its X rows once; plain order measured 1.5x
+  // slower on sequence groups).
+  const bool xcd = (int64_t)N * K * 4 <= (4 << 20);
+  if (xcd)
+    launch_gemm<float, G32_BM, 64, 32, 32, 256, 64, 3, 1>(s, X, ldx, W, ldw, b, Y, ldy, M, N, K, act, true, skip_rows,
+                                                          skip_T);
   else
-    hipLaunchKernelGGL(k_gemm_f32<RB_ACT_NONE>, dim3(g), dim3(256), 0, s, X, ldx, W, ldw, b, Y, ldy, M, N, K,
-                       skip_rows, skip_T);
+    launch_gemm<float, G32_BM, 64, 32, 32, 256, 64, 3, 0>(s, X, ldx, W, ldw, b, Y, ldy, M, N, K, act, true, skip_rows,
+                                                          skip_T);
   return launch_status();
 }
 

@@ -330,7 +330,8 @@ def test_gemm_bf16_matches_fp64(M, N, K, act, out_f32, pad_y):
 
 
 @pytest.mark.parametrize("M,N,K,act", [(1, 64, 64, rb.RB_ACT_RELU), (257, 1024, 256, rb.RB_ACT_RELU),
-                                       (1000, 64, 1024, rb.RB_ACT_NONE), (64 * 64, 512, 256, rb.RB_ACT_RELU)])
+                                       (1000, 64, 1024, rb.RB_ACT_NONE), (64 * 64, 512, 256, rb.RB_ACT_RELU),
+                                       (300, 1024, 1088, rb.RB_ACT_SIGMOID), (70, 192, 32, rb.RB_ACT_RELU)])
 def test_gemm_f32_matches_fp64(M, N, K, act):
     rng = np.random.default_rng(5)
     X = rng.standard_normal((M, K)).astype(np.float32)
@@ -341,8 +342,41 @@ def test_gemm_f32_matches_fp64(M, N, K, act):
     rb.check(rb.lib().rb_k_gemm_f32(_stream(), rb.dptr(Xd), K, rb.dptr(Wd), K, rb.dptr(bd),
                                     rb.dptr(Y), N, M, N, K, act, None, 0), "gemm_f32")
     torch.cuda.synchronize()
-    ref = nx.dense(X, W, b, "relu" if act == rb.RB_ACT_RELU else "none")
+    ref = nx.dense(X, W, b, {rb.RB_ACT_NONE: "none", rb.RB_ACT_RELU: "relu", rb.RB_ACT_SIGMOID: "sigmoid"}[act])
     assert _row_scaled_err(Y.cpu().numpy(), ref) <= 1e-5
+
+
+@pytest.mark.parametrize("dtype,N,K", [("f32", 512, 256), ("f32", 1024, 1088), ("bf16", 512, 256),
+                                        ("bf16", 1024, 2112)])
+def test_gemm_rows_independent_of_batch(dtype, N, K):
+    # a row's output bits do not depend on how many rows share the launch or on
+    # where it sits among them: the same k order for every M, tile shape and
+    # tile order (K = 1088 / 2112 puts W above 4 MB: plain tile order; the bf16
+    # launch of all rows takes a larger tile than the partial ones)
+    rng = np.random.default_rng(11)
+    M = 16384
+    X = rng.standard_normal((M, K)).astype(np.float32)
+    W = (rng.standard_normal((N, K)) / np.sqrt(K)).astype(np.float32)
+    b = rng.uniform(-0.5, 0.5, N).astype(np.float32)
+    bd = _dev(b)
+    if dtype == "f32":
+        Xd, Wd = _dev(X), _dev(W)
+        esz, call = 4, rb.lib().rb_k_gemm_f32
+        extra = (None, 0)
+    else:
+        Xd, _ = _bf16_dev(X)
+        Wd, _ = _bf16_dev(W)
+        esz, call = 2, rb.lib().rb_k_gemm_bf16
+        extra = (1,)
+    Y = torch.empty((M, N), dtype=torch.float32, device=DEV)
+    rb.check(call(_stream(), rb.dptr(Xd), K, rb.dptr(Wd), K, rb.dptr(bd), rb.dptr(Y), N, M, N, K,
+                  rb.RB_ACT_RELU, *extra), "gemm")
+    for r0, m in ((0, 1), (8191, 1), (M - 1, 1), (64, 300), (10257, 443)):
+        Yp = torch.empty((m, N), dtype=torch.float32, device=DEV)
+        rb.check(call(_stream(), rb.dptr(Xd) + r0 * K * esz, K, rb.dptr(Wd), K, rb.dptr(bd), rb.dptr(Yp), N, m,
+                      N, K, rb.RB_ACT_RELU, *extra), "gemm")
+        torch.cuda.synchronize()
+        assert torch.equal(Yp, Y[r0:r0 + m]), (r0, m)
 
 
 @pytest.mark.parametrize("T", [64, 128, 256])
