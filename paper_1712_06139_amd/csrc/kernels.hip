@@ -623,10 +623,9 @@ constexpr int G32_KALIGN = 32;  // K multiple the fp32 entry point accepts
 constexpr int G32_BM = 64;      // fp32 tile height (the padding-token skip granularity)
 
 template <typename TI, int BM, int BN, int WM, int WN, int NT, int RB, int S, int ORDER, int ACT, bool OUT_F32>
-__global__ __launch_bounds__(NT) void k_gemm_mfma(const TI* __restrict__ X, int ldx, const TI* __restrict__ W,
-                                                  int ldw, const float* __restrict__ bias, void* __restrict__ Y,
-                                                  int ldy, int M, int N, int K,
-                                                  const rb_k_row* __restrict__ skip_rows, int skip_T) {
+__device__ __forceinline__ void gemm_mfma(const TI* __restrict__ X, int ldx, const TI* __restrict__ W, int ldw,
+                                          const float* __restrict__ bias, void* __restrict__ Y, int ldy, int M,
+                                          int N, int K, const rb_k_row* __restrict__ skip_rows, int skip_T) {
   constexpr bool F32 = sizeof(TI) == 4;
   constexpr int ES = sizeof(TI);  // bytes per element
   constexpr int BK = RB / ES;     // k values per k-step
@@ -802,6 +801,24 @@ __global__ __launch_bounds__(NT) void k_gemm_mfma(const TI* __restrict__ X, int 
   }
 }
 
+// The two operand types as separately named kernels (so that traces and
+// counters tell them apart).
+template <int BM, int BN, int WM, int WN, int NT, int RB, int S, int ORDER, int ACT, bool OUT_F32>
+__global__ __launch_bounds__(NT) void k_gemm_bf16(const bf16_t* __restrict__ X, int ldx,
+                                                  const bf16_t* __restrict__ W, int ldw,
+                                                  const float* __restrict__ bias, void* __restrict__ Y, int ldy,
+                                                  int M, int N, int K) {
+  gemm_mfma<bf16_t, BM, BN, WM, WN, NT, RB, S, ORDER, ACT, OUT_F32>(X, ldx, W, ldw, bias, Y, ldy, M, N, K, nullptr, 0);
+}
+template <int BM, int BN, int WM, int WN, int NT, int RB, int S, int ORDER, int ACT>
+__global__ __launch_bounds__(NT) void k_gemm_f32(const float* __restrict__ X, int ldx, const float* __restrict__ W,
+                                                 int ldw, const float* __restrict__ bias, void* __restrict__ Y,
+                                                 int ldy, int M, int N, int K,
+                                                 const rb_k_row* __restrict__ skip_rows, int skip_T) {
+  gemm_mfma<float, BM, BN, WM, WN, NT, RB, S, ORDER, ACT, true>(X, ldx, W, ldw, bias, Y, ldy, M, N, K, skip_rows,
+                                                                skip_T);
+}
+
 // ---------------------------------------------------------------- heads and split
 
 // One wave per row: a K-long dot product (lane-strided, then a butterfly),
@@ -940,19 +957,29 @@ template <typename TI, int BM, int BN, int WM, int WN, int NT, int RB, int S, in
 void launch_gemm(hipStream_t s, const TI* x, int ldx, const TI* w, int ldw, const float* b, void* Y, int ldy,
                  int M, int N, int K, int act, bool out_f32, const rb_k_row* skip_rows, int skip_T) {
   const unsigned g = (unsigned)(((M + BM - 1) / BM) * (N / BN));
-#define RB_G(A, F)                                                                                              \
-  hipLaunchKernelGGL((k_gemm_mfma<TI, BM, BN, WM, WN, NT, RB, S, ORDER, A, F>), dim3(g), dim3(NT), 0, s, x, ldx, \
-                     w, ldw, b, Y, ldy, M, N, K, skip_rows, skip_T)
-  if (out_f32 || sizeof(TI) == 4) {
-    if (act == RB_ACT_RELU) RB_G(RB_ACT_RELU, true);
-    else if (act == RB_ACT_SIGMOID) RB_G(RB_ACT_SIGMOID, true);
-    else RB_G(RB_ACT_NONE, true);
-  } else if constexpr (sizeof(TI) == 2) {
-    if (act == RB_ACT_RELU) RB_G(RB_ACT_RELU, false);
-    else if (act == RB_ACT_SIGMOID) RB_G(RB_ACT_SIGMOID, false);
-    else RB_G(RB_ACT_NONE, false);
-  }
+  if constexpr (sizeof(TI) == 4) {
+#define RB_G(A)                                                                                                     \
+  hipLaunchKernelGGL((k_gemm_f32<BM, BN, WM, WN, NT, RB, S, ORDER, A>), dim3(g), dim3(NT), 0, s, x, ldx, w, ldw, b, \
+                     Y, ldy, M, N, K, skip_rows, skip_T)
+    if (act == RB_ACT_RELU) RB_G(RB_ACT_RELU);
+    else if (act == RB_ACT_SIGMOID) RB_G(RB_ACT_SIGMOID);
+    else RB_G(RB_ACT_NONE);
 #undef RB_G
+  } else {
+#define RB_G(A, F)                                                                                             \
+  hipLaunchKernelGGL((k_gemm_bf16<BM, BN, WM, WN, NT, RB, S, ORDER, A, F>), dim3(g), dim3(NT), 0, s, x, ldx, w, \
+                     ldw, b, Y, ldy, M, N, K)
+    if (out_f32) {
+      if (act == RB_ACT_RELU) RB_G(RB_ACT_RELU, true);
+      else if (act == RB_ACT_SIGMOID) RB_G(RB_ACT_SIGMOID, true);
+      else RB_G(RB_ACT_NONE, true);
+    } else {
+      if (act == RB_ACT_RELU) RB_G(RB_ACT_RELU, false);
+      else if (act == RB_ACT_SIGMOID) RB_G(RB_ACT_SIGMOID, false);
+      else RB_G(RB_ACT_NONE, false);
+    }
+#undef RB_G
+  }
 }
 
 // bf16 operands, k-step BK bf16 values
