@@ -52,6 +52,7 @@ DESCRIPTION = {
     "ragged_seq": "ragged sequences: fp32 per-token 256-512(ReLU)-256, masked mean-pool, 256-2 softmax; 50k requests "
                   "of 1-4 sequences of 1-512 tokens; length buckets {64,128,256,512}, max 64 sequences per batch",
 }
+PACK_NOTE = "; token-wise layers on the real tokens packed into consecutive rows (sub-graph batching)"
 
 
 def log(msg):
@@ -68,7 +69,8 @@ def algorithmic_work(w, t, a, logd, qindex):
     dimensions; padded rows count as rows, since the method pads them and
     computes them. Sequence groups: padding tokens are not written by the
     assembler and 64-token blocks of them are not computed by the GEMMs (the
-    pooling never reads them), so both count real tokens only."""
+    pooling never reads them; with --seq-pack the layers run on the real tokens
+    alone), so both count real tokens only."""
     work = collections.defaultdict(lambda: {"bytes": 0, "flops": 0})
     nb = logd["n_batches"]
     beg = logd["b_req_begin"][:nb + 1]
@@ -184,7 +186,7 @@ def cpu_baseline(w, t, a, seconds):
             "cpu_model": cpu_model(), "one_thread": one}
 
 
-def serving_rate(w, t, a, ctx, models, n):
+def serving_rate(w, t, a, ctx, models, n, seq_pack=False):
     """The serving API with host payloads: the first n requests submitted in
     arrival order from host memory (rb_submit copies them), every batch run
     as soon as it closes (rb_run_next: one launch chain per batch, payload
@@ -195,7 +197,7 @@ def serving_rate(w, t, a, ctx, models, n):
     from paper_1712_06139_amd import rb
     from paper_1712_06139_amd.deploy import Deployment
     n = min(n, t.n)
-    dep = Deployment(w, ctx, device=True, models=models)
+    dep = Deployment(w, ctx, device=True, models=models, seq_pack=seq_pack)
     try:
         payloads = [a.payload(r) for r in range(n)]
         qs = [dep.queue_for(t, r) for r in range(n)]
@@ -250,7 +252,7 @@ def _subset(t, a, idx):
     return st, synth.Arenas(dense, lens, ids, doff, loff, ioff)
 
 
-def calibrate_latency(w, t, a, dt, ctx, dep, window):
+def calibrate_latency(w, t, a, dt, ctx, dep, window, seq_pack=False):
     """Per-request latency on the simulated clock (nearest-rank p50 / p99).
     Each queue's service time per batch size is measured on this GPU: the
     queue's first requests of the trace replayed through a queue whose every
@@ -287,7 +289,8 @@ def calibrate_latency(w, t, a, dt, ctx, dep, window):
         for P in sizes:
             cw = synth.Workload(w.name, w.wid, (w.models[m_idx],),
                                 (synth.Queue(0, P, (P,), None, q.bucket_len),), len(idx), w.rows, w.rate_per_s)
-            cdep = Deployment(cw, ctx, device=True, window_batches=window, models=[dep.models[m_idx]])
+            cdep = Deployment(cw, ctx, device=True, window_batches=window, models=[dep.models[m_idx]],
+                              seq_pack=seq_pack)
             try:
                 if prefix:
                     out_off = cdep.out_offsets(st)
@@ -356,6 +359,8 @@ def main():
     ap.add_argument("--warmup", type=int, default=2)
     ap.add_argument("--workload", default="ranking", choices=sorted(DESCRIPTION))
     ap.add_argument("--window", type=int, default=64, help="dispatched batches per launch window")
+    ap.add_argument("--seq-pack", action="store_true",
+                    help="sequence models: pack the real tokens of each launch group (no time padding)")
     ap.add_argument("--streams", type=int, default=8,
                     help="HIP streams for concurrent launch chains of different models")
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
@@ -401,7 +406,7 @@ def main():
 
     def make(window, profile=False, n_streams=1):
         d = Deployment(w, ctx, device=True, window_batches=window, profile=profile, models=shared.get("m"),
-                       n_streams=n_streams)
+                       n_streams=n_streams, seq_pack=args.seq_pack)
         shared.setdefault("m", d.models)
         return d
 
@@ -503,13 +508,13 @@ def main():
 
     latency = None
     if not args.no_latency:
-        latency = calibrate_latency(w, t, a, dt, ctx, dep, args.window)
+        latency = calibrate_latency(w, t, a, dt, ctx, dep, args.window, args.seq_pack)
         log(f"latency: {json.dumps(latency)}")
 
     serving = None
     if args.serving_requests > 0:
         log(f"serving API with host payloads ({args.serving_requests} requests)")
-        serving = serving_rate(w, t, a, ctx, shared["m"], args.serving_requests)
+        serving = serving_rate(w, t, a, ctx, shared["m"], args.serving_requests, args.seq_pack)
         log(f"serving: {json.dumps(serving)}")
 
     cpu = None
@@ -522,7 +527,8 @@ def main():
         "metric": METRIC, "value": round(value, 1), "unit": "examples/s", "n_gpus": 1, "steps": args.steps,
         "warmup": args.warmup, "ms_per_step": round(ms_per_step, 3), "higher_is_better": True, "scaling": "weak",
         "vs_baseline": None, "dtype": dtypes.pop() if len(dtypes) == 1 else "bf16+f32", "data": "synthetic",
-        "config": {"workload": DESCRIPTION[w.name], "requests_per_step": t.n, "examples_per_step": examples,
+        "config": {"workload": DESCRIPTION[w.name] + (PACK_NOTE if args.seq_pack and w.name == "ragged_seq" else ""),
+                   "requests_per_step": t.n, "examples_per_step": examples,
                    "batches_per_step": n_batches, "window_batches": args.window, "streams": args.streams,
                    "parallelism": "single GPU"},
         "latency": latency,

@@ -135,6 +135,13 @@ typedef struct {
    * Each model keeps one stream, assigned in order of first use, so its
    * chains stay in order; outputs do not depend on this setting. */
   int32_t n_streams;
+  /* Device mode, fp32 seqpool models: 1 packs the real tokens of a launch
+   * group's sequences into consecutive rows (no time padding) for the
+   * token-wise layers, then pools each sequence from its own rows (the
+   * sub-graph batching the paper's Batch/Unbatch operations allow, section on
+   * batching); 0 pads every sequence to its queue's bucket. Outputs are
+   * identical either way. */
+  int32_t seq_pack;
 } rb_sched_opts;
 
 /* One scheduler owns one HIP stream of the context's device (device mode),
@@ -299,10 +306,12 @@ rb_status rb_sim_run(rb_sched* s, const rb_servable* servables, int32_t n_servab
  * device arrays too. */
 
 /* A request of a launch group: [dense_off, dense_end) of the dense arena,
- * lens from lens_off, [ids_off, ids_end) of the ids arena, output at out_off. */
+ * lens from lens_off, [ids_off, ids_end) of the ids arena, output at out_off;
+ * tok_off (seqpool): the row of the request's first token among the group's
+ * packed tokens (the requests' token counts summed in group order). */
 typedef struct {
   int64_t dense_off, dense_end, lens_off, ids_off, ids_end, out_off;
-  int32_t n_rows, pad_;
+  int32_t n_rows, tok_off;
 } rb_k_req;
 
 typedef struct {
@@ -315,13 +324,16 @@ typedef struct {
 
 /* Per padded row: src = element offset of the row's dense input (-1: padding),
  * aux = ranking: offset of the row's first id; seqpool: sequence length,
- * lens = ranking: offset of the row's bag lengths, out = offset of the row's
- * output (-1: padding). */
+ * lens = ranking: offset of the row's bag lengths; seqpool: the row of the
+ * sequence's first token among the group's packed tokens (its request's
+ * tok_off plus the tokens of the request's earlier sequences; -1 when the
+ * request is rejected), out = offset of the row's output (-1: padding). */
 typedef struct {
   int64_t src, aux, lens, out;
 } rb_k_row;
 
-/* Row routing (exclusive prefix scans): fills rows[row_base .. row_base + P)
+/* Row routing (exclusive prefix scans; the concatenation of a batch's request
+ * tensors in the paper's batching section): fills rows[row_base .. row_base + P)
  * of every batch (P <= RB_MAX_BATCH_ROWS; every request has >= 1 row). kind = RB_MODEL_*; d_in floats per row (per token for
  * seqpool); d_out floats per output row; n_tables bags per ranking row.
  * A request whose payload does not match its n_rows (dense length, bag
@@ -333,10 +345,13 @@ rb_status rb_k_route(void* stream, int32_t kind, const rb_k_batch* batches, int3
 /* Gather rows into X [n_rows_total, ldx] (ldx >= d_in, columns [d_in, ldx)
  * zeroed), padding rows set to pad; out_bf16 != 0 writes bf16 (RNE), else fp32.
  * Seqpool (seq_T > 0): row r*T + t is token t of sequence slot r (pad past L).
- * seq_real_only != 0 (seqpool, fp32 out, n_rows_total a multiple of seq_T):
+ * seq_real_only == 1 (seqpool, fp32 out, n_rows_total a multiple of seq_T):
  * rows t >= L and every row of a padding slot are not written and keep
  * whatever X held; every layer maps row i to row i alone and the pooling reads
- * t < L only, so no value there reaches an output. */
+ * t < L only, so no value there reaches an output.
+ * seq_real_only == 2: packed tokens: token t of slot r goes to row
+ * rows[r].lens + t (n_rows_total / seq_T slots; those rows must lie below
+ * n_rows_total, else *err = 1 and the sequence is not copied). */
 rb_status rb_k_assemble(void* stream, const rb_k_row* rows, int32_t n_rows_total, int32_t seq_T,
                         int32_t seq_real_only, const float* dense, int64_t dense_len, int32_t d_in, void* X,
                         int32_t ldx, int32_t out_bf16, float pad, int32_t* err);
@@ -375,10 +390,12 @@ rb_status rb_k_head(void* stream, const rb_k_row* rows, int32_t n_rows_total, co
 /* Seqpool head fused with the split: per sequence slot r with L = rows[r].aux
  * real tokens (clamped to [0, seq_T]), pooled = mean of H[r*T + t, :D] over t < L (fp32; tokens past L
  * are never read), then out[rows[r].out + j] = act(Wh pooled + bh)[j], j < n_out
- * (act RB_ACT_SOFTMAX or RB_ACT_NONE; D <= 1024, n_out <= 16). */
-rb_status rb_k_seqpool(void* stream, const rb_k_row* rows, int32_t n_seqs, int32_t seq_T, const float* H,
-                       int32_t ldh, int32_t D, const float* Wh, const float* bh, int32_t n_out, int32_t act,
-                       float* out);
+ * (act RB_ACT_SOFTMAX or RB_ACT_NONE; D <= 1024, n_out <= 16).
+ * packed_rows > 0: packed tokens: token t of slot r is row rows[r].lens + t of
+ * H [packed_rows, ldh]; a sequence whose rows would leave H pools nothing. */
+rb_status rb_k_seqpool(void* stream, const rb_k_row* rows, int32_t n_seqs, int32_t seq_T, int64_t packed_rows,
+                       const float* H, int32_t ldh, int32_t D, const float* Wh, const float* bh, int32_t n_out,
+                       int32_t act, float* out);
 /* Split: out[rows[r].out + j] = Y[r, j] for real rows, j < d_out. */
 rb_status rb_k_split(void* stream, const rb_k_row* rows, int32_t n_rows_total, const float* Y, int32_t ldy,
                      int32_t d_out, float* out);

@@ -101,7 +101,9 @@ __device__ __forceinline__ int64_t block_exclusive_scan(int64_t v, int64_t* s_w,
 //  3. exclusive scan of those counts over the batch's rows; a row's first id
 //     (token) is its request's base plus the scan difference to the request's
 //     first row; each request is checked against its payload extent;
-//  4. the row map entries, then padding rows.
+//  4. the row map entries, then padding rows. A sequence's entry also names
+//     the row of its first token when the group's real tokens are packed
+//     (its request's first packed row, set by the host, plus the scan).
 __global__ __launch_bounds__(256) void k_route(int kind, const rb_k_batch* __restrict__ batches,
                                                const rb_k_req* __restrict__ reqs,
                                                const int32_t* __restrict__ lens, int d_in, int d_out,
@@ -198,7 +200,7 @@ __global__ __launch_bounds__(256) void k_route(int kind, const rb_k_batch* __res
       if (kind == RB_MODEL_SEQPOOL) {
         rw.src = ok ? rq.dense_off + within * d_in : -1;
         rw.aux = ok ? s_ex[p + 1] - s_ex[p] : 0;
-        rw.lens = rq.lens_off + e;
+        rw.lens = ok ? rq.tok_off + within : -1;  // first row among the group's packed tokens
       } else {
         rw.src = ok ? rq.dense_off + (int64_t)e * d_in : -1;
         rw.aux = rq.ids_off + within;
@@ -225,18 +227,20 @@ __global__ __launch_bounds__(256) void k_route(int kind, const rb_k_batch* __res
 // [16 j, 16 j + 16) of slot e that lie below its length L (8 columns per thread
 // and chunk, two chunks in flight, columns past d_in zeroed); blocks past L,
 // rows t >= L and padding slots are not written (8..64-token blocks and 1..4
-// chunks in flight measured no faster). lg_c = log2(ldx / 8) when that is a power of two,
-// else -1.
+// chunks in flight measured no faster). Token t goes to row e T + t of X, or,
+// with PACKED, to row rows[e].lens + t of the group's packed tokens (x_rows
+// rows). lg_c = log2(ldx / 8) when that is a power of two, else -1.
 constexpr int SEQ_TOK = 16, SEQ_U = 2;
+template <bool PACKED>
 __global__ __launch_bounds__(256) void k_assemble_seq(const rb_k_row* __restrict__ rows, int T,
                                                       const float* __restrict__ dense, int64_t dense_len, int d_in,
-                                                      float* __restrict__ X, int ldx, int* __restrict__ err,
-                                                      int lg_c) {
+                                                      float* __restrict__ X, int ldx, int64_t x_rows,
+                                                      int* __restrict__ err, int lg_c) {
   const rb_k_row rw = rows[blockIdx.x];
   const int t0 = blockIdx.y * SEQ_TOK;
   if (rw.src < 0 || t0 >= rw.aux) return;
   const int64_t L = rw.aux;
-  if (L > T || rw.src + L * d_in > dense_len) {
+  if (L > T || rw.src + L * d_in > dense_len || (PACKED && (rw.lens < 0 || rw.lens + L > x_rows))) {
     if (threadIdx.x == 0) *err = 1;
     return;
   }
@@ -244,7 +248,7 @@ __global__ __launch_bounds__(256) void k_assemble_seq(const rb_k_row* __restrict
   const int n_tok = (int)min((int64_t)SEQ_TOK, L - t0);
   const int total = n_tok * cpr;
   const float* src = dense + rw.src + (int64_t)t0 * d_in;
-  float* xb = X + ((int64_t)blockIdx.x * T + t0) * ldx;
+  float* xb = X + ((PACKED ? rw.lens : (int64_t)blockIdx.x * T) + t0) * ldx;
   const bool vec = (d_in & 3) == 0 && (rw.src & 3) == 0;
   // SEQ_U chunks per thread and step: all loads issued before the stores
   for (int base = threadIdx.x; base < total; base += 256 * SEQ_U) {
@@ -850,19 +854,21 @@ constexpr int POOL_MAX_D = 1024, POOL_MAX_OUT = 16;
 // fixed-order reductions and thread 0 applies the softmax and writes the
 // request's output row.
 __global__ __launch_bounds__(256) void k_seqpool(const rb_k_row* __restrict__ rows, int n_seqs, int T,
-                                                 const float* __restrict__ H, int ldh, int D,
+                                                 int64_t packed_rows, const float* __restrict__ H, int ldh, int D,
                                                  const float* __restrict__ Wh,
                                                  const float* __restrict__ bh, int n_out, int act,
                                                  float* __restrict__ out) {
   const int r = blockIdx.x;
   const rb_k_row rw = rows[r];
   if (rw.out < 0) return;
-  const int L = (int)min(max(rw.aux, (int64_t)0), (int64_t)T);  // reads stay inside the slot
+  int L = (int)min(max(rw.aux, (int64_t)0), (int64_t)T);  // reads stay inside the slot
+  // packed tokens: the sequence's rows [rows[r].lens, + L) of packed_rows
+  if (packed_rows > 0 && (rw.lens < 0 || rw.lens + L > packed_rows)) L = 0;
   const int tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
   __shared__ float psum[4][POOL_MAX_D];
   __shared__ float pooled[POOL_MAX_D];
   __shared__ float part[4][POOL_MAX_OUT];
-  const float* h = H + (int64_t)r * T * ldh;
+  const float* h = H + (packed_rows > 0 ? rw.lens : (int64_t)r * T) * ldh;
   const int t0 = (int)((int64_t)L * wid / 4), t1 = (int)((int64_t)L * (wid + 1) / 4);
   if ((D & 3) == 0 && (ldh & 3) == 0) {
     for (int c = lane * 4; c < D; c += 256) {
@@ -1032,13 +1038,18 @@ rb_status rb_k_assemble(void* stream, const rb_k_row* rows, int32_t n_rows_total
                         int32_t ldx, int32_t out_bf16, float pad, int32_t* err) {
   if (n_rows_total < 0 || seq_T < 0 || d_in < 1 || ldx < d_in || (ldx & 7) || !rows || !X || !err)
     return RB_EINVAL;
+  if (seq_real_only < 0 || seq_real_only > 2) return RB_EINVAL;
   if (seq_real_only && (seq_T == 0 || n_rows_total % seq_T || out_bf16)) return RB_EINVAL;
   if (n_rows_total == 0) return RB_OK;
   auto lg2 = [](int v) { int l = 0; while ((1 << l) < v) ++l; return (1 << l) == v ? l : -1; };
   if (seq_real_only) {
     const dim3 grid(n_rows_total / seq_T, (seq_T + SEQ_TOK - 1) / SEQ_TOK);
-    hipLaunchKernelGGL(k_assemble_seq, grid, dim3(256), 0, (hipStream_t)stream, rows, seq_T, dense, dense_len, d_in,
-                       (float*)X, ldx, err, lg2(ldx / 8));
+    if (seq_real_only == 2)
+      hipLaunchKernelGGL(k_assemble_seq<true>, grid, dim3(256), 0, (hipStream_t)stream, rows, seq_T, dense, dense_len,
+                         d_in, (float*)X, ldx, (int64_t)n_rows_total, err, lg2(ldx / 8));
+    else
+      hipLaunchKernelGGL(k_assemble_seq<false>, grid, dim3(256), 0, (hipStream_t)stream, rows, seq_T, dense,
+                         dense_len, d_in, (float*)X, ldx, (int64_t)n_rows_total, err, lg2(ldx / 8));
     return launch_status();
   }
   const int64_t threads = (int64_t)n_rows_total * (ldx / 8);
@@ -1158,16 +1169,17 @@ rb_status rb_k_head(void* stream, const rb_k_row* rows, int32_t n_rows_total, co
   return launch_status();
 }
 
-rb_status rb_k_seqpool(void* stream, const rb_k_row* rows, int32_t n_seqs, int32_t seq_T, const float* H,
-                       int32_t ldh, int32_t D, const float* Wh, const float* bh, int32_t n_out, int32_t act,
-                       float* out) {
-  if (n_seqs < 0 || seq_T < 1 || D < 1 || D > POOL_MAX_D || ldh < D || n_out < 1 || n_out > POOL_MAX_OUT)
+rb_status rb_k_seqpool(void* stream, const rb_k_row* rows, int32_t n_seqs, int32_t seq_T, int64_t packed_rows,
+                       const float* H, int32_t ldh, int32_t D, const float* Wh, const float* bh, int32_t n_out,
+                       int32_t act, float* out) {
+  if (n_seqs < 0 || seq_T < 1 || packed_rows < 0 || D < 1 || D > POOL_MAX_D || ldh < D || n_out < 1 ||
+      n_out > POOL_MAX_OUT)
     return RB_EINVAL;
   if (act != RB_ACT_NONE && act != RB_ACT_SOFTMAX) return RB_EINVAL;
   if (!rows || !H || !Wh || !bh || !out) return RB_EINVAL;
   if (n_seqs == 0) return RB_OK;
-  hipLaunchKernelGGL(k_seqpool, dim3(n_seqs), dim3(256), 0, (hipStream_t)stream, rows, n_seqs, seq_T, H, ldh, D,
-                     Wh, bh, n_out, act, out);
+  hipLaunchKernelGGL(k_seqpool, dim3(n_seqs), dim3(256), 0, (hipStream_t)stream, rows, n_seqs, seq_T, packed_rows, H,
+                     ldh, D, Wh, bh, n_out, act, out);
   return launch_status();
 }
 

@@ -144,8 +144,10 @@ struct Group {  // the batches of one queue inside one window
   rb_queue* q = nullptr;
   std::vector<rb_k_batch> batches;
   std::vector<rb_k_req> reqs;
-  int64_t slots = 0;  // sum of padded sizes
+  int64_t slots = 0;   // sum of padded sizes
+  int64_t tokens = 0;  // seqpool: real tokens of its requests (packed rows)
 };
+
 
 struct Slot {
   hipEvent_t ev = nullptr;
@@ -474,16 +476,19 @@ rb_status run_group(rb_sched* s, hipStream_t st_h, const Group& g, const rb_k_ba
   const int Kp0 = m->layers[0].Kp;
   // sequence groups: padding tokens are not assembled and 64-token blocks of
   // them are not computed (every layer is row-wise and the pooling reads
-  // tokens t < L only)
-  const bool seq_skip = m->kind == RB_MODEL_SEQPOOL && g.q->bucket % 64 == 0;
+  // tokens t < L only); with seq_pack the real tokens are packed into g.tokens
+  // consecutive rows and the layers run on those rows alone
+  const bool pack = m->kind == RB_MODEL_SEQPOOL && s->opts.seq_pack && !bf16;
+  const bool seq_skip = m->kind == RB_MODEL_SEQPOOL && !pack && g.q->bucket % 64 == 0;
+  const int64_t Ml = pack ? g.tokens : M;  // rows of the layers
   if (m->kind == RB_MODEL_RANKING) {
     RB_LAUNCH(s, st_h, "embbag", rb_k_embbag(hs, w->rows, (int)slots, lens, ids, ids_len, (const void* const*)m->tables_dev,
                                        m->n_tables, m->table_rows, m->emb_dim, dense, m->n_dense, w->X, Kp0, pad,
                                        s->err_dev));
   } else {
     RB_LAUNCH(s, st_h, "assemble", rb_k_assemble(hs, w->rows, (int)M, m->kind == RB_MODEL_SEQPOOL ? g.q->bucket : 0,
-                                           seq_skip ? 1 : 0, dense, dense_len, m->d_in, w->X, Kp0, bf16 ? 1 : 0,
-                                           pad, s->err_dev));
+                                           pack ? 2 : (seq_skip ? 1 : 0), dense, dense_len, m->d_in, w->X, Kp0,
+                                           bf16 ? 1 : 0, pad, s->err_dev));
   }
   const size_t nL = m->layers.size() - (m->head_last ? 1 : 0);
   void* h = w->X;
@@ -493,11 +498,11 @@ rb_status run_group(rb_sched* s, hipStream_t st_h, const Group& g, const rb_k_ba
     const bool last = (i + 1 == nL) && !m->head_last;
     void* y = last ? (void*)w->Y : (i % 2 == 0 ? w->A : w->B);
     if (bf16) {
-      RB_LAUNCH(s, st_h, "gemm_bf16", rb_k_gemm_bf16(hs, h, ldh, L.w, L.Kp, L.b, y, L.Np, (int)M, L.Np, L.Kp, L.act,
+      RB_LAUNCH(s, st_h, "gemm_bf16", rb_k_gemm_bf16(hs, h, ldh, L.w, L.Kp, L.b, y, L.Np, (int)Ml, L.Np, L.Kp, L.act,
                                                last ? 1 : 0));
     } else {
       RB_LAUNCH(s, st_h, "gemm_f32", rb_k_gemm_f32(hs, (const float*)h, ldh, (const float*)L.w, L.Kp, L.b, (float*)y,
-                                             L.Np, (int)M, L.Np, L.Kp, L.act, seq_skip ? w->rows : nullptr,
+                                             L.Np, (int)Ml, L.Np, L.Kp, L.act, seq_skip ? w->rows : nullptr,
                                              seq_skip ? g.q->bucket : 0));
     }
     h = y;
@@ -507,8 +512,9 @@ rb_status run_group(rb_sched* s, hipStream_t st_h, const Group& g, const rb_k_ba
     const DevLayer& L = m->layers.back();
     RB_LAUNCH(s, st_h, "head", rb_k_head(hs, w->rows, (int)slots, h, ldh, L.w, m->head_bias, L.K, L.act, out));
   } else if (m->kind == RB_MODEL_SEQPOOL) {
-    RB_LAUNCH(s, st_h, "seqpool", rb_k_seqpool(hs, w->rows, (int)slots, g.q->bucket, (const float*)h, ldh, m->sp_in,
-                                         m->sp_w, m->sp_b, m->sp_out, m->sp_act, out));
+    RB_LAUNCH(s, st_h, "seqpool", rb_k_seqpool(hs, w->rows, (int)slots, g.q->bucket, pack ? std::max<int64_t>(Ml, 1) : 0,
+                                         (const float*)h, ldh, m->sp_in, m->sp_w, m->sp_b, m->sp_out, m->sp_act,
+                                         out));
   } else {
     RB_LAUNCH(s, st_h, "split", rb_k_split(hs, w->rows, (int)slots, w->Y, ldh, m->d_out, out));
   }
@@ -618,6 +624,17 @@ void close_window(rb_sched* s) {
 }
 
 // Add a dispatched batch (its requests already described) to the window.
+// Seqpool: give request r its first packed token row in group g and count its
+// tokens (its dense extent over d_in, at most n_rows full buckets: a request
+// whose extent is inconsistent is rejected by the routing, and the packed rows
+// of the group never exceed its padded token rows).
+void add_tokens(Group& g, const rb_model* m, rb_k_req& r) {
+  r.tok_off = (int32_t)g.tokens;
+  if (m->kind != RB_MODEL_SEQPOOL) return;
+  const int64_t t = (r.dense_end - r.dense_off) / m->d_in;
+  g.tokens += std::min<int64_t>(std::max<int64_t>(t, 0), (int64_t)r.n_rows * g.q->bucket);
+}
+
 void window_add(rb_sched* s, rb_queue* q, const Batch& b, std::vector<rb_k_req>& reqs) {
   Group* g = nullptr;
   for (Group& x : s->window)
@@ -635,6 +652,7 @@ void window_add(rb_sched* s, rb_queue* q, const Batch& b, std::vector<rb_k_req>&
   kb.real = b.s;
   kb.seq_T = q->m->kind == RB_MODEL_SEQPOOL ? q->bucket : 0;
   g->batches.push_back(kb);
+  for (rb_k_req& r : reqs) add_tokens(*g, q->m, r);
   g->reqs.insert(g->reqs.end(), reqs.begin(), reqs.end());
   g->slots += b.P;
   s->window_batches++;
@@ -849,6 +867,7 @@ rb_status rb_sched_create(rb_ctx* ctx, const rb_sched_opts* o, rb_sched** out) {
   if (o->mode != RB_MODE_DEVICE && o->mode != RB_MODE_NO_DEVICE) return RB_EINVAL;
   if (o->mode == RB_MODE_DEVICE && ctx->device < 0) return RB_EDEVICE;
   if (o->window_batches < 1 || o->n_streams < 0 || o->n_streams > RB_MAX_STREAMS) return RB_EINVAL;
+  if (o->seq_pack < 0 || o->seq_pack > 1) return RB_EINVAL;
   if (o->profile < 0 || o->profile > 2) return RB_EINVAL;
   rb_sched* s = new (std::nothrow) rb_sched();
   if (!s) return RB_ENOMEM;
@@ -1127,6 +1146,7 @@ static rb_status run_serving_batch(rb_sched* s, rb_queue* q, const Batch& b) {
     kr.ids_end = ci + (int64_t)h.ids.size();
     kr.out_off = co;
     kr.n_rows = h.n_rows;
+    add_tokens(g, m, kr);
     std::memcpy(sl->host + o_dense + cd * 4, h.dense.data(), h.dense.size() * 4);
     if (!h.lens.empty()) std::memcpy(sl->host + o_lens + cl * 4, h.lens.data(), h.lens.size() * 4);
     if (!h.ids.empty()) std::memcpy(sl->host + o_ids + ci * 4, h.ids.data(), h.ids.size() * 4);

@@ -38,7 +38,8 @@ class DeviceTrace:
 class Deployment:
     def __init__(self, w, ctx: rb.Ctx, device: bool = True, window_batches: int = 1, pad_value: float = 0.0,
                  profile: int = 0, service_ns: Optional[Sequence[Sequence[int]]] = None,
-                 with_params: bool = True, models: Optional[List[rb.Model]] = None, n_streams: int = 1):
+                 with_params: bool = True, models: Optional[List[rb.Model]] = None, n_streams: int = 1,
+                 seq_pack: bool = False):
         import synth
         self.w = w
         self.ctx = ctx
@@ -62,7 +63,7 @@ class Deployment:
                                              np.zeros(m.head.fan_out, np.float32), m.head.act),
                                             shapes=shapes, table_rows=m.table_rows))
         self.sched = rb.Sched(ctx, device=device, window_batches=window_batches, pad_value=pad_value,
-                              profile=profile, n_streams=n_streams)
+                              profile=profile, n_streams=n_streams, seq_pack=seq_pack)
         self.queues: List[rb.Queue] = []
         for qi, q in enumerate(w.queues):
             svc = None if service_ns is None else service_ns[qi]

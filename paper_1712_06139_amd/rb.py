@@ -51,7 +51,7 @@ class rb_model_desc(C.Structure):
 
 class rb_sched_opts(C.Structure):
     _fields_ = [("mode", C.c_int32), ("window_batches", C.c_int32), ("pad_value", C.c_float),
-                ("profile", C.c_int32), ("n_streams", C.c_int32)]
+                ("profile", C.c_int32), ("n_streams", C.c_int32), ("seq_pack", C.c_int32)]
 
 
 class rb_queue_opts(C.Structure):
@@ -92,7 +92,7 @@ class rb_log(C.Structure):
 class rb_k_req(C.Structure):
     _fields_ = [("dense_off", C.c_int64), ("dense_end", C.c_int64), ("lens_off", C.c_int64),
                 ("ids_off", C.c_int64), ("ids_end", C.c_int64), ("out_off", C.c_int64),
-                ("n_rows", C.c_int32), ("pad_", C.c_int32)]
+                ("n_rows", C.c_int32), ("tok_off", C.c_int32)]
 
 
 class rb_k_batch(C.Structure):
@@ -106,7 +106,7 @@ class rb_k_row(C.Structure):
 
 # numpy views of the device-side descriptor records
 K_REQ_DTYPE = np.dtype([("dense_off", "<i8"), ("dense_end", "<i8"), ("lens_off", "<i8"), ("ids_off", "<i8"),
-                        ("ids_end", "<i8"), ("out_off", "<i8"), ("n_rows", "<i4"), ("pad_", "<i4")])
+                        ("ids_end", "<i8"), ("out_off", "<i8"), ("n_rows", "<i4"), ("tok_off", "<i4")])
 K_BATCH_DTYPE = np.dtype([("req_begin", "<i4"), ("n_req", "<i4"), ("row_base", "<i4"), ("padded", "<i4"),
                           ("real", "<i4"), ("seq_T", "<i4")])
 K_ROW_DTYPE = np.dtype([("src", "<i8"), ("aux", "<i8"), ("lens", "<i8"), ("out", "<i8")])
@@ -149,8 +149,8 @@ _SIGS = {
                                   C.c_void_p, C.c_int32]),
     "rb_k_head": (C.c_int32, [C.c_void_p, C.c_void_p, C.c_int32, C.c_void_p, C.c_int32, C.c_void_p, C.c_float,
                               C.c_int32, C.c_int32, C.c_void_p]),
-    "rb_k_seqpool": (C.c_int32, [C.c_void_p, C.c_void_p, C.c_int32, C.c_int32, C.c_void_p, C.c_int32, C.c_int32,
-                                 C.c_void_p, C.c_void_p, C.c_int32, C.c_int32, C.c_void_p]),
+    "rb_k_seqpool": (C.c_int32, [C.c_void_p, C.c_void_p, C.c_int32, C.c_int32, C.c_int64, C.c_void_p, C.c_int32,
+                                 C.c_int32, C.c_void_p, C.c_void_p, C.c_int32, C.c_int32, C.c_void_p]),
     "rb_k_split": (C.c_int32, [C.c_void_p, C.c_void_p, C.c_int32, C.c_void_p, C.c_int32, C.c_int32,
                                C.c_void_p]),
 }
@@ -295,9 +295,9 @@ class Queue:
 
 class Sched:
     def __init__(self, ctx: Ctx, device: bool = True, window_batches: int = 1, pad_value: float = 0.0,
-                 profile: int = 0, n_streams: int = 1):
+                 profile: int = 0, n_streams: int = 1, seq_pack: bool = False):
         o = rb_sched_opts(RB_MODE_DEVICE if device else RB_MODE_NO_DEVICE, window_batches, pad_value,
-                          int(profile), n_streams)
+                          int(profile), n_streams, int(seq_pack))
         h = C.c_void_p()
         check(_lib().rb_sched_create(ctx.h, C.byref(o), C.byref(h)), "rb_sched_create")
         self.h = h

@@ -95,6 +95,9 @@ def test_stream_count_bounds(ctx):
     assert status(lambda: rb.Sched(ctx, device=False, n_streams=-1)) == rb.RB_EINVAL
     assert status(lambda: rb.Sched(ctx, device=False, n_streams=17)) == rb.RB_EINVAL
     rb.Sched(ctx, device=False, n_streams=16).destroy()
+    assert status(lambda: rb.Sched(ctx, device=False, seq_pack=2)) == rb.RB_EINVAL
+    assert status(lambda: rb.Sched(ctx, device=False, seq_pack=-1)) == rb.RB_EINVAL
+    rb.Sched(ctx, device=False, seq_pack=True).destroy()
     assert status(lambda: rb.Sched(ctx, device=False, profile=3)) == rb.RB_EINVAL
     assert status(lambda: rb.Sched(ctx, device=False, profile=-1)) == rb.RB_EINVAL
 

@@ -51,12 +51,12 @@ def row_scaled_err(y, ref):
     return float(np.max(np.abs(y.astype(np.float64) - ref) / scale))
 
 
-def run(ctx, name, n, window=1, pad=0.0, profile=False, n_streams=1):
+def run(ctx, name, n, window=1, pad=0.0, profile=False, n_streams=1, seq_pack=False):
     w = synth.workload(name)
     t, a = trace_and_arenas(name, n)
     svc = service_table(w)
     dep = Deployment(w, ctx, device=True, window_batches=window, pad_value=pad, service_ns=svc, profile=profile,
-                     n_streams=n_streams)
+                     n_streams=n_streams, seq_pack=seq_pack)
     try:
         dt = dep.upload(t, a)
         log = dep.replay(dt)
@@ -120,6 +120,21 @@ def test_outputs_independent_of_stream_count(ctx, name, n_streams):
     check_outputs(name, t, a, outk, out_off, range(0, t.n, 7))
 
 
+@pytest.mark.parametrize("window,pad", [(1, 0.0), (16, float("nan"))])
+def test_packed_tokens_match_padded(ctx, window, pad):
+    # sub-graph batching of the token-wise layers (real tokens packed, no time
+    # padding): same batches, outputs bit-identical to the padded path, so
+    # within the oracle's tolerance too
+    name = "ragged_seq"
+    n = min(PREFIX[name], 1500)
+    w, t, a, qindex, log0, out0, out_off = run(ctx, name, n, window=window)
+    _, _, _, _, log1, out1, _ = run(ctx, name, n, window=window, pad=pad, seq_pack=True)
+    assert lib_batches(log0, qindex) == lib_batches(log1, qindex)
+    assert np.isfinite(out1).all()
+    assert np.array_equal(out0, out1)
+    check_outputs(name, t, a, out1, out_off, range(0, t.n, 5))
+
+
 def test_serving_api_matches_oracle(ctx):
     name = "small_mlp"
     w = synth.workload(name)
@@ -150,10 +165,10 @@ def test_serving_api_matches_oracle(ctx):
 
 
 def test_serving_api_ranking_and_seqpool(ctx):
-    for name, n in (("ranking", 120), ("ragged_seq", 60)):
+    for name, n, pack in (("ranking", 120, False), ("ragged_seq", 60, False), ("ragged_seq", 60, True)):
         w = synth.workload(name)
         t, a = trace_and_arenas(name, n)
-        dep = Deployment(w, ctx, device=True)
+        dep = Deployment(w, ctx, device=True, seq_pack=pack)
         try:
             ids = []
             maxlen = dep.max_len(t)
@@ -207,5 +222,31 @@ def test_device_bounds_errors_are_reported(ctx):
         dt = dep.upload(t, a)
         dep.replay(dt)
         dep.sched.sync()
+    finally:
+        dep.destroy()
+
+
+def test_packed_tokens_bounds_errors_are_reported(ctx):
+    # sequence lengths that disagree with a request's tokens: the routing
+    # rejects the request, the packed rows of the others stay where the host
+    # put them, and the scheduler keeps serving
+    name = "ragged_seq"
+    w = synth.workload(name)
+    t, a = trace_and_arenas(name, 200)
+    dep = Deployment(w, ctx, device=True, window_batches=8, seq_pack=True)
+    try:
+        for k in (3, 40):
+            bad_lens = a.lens.copy()
+            bad_lens[k] += 1 if k == 3 else 10_000
+            a2 = synth.Arenas(a.dense, bad_lens, a.ids, a.dense_off, a.lens_off, a.ids_off)
+            dt = dep.upload(t, a2)
+            dep.replay(dt)
+            with pytest.raises(rb.RBError) as e:
+                dep.sched.sync()
+            assert e.value.status == rb.RB_ERANGE
+        dt = dep.upload(t, a)
+        dep.replay(dt)
+        dep.sched.sync()
+        check_outputs(name, t, a, dt.out.cpu().numpy(), dt.out_off, range(t.n))
     finally:
         dep.destroy()

@@ -69,8 +69,11 @@ def _make_group(rng, kind, n_batches, B, allowed, d_in, d_out, n_tables=0, seq_T
         row_base += P
     kb = np.array(batches, dtype=np.int32).view(rb.K_BATCH_DTYPE).ravel()
     kr = np.zeros(len(reqs), dtype=rb.K_REQ_DTYPE)
+    tok = 0  # seqpool: each request's first row among the group's packed tokens
     for i, r in enumerate(reqs):
-        kr[i] = r + (0,)
+        kr[i] = r + (tok,)
+        if kind == rb.RB_MODEL_SEQPOOL:
+            tok += (r[1] - r[0]) // d_in
     arena = dict(dense=np.concatenate(dense), lens=np.concatenate(lens) if lens_off else np.zeros(1, np.int32),
                  ids=np.concatenate(ids) if ids_off else np.zeros(1, np.int32), out_len=out_off)
     return kb, kr, arena, row_base
@@ -102,7 +105,7 @@ def _expected_rows(kind, kb, kr, arena, d_in, d_out, n_tables=0):
                 L = arena["lens"][q["lens_off"]:q["lens_off"] + n]
                 t0 = np.concatenate([[0], np.cumsum(L)[:-1]])
                 for e in range(n):
-                    rows[d0 + e] = (q["dense_off"] + t0[e] * d_in, int(L[e]), q["lens_off"] + e,
+                    rows[d0 + e] = (q["dense_off"] + t0[e] * d_in, int(L[e]), q["tok_off"] + t0[e],
                                     q["out_off"] + e * d_out)
             else:
                 id0 = q["ids_off"]
@@ -159,6 +162,44 @@ def test_assemble_bit_exact(bf16, d_in, ldx):
         blk = got[b["row_base"]:b["row_base"] + b["padded"]]
         assert np.array_equal(blk[:, :d_in], ref, equal_nan=True)
         assert np.all(blk[:, d_in:] == 0)
+
+
+@pytest.mark.parametrize("T,ldx", [(64, 16), (48, 24), (128, 16)])
+def test_assemble_seq_packed_bit_exact(T, ldx):
+    # packed tokens: the real tokens of every sequence of the group in
+    # consecutive rows (request order, then sequence order), nothing else written
+    rng = np.random.default_rng(6)
+    d_in = 16
+    kb, kr, arena, R = _make_group(rng, rb.RB_MODEL_SEQPOOL, 5, 16, (8, 16), d_in, 2, 0, T, max_n=4)
+    rows, err = _route(rb.RB_MODEL_SEQPOOL, kb, kr, arena, R, d_in, 2)
+    dense = _dev(arena["dense"])
+    M = R * T
+    X = torch.full((M, ldx), -3.0, dtype=torch.float32, device=DEV)
+    rb.check(rb.lib().rb_k_assemble(_stream(), rb.dptr(rows), M, T, 2, rb.dptr(dense), dense.numel(), d_in,
+                                    rb.dptr(X), ldx, 0, float("nan"), rb.dptr(err)), "rb_k_assemble")
+    torch.cuda.synchronize()
+    assert int(err.item()) == 0
+    got = X.cpu().numpy()
+    n_tok = int(sum((q["dense_end"] - q["dense_off"]) // d_in for q in kr))
+    want = np.concatenate([arena["dense"][q["dense_off"]:q["dense_end"]].reshape(-1, d_in) for b in kb
+                           for q in kr[b["req_begin"]:b["req_begin"] + b["n_req"]]])
+    assert want.shape[0] == n_tok
+    assert np.array_equal(got[:n_tok, :d_in], want)
+    assert np.all(got[:n_tok, d_in:] == 0)
+    assert np.all(got[n_tok:] == -3.0)
+    # a packed row past the arena is reported, and nothing is written for it
+    r_np = _rows_np(rows).copy()
+    live = np.flatnonzero(r_np["src"] >= 0)
+    r_np["lens"][live[-1]] = M - 1
+    rows_bad = _dev(r_np.view(np.uint8))
+    err2 = _err()
+    X2 = torch.full((M, ldx), -3.0, dtype=torch.float32, device=DEV)
+    rb.check(rb.lib().rb_k_assemble(_stream(), rb.dptr(rows_bad), M, T, 2, rb.dptr(dense), dense.numel(), d_in,
+                                    rb.dptr(X2), ldx, 0, 0.0, rb.dptr(err2)), "rb_k_assemble")
+    torch.cuda.synchronize()
+    L_last = int(r_np["aux"][live[-1]])
+    assert int(err2.item()) == (1 if L_last > 1 else 0)
+    assert np.all(X2.cpu().numpy()[M - 1, :d_in] == (-3.0 if L_last > 1 else want[-1]))
 
 
 @pytest.mark.parametrize("T,ldx,skip", [(64, 16, 0), (48, 16, 0), (64, 24, 0), (128, 16, 0), (128, 16, 1),
@@ -464,10 +505,23 @@ def test_seqpool_matches_oracle(S, T, D):
     rows = _rows_dev(np.zeros(S), L, out_idx)
     out = torch.full((S * n_out,), -7.0, device=DEV)
     Hd, Whd, bhd = _dev(Hn), _dev(Wh), _dev(bh)
-    rb.check(rb.lib().rb_k_seqpool(_stream(), rb.dptr(rows), S, T, rb.dptr(Hd), D, D, rb.dptr(Whd),
+    rb.check(rb.lib().rb_k_seqpool(_stream(), rb.dptr(rows), S, T, 0, rb.dptr(Hd), D, D, rb.dptr(Whd),
                                    rb.dptr(bhd), n_out, rb.RB_ACT_SOFTMAX, rb.dptr(out)), "seqpool")
+    # the same sequences packed: sequence s's tokens at rows [off_s, off_s + L_s)
+    # of a [sum L, D] matrix, with NaN rows after it
+    off = np.concatenate([[0], np.cumsum(L)[:-1]])
+    Hp = np.concatenate([H[s * T:s * T + L[s]] for s in range(S)] + [np.full((7, D), np.nan, np.float32)])
+    a = np.zeros(S, dtype=rb.K_ROW_DTYPE)
+    a["src"], a["aux"], a["lens"], a["out"] = 0, L, off, out_idx
+    rows_p = _dev(a.view(np.uint8))
+    out_p = torch.full((S * n_out,), -7.0, device=DEV)
+    Hpd = _dev(Hp)
+    rb.check(rb.lib().rb_k_seqpool(_stream(), rb.dptr(rows_p), S, T, int(L.sum()), rb.dptr(Hpd), D, D, rb.dptr(Whd),
+                                   rb.dptr(bhd), n_out, rb.RB_ACT_SOFTMAX, rb.dptr(out_p)), "seqpool packed")
     torch.cuda.synchronize()
     o = out.cpu().numpy().reshape(S, n_out)
+    # same partition of each sequence, same order: bit-identical to the slot layout
+    assert np.array_equal(out_p.cpu().numpy().reshape(S, n_out), o)
     for s in range(S):
         if out_idx[s] < 0:
             assert np.all(o[s] == -7.0)
