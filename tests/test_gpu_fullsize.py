@@ -77,3 +77,30 @@ def test_full_trace(ctx, name):
         worst = max(worst, e)
         assert e <= RTOL[w.models[s].dtype], (name, r, e)
     print(f"{name}: {t.n} requests, {len(ours)} batches, {len(reqs)} sampled, worst row-scaled error {worst:.3g}")
+
+
+def test_full_ragged_seq_packed_tokens_bit_identical(ctx):
+    # the whole ragged-sequence trace with the token-wise layers on packed
+    # real tokens: the same batches, and every output bit-identical to the
+    # padded path (whose sampled outputs test_full_trace checks against the
+    # oracle)
+    name = "ragged_seq"
+    w = synth.workload(name)
+    t = synth.trace(w)
+    a = synth.arenas(t)
+    svc = service_table(w)
+    logs, outs = [], []
+    for pack in (False, True):
+        dep = Deployment(w, ctx, device=True, window_batches=WINDOW, service_ns=svc, seq_pack=pack)
+        try:
+            dt = dep.upload(t, a)
+            log = dep.replay(dt)
+            dep.sched.sync()
+            logs.append(lib_batches(log, dep.qindex))
+            outs.append(dt.out.cpu().numpy())
+            del dt
+        finally:
+            dep.destroy()
+    assert logs[0] == logs[1]
+    assert np.isfinite(outs[1]).all()
+    assert np.array_equal(outs[0], outs[1])
