@@ -481,7 +481,7 @@ def main():
         roof = {"bound": "hbm", "achieved": round(ach, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
                 "frac": round(ach / HBM_PEAK_GBS, 4)}
         roof["algorithmic_bytes_per_launch"] = round(wk["bytes"] / dk["launches"])
-    roof["traffic"] = recorded_traffic(w.name, dom)
+    roof["traffic"] = recorded_traffic(w.name + ("_packed" if args.seq_pack and w.name == "ragged_seq" else ""), dom)
     if "cold_avg_us" in dk:
         roof["cold"] = {"avg_launch_us": dk["cold_avg_us"],
                         "achieved": round(roof["achieved"] * dk["avg_us"] / dk["cold_avg_us"], 2),
