@@ -252,6 +252,73 @@ def _subset(t, a, idx):
     return st, synth.Arenas(dense, lens, ids, doff, loff, ioff)
 
 
+def version_swap(w, t, a, dt, ctx, args):
+    """Version transitions under load (availability-preserving policy): a
+    loader thread keeps building new versions of the largest servable while
+    the main thread replays the trace; after each step a loaded version
+    replaces the old one (rb_queue_set_model) and the old one is destroyed
+    (freed on the library's deleter thread). Step times with loading against
+    the same deployment's steps without it."""
+    import threading
+    import synth
+    from paper_1712_06139_amd.deploy import Deployment
+
+    def size(s):
+        p = synth.model_params(w, s)
+        return sum(W.size for W, _ in p.weights) + sum(T.size for T in p.tables)
+    S = max(range(len(w.models)), key=size)
+    versions = [synth.model_params(w, S), synth.next_version(synth.model_params(w, S))]
+    dep = Deployment(w, ctx, device=True, window_batches=args.window, n_streams=args.streams, seq_pack=args.seq_pack)
+    st = {"ready": None, "stop": False, "load_s": []}
+
+    def step():
+        t0 = time.perf_counter()
+        dep.replay(dt)
+        dep.sched.sync()
+        return (time.perf_counter() - t0) * 1e3
+
+    def loader():
+        v = 1
+        while not st["stop"]:
+            if st["ready"] is None:
+                t0 = time.perf_counter()
+                m = dep.build_model(S, versions[v % 2])
+                st["load_s"].append(time.perf_counter() - t0)
+                st["ready"] = m
+                v += 1
+            else:
+                time.sleep(0.001)
+
+    try:
+        for _ in range(2):
+            step()
+        idle = [step() for _ in range(args.version_swap)]
+        th = threading.Thread(target=loader)
+        th.start()
+        busy, swaps, t_end = [], 0, time.perf_counter() + 60
+        while (len(busy) < args.version_swap or swaps < 3) and time.perf_counter() < t_end:
+            busy.append(step())
+            m = st["ready"]
+            if m is not None:
+                dep.swap(S, m).destroy()
+                st["ready"] = None
+                swaps += 1
+        st["stop"] = True
+        th.join()
+        if st["ready"] is not None:
+            st["ready"].destroy()
+    finally:
+        dep.destroy()
+
+    def pct(v, q):
+        return round(float(np.percentile(v, q)), 3)
+    return {"policy": "availability-preserving", "servable": S, "versions_swapped": swaps,
+            "load_ms_mean": round(1e3 * float(np.mean(st["load_s"])), 1) if st["load_s"] else None,
+            "steps_idle": len(idle), "steps_loading": len(busy),
+            "ms_per_step_idle": {"p50": pct(idle, 50), "p99": pct(idle, 99), "max": round(max(idle), 3)},
+            "ms_per_step_loading": {"p50": pct(busy, 50), "p99": pct(busy, 99), "max": round(max(busy), 3)}}
+
+
 def calibrate_latency(w, t, a, dt, ctx, dep, window, seq_pack=False):
     """Per-request latency on the simulated clock (nearest-rank p50 / p99).
     Each queue's service time per batch size is measured on this GPU: the
@@ -359,6 +426,8 @@ def main():
     ap.add_argument("--warmup", type=int, default=2)
     ap.add_argument("--workload", default="ranking", choices=sorted(DESCRIPTION))
     ap.add_argument("--window", type=int, default=64, help="dispatched batches per launch window")
+    ap.add_argument("--version-swap", type=int, default=0,
+                    help="also time this many steps while new versions of the largest servable load and swap in")
     ap.add_argument("--seq-pack", action="store_true",
                     help="sequence models: pack the real tokens of each launch group (no time padding)")
     ap.add_argument("--streams", type=int, default=8,
@@ -517,6 +586,12 @@ def main():
         serving = serving_rate(w, t, a, ctx, shared["m"], args.serving_requests, args.seq_pack)
         log(f"serving: {json.dumps(serving)}")
 
+    swap = None
+    if args.version_swap > 0:
+        log(f"version transitions under load ({args.version_swap} steps)")
+        swap = version_swap(w, t, a, dt, ctx, args)
+        log(f"version swap: {json.dumps(swap)}")
+
     cpu = None
     if not args.no_cpu_baseline:
         log("timing the CPU oracle")
@@ -539,6 +614,7 @@ def main():
         "roofline": roof,
         "cpu_baseline": cpu,
         "serving_pcie": serving,
+        **({"version_swap": swap} if swap is not None else {}),
     }
     print(json.dumps(out), flush=True)
     dep.destroy()

@@ -23,6 +23,7 @@
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
+#include <atomic>
 #include <climits>
 #include <cmath>
 #include <condition_variable>
@@ -105,7 +106,12 @@ struct rb_model {
   float* sp_w = nullptr;
   float* sp_b = nullptr;
   int sp_in = 0, sp_out = 0, sp_act = 0;
-  int bound = 0;
+  std::atomic<int> bound{0};  // queues serving it
+  // versions of one servable share a lineage: a scheduler keys its work
+  // buffers and launch stream by lineage, so a new version takes them over
+  // in stream order (rb_queue_set_model)
+  int64_t lineage = 0;
+  hipStream_t upload = nullptr;  // private non-blocking stream of rb_model_create
   std::vector<void*> allocs;
   std::vector<hipStream_t> used;  // streams that ran this model
 };
@@ -193,7 +199,7 @@ struct rb_sched {
   std::vector<hipStream_t> lanes;
   std::vector<hipEvent_t> lane_done;
   hipEvent_t ev_copy = nullptr;
-  std::map<int64_t, int> lane_of;  // model id -> lane, in order of first use
+  std::map<int64_t, int> lane_of;  // model lineage -> lane, in order of first use
   // cold-cache profiling: written before every timed launch
   void* scrub = nullptr;
   std::vector<rb_queue*> queues;  // by id; null once destroyed
@@ -258,6 +264,14 @@ rb_status dev_alloc(rb_model* m, size_t bytes, void** out) {
   return RB_OK;
 }
 
+// Host -> device copy of model data on the model's private non-blocking
+// stream: a version loaded while a scheduler serves neither waits for nor
+// holds up the scheduler's streams (the null stream would); only the loading
+// thread waits, for its own copy.
+bool copy_h2d(rb_model* m, void* dst, const void* src, size_t n) {
+  return hip_ok(hipMemcpyAsync(dst, src, n, hipMemcpyHostToDevice, m->upload)) && hip_ok(hipStreamSynchronize(m->upload));
+}
+
 bool valid_hidden_act(int a) { return a == RB_ACT_NONE || a == RB_ACT_RELU; }
 bool valid_last_act(int a) { return a == RB_ACT_NONE || a == RB_ACT_RELU || a == RB_ACT_SIGMOID; }
 
@@ -275,19 +289,19 @@ rb_status upload_layer(rb_model* m, const rb_layer_desc& L, DevLayer& d, bool bf
     for (int j = 0; j < d.N; ++j)
       for (int k = 0; k < d.K; ++k) h[(size_t)j * d.Kp + k] = host_f2bf(L.w[(size_t)j * d.K + k]);
     if ((st = dev_alloc(m, n * 2, &d.w)) != RB_OK) return st;
-    if (!hip_ok(hipMemcpy(d.w, h.data(), n * 2, hipMemcpyHostToDevice))) return RB_EDEVICE;
+    if (!copy_h2d(m, d.w, h.data(), n * 2)) return RB_EDEVICE;
   } else {
     std::vector<float> h(n, 0.f);
     for (int j = 0; j < d.N; ++j) std::memcpy(&h[(size_t)j * d.Kp], L.w + (size_t)j * d.K, sizeof(float) * d.K);
     if ((st = dev_alloc(m, n * 4, &d.w)) != RB_OK) return st;
-    if (!hip_ok(hipMemcpy(d.w, h.data(), n * 4, hipMemcpyHostToDevice))) return RB_EDEVICE;
+    if (!copy_h2d(m, d.w, h.data(), n * 4)) return RB_EDEVICE;
   }
   std::vector<float> hb(d.Np, 0.f);
   std::memcpy(hb.data(), L.b, sizeof(float) * d.N);
   void* pb = nullptr;
   if ((st = dev_alloc(m, (size_t)d.Np * 4, &pb)) != RB_OK) return st;
   d.b = (float*)pb;
-  if (!hip_ok(hipMemcpy(d.b, hb.data(), (size_t)d.Np * 4, hipMemcpyHostToDevice))) return RB_EDEVICE;
+  if (!copy_h2d(m, d.b, hb.data(), (size_t)d.Np * 4)) return RB_EDEVICE;
   return RB_OK;
 }
 
@@ -421,13 +435,13 @@ void sync_all(rb_sched* s) {
 // Stream of a model's launch chains in a replay.
 hipStream_t lane_for(rb_sched* s, const rb_model* m) {
   if (s->lanes.empty()) return s->stream;
-  auto it = s->lane_of.find(m->id);
-  if (it == s->lane_of.end()) it = s->lane_of.emplace(m->id, (int)(s->lane_of.size() % s->lanes.size())).first;
+  auto it = s->lane_of.find(m->lineage);
+  if (it == s->lane_of.end()) it = s->lane_of.emplace(m->lineage, (int)(s->lane_of.size() % s->lanes.size())).first;
   return s->lanes[(size_t)it->second];
 }
 
 rb_status ensure_work(rb_sched* s, rb_model* m, int64_t rows, int64_t slots, Work** out) {
-  Work& w = s->work[m->id];
+  Work& w = s->work[m->lineage];
   if (rows > w.rows_cap || slots > w.slots_cap) {
     // capacities only grow (both at once), so groups of different shapes
     // never make the buffers shrink and grow back
@@ -744,7 +758,11 @@ rb_status rb_model_create(rb_ctx* ctx, const rb_model_desc* d, rb_model** out) {
   rb_model* m = new (std::nothrow) rb_model();
   if (!m) return RB_ENOMEM;
   m->ctx = ctx;
-  m->id = ctx->next_model_id++;
+  {
+    std::lock_guard<std::mutex> lk(ctx->mu);
+    m->id = ctx->next_model_id++;
+  }
+  m->lineage = m->id;
   m->kind = d->kind;
   m->dtype = d->dtype;
   m->d_in = d->kind == RB_MODEL_RANKING ? d->n_dense : d->layers[0].fan_in;
@@ -755,7 +773,13 @@ rb_status rb_model_create(rb_ctx* ctx, const rb_model_desc* d, rb_model** out) {
   m->table_rows = d->table_rows;
   m->head_last = d->kind != RB_MODEL_SEQPOOL && d->dtype == RB_DT_BF16 && last.fan_out == 1 && d->n_layers >= 2 &&
                  (last.act == RB_ACT_SIGMOID || last.act == RB_ACT_NONE);
-  if (dev) hipSetDevice(ctx->device);
+  if (dev) {
+    hipSetDevice(ctx->device);
+    if (!hip_ok(hipStreamCreateWithFlags(&m->upload, hipStreamNonBlocking))) {
+      delete m;
+      return RB_EDEVICE;
+    }
+  }
   m->layers.resize(d->n_layers);
   rb_status st = RB_OK;
   for (int i = 0; i < d->n_layers && st == RB_OK; ++i) {
@@ -772,7 +796,7 @@ rb_status rb_model_create(rb_ctx* ctx, const rb_model_desc* d, rb_model** out) {
         std::vector<uint16_t> h(H.Kp, 0);
         for (int k = 0; k < L.fan_in; ++k) h[k] = host_f2bf(L.w[k]);
         st = dev_alloc(m, (size_t)H.Kp * 2, &H.w);
-        if (st == RB_OK && !hip_ok(hipMemcpy(H.w, h.data(), (size_t)H.Kp * 2, hipMemcpyHostToDevice))) st = RB_EDEVICE;
+        if (st == RB_OK && !copy_h2d(m, H.w, h.data(), (size_t)H.Kp * 2)) st = RB_EDEVICE;
         m->head_bias = L.b[0];
       }
     } else {
@@ -790,7 +814,7 @@ rb_status rb_model_create(rb_ctx* ctx, const rb_model_desc* d, rb_model** out) {
       for (size_t i = 0; i < per; ++i) h[i] = host_f2bf(d->tables[t][i]);
       void* p = nullptr;
       st = dev_alloc(m, per * 2, &p);
-      if (st == RB_OK && !hip_ok(hipMemcpy(p, h.data(), per * 2, hipMemcpyHostToDevice))) st = RB_EDEVICE;
+      if (st == RB_OK && !copy_h2d(m, p, h.data(), per * 2)) st = RB_EDEVICE;
       m->tables.push_back(p);
     }
     if (st == RB_OK) {
@@ -798,7 +822,7 @@ rb_status rb_model_create(rb_ctx* ctx, const rb_model_desc* d, rb_model** out) {
       st = dev_alloc(m, sizeof(void*) * d->n_tables, &p);
       m->tables_dev = (void**)p;
       if (st == RB_OK &&
-          !hip_ok(hipMemcpy(m->tables_dev, m->tables.data(), sizeof(void*) * d->n_tables, hipMemcpyHostToDevice)))
+          !copy_h2d(m, m->tables_dev, m->tables.data(), sizeof(void*) * d->n_tables))
         st = RB_EDEVICE;
     }
   }
@@ -811,20 +835,25 @@ rb_status rb_model_create(rb_ctx* ctx, const rb_model_desc* d, rb_model** out) {
       const size_t nw = (size_t)m->sp_in * m->sp_out;
       st = dev_alloc(m, nw * 4, &pw);
       if (st == RB_OK) st = dev_alloc(m, (size_t)m->sp_out * 4, &pb);
-      if (st == RB_OK && (!hip_ok(hipMemcpy(pw, d->head.w, nw * 4, hipMemcpyHostToDevice)) ||
-                          !hip_ok(hipMemcpy(pb, d->head.b, (size_t)m->sp_out * 4, hipMemcpyHostToDevice))))
+      if (st == RB_OK && (!copy_h2d(m, pw, d->head.w, nw * 4) ||
+                          !copy_h2d(m, pb, d->head.b, (size_t)m->sp_out * 4)))
         st = RB_EDEVICE;
       m->sp_w = (float*)pw;
       m->sp_b = (float*)pb;
     }
   }
+  if (m->upload) hipStreamDestroy(m->upload);
+  m->upload = nullptr;
   if (st != RB_OK) {
     free_model_now(m);
     delete m;
     return st;
   }
-  ctx->n_models++;
-  ctx->models.push_back(m);
+  {
+    std::lock_guard<std::mutex> lk(ctx->mu);
+    ctx->n_models++;
+    ctx->models.push_back(m);
+  }
   *out = m;
   return RB_OK;
 }
@@ -856,8 +885,11 @@ rb_status rb_model_destroy(rb_model* m) {
     }
     c->cv.notify_all();
   }
-  c->n_models--;
-  c->models.erase(std::remove(c->models.begin(), c->models.end(), m), c->models.end());
+  {
+    std::lock_guard<std::mutex> lk(c->mu);
+    c->n_models--;
+    c->models.erase(std::remove(c->models.begin(), c->models.end(), m), c->models.end());
+  }
   delete m;
   return RB_OK;
 }
@@ -939,8 +971,11 @@ rb_status rb_sched_destroy(rb_sched* s) {
     // the streams are drained: models no longer need to wait on them
     std::vector<hipStream_t> mine = s->lanes;
     mine.push_back(s->stream);
-    for (rb_model* m : s->ctx->models)
-      for (hipStream_t st : mine) m->used.erase(std::remove(m->used.begin(), m->used.end(), st), m->used.end());
+    {
+      std::lock_guard<std::mutex> lk(s->ctx->mu);
+      for (rb_model* m : s->ctx->models)
+        for (hipStream_t st : mine) m->used.erase(std::remove(m->used.begin(), m->used.end(), st), m->used.end());
+    }
     for (hipStream_t l : s->lanes) hipStreamDestroy(l);
     for (hipEvent_t e : s->lane_done) hipEventDestroy(e);
     if (s->ev_copy) hipEventDestroy(s->ev_copy);
@@ -1027,6 +1062,31 @@ rb_status rb_queue_destroy(rb_queue* q) {
   s->n_live_queues--;
   q->m->bound--;
   delete q;
+  return RB_OK;
+}
+
+rb_status rb_queue_set_model(rb_queue* q, rb_model* m) {
+  if (!q || !m) return RB_EINVAL;
+  rb_model* o = q->m;
+  if (m == o) return RB_OK;
+  bool same = m->ctx == o->ctx && m->kind == o->kind && m->dtype == o->dtype && m->d_in == o->d_in &&
+              m->d_out == o->d_out && m->n_tables == o->n_tables && m->emb_dim == o->emb_dim &&
+              m->n_dense == o->n_dense && m->head_last == o->head_last && m->sp_in == o->sp_in &&
+              m->sp_out == o->sp_out && m->layers.size() == o->layers.size();
+  for (size_t i = 0; same && i < m->layers.size(); ++i)
+    same = m->layers[i].Kp == o->layers[i].Kp && m->layers[i].Np == o->layers[i].Np;
+  if (!same) return RB_EINVAL;
+  rb_sched* s = q->s;
+  // batches dispatched into a window that has not been handed to the device
+  // yet would run the new version: only swap between launches
+  if (!s->window.empty() || !s->chunk.empty()) return RB_EBUSY;
+  // an unbound new version takes over the old one's lineage: its launch
+  // chains follow the old version's on the same stream and reuse its work
+  // buffers (no allocation and no device drain when the first batch runs)
+  if (m->bound.load() == 0 && m->lineage == m->id) m->lineage = o->lineage;
+  m->bound++;
+  o->bound--;
+  q->m = m;
   return RB_OK;
 }
 

@@ -47,11 +47,7 @@ class Deployment:
         self.models: List[rb.Model] = [] if models is None else list(models)
         for si, m in enumerate(w.models if models is None else ()):
             if with_params:
-                p = synth.model_params(w, si)
-                layers = [(W, b, L.act) for (W, b), L in zip(p.weights, m.layers)]
-                head = None if m.head is None else (p.head[0], p.head[1], m.head.act)
-                self.models.append(rb.Model(ctx, m.kind, m.dtype, layers, tables=p.tables or None,
-                                            n_dense=m.n_dense, head=head))
+                self.models.append(self.build_model(si, synth.model_params(w, si)))
             else:
                 shapes = [(L.fan_out, L.fan_in) for L in m.layers]
                 if m.kind == "ranking":
@@ -72,6 +68,24 @@ class Deployment:
         self.servables = [[self.queues[qi] for qi, q in enumerate(w.queues) if q.servable == s]
                           for s in range(len(w.models))]
         self.qindex = {q.id: i for i, q in enumerate(self.queues)}
+
+    def build_model(self, si: int, p) -> rb.Model:
+        """Servable si's model with parameters p (a synth.Params); safe to call
+        on another thread while the scheduler serves (a new version)."""
+        m = self.w.models[si]
+        layers = [(W, b, L.act) for (W, b), L in zip(p.weights, m.layers)]
+        head = None if m.head is None else (p.head[0], p.head[1], m.head.act)
+        return rb.Model(self.ctx, m.kind, m.dtype, layers, tables=p.tables or None, n_dense=m.n_dense, head=head)
+
+    def swap(self, si: int, new: rb.Model) -> rb.Model:
+        """Availability-preserving version transition of servable si: its
+        queues dispatch to `new` from now on; returns the old version, which
+        the caller destroys (its memory is freed off the inference path)."""
+        old = self.models[si]
+        for q in self.servables[si]:
+            q.set_model(new)
+        self.models[si] = new
+        return old
 
     def queue_for(self, t, r: int) -> rb.Queue:
         """The queue request r of trace t is submitted to: its servable's

@@ -128,6 +128,7 @@ _SIGS = {
     "rb_queue_create": (C.c_int32, [C.c_void_p, C.c_void_p, C.POINTER(rb_queue_opts), C.POINTER(C.c_void_p)]),
     "rb_queue_destroy": (C.c_int32, [C.c_void_p]),
     "rb_queue_id": (C.c_int32, [C.c_void_p, p_i32]),
+    "rb_queue_set_model": (C.c_int32, [C.c_void_p, C.c_void_p]),
     "rb_submit": (C.c_int32, [C.c_void_p, C.POINTER(rb_request), C.c_int64, C.POINTER(C.c_uint64)]),
     "rb_advance": (C.c_int32, [C.c_void_p, C.c_int64]),
     "rb_flush": (C.c_int32, [C.c_void_p]),
@@ -286,6 +287,11 @@ class Queue:
         qid = C.c_int32()
         check(_lib().rb_queue_id(h, C.byref(qid)), "rb_queue_id")
         self.id = qid.value
+
+    def set_model(self, model: Model):
+        """Version transition: batches dispatched from now on run `model`."""
+        check(_lib().rb_queue_set_model(self.h, model.h), "rb_queue_set_model")
+        self.model = model
 
     def destroy(self):
         if self.h:

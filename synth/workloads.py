@@ -204,6 +204,15 @@ class Params:
 _param_cache: Dict[Tuple[str, int], Params] = {}
 
 
+def next_version(p: Params) -> Params:
+    """Parameters of a new version of a servable: weights halved, tables
+    doubled (power-of-two scalings, so bf16 storage stays exact), biases
+    shifted by 0.25 so that every output changes."""
+    return Params([(W * np.float32(0.5), b + np.float32(0.25)) for W, b in p.weights],
+                  [T * np.float32(2.0) for T in p.tables],
+                  None if p.head is None else (p.head[0] * np.float32(0.5), p.head[1]))
+
+
 def model_params(w: Workload, servable: int, cache: bool = True) -> Params:
     key = (w.name, servable)
     if cache and key in _param_cache:

@@ -133,6 +133,31 @@ def test_ownership_and_busy_rules(ctx):
     s.destroy()
 
 
+def test_version_transition_rules(ctx):
+    # a queue switches to a new version of the same shape; the old version is
+    # then unbound (destroyable) and the new one bound (busy)
+    s = rb.Sched(ctx, device=False)
+    old, new, other = mlp(ctx), mlp(ctx), mlp(ctx, d_in=5)
+    q1 = rb.Queue(s, old, 8, (), None)
+    q2 = rb.Queue(s, old, 8, (), None)
+    assert status(lambda: q1.set_model(other)) == rb.RB_EINVAL   # different input width
+    assert status(lambda: rb.check(rb.lib().rb_queue_set_model(q1.h, None), "x")) == rb.RB_EINVAL
+    q1.set_model(new)
+    assert status(old.destroy) == rb.RB_EBUSY      # q2 still serves the old version
+    rid = s.submit(q1, 2, np.zeros((2, 4), np.float32), arrival_ns=0)
+    q2.set_model(new)
+    old.destroy()
+    assert status(new.destroy) == rb.RB_EBUSY
+    rb.check(rb.lib().rb_flush(q1.h), "rb_flush")
+    assert s.run_next()["reqs"] == [rid]
+    q1.set_model(new)                              # same model: no-op
+    q1.destroy()
+    q2.destroy()
+    new.destroy()
+    other.destroy()
+    s.destroy()
+
+
 def test_sim_run_argument_checks(ctx):
     s = rb.Sched(ctx, device=False)
     m = mlp(ctx)

@@ -250,3 +250,48 @@ def test_packed_tokens_bounds_errors_are_reported(ctx):
         check_outputs(name, t, a, dt.out.cpu().numpy(), dt.out_off, range(t.n))
     finally:
         dep.destroy()
+
+
+def test_version_transition_while_serving(ctx):
+    # availability-preserving transition (the paper's Aspired Versions
+    # Manager): a new version of a ranking servable is loaded on another
+    # thread while the scheduler replays the trace, then replaces the old one
+    import threading
+    name = "multi_tenant"
+    w = synth.workload(name)
+    t, a = trace_and_arenas(name, 1500)
+    S = 4  # a ranking model (26 tables of 100k rows)
+    dep = Deployment(w, ctx, device=True, window_batches=16, service_ns=service_table(w), n_streams=4)
+    try:
+        dt = dep.upload(t, a)
+        dep.replay(dt)
+        dep.sched.sync()
+        out1 = dt.out.cpu().numpy()
+        p2 = synth.next_version(synth.model_params(w, S))
+        loaded = {}
+        th = threading.Thread(target=lambda: loaded.setdefault("m", dep.build_model(S, p2)))
+        th.start()
+        for _ in range(3):  # serving goes on while the new version loads
+            dep.replay(dt)
+            dep.sched.sync()
+            assert np.array_equal(dt.out.cpu().numpy(), out1)
+        th.join()
+        old = dep.swap(S, loaded["m"])
+        old.destroy()
+        dep.replay(dt)
+        dep.sched.sync()
+        out2 = dt.out.cpu().numpy()
+    finally:
+        dep.destroy()
+    mine = np.nonzero(t.servable == S)[0]
+    others = np.nonzero(t.servable != S)[0]
+    assert len(mine) > 10
+    for r in others:
+        o0, o1 = int(dt.out_off[r]), int(dt.out_off[r + 1])
+        assert np.array_equal(out2[o0:o1], out1[o0:o1]), r
+    om2 = OracleModel(w.models[S], p2)
+    for r in mine[::3]:
+        ref = om2.forward(a.payload(r)).astype(np.float64)
+        y = out2[int(dt.out_off[r]):int(dt.out_off[r + 1])].reshape(ref.shape)
+        assert row_scaled_err(y, ref) <= RTOL["bf16"], r
+        assert not np.array_equal(y, out1[int(dt.out_off[r]):int(dt.out_off[r + 1])].reshape(ref.shape))
