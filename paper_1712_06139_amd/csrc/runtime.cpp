@@ -199,7 +199,8 @@ struct rb_sched {
   std::vector<hipStream_t> lanes;
   std::vector<hipEvent_t> lane_done;
   hipEvent_t ev_copy = nullptr;
-  std::map<int64_t, int> lane_of;  // model lineage -> lane, in order of first use
+  std::map<int64_t, int> lane_of;  // work key -> lane, in order of first use
+  std::map<int64_t, int> pipe_next; // lineage -> work slot of its next launch chain
   // cold-cache profiling: written before every timed launch
   void* scrub = nullptr;
   std::vector<rb_queue*> queues;  // by id; null once destroyed
@@ -433,15 +434,30 @@ void sync_all(rb_sched* s) {
 }
 
 // Stream of a model's launch chains in a replay.
-hipStream_t lane_for(rb_sched* s, const rb_model* m) {
+// Work buffers and launch streams belong to (lineage, slot) pairs. With two or
+// more lanes a lineage's consecutive launch chains alternate between two slots
+// on two lanes, so one window's gathers and another's GEMMs can run at once;
+// each slot's buffers are reused only on its own lane, in stream order.
+int64_t work_key(const rb_model* m, int slot) { return m->lineage * 2 + slot; }
+
+int next_slot(rb_sched* s, const rb_model* m) {
+  if (s->lanes.size() < 2) return 0;
+  int& n = s->pipe_next[m->lineage];
+  const int k = n;
+  n ^= 1;
+  return k;
+}
+
+hipStream_t lane_for(rb_sched* s, const rb_model* m, int slot) {
   if (s->lanes.empty()) return s->stream;
-  auto it = s->lane_of.find(m->lineage);
-  if (it == s->lane_of.end()) it = s->lane_of.emplace(m->lineage, (int)(s->lane_of.size() % s->lanes.size())).first;
+  const int64_t key = work_key(m, slot);
+  auto it = s->lane_of.find(key);
+  if (it == s->lane_of.end()) it = s->lane_of.emplace(key, (int)(s->lane_of.size() % s->lanes.size())).first;
   return s->lanes[(size_t)it->second];
 }
 
-rb_status ensure_work(rb_sched* s, rb_model* m, int64_t rows, int64_t slots, Work** out) {
-  Work& w = s->work[m->lineage];
+rb_status ensure_work(rb_sched* s, rb_model* m, int slot, int64_t rows, int64_t slots, Work** out) {
+  Work& w = s->work[work_key(m, slot)];
   if (rows > w.rows_cap || slots > w.slots_cap) {
     // capacities only grow (both at once), so groups of different shapes
     // never make the buffers shrink and grow back
@@ -472,14 +488,14 @@ rb_status ensure_work(rb_sched* s, rb_model* m, int64_t rows, int64_t slots, Wor
 
 // Launch chain of one group on stream st_h: route -> assemble | embbag ->
 // layers -> head | seqpool | split.
-rb_status run_group(rb_sched* s, hipStream_t st_h, const Group& g, const rb_k_batch* d_batches,
+rb_status run_group(rb_sched* s, hipStream_t st_h, int slot, const Group& g, const rb_k_batch* d_batches,
                     const rb_k_req* d_reqs, const float* dense, int64_t dense_len, const int32_t* lens,
                     const int32_t* ids, int64_t ids_len, float* out) {
   rb_model* m = g.q->m;
   const int64_t slots = g.slots;
   const int64_t M = group_rows(m, g.q, slots);
   Work* w = nullptr;
-  rb_status st = ensure_work(s, m, M, slots, &w);
+  rb_status st = ensure_work(s, m, slot, M, slots, &w);
   if (st != RB_OK) return st;
   if (std::find(m->used.begin(), m->used.end(), st_h) == m->used.end()) m->used.push_back(st_h);
   void* hs = (void*)st_h;
@@ -614,7 +630,8 @@ rb_status flush_chunk(rb_sched* s) {
   size_t gi = 0;
   for (auto& win : s->chunk)
     for (Group& g : win) {
-      st = run_group(s, lane_for(s, g.q->m), g, (const rb_k_batch*)(sl->dev + offs[gi].first),
+      const int slot = next_slot(s, g.q->m);
+      st = run_group(s, lane_for(s, g.q->m, slot), slot, g, (const rb_k_batch*)(sl->dev + offs[gi].first),
                      (const rb_k_req*)(sl->dev + offs[gi].second), s->a_dense, s->a_dense_len, s->a_lens, s->a_ids,
                      s->a_ids_len, s->a_out);
       ++gi;
@@ -637,7 +654,6 @@ void close_window(rb_sched* s) {
   s->window_batches = 0;
 }
 
-// Add a dispatched batch (its requests already described) to the window.
 // Seqpool: give request r its first packed token row in group g and count its
 // tokens (its dense extent over d_in, at most n_rows full buckets: a request
 // whose extent is inconsistent is rejected by the routing, and the packed rows
@@ -649,6 +665,7 @@ void add_tokens(Group& g, const rb_model* m, rb_k_req& r) {
   g.tokens += std::min<int64_t>(std::max<int64_t>(t, 0), (int64_t)r.n_rows * g.q->bucket);
 }
 
+// Add a dispatched batch (its requests already described) to the window.
 void window_add(rb_sched* s, rb_queue* q, const Batch& b, std::vector<rb_k_req>& reqs) {
   Group* g = nullptr;
   for (Group& x : s->window)
@@ -1224,7 +1241,7 @@ static rb_status run_serving_batch(rb_sched* s, rb_queue* q, const Batch& b) {
   std::memcpy(sl->host + o_reqs, g.reqs.data(), g.reqs.size() * sizeof(rb_k_req));
   if (!hip_ok(hipMemcpyAsync(sl->dev, sl->host, o_out, hipMemcpyHostToDevice, s->stream))) return RB_EDEVICE;
   float* dout = (float*)(sl->dev + o_out);
-  st = run_group(s, s->stream, g, (const rb_k_batch*)(sl->dev + o_batch), (const rb_k_req*)(sl->dev + o_reqs),
+  st = run_group(s, s->stream, 0, g, (const rb_k_batch*)(sl->dev + o_batch), (const rb_k_req*)(sl->dev + o_reqs),
                  (const float*)(sl->dev + o_dense), nd, (const int32_t*)(sl->dev + o_lens),
                  (const int32_t*)(sl->dev + o_ids), ni, dout);
   if (st != RB_OK) return st;

@@ -108,10 +108,13 @@ def test_outputs_independent_of_launch_window(ctx, name):
     assert np.array_equal(out1, out8)
 
 
-@pytest.mark.parametrize("name,n_streams", [("multi_tenant", 4), ("multi_tenant", 3), ("ragged_seq", 4)])
+@pytest.mark.parametrize("name,n_streams", [("multi_tenant", 4), ("multi_tenant", 3), ("ragged_seq", 4),
+                                            ("ranking", 2)])
 def test_outputs_independent_of_stream_count(ctx, name, n_streams):
-    # concurrent launch chains of different models (ragged_seq: one model over
-    # four bucket queues, so its chains share one stream) change nothing
+    # concurrent launch chains of different models, and consecutive chains of
+    # one model alternating between two work-buffer slots on two lanes
+    # (ranking: one model; ragged_seq: one model over four bucket queues),
+    # change nothing
     n = min(PREFIX[name], 1500)
     w, t, a, qindex, log1, out1, _ = run(ctx, name, n, window=16)
     _, _, _, _, logk, outk, out_off = run(ctx, name, n, window=16, n_streams=n_streams)
