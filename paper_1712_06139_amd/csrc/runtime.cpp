@@ -438,13 +438,15 @@ void sync_all(rb_sched* s) {
 // more lanes a lineage's consecutive launch chains alternate between two slots
 // on two lanes, so one window's gathers and another's GEMMs can run at once;
 // each slot's buffers are reused only on its own lane, in stream order.
-int64_t work_key(const rb_model* m, int slot) { return m->lineage * 2 + slot; }
+constexpr int PIPE_SLOTS = 2;
+
+int64_t work_key(const rb_model* m, int slot) { return m->lineage * PIPE_SLOTS + slot; }
 
 int next_slot(rb_sched* s, const rb_model* m) {
   if (s->lanes.size() < 2) return 0;
   int& n = s->pipe_next[m->lineage];
   const int k = n;
-  n ^= 1;
+  n = (n + 1) % PIPE_SLOTS;
   return k;
 }
 
