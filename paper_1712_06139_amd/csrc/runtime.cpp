@@ -434,16 +434,19 @@ void sync_all(rb_sched* s) {
 }
 
 // Stream of a model's launch chains in a replay.
-// Work buffers and launch streams belong to (lineage, slot) pairs. With two or
-// more lanes a lineage's consecutive launch chains alternate between two slots
-// on two lanes, so one window's gathers and another's GEMMs can run at once;
-// each slot's buffers are reused only on its own lane, in stream order.
+// Work buffers and launch streams belong to (lineage, slot) pairs. When the
+// lanes outnumber the lineages of a chunk at least PIPE_SLOTS times, a
+// lineage's consecutive launch chains rotate over PIPE_SLOTS slots on their
+// own lanes, so one window's gathers and another's GEMMs can run at once
+// (with fewer lanes, each lineage keeps one slot and different models overlap
+// instead); each slot's buffers are reused only on its own lane, in stream
+// order.
 constexpr int PIPE_SLOTS = 2;
 
 int64_t work_key(const rb_model* m, int slot) { return m->lineage * PIPE_SLOTS + slot; }
 
-int next_slot(rb_sched* s, const rb_model* m) {
-  if (s->lanes.size() < 2) return 0;
+int next_slot(rb_sched* s, const rb_model* m, bool pipe) {
+  if (!pipe) return 0;
   int& n = s->pipe_next[m->lineage];
   const int k = n;
   n = (n + 1) % PIPE_SLOTS;
@@ -629,10 +632,16 @@ rb_status flush_chunk(rb_sched* s) {
     hipEventRecord(s->ev_copy, s->stream);
     for (hipStream_t l : s->lanes) hipStreamWaitEvent(l, s->ev_copy, 0);
   }
+  std::vector<int64_t> lin;
+  for (auto& win : s->chunk)
+    for (Group& g : win) lin.push_back(g.q->m->lineage);
+  std::sort(lin.begin(), lin.end());
+  const size_t n_lin = (size_t)(std::unique(lin.begin(), lin.end()) - lin.begin());
+  const bool pipe = s->lanes.size() >= (size_t)PIPE_SLOTS * n_lin;
   size_t gi = 0;
   for (auto& win : s->chunk)
     for (Group& g : win) {
-      const int slot = next_slot(s, g.q->m);
+      const int slot = next_slot(s, g.q->m, pipe);
       st = run_group(s, lane_for(s, g.q->m, slot), slot, g, (const rb_k_batch*)(sl->dev + offs[gi].first),
                      (const rb_k_req*)(sl->dev + offs[gi].second), s->a_dense, s->a_dense_len, s->a_lens, s->a_ids,
                      s->a_ids_len, s->a_out);
