@@ -779,22 +779,46 @@ __global__ __launch_bounds__(NT) void k_gemm_f32(const float* __restrict__ X, in
 
 // ---------------------------------------------------------------- heads and split
 
-// One wave per row: a K-long dot product (lane-strided, then a butterfly),
-// bias, activation, and the store into the request's output row.
+// 16 lanes per row (16 rows per workgroup): a K-long dot product, each lane
+// taking 8 consecutive elements of every 128 with 16-byte loads (or every
+// 16th element when rows are not 16-byte aligned), a 16-lane butterfly, bias,
+// activation, and the store into the request's output row (one wave per row
+// with 2-byte loads measured 1.5x slower on 256-wide rows).
 template <int ACT>
 __global__ __launch_bounds__(256) void k_head(const rb_k_row* __restrict__ rows, int n,
                                               const bf16_t* __restrict__ H, int ldh,
-                                              const bf16_t* __restrict__ w, float b, int K,
+                                              const bf16_t* __restrict__ w, float b, int K, int vec,
                                               float* __restrict__ out) {
-  const int r = blockIdx.x * 4 + (threadIdx.x >> 6), lane = threadIdx.x & 63;
-  if (r >= n) return;
-  const int64_t o = rows[r].out;
-  if (o < 0) return;
-  const bf16_t* h = H + (int64_t)r * ldh;
+  const int r = blockIdx.x * 16 + (threadIdx.x >> 4), l = threadIdx.x & 15;
   float s = 0.f;
-  for (int k = lane; k < K; k += 64) s += bf2f(h[k]) * bf2f(w[k]);
-  s = wave_sum(s);
-  if (lane == 0) out[o] = act_fn<ACT>(s + b);
+  int64_t o = -1;
+  if (r < n) {
+    o = rows[r].out;
+    if (o >= 0) {
+      const bf16_t* h = H + (int64_t)r * ldh;
+      if (vec) {
+        for (int k = l * 8; k < K; k += 128) {
+          const u32x4_t hv = *(const u32x4_t*)(h + k), wv = *(const u32x4_t*)(w + k);
+          s += bf2f(hv.x & 0xffffu) * bf2f(wv.x & 0xffffu);
+          s += bf2f(hv.x >> 16) * bf2f(wv.x >> 16);
+          s += bf2f(hv.y & 0xffffu) * bf2f(wv.y & 0xffffu);
+          s += bf2f(hv.y >> 16) * bf2f(wv.y >> 16);
+          s += bf2f(hv.z & 0xffffu) * bf2f(wv.z & 0xffffu);
+          s += bf2f(hv.z >> 16) * bf2f(wv.z >> 16);
+          s += bf2f(hv.w & 0xffffu) * bf2f(wv.w & 0xffffu);
+          s += bf2f(hv.w >> 16) * bf2f(wv.w >> 16);
+        }
+      } else {
+        for (int k = l; k < K; k += 16) s += bf2f(h[k]) * bf2f(w[k]);
+      }
+    }
+  }
+  // 16-lane sum: every lane of the wave takes part in the exchanges
+  s += __shfl_xor(s, 1);
+  s += __shfl_xor(s, 2);
+  s += __shfl_xor(s, 4);
+  s += __shfl_xor(s, 8);
+  if (l == 0 && o >= 0) out[o] = act_fn<ACT>(s + b);
 }
 
 constexpr int POOL_MAX_D = 1024, POOL_MAX_OUT = 16;
@@ -1116,13 +1140,15 @@ rb_status rb_k_head(void* stream, const rb_k_row* rows, int32_t n_rows_total, co
   if (n_rows_total < 0 || K < 1 || ldh < K || !rows || !H || !w || !out) return RB_EINVAL;
   if (act != RB_ACT_NONE && act != RB_ACT_SIGMOID) return RB_EINVAL;
   if (n_rows_total == 0) return RB_OK;
-  const unsigned g = (unsigned)((n_rows_total + 3) / 4);
+  const unsigned g = (unsigned)((n_rows_total + 15) / 16);
+  // 16-byte loads when every row and the weight vector start 16-byte aligned
+  const int vec = (K % 8 == 0) && (ldh % 8 == 0) && ((uintptr_t)H % 16 == 0) && ((uintptr_t)w % 16 == 0);
   if (act == RB_ACT_SIGMOID)
     hipLaunchKernelGGL(k_head<RB_ACT_SIGMOID>, dim3(g), dim3(256), 0, (hipStream_t)stream, rows, n_rows_total,
-                       (const bf16_t*)H, ldh, (const bf16_t*)w, b, K, out);
+                       (const bf16_t*)H, ldh, (const bf16_t*)w, b, K, vec, out);
   else
     hipLaunchKernelGGL(k_head<RB_ACT_NONE>, dim3(g), dim3(256), 0, (hipStream_t)stream, rows, n_rows_total,
-                       (const bf16_t*)H, ldh, (const bf16_t*)w, b, K, out);
+                       (const bf16_t*)H, ldh, (const bf16_t*)w, b, K, vec, out);
   return launch_status();
 }
 

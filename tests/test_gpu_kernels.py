@@ -458,15 +458,19 @@ def _rows_dev(src, aux, out):
     return _dev(a.view(np.uint8))
 
 
-def test_head_and_split():
+@pytest.mark.parametrize("K,ldh", [(256, 256), (264, 272), (100, 100), (1000, 1004)])
+def test_head_and_split(K, ldh):
+    # 16-byte path (K and ldh multiples of 8) and element path; rows whose
+    # output is -1 are skipped
     rng = np.random.default_rng(6)
-    R, K = 300, 256
+    R = 300
     out_idx = np.where(rng.random(R) < 0.8, np.arange(R) * 3, -1)
     rows = _rows_dev(np.zeros(R), np.zeros(R), out_idx)
-    Hd, H = _bf16_dev(rng.standard_normal((R, K)))
+    Hd, Hf = _bf16_dev(rng.standard_normal((R, ldh)))
+    H = Hf[:, :K]
     wd, w = _bf16_dev(rng.standard_normal(K) / 16)
     out = torch.full((R * 3,), -7.0, device=DEV)
-    rb.check(rb.lib().rb_k_head(_stream(), rb.dptr(rows), R, rb.dptr(Hd), K, rb.dptr(wd), 0.25, K,
+    rb.check(rb.lib().rb_k_head(_stream(), rb.dptr(rows), R, rb.dptr(Hd), ldh, rb.dptr(wd), 0.25, K,
                                 rb.RB_ACT_SIGMOID, rb.dptr(out)), "head")
     Y = rng.standard_normal((R, 64)).astype(np.float32)
     out2 = torch.full((R * 3 * 10,), -7.0, device=DEV)
