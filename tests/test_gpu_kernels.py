@@ -262,7 +262,7 @@ def synth_payload(d):
 
 
 def _lens_skewed(rng, n, nt):
-    # mostly empty bags, now and then one long bag (past the ids staged in LDS)
+    # mostly empty bags, now and then one long bag (many chunks of 8 ids)
     ln = rng.integers(0, 2, size=(n, nt)) * (rng.random((n, nt)) < 0.2)
     long = rng.random(n) < 0.3
     ln[long, rng.integers(0, nt, size=int(long.sum()))] = rng.integers(30, 700, size=int(long.sum()))
