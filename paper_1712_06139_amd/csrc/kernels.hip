@@ -409,12 +409,15 @@ __global__ __launch_bounds__(256) void k_embbag(const rb_k_row* __restrict__ row
       float acc[8];
 #pragma unroll
       for (int k = 0; k < 8; ++k) acc[k] = 0.f;
+      // lane i's id of chunk c (-1: past the bag or outside the ids arena)
+      auto chunk_id = [&](int c) {
+        const int64_t pos = id0 + c + l8;
+        return (c + l8 < L && pos >= 0 && pos < ids_len) ? ids[pos] : -1;
+      };
+      int nxt = chunk_id(0);
       for (int c = 0; c < L; c += EMB_CHUNK) {
-        int my = -1;
-        if (c + l8 < L) {
-          const int64_t pos = id0 + c + l8;
-          my = (pos >= 0 && pos < ids_len) ? ids[pos] : -1;
-        }
+        const int my = nxt;
+        nxt = chunk_id(c + EMB_CHUNK);  // the next chunk's ids load during this chunk's gathers
         u32x4_t q[EMB_CHUNK];
 #pragma unroll
         for (int u = 0; u < EMB_CHUNK; ++u) {
