@@ -185,16 +185,23 @@ rb_status rb_queue_create(rb_sched* s, rb_model* m, const rb_queue_opts* opts, r
 /* RB_EBUSY while the queue holds requests that have not run. */
 rb_status rb_queue_destroy(rb_queue* q);
 rb_status rb_queue_id(const rb_queue* q, int32_t* id);
-/* Version transition (the availability-preserving policy of the paper's
- * Aspired Versions Manager, section 2.1: the new version is loaded while the
- * old one serves, then replaces it): batches the queue dispatches after this
- * call run model m. m must have the old model's kind, dtype, widths and
- * padded layer shapes (RB_EINVAL otherwise); it may be created on another
- * thread while the scheduler serves (rb_model_create uploads on a private
- * non-blocking stream). RB_EBUSY while a launch window is being filled (only
- * between rb_sim_run / rb_run_next calls). The old model stays bound to any
- * other queue that uses it; once unbound, rb_model_destroy frees it off the
- * inference path. */
+/* Version transition (the version transition policies of the paper's
+ * Aspired Versions Manager, section 2.1): batches the queue dispatches after
+ * this call run model m. m must have the bound model's kind, dtype, input and
+ * output widths and table count (RB_EINVAL otherwise); it may be created on
+ * another thread while the scheduler serves (rb_model_create uploads on a
+ * private non-blocking stream).
+ *   Availability-preserving: load the new version, call this, then destroy
+ *   the old one; with the old version's padded layer shapes the new one also
+ *   takes over its launch stream and work buffers.
+ *   Resource-preserving: m = NULL holds the queue (no version bound, so the
+ *   old one can be destroyed before the new one is loaded): it keeps
+ *   accepting requests and closing batches, validated against the old
+ *   version's interface, but dispatches nothing (rb_run_next skips it;
+ *   rb_sim_run refuses it with RB_EBUSY) until a version is set again.
+ * RB_EBUSY while a launch window is being filled (only between rb_sim_run /
+ * rb_run_next calls). The old model stays bound to any other queue that uses
+ * it; once unbound, rb_model_destroy frees it off the inference path. */
 rb_status rb_queue_set_model(rb_queue* q, rb_model* m);
 
 /* ---------------------------------------------------------------- serving */

@@ -129,6 +129,7 @@ struct Batch {
 struct HostReq {
   rb_queue* q = nullptr;
   int32_t n_rows = 0;
+  int32_t d_out = 0;  // output width (its queue may change version or be held meanwhile)
   std::vector<float> dense;
   std::vector<int32_t> lens, ids;
   std::vector<float> out;
@@ -174,9 +175,21 @@ struct Prof {
 
 }  // namespace
 
+// What requests of a queue must look like: the bound version's interface,
+// kept while the queue is held between versions (no version bound).
+struct QShape {
+  int kind = 0, dtype = 0, d_in = 0, d_out = 0, n_dense = 0, n_tables = 0;
+  int64_t table_rows = 0;
+};
+
+QShape shape_of(const rb_model* m) {
+  return QShape{m->kind, m->dtype, m->d_in, m->d_out, m->n_dense, m->n_tables, m->table_rows};
+}
+
 struct rb_queue {
   rb_sched* s = nullptr;
-  rb_model* m = nullptr;
+  rb_model* m = nullptr;  // nullptr: held (resource-preserving transition)
+  QShape shape;
   int id = 0;
   int B = 0;
   std::vector<int> allowed;
@@ -368,7 +381,7 @@ rb_queue* pick_round_robin(rb_sched* s) {
   const int nq = (int)s->queues.size();
   for (int k = 1; k <= nq; ++k) {
     rb_queue* q = s->queues[(size_t)((s->last_served + k) % nq + nq) % nq];
-    if (q && !q->closed.empty()) return q;
+    if (q && q->m && !q->closed.empty()) return q;  // held queues keep their batches
   }
   return nullptr;
 }
@@ -560,7 +573,7 @@ rb_status run_group(rb_sched* s, hipStream_t st_h, int slot, const Group& g, con
 void retire_slot(rb_sched* s, Slot& sl) {
   for (int64_t id : sl.serving_reqs) {
     HostReq& r = s->hreqs[(size_t)id];
-    const int64_t n = (int64_t)r.n_rows * r.q->m->d_out;
+    const int64_t n = (int64_t)r.n_rows * r.d_out;
     r.out.assign(sl.host_out + r.out_off, sl.host_out + r.out_off + n);
     r.state = 2;
     r.slot = -1;
@@ -1066,6 +1079,7 @@ rb_status rb_queue_create(rb_sched* s, rb_model* m, const rb_queue_opts* o, rb_q
   if (!q) return RB_ENOMEM;
   q->s = s;
   q->m = m;
+  q->shape = shape_of(m);
   q->id = (int)s->queues.size();
   q->B = o->max_batch_size;
   q->allowed.assign(o->allowed_batch_sizes, o->allowed_batch_sizes + o->n_allowed);
@@ -1088,32 +1102,41 @@ rb_status rb_queue_destroy(rb_queue* q) {
     if (g.q == q) return RB_EBUSY;
   s->queues[(size_t)q->id] = nullptr;
   s->n_live_queues--;
-  q->m->bound--;
+  if (q->m) q->m->bound--;
   delete q;
   return RB_OK;
 }
 
 rb_status rb_queue_set_model(rb_queue* q, rb_model* m) {
-  if (!q || !m) return RB_EINVAL;
+  if (!q) return RB_EINVAL;
   rb_model* o = q->m;
   if (m == o) return RB_OK;
-  bool same = m->ctx == o->ctx && m->kind == o->kind && m->dtype == o->dtype && m->d_in == o->d_in &&
-              m->d_out == o->d_out && m->n_tables == o->n_tables && m->emb_dim == o->emb_dim &&
-              m->n_dense == o->n_dense && m->head_last == o->head_last && m->sp_in == o->sp_in &&
-              m->sp_out == o->sp_out && m->layers.size() == o->layers.size();
-  for (size_t i = 0; same && i < m->layers.size(); ++i)
-    same = m->layers[i].Kp == o->layers[i].Kp && m->layers[i].Np == o->layers[i].Np;
-  if (!same) return RB_EINVAL;
   rb_sched* s = q->s;
+  if (m) {
+    const QShape a = shape_of(m), &b = q->shape;
+    if (m->ctx != s->ctx || a.kind != b.kind || a.dtype != b.dtype || a.d_in != b.d_in || a.d_out != b.d_out ||
+        a.n_dense != b.n_dense || a.n_tables != b.n_tables)
+      return RB_EINVAL;
+  }
   // batches dispatched into a window that has not been handed to the device
   // yet would run the new version: only swap between launches
   if (!s->window.empty() || !s->chunk.empty()) return RB_EBUSY;
-  // an unbound new version takes over the old one's lineage: its launch
-  // chains follow the old version's on the same stream and reuse its work
-  // buffers (no allocation and no device drain when the first batch runs)
-  if (m->bound.load() == 0 && m->lineage == m->id) m->lineage = o->lineage;
-  m->bound++;
-  o->bound--;
+  // an unbound new version with the old one's padded layer shapes takes over
+  // the old one's lineage: its launch chains follow the old version's on the
+  // same stream and reuse its work buffers (no allocation and no device drain
+  // when the first batch runs)
+  if (m && o && m->bound.load() == 0 && m->lineage == m->id && m->layers.size() == o->layers.size() &&
+      m->head_last == o->head_last && m->sp_in == o->sp_in) {
+    bool same = true;
+    for (size_t i = 0; same && i < m->layers.size(); ++i)
+      same = m->layers[i].Kp == o->layers[i].Kp && m->layers[i].Np == o->layers[i].Np;
+    if (same) m->lineage = o->lineage;
+  }
+  if (m) {
+    m->bound++;
+    q->shape.table_rows = m->table_rows;
+  }
+  if (o) o->bound--;
   q->m = m;
   return RB_OK;
 }
@@ -1127,7 +1150,7 @@ rb_status rb_queue_id(const rb_queue* q, int32_t* id) {
 // ---------------------------------------------------------------- serving
 
 static rb_status validate_request(const rb_queue* q, const rb_request* r) {
-  const rb_model* m = q->m;
+  const QShape* m = &q->shape;
   if (r->n_rows < 1 || r->n_rows > q->B) return RB_EINVAL;
   const int64_t n = r->n_rows;
   if (r->n_dense < 0 || r->n_lens < 0 || r->n_ids < 0) return RB_EINVAL;
@@ -1167,6 +1190,7 @@ rb_status rb_submit(rb_queue* q, const rb_request* r, int64_t arrival_ns, uint64
   HostReq h;
   h.q = q;
   h.n_rows = r->n_rows;
+  h.d_out = q->shape.d_out;
   try {
     h.dense.assign(r->dense, r->dense + r->n_dense);
     if (r->n_lens) h.lens.assign(r->lens, r->lens + r->n_lens);
@@ -1336,6 +1360,7 @@ rb_status rb_sim_run(rb_sched* s, const rb_servable* sv, int32_t n_sv, const rb_
     for (int32_t j = 0; j < sv[i].n_queues; ++j) {
       rb_queue* q = sv[i].queues[j];
       if (!q || q->s != s || q->undispatched || !q->closed.empty()) return RB_EINVAL;
+      if (!q->m) return RB_EBUSY;  // a held queue could not leave the replay empty
     }
   }
   const bool dev = s->stream != nullptr;
@@ -1361,7 +1386,7 @@ rb_status rb_sim_run(rb_sched* s, const rb_servable* sv, int32_t n_sv, const rb_
     if (tr->n_rows[r] < 1 || tr->n_rows[r] > q->B) return RB_EINVAL;
     if (r > 0 && tr->arrival_ns[r] < tr->arrival_ns[r - 1]) return RB_EINVAL;
     if (dev) {
-      const rb_model* m = q->m;
+      const QShape* m = &q->shape;
       const int64_t n = tr->n_rows[r];
       if (tr->out_off[r + 1] - tr->out_off[r] != n * m->d_out || tr->out_off[r] < 0) return RB_EINVAL;
       if (tr->dense_off[r] < 0 || tr->dense_off[r + 1] < tr->dense_off[r]) return RB_EINVAL;
@@ -1399,6 +1424,7 @@ rb_status rb_sim_run(rb_sched* s, const rb_servable* sv, int32_t n_sv, const rb_
   auto dispatch_at = [&](int64_t t) -> rb_status {
     while (s->device_free <= t && s->n_closed > 0) {
       rb_queue* q = pick_round_robin(s);
+      if (!q) break;
       Batch b = std::move(q->closed.front());
       q->closed.pop_front();
       s->n_closed--;

@@ -288,9 +288,10 @@ class Queue:
         check(_lib().rb_queue_id(h, C.byref(qid)), "rb_queue_id")
         self.id = qid.value
 
-    def set_model(self, model: Model):
-        """Version transition: batches dispatched from now on run `model`."""
-        check(_lib().rb_queue_set_model(self.h, model.h), "rb_queue_set_model")
+    def set_model(self, model: Optional[Model]):
+        """Version transition: batches dispatched from now on run `model`;
+        None holds the queue (no version bound, nothing dispatched)."""
+        check(_lib().rb_queue_set_model(self.h, None if model is None else model.h), "rb_queue_set_model")
         self.model = model
 
     def destroy(self):

@@ -141,7 +141,7 @@ def test_version_transition_rules(ctx):
     q1 = rb.Queue(s, old, 8, (), None)
     q2 = rb.Queue(s, old, 8, (), None)
     assert status(lambda: q1.set_model(other)) == rb.RB_EINVAL   # different input width
-    assert status(lambda: rb.check(rb.lib().rb_queue_set_model(q1.h, None), "x")) == rb.RB_EINVAL
+    assert status(lambda: rb.check(rb.lib().rb_queue_set_model(None, new.h), "x")) == rb.RB_EINVAL
     q1.set_model(new)
     assert status(old.destroy) == rb.RB_EBUSY      # q2 still serves the old version
     rid = s.submit(q1, 2, np.zeros((2, 4), np.float32), arrival_ns=0)
@@ -155,6 +155,45 @@ def test_version_transition_rules(ctx):
     q2.destroy()
     new.destroy()
     other.destroy()
+    s.destroy()
+
+
+def test_resource_preserving_transition(ctx):
+    # the queue is held (no version bound): the old version can be destroyed
+    # before the new one exists; requests keep arriving and batches keep
+    # closing, but nothing is dispatched until a version is set again
+    s = rb.Sched(ctx, device=False)
+    old, other = mlp(ctx), mlp(ctx, d_out=5)
+    q = rb.Queue(s, old, 8, (), None)
+    q2 = rb.Queue(s, mlp(ctx), 8, (), None)
+    r1 = s.submit(q, 2, np.zeros((2, 4), np.float32), arrival_ns=0)
+    rb.check(rb.lib().rb_flush(q.h), "rb_flush")
+    q.set_model(None)
+    old.destroy()                                   # nothing serves it any more
+    r2 = s.submit(q, 3, np.zeros((3, 4), np.float32), arrival_ns=10)
+    assert status(lambda: s.submit(q, 1, np.zeros((1, 5), np.float32), arrival_ns=10)) == rb.RB_EINVAL
+    rb.check(rb.lib().rb_flush(q.h), "rb_flush")
+    r3 = s.submit(q2, 1, np.zeros((1, 4), np.float32), arrival_ns=20)
+    rb.check(rb.lib().rb_flush(q2.h), "rb_flush")
+    assert s.run_next()["reqs"] == [r3]             # other queues keep being served
+    assert s.run_next() is None                     # the held queue dispatches nothing
+    m3 = mlp(ctx)
+    q3 = rb.Queue(s, m3, 8, (), None)
+    q3.set_model(None)                              # held and empty: a replay could not drain it
+    assert status(lambda: s.sim_run([[q3]], np.zeros(1), np.zeros(1), np.ones(1))) == rb.RB_EBUSY
+    q3.destroy()
+    m3.destroy()
+    assert status(lambda: q.set_model(other)) == rb.RB_EINVAL   # different output width
+    new = mlp(ctx)
+    q.set_model(new)
+    assert s.run_next()["reqs"] == [r1]
+    assert s.run_next()["reqs"] == [r2]
+    assert s.run_next() is None
+    q.destroy()
+    q2.model_ = q2.model
+    q2.destroy()
+    for m in (new, other, q2.model_):
+        m.destroy()
     s.destroy()
 
 

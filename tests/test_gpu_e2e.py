@@ -298,3 +298,54 @@ def test_version_transition_while_serving(ctx):
         y = out2[int(dt.out_off[r]):int(dt.out_off[r + 1])].reshape(ref.shape)
         assert row_scaled_err(y, ref) <= RTOL["bf16"], r
         assert not np.array_equal(y, out1[int(dt.out_off[r]):int(dt.out_off[r + 1])].reshape(ref.shape))
+
+
+def test_resource_preserving_transition_serving_api(ctx):
+    # resource-preserving policy: servable S's queue is held, its old version
+    # destroyed before the new one is loaded; requests arriving meanwhile wait
+    # while the other servables are served, then run on the new version
+    name = "multi_tenant"
+    w = synth.workload(name)
+    t, a = trace_and_arenas(name, 400)
+    S = 0  # an fp32 MLP tenant
+    dep = Deployment(w, ctx, device=True)
+    try:
+        half = t.n // 2
+        ids = {}
+
+        def submit(rs):
+            for r in rs:
+                p = a.payload(r)
+                q = dep.servables[int(t.servable[r])][0]
+                ids[r] = dep.sched.submit(q, int(t.n_rows[r]), p.dense, p.lens, p.ids, int(t.arrival_ns[r]))
+            for q in dep.queues:
+                rb.check(rb.lib().rb_flush(q.h), "rb_flush")
+
+        def drain():
+            ran = []
+            while (b := dep.sched.run_next()) is not None:
+                ran.extend(b["reqs"])
+            return ran
+
+        submit(range(half))
+        drain()
+        q = dep.servables[S][0]
+        q.set_model(None)
+        dep.models[S].destroy()
+        submit(range(half, t.n))
+        ran = drain()
+        held = [r for r in range(half, t.n) if int(t.servable[r]) == S]
+        assert held and not set(ids[r] for r in held) & set(ran)
+        p2 = synth.next_version(synth.model_params(w, S))
+        dep.models[S] = dep.build_model(S, p2)
+        q.set_model(dep.models[S])
+        drain()
+        dep.sched.sync()
+        for r in range(t.n):
+            s = int(t.servable[r])
+            om = OracleModel(w.models[S], p2) if (s == S and r >= half) else oracle_model(name, s)
+            ref = om.forward(a.payload(r)).astype(np.float64)
+            y = dep.sched.collect(ids[r], int(t.n_rows[r]), ref.shape[1])
+            assert row_scaled_err(y, ref) <= RTOL[w.models[s].dtype], (r, s)
+    finally:
+        dep.destroy()
