@@ -24,6 +24,8 @@
 #include <stdint.h>
 
 #include <type_traits>
+#include <algorithm>
+#include <atomic>
 
 #include "../../include/rb.h"
 
@@ -460,32 +462,38 @@ __global__ __launch_bounds__(256) void k_embbag(const rb_k_row* __restrict__ row
 
 // ---------------------------------------------------------------- GEMM (bf16 and fp32)
 
+// value of v in lane l ^ 2 / l ^ 1 of the same quad (DPP quad permutations:
+// plain VALU moves, no LDS traffic)
+__device__ __forceinline__ float quad_xor2(float v) {
+  return __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(v), 0x4E, 0xF, 0xF, false));  // [2,3,0,1]
+}
+__device__ __forceinline__ float quad_xor1(float v) {
+  return __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(v), 0xB1, 0xF, 0xF, false));  // [1,0,3,2]
+}
+
 // 4 x 4 transpose across the four lanes of a quad: lane 4q + i holding x[k] =
 // element (k, i) ends up holding x[j] = element (i, j), where element (k, c)
 // is the value lane 4q + c held in x[k]. Two exchange rounds (lane xor 2, then
-// lane xor 1).
+// lane xor 1), each sending two values and keeping two, with selects only.
 __device__ __forceinline__ void quad_transpose4(float (&x)[4], int lane) {
   const bool b1 = lane & 2, b0 = lane & 1;
-  float s0 = b1 ? x[0] : x[2], s1 = b1 ? x[1] : x[3];
-  float r0 = __shfl_xor(s0, 2), r1 = __shfl_xor(s1, 2);
-  if (b1) {
-    x[0] = r0;
-    x[1] = r1;
-  } else {
-    x[2] = r0;
-    x[3] = r1;
-  }
-  s0 = b0 ? x[0] : x[1];
-  s1 = b0 ? x[2] : x[3];
-  r0 = __shfl_xor(s0, 1);
-  r1 = __shfl_xor(s1, 1);
-  if (b0) {
-    x[0] = r0;
-    x[2] = r1;
-  } else {
-    x[1] = r0;
-    x[3] = r1;
-  }
+  float r0 = quad_xor2(b1 ? x[0] : x[2]), r1 = quad_xor2(b1 ? x[1] : x[3]);
+  const float y0 = b1 ? r0 : x[0], y1 = b1 ? r1 : x[1], y2 = b1 ? x[2] : r0, y3 = b1 ? x[3] : r1;
+  r0 = quad_xor1(b0 ? y0 : y1);
+  r1 = quad_xor1(b0 ? y2 : y3);
+  x[0] = b0 ? r0 : y0;
+  x[1] = b0 ? y1 : r0;
+  x[2] = b0 ? r1 : y2;
+  x[3] = b0 ? y3 : r1;
+}
+
+// two floats rounded to bf16 (round to nearest even, v_cvt_pk_bf16_f32),
+// the first in the low half
+__device__ __forceinline__ uint32_t pack2_rne(float a, float b) {
+  typedef __bf16 bf16x2_hw __attribute__((ext_vector_type(2)));
+  typedef float float2_hw __attribute__((ext_vector_type(2)));
+  const float2_hw f = {a, b};
+  return __builtin_bit_cast(uint32_t, __builtin_convertvector(f, bf16x2_hw));
 }
 
 // s_waitcnt vmcnt(N) lgkmcnt(0) (gfx9 encoding: vmcnt[3:0], expcnt[6:4],
@@ -584,7 +592,8 @@ constexpr int G16_KALIGN = 64;  // K multiple the bf16 entry point accepts
 constexpr int G32_KALIGN = 32;  // K multiple the fp32 entry point accepts
 constexpr int G32_BM = 64;      // fp32 tile height (the padding-token skip granularity)
 
-template <typename TI, int BM, int BN, int WM, int WN, int NT, int RB, int S, int ORDER, int ACT, bool OUT_F32>
+template <typename TI, int BM, int BN, int WM, int WN, int NT, int RB, int S, int ORDER, int ACT, bool OUT_F32,
+          bool PERSIST>
 __device__ __forceinline__ void gemm_mfma(const TI* __restrict__ X, int ldx, const TI* __restrict__ W, int ldw,
                                           const float* __restrict__ bias, void* __restrict__ Y, int ldy, int M,
                                           int N, int K, const rb_k_row* __restrict__ skip_rows, int skip_T) {
@@ -617,9 +626,19 @@ __device__ __forceinline__ void gemm_mfma(const TI* __restrict__ X, int ldx, con
   const int wid = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int wm = wid / (BN / WN), wn = wid % (BN / WN);
   const int tiles_n = N / BN;
-  const int tile = ORDER ? xcd_tile(blockIdx.x, gridDim.x) : (int)blockIdx.x;
-  const int bm = tile / tiles_n, bn = tile - bm * tiles_n;
-  const int m0 = bm * BM, n0 = bn * BN;
+  const int ntiles = ((M + BM - 1) / BM) * tiles_n;
+  // v: this workgroup's index in the tile sequence (blockIdx.x, then + gridDim.x
+  // per tile when persistent; gridDim.x is a multiple of 8, so v % 8 stays the
+  // XCD the workgroup runs on)
+  int v = blockIdx.x;
+  auto tile_origin = [&](int vv, int& m0_, int& n0_) {
+    const int tile = ORDER ? xcd_tile(vv, ntiles) : vv;
+    const int bm = tile / tiles_n;
+    m0_ = bm * BM;
+    n0_ = (tile - bm * tiles_n) * BN;
+  };
+  int m0, n0;
+  tile_origin(v, m0, n0);
   if (skip_rows) {  // uniform per workgroup
     const int e = m0 / skip_T;
     const rb_k_row rw = skip_rows[e];
@@ -630,39 +649,82 @@ __device__ __forceinline__ void gemm_mfma(const TI* __restrict__ X, int ldx, con
   const int lr = lane / CPR, lc = lane % CPR;
   // byte offsets from the tile's first row (buffer resources based there; the
   // k-step's byte offset goes in the scalar offset)
-  const i32x4_t rA = buffer_rsrc(X + (int64_t)m0 * ldx), rB = buffer_rsrc(W + (int64_t)n0 * ldw);
-  uint32_t va[SA], vb[SB];
+  auto a_offsets = [&](int m0_, uint32_t (&va_)[SA]) {
 #pragma unroll
-  for (int i = 0; i < SA; ++i) {
-    const int row = (wid * SA + i) * RPI + lr;
-    const int ra = min(row, M - 1 - m0);  // rows past M are computed on a copy and never stored
-    va[i] = (uint32_t)(ra * ldx + (lc ^ ((row / SWZ) % CPR)) * EPC) * (uint32_t)ES;
-  }
+    for (int i = 0; i < SA; ++i) {
+      const int row = (wid * SA + i) * RPI + lr;
+      const int ra = min(row, M - 1 - m0_);  // rows past M are computed on a copy and never stored
+      va_[i] = (uint32_t)(ra * ldx + (lc ^ ((row / SWZ) % CPR)) * EPC) * (uint32_t)ES;
+    }
+  };
+  i32x4_t rA = buffer_rsrc(X + (int64_t)m0 * ldx), rB = buffer_rsrc(W + (int64_t)n0 * ldw);
+  uint32_t va[SA], vb[SB];
+  a_offsets(m0, va);
 #pragma unroll
   for (int i = 0; i < SB; ++i) {
     const int row = (wid * SB + i) * RPI + lr;
     vb[i] = (uint32_t)(row * ldw + (lc ^ ((row / SWZ) % CPR)) * EPC) * (uint32_t)ES;
   }
+  // persistent: the next tile's origin, resources and A offsets (a copy of the
+  // current tile's when there is none)
+  int m0n = m0, n0n = n0;
+  bool has_next = false;
+  i32x4_t rAn = rA, rBn = rB;
+  uint32_t van[SA];
+#pragma unroll
+  for (int i = 0; i < SA; ++i) van[i] = va[i];
+  auto next_tile = [&]() {
+    has_next = v + (int)gridDim.x < ntiles;
+    if (has_next) {
+      tile_origin(v + (int)gridDim.x, m0n, n0n);
+      rAn = buffer_rsrc(X + (int64_t)m0n * ldx);
+      rBn = buffer_rsrc(W + (int64_t)n0n * ldw);
+      a_offsets(m0n, van);
+    } else {
+      m0n = m0;
+      n0n = n0;
+      rAn = rA;
+      rBn = rB;
+#pragma unroll
+      for (int i = 0; i < SA; ++i) van[i] = va[i];
+    }
+  };
+  if constexpr (PERSIST) next_tile();
 
   floatx16_t acc[TM][TN];
+  auto zero_acc = [&]() {
 #pragma unroll
-  for (int i = 0; i < TM; ++i)
+    for (int i = 0; i < TM; ++i)
 #pragma unroll
-    for (int j = 0; j < TN; ++j)
+      for (int j = 0; j < TN; ++j)
 #pragma unroll
-      for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
+        for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
+  };
+  zero_acc();
 
   const int nk = K / BK;
   // load instruction o (A rows for o < SA, then B rows) of k-step kt into
   // stage st. K-steps past the end reload the last one into a stage that is
-  // never read again, so every step runs the same branch-free code.
+  // never read again, so every step runs the same branch-free code; when
+  // persistent, they are the next tile's first k-steps instead (the load stream
+  // runs on across tiles, so the next tile's operands are in flight during this
+  // tile's last steps and epilogue).
   auto issue_one = [&](int kt, auto stc, auto oc) {
     constexpr int st = decltype(stc)::value, o = decltype(oc)::value;
-    const uint32_t kb = (uint32_t)(min(kt, nk - 1) * RB);
-    if constexpr (o < SA)
-      buffer_to_lds(rA, va[o], kb, lds_addr(&sA[st][0]) + (wid * SA + o) * 1024);
-    else
-      buffer_to_lds(rB, vb[o - SA], kb, lds_addr(&sB[st][0]) + (wid * SB + o - SA) * 1024);
+    if constexpr (PERSIST) {
+      const bool nx = kt >= nk;  // uniform
+      const uint32_t kb = (uint32_t)((nx ? (has_next ? kt - nk : nk - 1) : kt) * RB);
+      if constexpr (o < SA)
+        buffer_to_lds(nx ? rAn : rA, nx ? van[o] : va[o], kb, lds_addr(&sA[st][0]) + (wid * SA + o) * 1024);
+      else
+        buffer_to_lds(nx ? rBn : rB, vb[o - SA], kb, lds_addr(&sB[st][0]) + (wid * SB + o - SA) * 1024);
+    } else {
+      const uint32_t kb = (uint32_t)(min(kt, nk - 1) * RB);
+      if constexpr (o < SA)
+        buffer_to_lds(rA, va[o], kb, lds_addr(&sA[st][0]) + (wid * SA + o) * 1024);
+      else
+        buffer_to_lds(rB, vb[o - SA], kb, lds_addr(&sB[st][0]) + (wid * SB + o - SA) * 1024);
+    }
   };
   u32x4_t fa[2][TM], fb[2][TN];
   // fragment read q (A fragment q for q < TM, then B) of sub-step kk of stage st
@@ -720,18 +782,12 @@ __device__ __forceinline__ void gemm_mfma(const TI* __restrict__ X, int ldx, con
   wait_vmcnt_lds<(S - 2) * OPS>();
   lds_barrier();
   static_for<NR>([&](auto qc) { read_one(ic<0>{}, 0, qc, ic<0>{}); });
-  int kt = 0;
-  for (; kt + S <= nk; kt += S) {
+  auto group = [&](int kt) {  // S k-steps from a multiple of S
     step(kt, ic<0>{}, ic<1>{}, ic<S - 1>{});
     step(kt + 1, ic<1>{}, ic<2 % S>{}, ic<0>{});
     step(kt + 2, ic<2>{}, ic<3 % S>{}, ic<1>{});
     if constexpr (S > 3) step(kt + 3, ic<3>{}, ic<0>{}, ic<2>{});
-  }
-  if (kt < nk) step(kt, ic<0>{}, ic<1>{}, ic<S - 1>{});
-  if (kt + 1 < nk) step(kt + 1, ic<1>{}, ic<2 % S>{}, ic<0>{});
-  if (S > 3 && kt + 2 < nk) step(kt + 2, ic<2>{}, ic<3 % S>{}, ic<1>{});
-  // no load into LDS may still be in flight when the wave ends
-  wait_vmcnt_lds<0>();
+  };
 
   // accumulator (i, j) register r of lane l holds row 8*(r/4) + 4*(l/32) + r%4,
   // column l%32 of its 32 x 32 block. Bias and activation are applied per
@@ -739,6 +795,7 @@ __device__ __forceinline__ void gemm_mfma(const TI* __restrict__ X, int ldx, con
   // transposed across the four lanes of a quad, so that a lane holds four
   // consecutive columns of one row and stores them at once (8 bytes bf16, 16
   // bytes fp32) instead of four single elements.
+  auto epilogue = [&]() {
 #pragma unroll
   for (int j = 0; j < TN; ++j) {
     const float bb = bias[n0 + wn * WN + j * 32 + (lane & 31)];
@@ -747,38 +804,70 @@ __device__ __forceinline__ void gemm_mfma(const TI* __restrict__ X, int ldx, con
     for (int i = 0; i < TM; ++i)
 #pragma unroll
       for (int g = 0; g < 4; ++g) {
-        float v[4];
+        float q[4];
 #pragma unroll
-        for (int k = 0; k < 4; ++k) v[k] = act_fn<ACT>(acc[i][j][4 * g + k] + bb);
-        quad_transpose4(v, lane);
+        for (int k = 0; k < 4; ++k) q[k] = act_fn<ACT>(acc[i][j][4 * g + k] + bb);
+        quad_transpose4(q, lane);
         const int row = m0 + wm * WM + i * 32 + 8 * g + 4 * (lane >> 5) + (lane & 3);
         if (row < M) {
           if (OUT_F32) {
-            *(float4*)((float*)Y + (int64_t)row * ldy + colq) = make_float4(v[0], v[1], v[2], v[3]);
+            *(float4*)((float*)Y + (int64_t)row * ldy + colq) = make_float4(q[0], q[1], q[2], q[3]);
           } else {
-            *(uint2*)((bf16_t*)Y + (int64_t)row * ldy + colq) = make_uint2(pack2(v[0], v[1]), pack2(v[2], v[3]));
+            *(uint2*)((bf16_t*)Y + (int64_t)row * ldy + colq) = make_uint2(pack2_rne(q[0], q[1]), pack2_rne(q[2], q[3]));
           }
         }
       }
+  }
+  };
+
+  if constexpr (PERSIST) {
+    // K a multiple of S k-steps (so every tile starts at stage 0) and at least
+    // S k-steps (so the loads of a tile's last steps reach only the next tile)
+    for (;;) {
+      for (int kt = 0; kt < nk; kt += S) group(kt);
+      epilogue();
+      if (!has_next) break;
+      v += gridDim.x;
+      m0 = m0n;
+      n0 = n0n;
+      rA = rAn;
+      rB = rBn;
+#pragma unroll
+      for (int i = 0; i < SA; ++i) va[i] = van[i];
+      next_tile();
+      zero_acc();
+    }
+    // no load into LDS may still be in flight when the wave ends
+    wait_vmcnt_lds<0>();
+  } else {
+    int kt = 0;
+    for (; kt + S <= nk; kt += S) group(kt);
+    if (kt < nk) step(kt, ic<0>{}, ic<1>{}, ic<S - 1>{});
+    if (kt + 1 < nk) step(kt + 1, ic<1>{}, ic<2 % S>{}, ic<0>{});
+    if (S > 3 && kt + 2 < nk) step(kt + 2, ic<2>{}, ic<3 % S>{}, ic<1>{});
+    // no load into LDS may still be in flight when the wave ends
+    wait_vmcnt_lds<0>();
+    epilogue();
   }
 }
 
 // The two operand types as separately named kernels (so that traces and
 // counters tell them apart).
-template <int BM, int BN, int WM, int WN, int NT, int RB, int S, int ORDER, int ACT, bool OUT_F32>
+template <int BM, int BN, int WM, int WN, int NT, int RB, int S, int ORDER, int ACT, bool OUT_F32, bool PERSIST>
 __global__ __launch_bounds__(NT) void k_gemm_bf16(const bf16_t* __restrict__ X, int ldx,
                                                   const bf16_t* __restrict__ W, int ldw,
                                                   const float* __restrict__ bias, void* __restrict__ Y, int ldy,
                                                   int M, int N, int K) {
-  gemm_mfma<bf16_t, BM, BN, WM, WN, NT, RB, S, ORDER, ACT, OUT_F32>(X, ldx, W, ldw, bias, Y, ldy, M, N, K, nullptr, 0);
+  gemm_mfma<bf16_t, BM, BN, WM, WN, NT, RB, S, ORDER, ACT, OUT_F32, PERSIST>(X, ldx, W, ldw, bias, Y, ldy, M, N, K,
+                                                                            nullptr, 0);
 }
 template <int BM, int BN, int WM, int WN, int NT, int RB, int S, int ORDER, int ACT>
 __global__ __launch_bounds__(NT) void k_gemm_f32(const float* __restrict__ X, int ldx, const float* __restrict__ W,
                                                  int ldw, const float* __restrict__ bias, void* __restrict__ Y,
                                                  int ldy, int M, int N, int K,
                                                  const rb_k_row* __restrict__ skip_rows, int skip_T) {
-  gemm_mfma<float, BM, BN, WM, WN, NT, RB, S, ORDER, ACT, true>(X, ldx, W, ldw, bias, Y, ldy, M, N, K, skip_rows,
-                                                                skip_T);
+  gemm_mfma<float, BM, BN, WM, WN, NT, RB, S, ORDER, ACT, true, false>(X, ldx, W, ldw, bias, Y, ldy, M, N, K,
+                                                                       skip_rows, skip_T);
 }
 
 // ---------------------------------------------------------------- heads and split
@@ -941,10 +1030,14 @@ inline unsigned blocks_for(int64_t threads) { return (unsigned)((threads + 255) 
 
 namespace {
 
-template <typename TI, int BM, int BN, int WM, int WN, int NT, int RB, int S, int ORDER>
+// PERSIST: a grid of at most `cap` workgroups (a multiple of 8), each taking
+// every cap-th tile
+template <typename TI, int BM, int BN, int WM, int WN, int NT, int RB, int S, int ORDER, bool PERSIST = false>
 void launch_gemm(hipStream_t s, const TI* x, int ldx, const TI* w, int ldw, const float* b, void* Y, int ldy,
-                 int M, int N, int K, int act, bool out_f32, const rb_k_row* skip_rows, int skip_T) {
-  const unsigned g = (unsigned)(((M + BM - 1) / BM) * (N / BN));
+                 int M, int N, int K, int act, bool out_f32, const rb_k_row* skip_rows, int skip_T,
+                 unsigned cap = 0) {
+  const unsigned tiles = (unsigned)(((M + BM - 1) / BM) * (N / BN));
+  const unsigned g = PERSIST ? std::min(tiles, cap) : tiles;
   if constexpr (sizeof(TI) == 4) {
 #define RB_G(A)                                                                                                     \
   hipLaunchKernelGGL((k_gemm_f32<BM, BN, WM, WN, NT, RB, S, ORDER, A>), dim3(g), dim3(NT), 0, s, x, ldx, w, ldw, b, \
@@ -955,7 +1048,7 @@ void launch_gemm(hipStream_t s, const TI* x, int ldx, const TI* w, int ldw, cons
 #undef RB_G
   } else {
 #define RB_G(A, F)                                                                                             \
-  hipLaunchKernelGGL((k_gemm_bf16<BM, BN, WM, WN, NT, RB, S, ORDER, A, F>), dim3(g), dim3(NT), 0, s, x, ldx, w, \
+  hipLaunchKernelGGL((k_gemm_bf16<BM, BN, WM, WN, NT, RB, S, ORDER, A, F, PERSIST>), dim3(g), dim3(NT), 0, s, x, ldx, w, \
                      ldw, b, Y, ldy, M, N, K)
     if (out_f32) {
       if (act == RB_ACT_RELU) RB_G(RB_ACT_RELU, true);
@@ -971,11 +1064,24 @@ void launch_gemm(hipStream_t s, const TI* x, int ldx, const TI* w, int ldw, cons
 }
 
 // bf16 operands, k-step BK bf16 values
-template <int BM, int BN, int WM, int WN, int NT, int BK, int S, int ORDER>
+template <int BM, int BN, int WM, int WN, int NT, int BK, int S, int ORDER, bool PERSIST>
 void launch_gemm_bf16(hipStream_t s, const bf16_t* x, int ldx, const bf16_t* w, int ldw, const float* b, void* Y,
-                      int ldy, int M, int N, int K, int act, int out_f32) {
-  launch_gemm<bf16_t, BM, BN, WM, WN, NT, BK * 2, S, ORDER>(s, x, ldx, w, ldw, b, Y, ldy, M, N, K, act, out_f32 != 0,
-                                                           nullptr, 0);
+                      int ldy, int M, int N, int K, int act, int out_f32, unsigned cap) {
+  launch_gemm<bf16_t, BM, BN, WM, WN, NT, BK * 2, S, ORDER, PERSIST>(s, x, ldx, w, ldw, b, Y, ldy, M, N, K, act,
+                                                                    out_f32 != 0, nullptr, 0, cap);
+}
+
+// compute units of the current device (cached per device)
+unsigned device_cus() {
+  static std::atomic<int> cus[64];
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 256;
+  int c = cus[dev].load(std::memory_order_relaxed);
+  if (c <= 0) {
+    if (hipDeviceGetAttribute(&c, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || c <= 0) c = 256;
+    cus[dev].store(c, std::memory_order_relaxed);
+  }
+  return (unsigned)c;
 }
 
 }  // namespace
@@ -1093,19 +1199,42 @@ rb_status rb_k_gemm_bf16(void* stream, const void* X, int32_t ldx, const void* W
   // tile order when all of W fits in one XCD's L2 (each XCD then keeps its A
   // row-blocks and W in its own L2); plain order otherwise (contiguous ranges
   // would stream all of W through every XCD).
+  //
+  // With more tiles than compute units, the grid is persistent (one workgroup
+  // per CU, each taking every CU-count-th tile) when K is a multiple of the
+  // stage count in k-steps: the operand loads then run on across tile
+  // boundaries, so a tile's first k-steps load during the previous tile's last
+  // steps and epilogue.
   const int64_t rows256 = (M + 255) / 256;
   const bool xcd = (int64_t)N * K * 2 <= (4 << 20);
-#define RB_PICK(BM, BN, WM, WN, NT, BK, S)                                                                        \
-  do {                                                                                                            \
-    if (xcd) launch_gemm_bf16<BM, BN, WM, WN, NT, BK, S, 1>(s, x, ldx, w, ldw, b, Y, ldy, M, N, K, act, out_f32); \
-    else launch_gemm_bf16<BM, BN, WM, WN, NT, BK, S, 0>(s, x, ldx, w, ldw, b, Y, ldy, M, N, K, act, out_f32);     \
+  const unsigned cus = device_cus() & ~7u;
+#define RB_PICK(BM, BN, WM, WN, NT, BK, S, P)                                                                   \
+  do {                                                                                                          \
+    if (xcd)                                                                                                    \
+      launch_gemm_bf16<BM, BN, WM, WN, NT, BK, S, 1, P>(s, x, ldx, w, ldw, b, Y, ldy, M, N, K, act, out_f32, cus); \
+    else                                                                                                        \
+      launch_gemm_bf16<BM, BN, WM, WN, NT, BK, S, 0, P>(s, x, ldx, w, ldw, b, Y, ldy, M, N, K, act, out_f32, cus); \
   } while (0)
-  if (N % 256 == 0 && rows256 * (N / 256) >= 256)
-    RB_PICK(256, 256, 64, 128, 512, 32, 4);
-  else if (rows256 * (N / 128) >= 256)
-    RB_PICK(256, 128, 64, 64, 512, 64, 3);
-  else
-    RB_PICK(128, 128, 64, 32, 512, 64, 4);
+  auto persist = [&](int bm, int bn, int bk, int st) {
+    const int64_t tiles = ((M + bm - 1) / bm) * (int64_t)(N / bn);
+    const int nk = K / bk;
+    return cus >= 8 && tiles > (int64_t)cus && nk >= st && nk % st == 0;
+  };
+  if (N % 256 == 0 && rows256 * (N / 256) >= 256) {
+    if (persist(256, 256, 32, 4))
+      RB_PICK(256, 256, 64, 128, 512, 32, 4, true);
+    else if (persist(256, 256, 32, 3))
+      RB_PICK(256, 256, 64, 128, 512, 32, 3, true);
+    else
+      RB_PICK(256, 256, 64, 128, 512, 32, 4, false);
+  } else if (rows256 * (N / 128) >= 256) {
+    if (persist(256, 128, 64, 3))
+      RB_PICK(256, 128, 64, 64, 512, 64, 3, true);
+    else
+      RB_PICK(256, 128, 64, 64, 512, 64, 3, false);
+  } else {
+    RB_PICK(128, 128, 64, 32, 512, 64, 4, false);
+  }
 #undef RB_PICK
   return launch_status();
 }

@@ -340,7 +340,11 @@ def _row_scaled_err(y, ref):
 @pytest.mark.parametrize("M,N,K,act,out_f32,pad_y", [
     (1, 128, 64, rb.RB_ACT_NONE, 1, 0), (200, 256, 1728, rb.RB_ACT_RELU, 0, 0), (1024, 1024, 512, rb.RB_ACT_RELU, 0, 0),
     (333, 512, 1024, rb.RB_ACT_NONE, 1, 0), (130, 128, 4096, rb.RB_ACT_SIGMOID, 1, 0),
-    (77, 256, 128, rb.RB_ACT_RELU, 0, 8), (300, 384, 256, rb.RB_ACT_NONE, 1, 24)])
+    (77, 256, 128, rb.RB_ACT_RELU, 0, 8), (300, 384, 256, rb.RB_ACT_NONE, 1, 24),
+    # more tiles than compute units: persistent grids (256 x 256 tiles with 4
+    # and 3 stages, XCD and plain tile order; 256 x 128 tiles), ragged last rows
+    (4500, 4096, 512, rb.RB_ACT_RELU, 0, 0), (4500, 4096, 192, rb.RB_ACT_NONE, 1, 8),
+    (2100, 8192, 512, rb.RB_ACT_SIGMOID, 0, 0), (25600 - 37, 384, 192, rb.RB_ACT_RELU, 1, 0)])
 def test_gemm_bf16_matches_fp64(M, N, K, act, out_f32, pad_y):
     rng = np.random.default_rng(4)
     Xd, X = _bf16_dev(rng.standard_normal((M, K)))
@@ -388,12 +392,14 @@ def test_gemm_f32_matches_fp64(M, N, K, act):
 
 
 @pytest.mark.parametrize("dtype,N,K", [("f32", 512, 256), ("f32", 1024, 1088), ("bf16", 512, 256),
-                                        ("bf16", 1024, 2112)])
+                                        ("bf16", 1024, 2112), ("bf16", 4096, 512), ("bf16", 2048, 1728)])
 def test_gemm_rows_independent_of_batch(dtype, N, K):
     # a row's output bits do not depend on how many rows share the launch or on
     # where it sits among them: the same k order for every M, tile shape and
-    # tile order (K = 1088 / 2112 puts W above 4 MB: plain tile order; the bf16
-    # launch of all rows takes a larger tile than the partial ones)
+    # tile order (K = 1088 / 2112 / 1728 puts W above 4 MB: plain tile order; the
+    # bf16 launch of all rows takes a larger tile than the partial ones; N = 4096
+    # and 2048 give the full launch more tiles than compute units, a persistent
+    # grid with 4 and 3 stages, while the partial launches are not persistent)
     rng = np.random.default_rng(11)
     M = 16384
     X = rng.standard_normal((M, K)).astype(np.float32)
