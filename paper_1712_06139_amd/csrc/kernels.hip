@@ -37,6 +37,8 @@ typedef __attribute__((__vector_size__(4 * sizeof(float)))) float floatx4_t;
 typedef __attribute__((__vector_size__(16 * sizeof(float)))) float floatx16_t;
 typedef unsigned int u32x4_t __attribute__((ext_vector_type(4)));
 typedef int i32x4_t __attribute__((ext_vector_type(4)));
+typedef unsigned int u32x2_t __attribute__((ext_vector_type(2)));
+typedef float f32x4_t __attribute__((ext_vector_type(4)));
 
 __device__ __forceinline__ bf16_t f2bf(float f) {
   // round to nearest even on the 16 dropped bits; NaN stays a (quiet) NaN
@@ -809,11 +811,16 @@ __device__ __forceinline__ void gemm_mfma(const TI* __restrict__ X, int ldx, con
         for (int k = 0; k < 4; ++k) q[k] = act_fn<ACT>(acc[i][j][4 * g + k] + bb);
         quad_transpose4(q, lane);
         const int row = m0 + wm * WM + i * 32 + 8 * g + 4 * (lane >> 5) + (lane & 3);
+        // streaming (nontemporal) stores: the whole chip writes its tiles'
+        // outputs at about the same time, and these drain faster than
+        // stores that allocate in L2
         if (row < M) {
           if (OUT_F32) {
-            *(float4*)((float*)Y + (int64_t)row * ldy + colq) = make_float4(q[0], q[1], q[2], q[3]);
+            const f32x4_t o = {q[0], q[1], q[2], q[3]};
+            __builtin_nontemporal_store(o, (f32x4_t*)((float*)Y + (int64_t)row * ldy + colq));
           } else {
-            *(uint2*)((bf16_t*)Y + (int64_t)row * ldy + colq) = make_uint2(pack2_rne(q[0], q[1]), pack2_rne(q[2], q[3]));
+            const u32x2_t o = {pack2_rne(q[0], q[1]), pack2_rne(q[2], q[3])};
+            __builtin_nontemporal_store(o, (u32x2_t*)((bf16_t*)Y + (int64_t)row * ldy + colq));
           }
         }
       }
