@@ -557,10 +557,11 @@ __device__ __forceinline__ void buffer_to_lds(i32x4_t rsrc, uint32_t voff, uint3
 // Workgroup tile BM x BN, k-step of RB bytes per row (64 or 128: 32 or 64
 // bf16, 16 or 32 fp32), NT/64 waves each owning a WM x WN sub-tile
 // ((WM/32) x (WN/32) accumulators). Operand tiles go straight from global
-// memory into a ring of S >= 3 LDS stages (global_load_lds: each wave load
+// memory into a ring of S >= 2 LDS stages (global_load_lds: each wave load
 // instruction fills 1 KB of consecutive LDS rows; no register staging).
 // K-step kt reads stage kt % S while the stage of k-step kt - 1 is refilled
-// with k-step kt - 1 + S, its loads spread one every few MFMAs over the step:
+// with k-step kt - 1 + S, its loads spread one every few MFMAs over the step
+// (over its first half when S = 2, where that refill is the next k-step):
 // issued back to back they stall the wave on the texture path with no MFMA in
 // flight. A sub-step covers 32 bytes of every row (16 bf16 or 8 fp32 k values)
 // and its MFMAs have the next sub-step's fragment reads between them. In the
@@ -605,7 +606,7 @@ __device__ __forceinline__ void gemm_mfma(const TI* __restrict__ X, int ldx, con
   constexpr int NW = NT / 64;
   static_assert((BM / WM) * (BN / WN) == NW, "one wave per sub-tile");
   static_assert(RB == 64 || RB == 128, "k-step of 64 or 128 bytes per row");
-  static_assert(S >= 3 && S <= 4, "3..4 stages");
+  static_assert(S >= 2 && S <= 4, "2..4 stages");
   constexpr int CPR = RB / 16;   // 16-byte chunks per LDS row
   constexpr int RPI = 64 / CPR;  // rows filled per wave load instruction
   constexpr int SWZ = 16 / CPR;  // rows sharing one swizzle pattern
@@ -621,6 +622,10 @@ __device__ __forceinline__ void gemm_mfma(const TI* __restrict__ X, int ldx, con
   constexpr int NU = NM * MPF;   // MFMAs per sub-step
   constexpr int NR = TM + TN;    // fragment reads per sub-step
   constexpr int PRE = (KK - 1) * NU + NU / 2;  // MFMAs of a step before its barrier
+  // MFMA slots the refill loads are spread over: with two stages the stage
+  // refilled during a step is the one the next step reads, so its loads go in
+  // the first half of the step to land before the barrier
+  constexpr int LPOS = S == 2 ? PRE / 2 : PRE;
   __shared__ u32x4_t sA[S][BM * CPR];
   __shared__ u32x4_t sB[S][BN * CPR];
 
@@ -774,7 +779,7 @@ __device__ __forceinline__ void gemm_mfma(const TI* __restrict__ X, int ldx, con
         constexpr int pos = kk * NU + u;
         static_for<OPS>([&](auto oc) {
           constexpr int o = decltype(oc)::value;
-          if constexpr (o * PRE / OPS == pos) issue_one(kt - 1 + S, rstc, oc);
+          if constexpr (o * LPOS / OPS == pos) issue_one(kt - 1 + S, rstc, oc);
         });
         __builtin_amdgcn_sched_barrier(0);
       });
@@ -787,7 +792,7 @@ __device__ __forceinline__ void gemm_mfma(const TI* __restrict__ X, int ldx, con
   auto group = [&](int kt) {  // S k-steps from a multiple of S
     step(kt, ic<0>{}, ic<1>{}, ic<S - 1>{});
     step(kt + 1, ic<1>{}, ic<2 % S>{}, ic<0>{});
-    step(kt + 2, ic<2>{}, ic<3 % S>{}, ic<1>{});
+    if constexpr (S > 2) step(kt + 2, ic<2 % S>{}, ic<3 % S>{}, ic<1>{});
     if constexpr (S > 3) step(kt + 3, ic<3>{}, ic<0>{}, ic<2>{});
   };
 
@@ -851,7 +856,8 @@ __device__ __forceinline__ void gemm_mfma(const TI* __restrict__ X, int ldx, con
     for (; kt + S <= nk; kt += S) group(kt);
     if (kt < nk) step(kt, ic<0>{}, ic<1>{}, ic<S - 1>{});
     if (kt + 1 < nk) step(kt + 1, ic<1>{}, ic<2 % S>{}, ic<0>{});
-    if (S > 3 && kt + 2 < nk) step(kt + 2, ic<2>{}, ic<3 % S>{}, ic<1>{});
+    if constexpr (S > 3)
+      if (kt + 2 < nk) step(kt + 2, ic<2 % S>{}, ic<3 % S>{}, ic<1>{});
     // no load into LDS may still be in flight when the wave ends
     wait_vmcnt_lds<0>();
     epilogue();
@@ -1200,15 +1206,17 @@ rb_status rb_k_gemm_bf16(void* stream, const void* X, int32_t ldx, const void* W
   // Tile shape, k-step, stage count and tile order only change speed: every
   // choice accumulates each output in the same k order with the same
   // instruction (identical bits). The largest tile that still gives every CU a
-  // tile: 256 x 256 (8 waves of 64 x 128, k-step 32, 4 stages, 128 KB LDS),
-  // else 256 x 128 (8 waves of 64 x 64, k-step 64, 3 stages, 144 KB), else
+  // tile: 256 x 256 (4 waves of 128 x 128, k-step 64, 2 stages, 128 KB LDS:
+  // half the fragment reads per flop of 8 waves of 64 x 128, and every row's
+  // k-step a whole 128-byte line), else 256 x 128 (8 waves of 64 x 64, k-step
+  // 64, 3 stages, 144 KB), else
   // 128 x 128 (8 waves of 64 x 32, k-step 64, 4 stages, 128 KB). XCD-contiguous
   // tile order when all of W fits in one XCD's L2 (each XCD then keeps its A
   // row-blocks and W in its own L2); plain order otherwise (contiguous ranges
   // would stream all of W through every XCD).
   //
-  // With more tiles than compute units, the grid is persistent (one workgroup
-  // per CU, each taking every CU-count-th tile) when K is a multiple of the
+  // With more 256 x 128 tiles than compute units, the grid is persistent (one
+  // workgroup per CU, each taking every CU-count-th tile) when K is a multiple of the
   // stage count in k-steps: the operand loads then run on across tile
   // boundaries, so a tile's first k-steps load during the previous tile's last
   // steps and epilogue.
@@ -1228,12 +1236,7 @@ rb_status rb_k_gemm_bf16(void* stream, const void* X, int32_t ldx, const void* W
     return cus >= 8 && tiles > (int64_t)cus && nk >= st && nk % st == 0;
   };
   if (N % 256 == 0 && rows256 * (N / 256) >= 256) {
-    if (persist(256, 256, 32, 4))
-      RB_PICK(256, 256, 64, 128, 512, 32, 4, true);
-    else if (persist(256, 256, 32, 3))
-      RB_PICK(256, 256, 64, 128, 512, 32, 3, true);
-    else
-      RB_PICK(256, 256, 64, 128, 512, 32, 4, false);
+    RB_PICK(256, 256, 128, 128, 256, 64, 2, false);
   } else if (rows256 * (N / 128) >= 256) {
     if (persist(256, 128, 64, 3))
       RB_PICK(256, 128, 64, 64, 512, 64, 3, true);
