@@ -565,7 +565,7 @@ __device__ __forceinline__ void buffer_to_lds(i32x4_t rsrc, uint32_t voff, uint3
 // issued back to back they stall the wave on the texture path with no MFMA in
 // flight. A sub-step covers 32 bytes of every row (16 bf16 or 8 fp32 k values)
 // and its MFMAs have the next sub-step's fragment reads between them. In the
-// last sub-step, after half of its MFMAs, the wave waits for its loads of the
+// last sub-step, after half of its MFMAs (three quarters with S = 2), the wave waits for its loads of the
 // next k-step and for its LDS reads, and all waves meet at one barrier: the
 // next stage has landed and nobody reads the current one again. The other
 // half then runs with the next k-step's first fragment reads between the
@@ -621,11 +621,27 @@ __device__ __forceinline__ void gemm_mfma(const TI* __restrict__ X, int ldx, con
   constexpr int MPF = F32 ? 4 : 1;  // MFMAs per accumulator and sub-step
   constexpr int NU = NM * MPF;   // MFMAs per sub-step
   constexpr int NR = TM + TN;    // fragment reads per sub-step
-  constexpr int PRE = (KK - 1) * NU + NU / 2;  // MFMAs of a step before its barrier
+  // the last sub-step's MFMAs before the barrier: half of them, three quarters
+  // with two stages (more time for the loads of the next k-step to land)
+  constexpr int UB = S == 2 ? NU * 3 / 4 : NU / 2;
+  constexpr int PRE = (KK - 1) * NU + UB;  // MFMAs of a step before its barrier
   // MFMA slots the refill loads are spread over: with two stages the stage
   // refilled during a step is the one the next step reads, so its loads go in
   // the first half of the step to land before the barrier
   constexpr int LPOS = S == 2 ? PRE / 2 : PRE;
+  // fragment read slot -> fragment (A fragments q < TM, then B). With two
+  // stages (bf16) in the order the next sub-step's MFMAs consume them (A0, B0
+  // .. B(TN-1), A1 .. A(TM-1)), so the fragment needed first is read first;
+  // otherwise A0 .. A(TM-1), B0 .. B(TN-1).
+  auto qmap = [](auto sc) {
+    constexpr int q = decltype(sc)::value;
+    if constexpr (S != 2 || F32 || q == 0)
+      return ic<q>{};
+    else if constexpr (q <= TN)
+      return ic<TM + q - 1>{};
+    else
+      return ic<q - TN>{};
+  };
   __shared__ u32x4_t sA[S][BM * CPR];
   __shared__ u32x4_t sB[S][BN * CPR];
 
@@ -756,7 +772,7 @@ __device__ __forceinline__ void gemm_mfma(const TI* __restrict__ X, int ldx, con
       static_for<NU>([&](auto uc) {
         constexpr int u = decltype(uc)::value;
         constexpr int m = u % NM, t = u / NM;
-        if constexpr (last && u == NU / 2) {
+        if constexpr (last && u == UB) {
           wait_vmcnt_lds<(S - 2) * OPS>();
           lds_barrier();
         }
@@ -771,9 +787,9 @@ __device__ __forceinline__ void gemm_mfma(const TI* __restrict__ X, int ldx, con
         static_for<NR>([&](auto qc) {
           constexpr int q = decltype(qc)::value;
           if constexpr (!last) {
-            if constexpr (q * NU / NR == u) read_one(stc, kk + 1, qc, ic<nxt>{});
-          } else if constexpr (u >= NU / 2) {
-            if constexpr (NU / 2 + q * (NU / 2) / NR == u) read_one(nstc, 0, qc, ic<0>{});
+            if constexpr (q * NU / NR == u) read_one(stc, kk + 1, qmap(qc), ic<nxt>{});
+          } else if constexpr (u >= UB) {
+            if constexpr (UB + q * (NU - UB) / NR == u) read_one(nstc, 0, qmap(qc), ic<0>{});
           }
         });
         constexpr int pos = kk * NU + u;
@@ -788,7 +804,7 @@ __device__ __forceinline__ void gemm_mfma(const TI* __restrict__ X, int ldx, con
   static_for<S - 1>([&](auto sc) { static_for<OPS>([&](auto oc) { issue_one(decltype(sc)::value, sc, oc); }); });
   wait_vmcnt_lds<(S - 2) * OPS>();
   lds_barrier();
-  static_for<NR>([&](auto qc) { read_one(ic<0>{}, 0, qc, ic<0>{}); });
+  static_for<NR>([&](auto qc) { read_one(ic<0>{}, 0, qmap(qc), ic<0>{}); });
   auto group = [&](int kt) {  // S k-steps from a multiple of S
     step(kt, ic<0>{}, ic<1>{}, ic<S - 1>{});
     step(kt + 1, ic<1>{}, ic<2 % S>{}, ic<0>{});
@@ -1206,9 +1222,11 @@ rb_status rb_k_gemm_bf16(void* stream, const void* X, int32_t ldx, const void* W
   // Tile shape, k-step, stage count and tile order only change speed: every
   // choice accumulates each output in the same k order with the same
   // instruction (identical bits). The largest tile that still gives every CU a
-  // tile: 256 x 256 (4 waves of 128 x 128, k-step 64, 2 stages, 128 KB LDS:
-  // half the fragment reads per flop of 8 waves of 64 x 128, and every row's
-  // k-step a whole 128-byte line), else 256 x 128 (8 waves of 64 x 64, k-step
+  // tile: 256 x 256 (k-step 64, 2 stages, 128 KB LDS, every row's k-step a
+  // whole 128-byte line) as 4 waves of 128 x 128 when there are at least two
+  // tiles per CU (half the fragment reads per flop of 8 waves of 64 x 128), as
+  // 8 waves of 64 x 128 when fewer (two waves per SIMD hide more of the single
+  // round's start and end), else 256 x 128 (8 waves of 64 x 64, k-step
   // 64, 3 stages, 144 KB), else
   // 128 x 128 (8 waves of 64 x 32, k-step 64, 4 stages, 128 KB). XCD-contiguous
   // tile order when all of W fits in one XCD's L2 (each XCD then keeps its A
@@ -1236,7 +1254,10 @@ rb_status rb_k_gemm_bf16(void* stream, const void* X, int32_t ldx, const void* W
     return cus >= 8 && tiles > (int64_t)cus && nk >= st && nk % st == 0;
   };
   if (N % 256 == 0 && rows256 * (N / 256) >= 256) {
-    RB_PICK(256, 256, 128, 128, 256, 64, 2, false);
+    if (rows256 * (N / 256) >= 2 * (int64_t)cus)
+      RB_PICK(256, 256, 128, 128, 256, 64, 2, false);
+    else
+      RB_PICK(256, 256, 64, 128, 512, 64, 2, false);
   } else if (rows256 * (N / 128) >= 256) {
     if (persist(256, 128, 64, 3))
       RB_PICK(256, 128, 64, 64, 512, 64, 3, true);

@@ -341,11 +341,14 @@ def _row_scaled_err(y, ref):
     (1, 128, 64, rb.RB_ACT_NONE, 1, 0), (200, 256, 1728, rb.RB_ACT_RELU, 0, 0), (1024, 1024, 512, rb.RB_ACT_RELU, 0, 0),
     (333, 512, 1024, rb.RB_ACT_NONE, 1, 0), (130, 128, 4096, rb.RB_ACT_SIGMOID, 1, 0),
     (77, 256, 128, rb.RB_ACT_RELU, 0, 8), (300, 384, 256, rb.RB_ACT_NONE, 1, 24),
-    # more tiles than compute units: 256 x 256 tiles of 4 waves with 2 stages
+    # more tiles than compute units: 256 x 256 tiles of 8 waves with 2 stages
     # (XCD and plain tile order; K = 192, an odd number of k-steps), a
     # persistent grid of 256 x 128 tiles, ragged last rows
     (4500, 4096, 512, rb.RB_ACT_RELU, 0, 0), (4500, 4096, 192, rb.RB_ACT_NONE, 1, 8),
-    (2100, 8192, 512, rb.RB_ACT_SIGMOID, 0, 0), (25600 - 37, 384, 192, rb.RB_ACT_RELU, 1, 0)])
+    (2100, 8192, 512, rb.RB_ACT_SIGMOID, 0, 0), (25600 - 37, 384, 192, rb.RB_ACT_RELU, 1, 0),
+    # at least two 256 x 256 tiles per compute unit: 4 waves of 128 x 128 (XCD
+    # and plain tile order)
+    (8500, 4096, 192, rb.RB_ACT_RELU, 0, 0), (4500 + 11, 8192, 512, rb.RB_ACT_NONE, 1, 0)])
 def test_gemm_bf16_matches_fp64(M, N, K, act, out_f32, pad_y):
     rng = np.random.default_rng(4)
     Xd, X = _bf16_dev(rng.standard_normal((M, K)))
@@ -399,7 +402,8 @@ def test_gemm_rows_independent_of_batch(dtype, N, K):
     # where it sits among them: the same k order for every M, tile shape and
     # tile order (K = 1088 / 2112 / 1728 puts W above 4 MB: plain tile order; the
     # bf16 launch of all rows takes a larger tile than the partial ones: N = 4096
-    # and 2048 give the full launch 256 x 256 tiles of 4 waves with 2 stages,
+    # and 2048 give the full launch at least two 256 x 256 tiles per compute
+    # unit (4 waves of 128 x 128, 2 stages),
     # while the partial launches take 128 x 128 tiles of 8 waves with 4 stages)
     rng = np.random.default_rng(11)
     M = 16384
