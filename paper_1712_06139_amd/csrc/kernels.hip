@@ -162,11 +162,16 @@ __global__ __launch_bounds__(256) void k_route(int kind, const rb_k_batch* __res
       const int e = p - s_first[i];
       if (kind == RB_MODEL_RANKING) {
         const int32_t* l = lens + rq.lens_off + (int64_t)e * n_tables;
+        // the flag is kept in a register so that the unrolled loads are all
+        // issued before the first one is used
+        bool neg = false;
+#pragma unroll 8
         for (int f = 0; f < n_tables; ++f) {
           const int v = l[f];
-          if (v < 0) s_bad[i] = 1;
+          neg |= v < 0;
           c += v;
         }
+        if (neg) s_bad[i] = 1;
       } else {
         const int v = lens[rq.lens_off + e];
         if (v < 1 || v > b.seq_T) s_bad[i] = 1;
@@ -565,12 +570,12 @@ __device__ __forceinline__ void buffer_to_lds(i32x4_t rsrc, uint32_t voff, uint3
 // issued back to back they stall the wave on the texture path with no MFMA in
 // flight. A sub-step covers 32 bytes of every row (16 bf16 or 8 fp32 k values)
 // and its MFMAs have the next sub-step's fragment reads between them. In the
-// last sub-step, after half of its MFMAs (three quarters with S = 2), the wave waits for its loads of the
-// next k-step and for its LDS reads, and all waves meet at one barrier: the
-// next stage has landed and nobody reads the current one again. The other
-// half then runs with the next k-step's first fragment reads between the
-// MFMAs. The order of MFMAs, LDS reads and loads within a step is fixed with
-// scheduling barriers.
+// last sub-step, after half of its MFMAs (three quarters with S = 2), the wave
+// waits for its loads of the next k-step and for its LDS reads, and all waves
+// meet at one barrier: the next stage has landed and nobody reads the current
+// one again. The rest of the sub-step then runs with the next k-step's first
+// fragment reads between the MFMAs. The order of MFMAs, LDS reads and loads
+// within a step is fixed with scheduling barriers.
 //
 // A fragment is 16 bytes of one row: lane l holds row l % 32 and chunk
 // 2 kk + l / 32 of sub-step kk. bf16: one 32x32x16 MFMA per accumulator and
