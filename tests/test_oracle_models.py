@@ -130,13 +130,37 @@ def test_seqpool_constant_sequence_and_single_token():
     assert np.array_equal(om.OracleModel(m, p).forward(Payload(tok, np.array([1], np.int32))), [[0.5, 0.5]])
 
 
-def test_bf16_model_rounds_inputs_and_hidden():
+def test_bf16_model_rounds_inputs():
     # a bf16 model sees bf16 inputs: x and round_bf16(x) give the same output
     o = om.OracleModel(MLP16, _rand_params(MLP16, 4))
     x = np.random.default_rng(3).standard_normal((5, 16)).astype(np.float32)
     y1 = o.forward(Payload(x))
     y2 = o.forward(Payload(nx.round_bf16(x).astype(np.float32)))
     assert np.array_equal(y1, y2)
+
+
+def _golden_model(g, dtype):
+    W1, W2 = np.array(g["W1"], np.float32), np.array(g["W2"], np.float32)
+    m = Model(kind="mlp", dtype=dtype, seed_id=0,
+              layers=(Layer(W1.shape[1], W1.shape[0], g["act1"]), Layer(W2.shape[1], W2.shape[0], g["act2"])))
+    p = Params([(W1, np.array(g["b1"], np.float32)), (W2, np.array(g["b2"], np.float32))], [])
+    return om.OracleModel(m, p)
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+def test_model_storage_rounding_chain_hand_worked(golden_dir, dtype):
+    # every storage rounding of the model's forward (inputs, weights, biases,
+    # hidden outputs, last output) against exact hand arithmetic; the golden
+    # lists the value each plausible misplaced rounding would give instead
+    import json
+    import os
+    g = json.load(open(os.path.join(golden_dir, f"mlp_rounding_{dtype}.json")))
+    o = _golden_model(g, dtype)
+    y = o.forward(Payload(np.array([g["x"]], np.float32)))
+    assert y.dtype == np.float32
+    assert y.tolist() == [g["y"]], (y.tolist(), g["y"])
+    # the ranking and sequence models run the same layer chain
+    assert np.array_equal(o.mlp(o._round_in(np.array([g["x"]], np.float32))).astype(np.float32), y)
 
 
 def test_workload_models_build_and_run():
