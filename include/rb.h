@@ -142,6 +142,12 @@ typedef struct {
    * batching); 0 pads every sequence to its queue's bucket. Outputs are
    * identical either way. */
   int32_t seq_pack;
+  /* Device mode, rb_sim_run: 0 runs the trace as a backlogged device would
+   * (every launch window holds window_batches consecutive dispatched batches,
+   * whatever the simulated clock did: the replay measures capacity); 1 runs
+   * exactly the windows the simulated clock dispatched (see rb_sim_run). The
+   * serving API always runs the clock's windows. */
+  int32_t clocked_windows;
 } rb_sched_opts;
 
 /* One scheduler owns one HIP stream of the context's device (device mode),
@@ -176,6 +182,10 @@ typedef struct {
    * 0 <= P <= max_batch_size (n_service = max_batch_size + 1); NULL: 0. */
   const int64_t* service_ns;
   int32_t n_service;
+  /* Simulated fixed time of this queue's launch chain in a launch window
+   * (>= 0): a window taking batches of this queue costs window_ns once plus
+   * service_ns[P] per batch. */
+  int64_t window_ns;
 } rb_queue_opts;
 
 /* Queues may be created and destroyed while the scheduler runs (the set of
@@ -244,11 +254,24 @@ typedef struct {
   const uint64_t* req_ids; /* valid until the next rb_run_next */
 } rb_batch_info;
 
-/* Dispatch the next closed batch (round-robin over queues, oldest first in a
- * queue) at max(clock, simulated device free time) and, in device mode,
- * enqueue its assemble -> forward -> split on the scheduler's stream
- * (asynchronous). RB_EEMPTY if no queue has a closed batch. */
+/* Run the next batch the simulated clock has dispatched (see below) and, in
+ * device mode, enqueue its assemble -> forward -> split on the scheduler's
+ * stream (asynchronous). RB_EEMPTY if the clock has dispatched nothing that
+ * has not run. */
 rb_status rb_run_next(rb_sched* s, rb_batch_info* out);
+
+/* The batches of one launch window (valid until the next rb_run_next or
+ * rb_run_window call). */
+typedef struct {
+  int32_t n_batches;
+  const rb_batch_info* batches;
+} rb_window_info;
+
+/* Run the next launch window the simulated clock has dispatched: all of its
+ * batches, one launch chain per queue, their payloads staged to the device in
+ * one copy and their outputs copied back in one. RB_EEMPTY if nothing
+ * dispatched is waiting. */
+rb_status rb_run_window(rb_sched* s, rb_window_info* out);
 /* Copy request req_id's output rows ([n_rows, d_out] fp32) to dst (host).
  * RB_EAGAIN if its batch has not finished; RB_ESIZE if dst_bytes is too
  * small; RB_ENOENT if unknown or already collected. The library drops its copy

@@ -19,10 +19,15 @@ here are (each is a named choice in the design notes):
     at the end of the trace (count-only queues close there);
   * padded size P = the smallest allowed batch size >= the real size s, or
     s itself when no allowed sizes are given;
-  * one serial simulated device: when it is free, the next queue holding a
-    closed batch, scanning queue ids cyclically from the one after the
-    last-served queue, gets its oldest closed batch dispatched; the device is
-    then busy for service_ns[queue][P] nanoseconds;
+  * one serial simulated device that takes launch windows of up to W closed
+    batches: when it is free and some queue holds a closed batch, it picks
+    batches one at a time, each time the oldest closed batch of the next queue
+    holding one (queue ids scanned cyclically from the one after the
+    last-served queue), until it has W of them or none is left; every batch of
+    the window is dispatched then and completes when the window does, after
+    the sum over the window's queues of window_ns[queue] (a fixed time per
+    launch chain) plus the sum over its batches of service_ns[queue][P]
+    nanoseconds. W = 1 and window_ns = 0 is one batch at a time;
   * events at one timestamp: timeouts (queue id order), then arrivals
     (request id order), then the end-of-trace close, then dispatch;
   * within a batch, requests keep arrival order; request r's rows are rows
@@ -83,6 +88,7 @@ class Batch:
     close_ns: int
     dispatch_ns: int = -1
     done_ns: int = -1
+    window: int = -1                # index of the device dispatch (launch window) that took it
 
 
 @dataclasses.dataclass
@@ -96,10 +102,15 @@ class SimResult:
 
 
 def simulate(queues: Sequence[QueueCfg], req_queue: Sequence[int], arrival_ns: Sequence[int],
-             n_rows: Sequence[int], service_ns: Sequence[Sequence[int]]) -> SimResult:
+             n_rows: Sequence[int], service_ns: Sequence[Sequence[int]], window: int = 1,
+             window_ns: Optional[Sequence[int]] = None) -> SimResult:
     """Batch formation per queue plus round-robin dispatch on one simulated
-    serial device. service_ns[q][P] is the device time of a batch of padded
-    size P from queue q. Returns the batches in dispatch order."""
+    serial device that takes launch windows of up to `window` closed batches.
+    service_ns[q][P] is the device time of a batch of padded size P from queue
+    q, window_ns[q] (default 0) the fixed time of queue q's launch chain in a
+    window. Returns the batches in dispatch order."""
+    if window < 1:
+        raise ValueError("window must be >= 1")
     N = len(arrival_ns)
     arrival = [int(a) for a in arrival_ns]
     for i in range(1, N):
@@ -123,7 +134,9 @@ def simulate(queues: Sequence[QueueCfg], req_queue: Sequence[int], arrival_ns: S
         open_reqs[q] = []
         open_s[q] = 0
 
+    wns = [0] * nq if window_ns is None else [int(x) for x in window_ns]
     last_served = -1
+    n_windows = 0
     device_free = -(2 ** 62)
     end_t = arrival[-1] if N else 0
     flushed = N == 0
@@ -181,20 +194,27 @@ def simulate(queues: Sequence[QueueCfg], req_queue: Sequence[int], arrival_ns: S
                 if queues[q].timeout_ns is None and open_s[q] > 0:
                     close(q, t)
             flushed = True
-        # 4. dispatch while the device is free at t
+        # 4. dispatch windows while the device is free at t
         while device_free <= t and any(closed[q] for q in range(nq)):
-            for k in range(1, nq + 1):
-                q = (last_served + k) % nq
-                if closed[q]:
-                    break
-            b = closed[q].popleft()
-            b.dispatch_ns = t
-            b.done_ns = t + int(service_ns[q][b.P])
-            device_free = b.done_ns
-            for r in b.reqs:
-                done[r] = b.done_ns
-            order.append(b)
-            last_served = q
+            win: List[Batch] = []
+            while len(win) < window and any(closed[q] for q in range(nq)):
+                for k in range(1, nq + 1):
+                    q = (last_served + k) % nq
+                    if closed[q]:
+                        break
+                win.append(closed[q].popleft())
+                last_served = q
+            busy = sum(int(wns[q]) for q in sorted({b.queue for b in win}))
+            busy += sum(int(service_ns[b.queue][b.P]) for b in win)
+            for b in win:
+                b.dispatch_ns = t
+                b.done_ns = t + busy
+                b.window = n_windows
+                for r in b.reqs:
+                    done[r] = b.done_ns
+            order.extend(win)
+            n_windows += 1
+            device_free = t + busy
     return SimResult(order, done, np.asarray(req_queue, np.int64))
 
 

@@ -125,6 +125,12 @@ struct Batch {
   int64_t close_ns = 0, dispatch_ns = 0, done_ns = 0;
 };
 
+// A batch the simulated clock dispatched, with its queue.
+struct Disp {
+  rb_queue* q = nullptr;
+  Batch b;
+};
+
 // A served request submitted through rb_submit (host payload copied in).
 struct HostReq {
   rb_queue* q = nullptr;
@@ -202,6 +208,8 @@ struct rb_queue {
   int64_t open_t = 0;
   std::deque<Batch> closed;
   int64_t undispatched = 0;  // requests in the open batch or in closed batches
+  int64_t window_ns = 0;     // simulated fixed time of its launch chain in a window
+  int64_t pending_run = 0;   // serving: batches the clock dispatched that have not run yet
 };
 
 struct rb_sched {
@@ -223,10 +231,14 @@ struct rb_sched {
   int last_served = -1;
   int64_t n_closed = 0;
   int64_t batch_seq = 0;
+  int64_t window_seq = 0;  // simulated device dispatches (launch windows) so far
   // serving-mode requests, by request id
   std::vector<HostReq> hreqs;
-  std::vector<int64_t> last_batch_ids;
-  std::vector<uint64_t> last_batch_u64;
+  // serving: windows the clock dispatched whose batches have not run yet
+  std::deque<std::vector<Disp>> ready;
+  // what the last rb_run_next / rb_run_window returned (its pointers' targets)
+  std::vector<uint64_t> last_req_ids;
+  std::vector<rb_batch_info> last_infos;
   // executor
   std::map<int64_t, Work> work;
   std::vector<Group> window;     // current window, one group per queue
@@ -384,6 +396,73 @@ rb_queue* pick_round_robin(rb_sched* s) {
     if (q && q->m && !q->closed.empty()) return q;  // held queues keep their batches
   }
   return nullptr;
+}
+
+// Some queue with a version bound holds a closed batch (held queues keep
+// theirs until a version is set).
+bool has_pickable(const rb_sched* s) {
+  for (const rb_queue* q : s->queues)
+    if (q && q->m && !q->closed.empty()) return true;
+  return false;
+}
+
+// One dispatch of the simulated device at time t (the device is free): a
+// launch window of up to window_batches closed batches, each the oldest
+// closed batch of the next queue in round-robin order that holds one. Every
+// batch of the window completes when the window does: after the window_ns of
+// each queue it takes batches from, plus service_ns[P] per batch. Returns
+// false when no queue holds a closed batch.
+bool clock_dispatch(rb_sched* s, int64_t t, std::vector<Disp>& win) {
+  win.clear();
+  const int W = s->opts.window_batches;
+  while ((int)win.size() < W) {
+    rb_queue* q = pick_round_robin(s);
+    if (!q) break;
+    Disp d;
+    d.q = q;
+    d.b = std::move(q->closed.front());
+    q->closed.pop_front();
+    s->n_closed--;
+    q->undispatched -= (int64_t)d.b.reqs.size();
+    d.b.seq = s->batch_seq++;
+    d.b.dispatch_ns = t;
+    s->last_served = q->id;
+    win.push_back(std::move(d));
+  }
+  if (win.empty()) return false;
+  int64_t busy = 0;
+  for (size_t i = 0; i < win.size(); ++i) {
+    bool first = true;
+    for (size_t j = 0; j < i && first; ++j) first = win[j].q != win[i].q;
+    if (first) busy += win[i].q->window_ns;
+    busy += service(win[i].q, win[i].b.P);
+  }
+  for (Disp& d : win) d.b.done_ns = t + busy;
+  s->device_free = t + busy;
+  s->window_seq++;
+  return true;
+}
+
+// Serving: run the simulated clock's events (timeouts, and device dispatches
+// when the device is free and a batch waits) in time order, up to `limit`
+// (exclusive, or inclusive with `incl`). Arrivals are not events here: every
+// request submitted so far has been taken in at its arrival time, so a
+// dispatch at time t sees every batch that closed at or before t. Dispatched
+// windows wait in s->ready until rb_run_next / rb_run_window runs them.
+void serve_until(rb_sched* s, int64_t limit, bool incl) {
+  std::vector<Disp> win;
+  for (;;) {
+    int64_t e = next_timeout(s);
+    if (has_pickable(s)) e = std::min(e, std::max(s->device_free, s->now));
+    if (e == INT64_MAX || (incl ? e > limit : e >= limit)) break;
+    fire_timeouts_at(s, e);
+    s->now = std::max(s->now, e);
+    while (s->device_free <= e && clock_dispatch(s, e, win)) {
+      for (Disp& d : win) d.q->pending_run++;
+      s->ready.push_back(std::move(win));
+      win.clear();
+    }
+  }
 }
 
 // ---------------------------------------------------------------- executor
@@ -941,6 +1020,7 @@ rb_status rb_sched_create(rb_ctx* ctx, const rb_sched_opts* o, rb_sched** out) {
   if (o->mode == RB_MODE_DEVICE && ctx->device < 0) return RB_EDEVICE;
   if (o->window_batches < 1 || o->n_streams < 0 || o->n_streams > RB_MAX_STREAMS) return RB_EINVAL;
   if (o->seq_pack < 0 || o->seq_pack > 1) return RB_EINVAL;
+  if (o->clocked_windows < 0 || o->clocked_windows > 1) return RB_EINVAL;
   if (o->profile < 0 || o->profile > 2) return RB_EINVAL;
   rb_sched* s = new (std::nothrow) rb_sched();
   if (!s) return RB_ENOMEM;
@@ -1075,6 +1155,7 @@ rb_status rb_queue_create(rb_sched* s, rb_model* m, const rb_queue_opts* o, rb_q
   if (o->service_ns)
     for (int i = 0; i < o->n_service; ++i)
       if (o->service_ns[i] < 0) return RB_EINVAL;
+  if (o->window_ns < 0) return RB_EINVAL;
   rb_queue* q = new (std::nothrow) rb_queue();
   if (!q) return RB_ENOMEM;
   q->s = s;
@@ -1086,6 +1167,7 @@ rb_status rb_queue_create(rb_sched* s, rb_model* m, const rb_queue_opts* o, rb_q
   q->T = o->batch_timeout_ns;
   q->bucket = o->bucket_len;
   if (o->service_ns) q->svc.assign(o->service_ns, o->service_ns + o->n_service);
+  q->window_ns = o->window_ns;
   s->queues.push_back(q);
   s->n_live_queues++;
   m->bound++;
@@ -1095,7 +1177,7 @@ rb_status rb_queue_create(rb_sched* s, rb_model* m, const rb_queue_opts* o, rb_q
 
 rb_status rb_queue_destroy(rb_queue* q) {
   if (!q) return RB_OK;
-  if (q->undispatched) return RB_EBUSY;
+  if (q->undispatched || q->pending_run) return RB_EBUSY;
   rb_sched* s = q->s;
   // a queue with batches still in the unflushed window keeps them: flush first
   for (Group& g : s->window)
@@ -1119,8 +1201,9 @@ rb_status rb_queue_set_model(rb_queue* q, rb_model* m) {
       return RB_EINVAL;
   }
   // batches dispatched into a window that has not been handed to the device
-  // yet would run the new version: only swap between launches
-  if (!s->window.empty() || !s->chunk.empty()) return RB_EBUSY;
+  // yet would run the new version: only swap between launches (serving:
+  // after the batches the clock already dispatched from this queue have run)
+  if (!s->window.empty() || !s->chunk.empty() || q->pending_run) return RB_EBUSY;
   // an unbound new version with the old one's padded layer shapes takes over
   // the old one's lineage: its launch chains follow the old version's on the
   // same stream and reuse its work buffers (no allocation and no device drain
@@ -1199,7 +1282,10 @@ rb_status rb_submit(rb_queue* q, const rb_request* r, int64_t arrival_ns, uint64
   } catch (...) {
     return RB_ENOMEM;
   }
-  fire_timeouts_upto(s, arrival_ns);
+  // the clock's events before the arrival, then the timeouts due at it,
+  // then the arrival itself (dispatches at arrival_ns come after it)
+  serve_until(s, arrival_ns, false);
+  fire_timeouts_at(s, arrival_ns);
   s->now = arrival_ns;
   const int64_t id = (int64_t)s->hreqs.size() - 1;
   arrive(q, id, r->n_rows, arrival_ns);
@@ -1209,7 +1295,7 @@ rb_status rb_submit(rb_queue* q, const rb_request* r, int64_t arrival_ns, uint64
 
 rb_status rb_advance(rb_sched* s, int64_t now_ns) {
   if (!s || now_ns < s->now) return RB_EINVAL;
-  fire_timeouts_upto(s, now_ns);
+  serve_until(s, now_ns, true);
   s->now = now_ns;
   return RB_OK;
 }
@@ -1220,21 +1306,42 @@ rb_status rb_flush(rb_queue* q) {
   return RB_OK;
 }
 
-// Serving-mode device run of one batch: stage its payloads, run the chain,
-// copy the outputs back into the slot's pinned output buffer.
-static rb_status run_serving_batch(rb_sched* s, rb_queue* q, const Batch& b) {
-  const rb_model* m = q->m;
-  int64_t nd = 0, nl = 0, ni = 0, no = 0;
-  for (int64_t id : b.reqs) {
-    const HostReq& h = s->hreqs[(size_t)id];
-    nd += (int64_t)h.dense.size();
-    nl += (int64_t)h.lens.size();
-    ni += (int64_t)h.ids.size();
-    no += (int64_t)h.n_rows * m->d_out;
+// Serving-mode device run of dispatched batches (one launch window): stage
+// their payloads in one slot, run one launch chain per queue, copy the
+// outputs back into the slot's pinned output buffer.
+static rb_status run_serving_window(rb_sched* s, const std::vector<Disp>& win) {
+  // one launch group per queue, in order of first appearance
+  std::vector<Group> groups;
+  std::vector<std::vector<int64_t>> greqs;  // each group's request ids
+  for (const Disp& d : win) {
+    size_t gi = 0;
+    while (gi < groups.size() && groups[gi].q != d.q) ++gi;
+    if (gi == groups.size()) {
+      groups.push_back(Group{});
+      groups.back().q = d.q;
+      greqs.emplace_back();
+    }
+    Group& g = groups[gi];
+    rb_k_batch kb{(int32_t)greqs[gi].size(), (int32_t)d.b.reqs.size(), (int32_t)g.slots, d.b.P, d.b.s,
+                  d.q->m->kind == RB_MODEL_SEQPOOL ? d.q->bucket : 0};
+    g.batches.push_back(kb);
+    g.slots += d.b.P;
+    greqs[gi].insert(greqs[gi].end(), d.b.reqs.begin(), d.b.reqs.end());
   }
-  const size_t o_batch = 0;
-  const size_t o_reqs = 256;
-  const size_t o_dense = o_reqs + round_up((int64_t)(b.reqs.size() * sizeof(rb_k_req)), 256);
+  int64_t nd = 0, nl = 0, ni = 0, no = 0;
+  size_t desc = 0;
+  for (size_t gi = 0; gi < groups.size(); ++gi) {
+    desc += round_up((int64_t)(groups[gi].batches.size() * sizeof(rb_k_batch)), 256) +
+            round_up((int64_t)(greqs[gi].size() * sizeof(rb_k_req)), 256);
+    for (int64_t id : greqs[gi]) {
+      const HostReq& h = s->hreqs[(size_t)id];
+      nd += (int64_t)h.dense.size();
+      nl += (int64_t)h.lens.size();
+      ni += (int64_t)h.ids.size();
+      no += (int64_t)h.n_rows * h.d_out;
+    }
+  }
+  const size_t o_dense = desc;
   const size_t o_lens = o_dense + round_up(nd * 4, 256);
   const size_t o_ids = o_lens + round_up(nl * 4, 256);
   const size_t o_out = o_ids + round_up(ni * 4, 256);
@@ -1242,44 +1349,52 @@ static rb_status run_serving_batch(rb_sched* s, rb_queue* q, const Batch& b) {
   Slot* sl = nullptr;
   rb_status st = acquire_slot(s, total, (size_t)std::max<int64_t>(no, 1) * 4, &sl);
   if (st != RB_OK) return st;
-  Group g;
-  g.q = q;
-  g.slots = b.P;
-  rb_k_batch kb{0, (int32_t)b.reqs.size(), 0, b.P, b.s, m->kind == RB_MODEL_SEQPOOL ? q->bucket : 0};
-  g.batches.push_back(kb);
   int64_t cd = 0, cl = 0, ci = 0, co = 0;
-  for (int64_t id : b.reqs) {
-    HostReq& h = s->hreqs[(size_t)id];
-    rb_k_req kr{};
-    kr.dense_off = cd;
-    kr.dense_end = cd + (int64_t)h.dense.size();
-    kr.lens_off = cl;
-    kr.ids_off = ci;
-    kr.ids_end = ci + (int64_t)h.ids.size();
-    kr.out_off = co;
-    kr.n_rows = h.n_rows;
-    add_tokens(g, m, kr);
-    std::memcpy(sl->host + o_dense + cd * 4, h.dense.data(), h.dense.size() * 4);
-    if (!h.lens.empty()) std::memcpy(sl->host + o_lens + cl * 4, h.lens.data(), h.lens.size() * 4);
-    if (!h.ids.empty()) std::memcpy(sl->host + o_ids + ci * 4, h.ids.data(), h.ids.size() * 4);
-    h.out_off = co;
-    h.slot = (int)(sl - s->slots);
-    h.state = 1;
-    cd += (int64_t)h.dense.size();
-    cl += (int64_t)h.lens.size();
-    ci += (int64_t)h.ids.size();
-    co += (int64_t)h.n_rows * m->d_out;
-    g.reqs.push_back(kr);
-    sl->serving_reqs.push_back(id);
+  size_t off = 0;
+  std::vector<std::pair<size_t, size_t>> offs;
+  for (size_t gi = 0; gi < groups.size(); ++gi) {
+    Group& g = groups[gi];
+    const rb_model* m = g.q->m;
+    for (int64_t id : greqs[gi]) {
+      HostReq& h = s->hreqs[(size_t)id];
+      rb_k_req kr{};
+      kr.dense_off = cd;
+      kr.dense_end = cd + (int64_t)h.dense.size();
+      kr.lens_off = cl;
+      kr.ids_off = ci;
+      kr.ids_end = ci + (int64_t)h.ids.size();
+      kr.out_off = co;
+      kr.n_rows = h.n_rows;
+      add_tokens(g, m, kr);
+      std::memcpy(sl->host + o_dense + cd * 4, h.dense.data(), h.dense.size() * 4);
+      if (!h.lens.empty()) std::memcpy(sl->host + o_lens + cl * 4, h.lens.data(), h.lens.size() * 4);
+      if (!h.ids.empty()) std::memcpy(sl->host + o_ids + ci * 4, h.ids.data(), h.ids.size() * 4);
+      h.out_off = co;
+      h.slot = (int)(sl - s->slots);
+      h.state = 1;
+      cd += (int64_t)h.dense.size();
+      cl += (int64_t)h.lens.size();
+      ci += (int64_t)h.ids.size();
+      co += (int64_t)h.n_rows * h.d_out;
+      g.reqs.push_back(kr);
+      sl->serving_reqs.push_back(id);
+    }
+    const size_t bb = g.batches.size() * sizeof(rb_k_batch), rr = g.reqs.size() * sizeof(rb_k_req);
+    std::memcpy(sl->host + off, g.batches.data(), bb);
+    const size_t o1 = off;
+    off += round_up((int64_t)bb, 256);
+    std::memcpy(sl->host + off, g.reqs.data(), rr);
+    offs.push_back({o1, off});
+    off += round_up((int64_t)rr, 256);
   }
-  std::memcpy(sl->host + o_batch, &kb, sizeof(kb));
-  std::memcpy(sl->host + o_reqs, g.reqs.data(), g.reqs.size() * sizeof(rb_k_req));
   if (!hip_ok(hipMemcpyAsync(sl->dev, sl->host, o_out, hipMemcpyHostToDevice, s->stream))) return RB_EDEVICE;
   float* dout = (float*)(sl->dev + o_out);
-  st = run_group(s, s->stream, 0, g, (const rb_k_batch*)(sl->dev + o_batch), (const rb_k_req*)(sl->dev + o_reqs),
-                 (const float*)(sl->dev + o_dense), nd, (const int32_t*)(sl->dev + o_lens),
-                 (const int32_t*)(sl->dev + o_ids), ni, dout);
-  if (st != RB_OK) return st;
+  for (size_t gi = 0; gi < groups.size(); ++gi) {
+    st = run_group(s, s->stream, 0, groups[gi], (const rb_k_batch*)(sl->dev + offs[gi].first),
+                   (const rb_k_req*)(sl->dev + offs[gi].second), (const float*)(sl->dev + o_dense), nd,
+                   (const int32_t*)(sl->dev + o_lens), (const int32_t*)(sl->dev + o_ids), ni, dout);
+    if (st != RB_OK) return st;
+  }
   if (!hip_ok(hipMemcpyAsync(sl->host_out, dout, (size_t)no * 4, hipMemcpyDeviceToHost, s->stream)))
     return RB_EDEVICE;
   hipEventRecord(sl->ev, s->stream);
@@ -1287,35 +1402,62 @@ static rb_status run_serving_batch(rb_sched* s, rb_queue* q, const Batch& b) {
   return RB_OK;
 }
 
-rb_status rb_run_next(rb_sched* s, rb_batch_info* out) {
-  if (!s || !out) return RB_EINVAL;
-  rb_queue* q = pick_round_robin(s);
-  if (!q) return RB_EEMPTY;
-  Batch b = std::move(q->closed.front());
-  q->closed.pop_front();
-  s->n_closed--;
-  q->undispatched -= (int64_t)b.reqs.size();
-  b.seq = s->batch_seq++;
-  b.dispatch_ns = std::max(s->now, s->device_free);
-  b.done_ns = b.dispatch_ns + service(q, b.P);
-  s->device_free = b.done_ns;
-  s->last_served = q->id;
+// Run dispatched batches: on the device (asynchronous), or, without one,
+// mark their requests done. Then describe them for the caller.
+static rb_status run_dispatched(rb_sched* s, std::vector<Disp>& win) {
+  for (Disp& d : win) d.q->pending_run--;
   if (s->stream) {
-    rb_status st = run_serving_batch(s, q, b);
+    rb_status st = run_serving_window(s, win);
     if (st != RB_OK) return st;
   } else {
-    for (int64_t id : b.reqs) s->hreqs[(size_t)id].state = 2;
+    for (Disp& d : win)
+      for (int64_t id : d.b.reqs) s->hreqs[(size_t)id].state = 2;
   }
-  s->last_batch_u64.assign(b.reqs.begin(), b.reqs.end());
-  out->batch_id = (uint64_t)b.seq;
-  out->queue = q->id;
-  out->real_rows = b.s;
-  out->padded_rows = b.P;
-  out->n_req = (int32_t)b.reqs.size();
-  out->close_ns = b.close_ns;
-  out->dispatch_ns = b.dispatch_ns;
-  out->done_ns = b.done_ns;
-  out->req_ids = s->last_batch_u64.data();
+  s->last_req_ids.clear();
+  for (Disp& d : win) s->last_req_ids.insert(s->last_req_ids.end(), d.b.reqs.begin(), d.b.reqs.end());
+  s->last_infos.clear();
+  size_t k = 0;
+  for (Disp& d : win) {
+    rb_batch_info bi{};
+    bi.batch_id = (uint64_t)d.b.seq;
+    bi.queue = d.q->id;
+    bi.real_rows = d.b.s;
+    bi.padded_rows = d.b.P;
+    bi.n_req = (int32_t)d.b.reqs.size();
+    bi.close_ns = d.b.close_ns;
+    bi.dispatch_ns = d.b.dispatch_ns;
+    bi.done_ns = d.b.done_ns;
+    bi.req_ids = s->last_req_ids.data() + k;
+    k += d.b.reqs.size();
+    s->last_infos.push_back(bi);
+  }
+  return RB_OK;
+}
+
+rb_status rb_run_next(rb_sched* s, rb_batch_info* out) {
+  if (!s || !out) return RB_EINVAL;
+  serve_until(s, s->now, true);
+  if (s->ready.empty()) return RB_EEMPTY;
+  std::vector<Disp> one;
+  one.push_back(std::move(s->ready.front().front()));
+  s->ready.front().erase(s->ready.front().begin());
+  if (s->ready.front().empty()) s->ready.pop_front();
+  rb_status st = run_dispatched(s, one);
+  if (st != RB_OK) return st;
+  *out = s->last_infos[0];
+  return RB_OK;
+}
+
+rb_status rb_run_window(rb_sched* s, rb_window_info* out) {
+  if (!s || !out) return RB_EINVAL;
+  serve_until(s, s->now, true);
+  if (s->ready.empty()) return RB_EEMPTY;
+  std::vector<Disp> win = std::move(s->ready.front());
+  s->ready.pop_front();
+  rb_status st = run_dispatched(s, win);
+  if (st != RB_OK) return st;
+  out->n_batches = (int32_t)s->last_infos.size();
+  out->batches = s->last_infos.data();
   return RB_OK;
 }
 
@@ -1359,10 +1501,16 @@ rb_status rb_sim_run(rb_sched* s, const rb_servable* sv, int32_t n_sv, const rb_
     if (sv[i].n_queues < 1 || !sv[i].queues) return RB_EINVAL;
     for (int32_t j = 0; j < sv[i].n_queues; ++j) {
       rb_queue* q = sv[i].queues[j];
-      if (!q || q->s != s || q->undispatched || !q->closed.empty()) return RB_EINVAL;
+      if (!q || q->s != s) return RB_EINVAL;
       if (!q->m) return RB_EBUSY;  // a held queue could not leave the replay empty
     }
   }
+  // the replay runs the scheduler's clock over every queue it holds: any
+  // request still waiting anywhere on it (open, closed or dispatched but not
+  // run by the serving API) would be served as part of the replay
+  if (!s->ready.empty()) return RB_EBUSY;
+  for (const rb_queue* q : s->queues)
+    if (q && (q->undispatched || !q->closed.empty() || q->pending_run)) return RB_EBUSY;
   const bool dev = s->stream != nullptr;
   if (dev && N > 0 && (!tr->dense || !tr->dense_off || !tr->out || !tr->out_off)) return RB_EINVAL;
   // route every request to its queue and validate it against that queue
@@ -1421,33 +1569,27 @@ rb_status rb_sim_run(rb_sched* s, const rb_servable* sv, int32_t n_sv, const rb_
   int64_t nxt = 0;
   std::vector<rb_k_req> kreqs;
   rb_status st = RB_OK;
+  std::vector<Disp> win;
+  const bool clocked = s->opts.clocked_windows != 0;
   auto dispatch_at = [&](int64_t t) -> rb_status {
-    while (s->device_free <= t && s->n_closed > 0) {
-      rb_queue* q = pick_round_robin(s);
-      if (!q) break;
-      Batch b = std::move(q->closed.front());
-      q->closed.pop_front();
-      s->n_closed--;
-      q->undispatched -= (int64_t)b.reqs.size();
-      b.seq = s->batch_seq++;
-      b.dispatch_ns = t;
-      b.done_ns = t + service(q, b.P);
-      s->device_free = b.done_ns;
-      s->last_served = q->id;
-      log->b_queue[nb] = q->id;
-      log->b_real[nb] = b.s;
-      log->b_padded[nb] = b.P;
-      log->b_close_ns[nb] = b.close_ns;
-      log->b_dispatch_ns[nb] = b.dispatch_ns;
-      log->b_done_ns[nb] = b.done_ns;
-      log->b_req_begin[nb] = nreq_logged;
-      for (int64_t r : b.reqs) {
-        log->b_reqs[nreq_logged++] = (int32_t)r;
-        log->req_done_ns[r] = b.done_ns;
-        log->req_queue[r] = q->id;
-      }
-      ++nb;
-      if (dev) {
+    while (s->device_free <= t && clock_dispatch(s, t, win)) {
+      for (Disp& d : win) {
+        rb_queue* q = d.q;
+        const Batch& b = d.b;
+        log->b_queue[nb] = q->id;
+        log->b_real[nb] = b.s;
+        log->b_padded[nb] = b.P;
+        log->b_close_ns[nb] = b.close_ns;
+        log->b_dispatch_ns[nb] = b.dispatch_ns;
+        log->b_done_ns[nb] = b.done_ns;
+        log->b_req_begin[nb] = nreq_logged;
+        for (int64_t r : b.reqs) {
+          log->b_reqs[nreq_logged++] = (int32_t)r;
+          log->req_done_ns[r] = b.done_ns;
+          log->req_queue[r] = q->id;
+        }
+        ++nb;
+        if (!dev) continue;
         kreqs.clear();
         for (int64_t r : b.reqs) {
           rb_k_req k{};
@@ -1461,12 +1603,21 @@ rb_status rb_sim_run(rb_sched* s, const rb_servable* sv, int32_t n_sv, const rb_
           kreqs.push_back(k);
         }
         window_add(s, q, b, kreqs);
-        if (s->window_batches >= s->opts.window_batches) {
+        // a backlogged device runs window_batches consecutive batches per
+        // launch window; clocked replays run the clock's own windows
+        if (!clocked && s->window_batches >= s->opts.window_batches) {
           close_window(s);
           if ((int)s->chunk.size() >= CHUNK_WINDOWS) {
             rb_status e = flush_chunk(s);
             if (e != RB_OK) return e;
           }
+        }
+      }
+      if (dev && clocked) {
+        close_window(s);
+        if ((int)s->chunk.size() >= CHUNK_WINDOWS) {
+          rb_status e = flush_chunk(s);
+          if (e != RB_OK) return e;
         }
       }
     }
@@ -1477,7 +1628,7 @@ rb_status rb_sim_run(rb_sched* s, const rb_servable* sv, int32_t n_sv, const rb_
     if (nxt < N) t = std::min(t, tr->arrival_ns[nxt]);
     t = std::min(t, next_timeout(s));
     if (!flushed && nxt >= N) t = std::min(t, end_t);
-    if (s->n_closed > 0) t = std::min(t, s->device_free);
+    if (has_pickable(s)) t = std::min(t, s->device_free);
     if (t == INT64_MAX) break;
     fire_timeouts_at(s, t);
     while (nxt < N && tr->arrival_ns[nxt] == t) {

@@ -39,7 +39,7 @@ class Deployment:
     def __init__(self, w, ctx: rb.Ctx, device: bool = True, window_batches: int = 1, pad_value: float = 0.0,
                  profile: int = 0, service_ns: Optional[Sequence[Sequence[int]]] = None,
                  with_params: bool = True, models: Optional[List[rb.Model]] = None, n_streams: int = 1,
-                 seq_pack: bool = False):
+                 seq_pack: bool = False, window_ns: Optional[Sequence[int]] = None, clocked_windows: bool = False):
         import synth
         self.w = w
         self.ctx = ctx
@@ -59,12 +59,14 @@ class Deployment:
                                              np.zeros(m.head.fan_out, np.float32), m.head.act),
                                             shapes=shapes, table_rows=m.table_rows))
         self.sched = rb.Sched(ctx, device=device, window_batches=window_batches, pad_value=pad_value,
-                              profile=profile, n_streams=n_streams, seq_pack=seq_pack)
+                              profile=profile, n_streams=n_streams, seq_pack=seq_pack,
+                              clocked_windows=clocked_windows)
         self.queues: List[rb.Queue] = []
         for qi, q in enumerate(w.queues):
             svc = None if service_ns is None else service_ns[qi]
             self.queues.append(rb.Queue(self.sched, self.models[q.servable], q.max_batch_size, q.allowed,
-                                        q.timeout_ns, q.bucket_len, svc))
+                                        q.timeout_ns, q.bucket_len, svc,
+                                        0 if window_ns is None else int(window_ns[qi])))
         self.servables = [[self.queues[qi] for qi, q in enumerate(w.queues) if q.servable == s]
                           for s in range(len(w.models))]
         self.qindex = {q.id: i for i, q in enumerate(self.queues)}

@@ -51,13 +51,14 @@ class rb_model_desc(C.Structure):
 
 class rb_sched_opts(C.Structure):
     _fields_ = [("mode", C.c_int32), ("window_batches", C.c_int32), ("pad_value", C.c_float),
-                ("profile", C.c_int32), ("n_streams", C.c_int32), ("seq_pack", C.c_int32)]
+                ("profile", C.c_int32), ("n_streams", C.c_int32), ("seq_pack", C.c_int32),
+                ("clocked_windows", C.c_int32)]
 
 
 class rb_queue_opts(C.Structure):
     _fields_ = [("max_batch_size", C.c_int32), ("allowed_batch_sizes", p_i32), ("n_allowed", C.c_int32),
                 ("batch_timeout_ns", C.c_int64), ("bucket_len", C.c_int32), ("service_ns", p_i64),
-                ("n_service", C.c_int32)]
+                ("n_service", C.c_int32), ("window_ns", C.c_int64)]
 
 
 class rb_request(C.Structure):
@@ -69,6 +70,10 @@ class rb_batch_info(C.Structure):
     _fields_ = [("batch_id", C.c_uint64), ("queue", C.c_int32), ("real_rows", C.c_int32),
                 ("padded_rows", C.c_int32), ("n_req", C.c_int32), ("close_ns", C.c_int64),
                 ("dispatch_ns", C.c_int64), ("done_ns", C.c_int64), ("req_ids", C.POINTER(C.c_uint64))]
+
+
+class rb_window_info(C.Structure):
+    _fields_ = [("n_batches", C.c_int32), ("batches", C.POINTER(rb_batch_info))]
 
 
 class rb_servable(C.Structure):
@@ -133,6 +138,7 @@ _SIGS = {
     "rb_advance": (C.c_int32, [C.c_void_p, C.c_int64]),
     "rb_flush": (C.c_int32, [C.c_void_p]),
     "rb_run_next": (C.c_int32, [C.c_void_p, C.POINTER(rb_batch_info)]),
+    "rb_run_window": (C.c_int32, [C.c_void_p, C.POINTER(rb_window_info)]),
     "rb_collect": (C.c_int32, [C.c_void_p, C.c_uint64, p_f32, C.c_size_t, p_i32]),
     "rb_sim_run": (C.c_int32, [C.c_void_p, C.POINTER(rb_servable), C.c_int32, C.POINTER(rb_trace),
                                C.POINTER(rb_log)]),
@@ -198,6 +204,12 @@ def torch_stream_ptr(stream=None) -> int:
     import torch
     s = stream if stream is not None else torch.cuda.current_stream()
     return int(s.cuda_stream)
+
+
+def _batch_dict(info: rb_batch_info) -> dict:
+    return {"batch_id": info.batch_id, "queue": info.queue, "real": info.real_rows, "padded": info.padded_rows,
+            "reqs": [info.req_ids[i] for i in range(info.n_req)], "close_ns": info.close_ns,
+            "dispatch_ns": info.dispatch_ns, "done_ns": info.done_ns}
 
 
 # ---------------------------------------------------------------- objects
@@ -273,12 +285,12 @@ class Model:
 class Queue:
     def __init__(self, sched: "Sched", model: Model, max_batch_size: int, allowed: Sequence[int] = (),
                  timeout_ns: Optional[int] = None, bucket_len: int = 0,
-                 service_ns: Optional[Sequence[int]] = None):
+                 service_ns: Optional[Sequence[int]] = None, window_ns: int = 0):
         al = np.ascontiguousarray(allowed, dtype=np.int32)
         sv = None if service_ns is None else np.ascontiguousarray(service_ns, dtype=np.int64)
         o = rb_queue_opts(max_batch_size, _ptr(al, p_i32) if al.size else C.cast(None, p_i32), int(al.size),
                           INT64_MAX if timeout_ns is None else int(timeout_ns), bucket_len,
-                          _ptr(sv, p_i64), 0 if sv is None else int(sv.size))
+                          _ptr(sv, p_i64), 0 if sv is None else int(sv.size), int(window_ns))
         h = C.c_void_p()
         check(_lib().rb_queue_create(sched.h, model.h, C.byref(o), C.byref(h)), "rb_queue_create")
         self.h = h
@@ -302,9 +314,9 @@ class Queue:
 
 class Sched:
     def __init__(self, ctx: Ctx, device: bool = True, window_batches: int = 1, pad_value: float = 0.0,
-                 profile: int = 0, n_streams: int = 1, seq_pack: bool = False):
+                 profile: int = 0, n_streams: int = 1, seq_pack: bool = False, clocked_windows: bool = False):
         o = rb_sched_opts(RB_MODE_DEVICE if device else RB_MODE_NO_DEVICE, window_batches, pad_value,
-                          int(profile), n_streams, int(seq_pack))
+                          int(profile), n_streams, int(seq_pack), int(clocked_windows))
         h = C.c_void_p()
         check(_lib().rb_sched_create(ctx.h, C.byref(o), C.byref(h)), "rb_sched_create")
         self.h = h
@@ -349,9 +361,15 @@ class Sched:
         if st == RB_EEMPTY:
             return None
         check(st, "rb_run_next")
-        return {"batch_id": info.batch_id, "queue": info.queue, "real": info.real_rows, "padded": info.padded_rows,
-                "reqs": [info.req_ids[i] for i in range(info.n_req)], "close_ns": info.close_ns,
-                "dispatch_ns": info.dispatch_ns, "done_ns": info.done_ns}
+        return _batch_dict(info)
+
+    def run_window(self) -> Optional[List[dict]]:
+        info = rb_window_info()
+        st = _lib().rb_run_window(self.h, C.byref(info))
+        if st == RB_EEMPTY:
+            return None
+        check(st, "rb_run_window")
+        return [_batch_dict(info.batches[i]) for i in range(info.n_batches)]
 
     def collect(self, req_id: int, n_rows: int, d_out: int) -> np.ndarray:
         out = np.empty(n_rows * d_out, dtype=np.float32)

@@ -208,7 +208,7 @@ def test_sim_run_argument_checks(ctx):
     assert status(lambda: s.sim_run([[q]], np.zeros(3), np.sort(arr), np.array([1, 9, 1]))) == rb.RB_EINVAL
     # a queue that still holds requests cannot take part in a replay
     s.submit(q, 1, np.zeros((1, 4), np.float32), arrival_ns=0)
-    assert status(lambda: s.sim_run([[q]], np.zeros(3), np.sort(arr), n_rows)) == rb.RB_EINVAL
+    assert status(lambda: s.sim_run([[q]], np.zeros(3), np.sort(arr), n_rows)) == rb.RB_EBUSY
     rb.check(rb.lib().rb_flush(q.h), "rb_flush")
     s.run_next()
     log = s.sim_run([[q]], np.zeros(3), np.sort(arr), n_rows)
@@ -218,34 +218,93 @@ def test_sim_run_argument_checks(ctx):
     s.destroy()
 
 
-@pytest.mark.parametrize("seed", range(8))
+@pytest.mark.parametrize("seed", range(12))
 def test_serving_api_formation_matches_oracle(ctx, seed):
-    # submit/advance/run_next with timeouts: the batches (composition, close
-    # times) equal the oracle's formation on the same arrivals
+    # submit / advance / flush / run_next or run_window on several queues with
+    # timeouts, service tables, chain times and launch windows: the batches
+    # (composition, close, dispatch and done times, windows) equal the
+    # oracle's on the same arrivals. Arrivals of one timestamp are submitted
+    # before the batches are run; count-only queues are flushed after the last
+    # arrival (the end-of-trace close)
     rng = np.random.default_rng(seed)
-    B, T = int(rng.integers(2, 20)), int(rng.integers(5, 100))
+    nq = int(rng.integers(1, 4))
+    W = 1 if seed % 3 == 0 else int(rng.integers(2, 6))
+    use_window = seed % 2 == 1
+    cfg = []
+    for _ in range(nq):
+        B = int(rng.integers(2, 20))
+        T = None if rng.random() < 0.3 else int(rng.integers(5, 100))
+        cfg.append(ob.QueueCfg(B, (), T))
+    svc = [[int(rng.integers(0, 40)) for _ in range(c.max_batch_size + 1)] for c in cfg]
+    wns = [int(rng.integers(0, 30)) for _ in range(nq)]
     N = 300
     arrival = np.cumsum(rng.integers(0, 20, size=N))
-    n = rng.integers(1, B + 1, size=N)
-    s = rb.Sched(ctx, device=False)
+    rq = rng.integers(0, nq, size=N)
+    n = np.array([int(rng.integers(1, cfg[q].max_batch_size + 1)) for q in rq])
+    s = rb.Sched(ctx, device=False, window_batches=W)
     m = mlp(ctx)
-    q = rb.Queue(s, m, B, (), T)
+    qs = [rb.Queue(s, m, c.max_batch_size, (), c.timeout_ns, 0, svc[i], wns[i]) for i, c in enumerate(cfg)]
     got = []
-    for r in range(N):
-        s.submit(q, int(n[r]), np.zeros((int(n[r]), 4), np.float32), arrival_ns=int(arrival[r]))
+
+    def drain():
         while True:
-            b = s.run_next()
-            if b is None:
-                break
-            got.append((b["reqs"], b["close_ns"]))
-    s.advance(int(arrival[-1]) + T)
-    while True:
-        b = s.run_next()
-        if b is None:
-            break
-        got.append((b["reqs"], b["close_ns"]))
-    ref = ob.simulate([ob.QueueCfg(B, (), T)], [0] * N, arrival.tolist(), n.tolist(), [[0] * (B + 1)])
-    assert got == [(list(b.reqs), b.close_ns) for b in ref.batches]
-    q.destroy()
+            if use_window:
+                win = s.run_window()
+                if win is None:
+                    return
+                assert 1 <= len(win) <= W
+                assert len({(b["dispatch_ns"], b["done_ns"]) for b in win}) == 1
+                batches = win
+            else:
+                b = s.run_next()
+                if b is None:
+                    return
+                batches = [b]
+            for b in batches:
+                got.append((b["queue"], b["reqs"], b["close_ns"], b["dispatch_ns"], b["done_ns"]))
+
+    r = 0
+    while r < N:
+        t = int(arrival[r])
+        while r < N and arrival[r] == t:
+            s.submit(qs[rq[r]], int(n[r]), np.zeros((int(n[r]), 4), np.float32), arrival_ns=t)
+            r += 1
+        if r == N:
+            for q, c in zip(qs, cfg):
+                if c.timeout_ns is None:
+                    rb.check(rb.lib().rb_flush(q.h), "rb_flush")
+        drain()
+    s.advance(int(arrival[-1]) + 10 ** 12)   # past every timeout and the device's backlog
+    drain()
+    ref = ob.simulate(cfg, rq.tolist(), arrival.tolist(), n.tolist(), svc, W, wns)
+    assert got == [(b.queue, list(b.reqs), b.close_ns, b.dispatch_ns, b.done_ns) for b in ref.batches]
+    for q in qs:
+        q.destroy()
     m.destroy()
     s.destroy()
+
+
+def test_replay_refuses_a_scheduler_with_waiting_requests(ctx):
+    # a replay runs the scheduler's clock over all of its queues: a closed
+    # batch waiting on a queue outside the replay, served or held, makes the
+    # replay refuse (instead of serving it as part of the replay, or waiting
+    # forever for a held queue)
+    s = rb.Sched(ctx, device=False)
+    m1, m2 = mlp(ctx), mlp(ctx)
+    q1 = rb.Queue(s, m1, 8, (), None)
+    q2 = rb.Queue(s, m2, 8, (), None)
+    args = ([[q1]], np.zeros(2), np.array([0, 1]), np.array([1, 2]))
+    s.submit(q2, 2, np.zeros((2, 4), np.float32), arrival_ns=0)
+    rb.check(rb.lib().rb_flush(q2.h), "rb_flush")
+    assert status(lambda: s.sim_run(*args)) == rb.RB_EBUSY
+    assert s.run_next()["queue"] == q2.id
+    s.submit(q2, 1, np.zeros((1, 4), np.float32), arrival_ns=5)
+    rb.check(rb.lib().rb_flush(q2.h), "rb_flush")
+    q2.set_model(None)
+    assert status(lambda: s.sim_run(*args)) == rb.RB_EBUSY
+    q2.set_model(m2)
+    assert s.run_next()["queue"] == q2.id
+    log = s.sim_run(*args)
+    assert log["n_batches"] == 1 and log["b_reqs"].tolist() == [0, 1]
+    for o in (q1, q2, m1, m2, s):
+        o.destroy()

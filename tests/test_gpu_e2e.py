@@ -167,6 +167,54 @@ def test_serving_api_matches_oracle(ctx):
         dep.destroy()
 
 
+@pytest.mark.parametrize("name,n", [("multi_tenant", 400), ("ragged_seq", 120), ("large_mlp", 200)])
+def test_serving_api_launch_windows(ctx, name, n):
+    # rb_run_window: each launch window the clock dispatches (here up to 8
+    # batches, several queues and models in one window) runs as one staged
+    # copy and one launch chain per queue; every request's rows are
+    # bit-identical to the replay's, which the oracle checks
+    w = synth.workload(name)
+    t, a = trace_and_arenas(name, n)
+    *_, out_ref, out_off = run(ctx, name, n)
+    check_outputs(name, t, a, out_ref, out_off, range(0, t.n, 3))
+    dep = Deployment(w, ctx, device=True, window_batches=8, service_ns=service_table(w, base=10_000_000))
+    sizes, queues_in_window = [], []
+    try:
+        def drain():
+            while True:
+                win = dep.sched.run_window()
+                if win is None:
+                    return
+                sizes.append(len(win))
+                queues_in_window.append(len({b["queue"] for b in win}))
+        ids = []
+        r = 0
+        while r < t.n:
+            tt = int(t.arrival_ns[r])
+            while r < t.n and int(t.arrival_ns[r]) == tt:
+                p = a.payload(r)
+                ids.append(dep.sched.submit(dep.queue_for(t, r), int(t.n_rows[r]), p.dense, p.lens, p.ids,
+                                            arrival_ns=tt))
+                r += 1
+            drain()
+        for q, qc in zip(dep.queues, w.queues):
+            if qc.timeout_ns is None:
+                rb.check(rb.lib().rb_flush(q.h), "rb_flush")
+        dep.sched.advance(int(t.arrival_ns[-1]) + 10 ** 12)
+        drain()
+        dep.sched.sync()
+        for r in range(t.n):
+            d_out = dep.models[int(t.servable[r])].d_out
+            y = dep.sched.collect(ids[r], int(t.n_rows[r]), d_out)
+            assert np.array_equal(y.ravel(), out_ref[out_off[r]:out_off[r + 1]]), r
+    finally:
+        dep.destroy()
+    assert max(sizes) > 1
+    if len(w.queues) > 1:
+        assert max(queues_in_window) > 1
+    print(f"{name}: {len(sizes)} windows, largest {max(sizes)} batches")
+
+
 def test_serving_api_ranking_and_seqpool(ctx):
     for name, n, pack in (("ranking", 120, False), ("ragged_seq", 60, False), ("ragged_seq", 60, True)):
         w = synth.workload(name)

@@ -66,7 +66,7 @@ def test_full_trace(ctx, name):
         del dt
     finally:
         dep.destroy()
-    assert ours == oracle_batches(oracle_sim(w, t, svc))
+    assert ours == oracle_batches(oracle_sim(w, t, svc, WINDOW))
     worst = 0.0
     for r in reqs:
         s = int(t.servable[r])

@@ -16,7 +16,8 @@ from oracle import batching as ob
 def _run_case(c):
     qs = [ob.QueueCfg(q["max_batch_size"], tuple(q["allowed"]), q["timeout_ns"]) for q in c["queues"]]
     req = c["requests"]
-    return ob.simulate(qs, [r[1] for r in req], [r[0] for r in req], [r[2] for r in req], c["service_ns"])
+    return ob.simulate(qs, [r[1] for r in req], [r[0] for r in req], [r[2] for r in req], c["service_ns"],
+                       c.get("window", 1), c.get("window_ns"))
 
 
 def test_hand_worked_schedules(golden_dir):
@@ -199,6 +200,78 @@ def test_littles_law_sample_path(seed):
         t_prev = t
     assert cnt == 0
     assert int(lat.sum()) == area
+
+
+def _random_windowed(seed, n_req=400):
+    rng = np.random.default_rng(7000 + seed)
+    qs, rq, arrival, n, svc, _ = _random_sim(seed, n_req)
+    W = int(rng.integers(2, 7))
+    wns = [int(rng.integers(0, 300)) for _ in qs]
+    return qs, rq, arrival, n, svc, W, wns, ob.simulate(qs, rq.tolist(), arrival.tolist(), n.tolist(), svc, W, wns)
+
+
+@pytest.mark.parametrize("seed", range(25))
+def test_launch_window_invariants(seed):
+    # the windowed device restated declaratively from the batches' close
+    # times alone: each window starts when the device frees up (or at the
+    # next close when nothing waits), takes min(W, waiting) batches in
+    # round-robin order (FIFO within a queue), and lasts the sum of its
+    # queues' chain times and its batches' service times
+    qs, rq, arrival, n, svc, W, wns, res = _random_windowed(seed)
+    nq = len(qs)
+    wins = []
+    for b in res.batches:
+        if not wins or b.window != wins[-1][0].window:
+            wins.append([])
+        wins[-1].append(b)
+    assert [w[0].window for w in wins] == list(range(len(wins)))
+    done_prev, last, k = None, -1, 0
+    for w in wins:
+        rest = res.batches[k:]
+        t = w[0].dispatch_ns
+        earliest = min(x.close_ns for x in rest)
+        assert t == (earliest if done_prev is None else max(done_prev, earliest))
+        waiting = [x for x in rest if x.close_ns <= t]
+        assert len(w) == min(W, len(waiting))
+        picked = []
+        for b in w:
+            avail = [x for x in waiting if x not in picked]
+            cyc = [(last + j) % nq for j in range(1, nq + 1)]
+            q = next(q for q in cyc if any(x.queue == q for x in avail))
+            assert b.queue == q
+            assert b.close_ns == min(x.close_ns for x in avail if x.queue == q)
+            picked.append(b)
+            last = q
+        busy = sum(wns[q] for q in {b.queue for b in w}) + sum(svc[b.queue][b.P] for b in w)
+        assert all(b.dispatch_ns == t and b.done_ns == t + busy for b in w)
+        done_prev = t + busy
+        k += len(w)
+    assert sorted(r for b in res.batches for r in b.reqs) == list(range(len(arrival)))
+
+
+@pytest.mark.parametrize("seed", range(10))
+def test_window_of_one_adds_chain_time_to_service(seed):
+    # W = 1 with chain times a_q is the one-batch device with service S + a_q
+    qs, rq, arrival, n, svc, W, wns, _ = _random_windowed(seed)
+    r1 = ob.simulate(qs, rq.tolist(), arrival.tolist(), n.tolist(), svc, 1, wns)
+    svc2 = [[s + wns[q] for s in row] for q, row in enumerate(svc)]
+    r2 = ob.simulate(qs, rq.tolist(), arrival.tolist(), n.tolist(), svc2)
+    key = lambda r: [(b.queue, b.reqs, b.s, b.P, b.close_ns, b.dispatch_ns, b.done_ns) for b in r.batches]
+    assert key(r1) == key(r2)
+    assert np.array_equal(r1.done_ns, r2.done_ns)
+
+
+@pytest.mark.parametrize("seed", range(5))
+def test_littles_law_with_windows(seed):
+    qs, rq, arrival, n, svc, W, wns, res = _random_windowed(seed, n_req=300)
+    lat = res.latency_ns(arrival)
+    ev = sorted([(int(a), 1) for a in arrival] + [(int(d), -1) for d in res.done_ns])
+    area, cnt, t_prev = 0, 0, ev[0][0]
+    for t, d in ev:
+        area += cnt * (t - t_prev)
+        cnt += d
+        t_prev = t
+    assert cnt == 0 and int(lat.sum()) == area
 
 
 def test_composition_independent_of_service_times():

@@ -23,15 +23,18 @@ def ctx():
 
 
 @pytest.mark.parametrize("name", list(synth.WORKLOADS))
-def test_full_trace_log_matches_oracle(ctx, name):
+@pytest.mark.parametrize("window", [1, 64])
+def test_full_trace_log_matches_oracle(ctx, name, window):
     w = synth.workload(name)
     t = synth.trace(w)
     svc = service_table(w)
-    dep = Deployment(w, ctx, device=False, service_ns=svc, with_params=False)
+    wns = [3_000 + 1_000 * i for i in range(len(w.queues))]
+    dep = Deployment(w, ctx, device=False, service_ns=svc, with_params=False, window_batches=window,
+                     window_ns=wns)
     try:
         log = dep.replay_meta(t)
         ours = lib_batches(log, dep.qindex)
-        ref = oracle_sim(w, t, svc)
+        ref = oracle_sim(w, t, svc, window, wns)
         assert ours == oracle_batches(ref)
         assert np.array_equal(log["req_done_ns"], ref.done_ns)
         # a second replay on the same scheduler starts a fresh clock
@@ -44,9 +47,10 @@ def test_full_trace_log_matches_oracle(ctx, name):
 def test_hand_worked_schedules_through_library(ctx, golden_dir):
     g = json.load(open(os.path.join(golden_dir, "schedule_cases.json")))
     for c in g["cases"]:
-        sched = rb.Sched(ctx, device=False)
+        sched = rb.Sched(ctx, device=False, window_batches=c.get("window", 1))
         m = rb.Model(ctx, "mlp", "f32", [(None, None, "none")], shapes=[(4, 4)])
-        qs = [rb.Queue(sched, m, q["max_batch_size"], q["allowed"], q["timeout_ns"], 0, c["service_ns"][i])
+        wns = c.get("window_ns", [0] * len(c["queues"]))
+        qs = [rb.Queue(sched, m, q["max_batch_size"], q["allowed"], q["timeout_ns"], 0, c["service_ns"][i], wns[i])
               for i, q in enumerate(c["queues"])]
         req = c["requests"]
         log = sched.sim_run([[q] for q in qs], np.array([r[1] for r in req]), np.array([r[0] for r in req]),
@@ -77,10 +81,13 @@ def test_random_traces_match_oracle(ctx, seed):
     rq = rng.integers(0, nq, size=N)
     n = np.array([int(rng.integers(1, cfg[q].max_batch_size + 1)) for q in rq])
     svc = [[int(rng.integers(0, 200)) for _ in range(c.max_batch_size + 1)] for c in cfg]
-    ref = ob.simulate(cfg, rq.tolist(), arrival.tolist(), n.tolist(), svc)
-    sched = rb.Sched(ctx, device=False)
+    W = 1 if seed < 10 else int(rng.integers(2, 9))
+    wns = [0] * nq if seed < 10 else [int(rng.integers(0, 300)) for _ in range(nq)]
+    ref = ob.simulate(cfg, rq.tolist(), arrival.tolist(), n.tolist(), svc, W, wns)
+    sched = rb.Sched(ctx, device=False, window_batches=W)
     m = rb.Model(ctx, "mlp", "f32", [(None, None, "none")], shapes=[(4, 4)])
-    qs = [rb.Queue(sched, m, c.max_batch_size, c.allowed, c.timeout_ns, 0, svc[i]) for i, c in enumerate(cfg)]
+    qs = [rb.Queue(sched, m, c.max_batch_size, c.allowed, c.timeout_ns, 0, svc[i], wns[i])
+          for i, c in enumerate(cfg)]
     log = sched.sim_run([[q] for q in qs], rq, arrival, n)
     assert lib_batches(log, {q.id: i for i, q in enumerate(qs)}) == oracle_batches(ref)
     for q in qs:
