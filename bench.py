@@ -64,7 +64,7 @@ def nearest_rank(v, q):
     return int(v[max(1, int(math.ceil(q * len(v)))) - 1])
 
 
-def algorithmic_work(w, t, a, logd, qindex):
+def algorithmic_work(w, t, a, logd, qindex, window):
     """Algorithmic bytes / flops of one replay, per kernel. Real model
     dimensions; padded rows count as rows, since the method pads them and
     computes them. Sequence groups: padding tokens are not written by the
@@ -80,6 +80,7 @@ def algorithmic_work(w, t, a, logd, qindex):
         return np.add.reduceat(v[reqs], beg[:-1]) if nb else np.zeros(0)
 
     n_req = np.diff(beg)
+    seen_in_window = set()
     n_dense = per_batch(np.diff(a.dense_off))
     n_ids = per_batch(np.diff(a.ids_off))
     row_desc = 32
@@ -105,9 +106,17 @@ def algorithmic_work(w, t, a, logd, qindex):
         layers = m.layers[:-1] if (m.kind == "ranking" and bf16 and m.layers[-1].fan_out == 1) else m.layers
         key = "gemm_bf16" if bf16 else "gemm_f32"
         Mg = int(n_dense[b]) // m.d_in if m.kind == "seqpool" else M  # rows the layers must compute
+        # a launch group (one queue's batches in one launch window) reads each
+        # layer's weights once, however many batches it holds
+        qid = int(logd["b_queue"][b])
+        first_in_group = qid not in seen_in_window
+        seen_in_window.add(qid)
+        if (b + 1) % window == 0:
+            seen_in_window = set()
         for L in layers:
             work[key]["flops"] += 2 * Mg * L.fan_in * L.fan_out
-            work[key]["bytes"] += (Mg * L.fan_in + L.fan_in * L.fan_out + Mg * L.fan_out) * (2 if bf16 else 4)
+            work[key]["bytes"] += ((Mg * L.fan_in + Mg * L.fan_out + (L.fan_in * L.fan_out if first_in_group else 0))
+                                   * (2 if bf16 else 4))
         if m.kind == "ranking" and len(layers) < len(m.layers):
             last = m.layers[-1]
             work["head"]["bytes"] += P * row_desc + P * last.fan_in * 2 + last.fan_in * 2 + s * 4
@@ -147,17 +156,15 @@ def cpu_model():
 
 def cpu_baseline(w, t, a, seconds):
     """The oracle, as it stands, on the first requests of the trace for about
-    `seconds` of CPU time (model setup excluded), with the BLAS threads it
-    runs on by default; then the same requests again on one thread (a
-    bounded second pass, at most a quarter of the time)."""
+    `seconds` of CPU time (model setup excluded). The per-request forward is
+    too small to profit from BLAS threads (one thread measures as fast as
+    many), so it runs on one thread and reports one core; the same requests
+    are then run again with the BLAS threads numpy uses by default (a bounded
+    second pass, at most a quarter of the time), reported beside it."""
     from oracle.models import OracleModel
     import synth
-    try:
-        from threadpoolctl import threadpool_info, threadpool_limits
-        cores = max([d.get("num_threads", 1) for d in threadpool_info()] + [1])
-    except Exception:
-        threadpool_limits = None
-        cores = 1
+    from threadpoolctl import threadpool_info, threadpool_limits
+    blas_threads = max([d.get("num_threads", 1) for d in threadpool_info()] + [1])
     oms = {}
 
     def run(limit_s, max_n):
@@ -174,60 +181,89 @@ def cpu_baseline(w, t, a, seconds):
             n += 1
         return n, ex, el
 
-    n, ex, el = run(seconds, t.n)
-    one = None
-    if threadpool_limits is not None:
-        with threadpool_limits(limits=1):
-            n1, ex1, el1 = run(seconds / 4, n)
-        one = {"value": ex1 / el1, "cores": 1, "sample": f"first {n1} requests ({ex1} examples), {el1:.1f} s"}
-    return {"value": ex / el, "unit": "examples/s", "cores": int(cores), "kind": "oracle",
-            "sample": f"first {n} requests ({ex} examples) of the same trace, unbatched fp64 forward per request, "
-                      f"{el:.1f} s",
-            "cpu_model": cpu_model(), "one_thread": one}
+    with threadpool_limits(limits=1):
+        n, ex, el = run(seconds, t.n)
+    n2, ex2, el2 = run(seconds / 4, n)
+    return {"value": ex / el, "unit": "examples/s", "cores": 1, "kind": "oracle",
+            "sample": f"first {n} requests ({ex} examples) of the same trace, unbatched fp64 forward per request "
+                      f"on one thread, {el:.1f} s",
+            "cpu_model": cpu_model(),
+            "blas_threads": {"value": ex2 / el2, "cores": int(blas_threads),
+                             "sample": f"first {n2} requests ({ex2} examples), {el2:.1f} s"}}
 
 
-def serving_rate(w, t, a, ctx, models, n, seq_pack=False):
+def serving_rate(w, t, a, ctx, models, n, seq_pack=False, window=1, tables=None, alpha=None, tail=None, rate=None):
     """The serving API with host payloads: the first n requests submitted in
-    arrival order from host memory (rb_submit copies them), every batch run
-    as soon as it closes (rb_run_next: one launch chain per batch, payload
-    staged to HBM and outputs copied back over PCIe), the rest flushed, and
-    every request's rows collected on the host (rb_collect). Wall time from
-    the first submit to the last collect, Python call overhead included."""
+    arrival order from host memory (rb_submit copies them), every launch
+    window run as soon as the simulated clock dispatches it (rb_run_window:
+    the window's payloads staged to HBM in one copy, one launch chain per
+    queue, outputs copied back over PCIe), the rest flushed, and every
+    request's rows collected on the host (rb_collect). With the calibrated
+    service tables and arrivals at `rate` (above the device's capacity) the
+    clock keeps a backlog, so windows fill up to `window` batches. Wall time
+    from the first submit to the last collect, Python call overhead
+    included; timed on a second pass over the same requests, after a first
+    one has sized the scheduler's staging buffers."""
     import torch
+    import synth
     from paper_1712_06139_amd import rb
     from paper_1712_06139_amd.deploy import Deployment
     n = min(n, t.n)
-    dep = Deployment(w, ctx, device=True, models=models, seq_pack=seq_pack)
+    arrival = t.arrival_ns if rate is None else synth.trace(w, rate_per_s=rate).arrival_ns
+    dep = Deployment(w, ctx, device=True, models=models, seq_pack=seq_pack, window_batches=window,
+                     service_ns=tables, window_ns=alpha, window_tail_ns=tail)
+    sizes = []
     try:
         payloads = [a.payload(r) for r in range(n)]
         qs = [dep.queue_for(t, r) for r in range(n)]
         d_out = [dep.models[int(t.servable[r])].d_out for r in range(n)]
         sched = dep.sched
+
+        def drain():
+            while True:
+                win = sched.run_window()
+                if win is None:
+                    return
+                sizes.append(len(win))
+
+        def one_pass(t_off):
+            # the same requests again, later on the same clock
+            ids = []
+            for r in range(n):
+                p = payloads[r]
+                ids.append(sched.submit(qs[r], int(t.n_rows[r]), p.dense, p.lens, p.ids,
+                                        arrival_ns=t_off + int(arrival[r])))
+                if r + 1 == n or arrival[r + 1] != arrival[r]:
+                    drain()
+            for q, qc in zip(dep.queues, w.queues):
+                if qc.timeout_ns is None:
+                    rb.check(rb.lib().rb_flush(q.h), "rb_flush")
+            end = t_off + int(arrival[n - 1]) + 10 ** 15
+            sched.advance(end)
+            drain()
+            sched.sync()
+            rows = 0
+            for r in range(n):
+                rows += sched.collect(ids[r], int(t.n_rows[r]), d_out[r]).shape[0]
+            return rows, end
+
+        # a first pass sizes the scheduler's staging buffers; the second is timed
+        _, end = one_pass(0)
+        sizes.clear()
         torch.cuda.synchronize()
         t0 = time.perf_counter()
-        ids = []
-        for r in range(n):
-            p = payloads[r]
-            ids.append(sched.submit(qs[r], int(t.n_rows[r]), p.dense, p.lens, p.ids, arrival_ns=int(t.arrival_ns[r])))
-            while sched.run_next() is not None:
-                pass
-        for q in dep.queues:
-            rb.check(rb.lib().rb_flush(q.h), "rb_flush")
-        while sched.run_next() is not None:
-            pass
-        sched.sync()
-        rows = 0
-        for r in range(n):
-            rows += sched.collect(ids[r], int(t.n_rows[r]), d_out[r]).shape[0]
+        rows, _ = one_pass(end + 1)
         el = time.perf_counter() - t0
     finally:
         dep.destroy()
     ex = int(t.n_rows[:n].sum())
     assert rows == ex
     return {"value": round(ex / el, 1), "unit": "examples/s", "requests": n, "examples": ex,
-            "seconds": round(el, 3),
-            "path": "host payloads: rb_submit -> rb_run_next (one batch per launch chain, PCIe in and out) "
-                    "-> rb_collect"}
+            "seconds": round(el, 3), "window_batches": window, "windows": len(sizes),
+            "mean_batches_per_window": round(float(np.mean(sizes)), 2) if sizes else 0.0,
+            "arrival_rate_req_s": None if rate is None else round(rate, 1),
+            "path": "host payloads: rb_submit -> rb_run_window (the clock's launch windows: one staged copy, "
+                    "one launch chain per queue, PCIe in and out) -> rb_collect"}
 
 
 def _subset(t, a, idx):
@@ -319,21 +355,59 @@ def version_swap(w, t, a, dt, ctx, args):
             "ms_per_step_loading": {"p50": pct(busy, 50), "p99": pct(busy, 99), "max": round(max(busy), 3)}}
 
 
-def calibrate_latency(w, t, a, dt, ctx, dep, window, seq_pack=False):
-    """Per-request latency on the simulated clock (nearest-rank p50 / p99).
-    Each queue's service time per batch size is measured on this GPU: the
-    queue's first requests of the trace replayed through a queue whose every
-    batch is padded to P, for its allowed sizes (or B/8, B/4, B/2 and B,
-    interpolated linearly in between when the queue does not pad). The
-    no-device scheduler then replays arrivals with those service tables:
-    Poisson arrivals at rho x the simulated device's capacity for count-only
-    workloads, the trace's own arrivals for workloads with batch timeouts."""
+def _chain_ns(sched, run, reps):
+    """Median device time (ns) of `run` (one replay), each repetition on its
+    own: the device drained before and after it, HIP events on the
+    scheduler's stream around it (the host's enqueueing included, as a
+    served batch would see it)."""
+    import torch
+    st = torch.cuda.ExternalStream(sched.stream())
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    v = []
+    for _ in range(reps):
+        sched.sync()
+        torch.cuda.synchronize()
+        e0.record(st)
+        run()
+        e1.record(st)
+        sched.sync()
+        torch.cuda.synchronize()
+        v.append(e0.elapsed_time(e1) * 1e6)
+    return int(np.median(v))
+
+
+def calibrate_latency(w, t, a, dt, ctx, dep, window, seq_pack=False, n_streams=1):
+    """Per-request latency on the simulated clock (nearest-rank p50 / p99),
+    with the device modelled as the library runs it: launch windows of up to
+    `window` closed batches; a window holds the device for a fixed chain time
+    b per queue plus S(P) per batch of padded size P, and its results are
+    complete a tail time c per queue after that (the chain's fixed latency,
+    which the device overlaps with the next window: consecutive windows of a
+    model alternate between two launch lanes). All three are measured on this
+    GPU, in the bench's stream configuration, for every queue and allowed size
+    P (or B/8, B/4, B/2 and B, interpolated in between, for queues that do
+    not pad), from the queue's own requests run through a queue that pads
+    every batch to P:
+      c1     the median of 20 isolated launch chains of one batch (a lone
+             batch's latency): c1 = b + S(P) + c;
+      T1     up to 256 batches replayed back to back one per window: per
+             batch, T1 = b + S(P);
+      TW     n batches replayed back to back in m windows of `window`
+             batches, as the throughput replay runs them: TW = m b + n S(P)
+             (median of 3 timings).
+    b and c are averaged over P. The no-device scheduler replays arrivals with
+    these tables: Poisson arrivals at rho x the simulated device's capacity
+    for count-only workloads, the trace's own arrivals for workloads with
+    batch timeouts. Finally those arrivals are replayed on the GPU running
+    exactly the clock's windows, and the measured time is compared with the
+    simulated device-busy time."""
+    import dataclasses
     import synth
     import torch
     from paper_1712_06139_amd import rb
     from paper_1712_06139_amd.deploy import Deployment
     qsel = np.array([dep.qindex[dep.queue_for(t, r).id] for r in range(t.n)])
-    tables, measured = [], {}
+    tables, alphas, tails, measured = [], [], [], {}
     for qi, q in enumerate(w.queues):
         m_idx = q.servable
         mine = np.nonzero(qsel == qi)[0]
@@ -352,71 +426,161 @@ def calibrate_latency(w, t, a, dt, ctx, dep, window, seq_pack=False):
             sa = None
         else:
             st, sa = _subset(t, a, idx)
-        svc_at = {}
+        fit = {}
         for P in sizes:
+            # requests per batch when batches close at P rows (next-fit)
+            ends, acc = [], 0
+            for r_, nr in enumerate(st.n_rows[:len(idx)]):
+                if acc + int(nr) > P:
+                    ends.append(r_)
+                    acc = 0
+                acc += int(nr)
+            ends.append(len(idx))
+            nb = len(ends)
+            nw = -(-nb // window)
+            reps = max(1, -(-8 // nw))  # at least 8 windows back to back
+            n1 = min(nb, 256)
             cw = synth.Workload(w.name, w.wid, (w.models[m_idx],),
                                 (synth.Queue(0, P, (P,), None, q.bucket_len),), len(idx), w.rows, w.rate_per_s)
-            cdep = Deployment(cw, ctx, device=True, window_batches=window, models=[dep.models[m_idx]],
-                              seq_pack=seq_pack)
-            try:
-                if prefix:
-                    out_off = cdep.out_offsets(st)
-                    out = torch.empty(int(out_off[-1]), dtype=torch.float32, device="cuda")
-                    kw = dict(dense=dt.dense, dense_off=a.dense_off[:len(idx) + 1], lens=dt.lens,
-                              lens_off=None if a.lens.size == 0 else a.lens_off[:len(idx) + 1], ids=dt.ids,
-                              ids_off=None if a.ids.size == 0 else a.ids_off[:len(idx) + 1], out=out,
-                              out_off=out_off)
-                    run = lambda: cdep.sched.sim_run(cdep.servables, np.zeros(len(idx), np.int32), st.arrival_ns,
-                                                     st.n_rows, cdep.max_len(st), **kw)
-                else:
-                    sdt = cdep.upload(st, sa)
-                    run = lambda: cdep.replay(sdt)
-                run()
-                cdep.sched.sync()
-                torch.cuda.synchronize()
-                s0 = time.perf_counter()
-                lg = run()
-                cdep.sched.sync()
-                svc_at[P] = int((time.perf_counter() - s0) * 1e9 / lg["n_batches"])
-            finally:
-                cdep.destroy()
-        ps = sorted(svc_at)
+            times = {}
+            for win in (1, window):
+                cdep = Deployment(cw, ctx, device=True, window_batches=win, models=[dep.models[m_idx]],
+                                  seq_pack=seq_pack, n_streams=n_streams)
+                try:
+                    if prefix:
+                        out_off = cdep.out_offsets(st)
+                        out = torch.empty(int(out_off[-1]), dtype=torch.float32, device="cuda")
+
+                        def run(k, cdep=cdep, out=out, out_off=out_off):
+                            return cdep.sched.sim_run(
+                                cdep.servables, np.zeros(k, np.int32), np.zeros(k, np.int64), st.n_rows[:k],
+                                None if st.seq_lens is None else cdep.max_len(st)[:k], dense=dt.dense,
+                                dense_off=a.dense_off[:k + 1], lens=dt.lens,
+                                lens_off=None if a.lens.size == 0 else a.lens_off[:k + 1], ids=dt.ids,
+                                ids_off=None if a.ids.size == 0 else a.ids_off[:k + 1], out=out,
+                                out_off=out_off[:k + 1])
+                    else:
+                        sdt = cdep.upload(st, sa)
+
+                        def run(k, cdep=cdep, sdt=sdt):
+                            return cdep.sched.sim_run(
+                                cdep.servables, np.zeros(k, np.int32), np.zeros(k, np.int64), sdt.n_rows[:k],
+                                None if sdt.max_len is None else sdt.max_len[:k], dense=sdt.dense,
+                                dense_off=sdt.dense_off[:k + 1], lens=sdt.lens,
+                                lens_off=None if sdt.lens_off is None else sdt.lens_off[:k + 1], ids=sdt.ids,
+                                ids_off=None if sdt.ids_off is None else sdt.ids_off[:k + 1], out=sdt.out,
+                                out_off=sdt.out_off[:k + 1])
+                    if win == 1:
+                        k1 = ends[n1 - 1]
+                        run(k1)
+                        times["c1"] = _chain_ns(cdep.sched, lambda: run(ends[0]), 20)
+                        times["T1"] = _chain_ns(cdep.sched, lambda: run(k1), 3) / n1
+                    else:
+                        kall = len(idx)
+                        run(kall)
+                        times["TW"] = _chain_ns(cdep.sched, lambda: [run(kall) for _ in range(reps)], 3) / reps
+                finally:
+                    cdep.destroy()
+            S = max(1.0, (times["TW"] - nw * times["T1"]) / (nb - nw)) if nb > nw else times["T1"]
+            b_ = max(0.0, times["T1"] - S)
+            c_ = max(0.0, times["c1"] - times["T1"])
+            fit[P] = {"S": S, "b": b_, "c": c_, "c1": times["c1"], "T1": times["T1"], "TW": times["TW"],
+                      "batches": nb, "windows": nw}
+        ps = sorted(fit)
+        alpha = int(np.mean([fit[P]["b"] for P in ps]))
+        tail = int(np.mean([fit[P]["c"] for P in ps]))
         svc = np.zeros(q.max_batch_size + 1, dtype=np.int64)
         for s_ in range(1, q.max_batch_size + 1):
             if q.allowed:
-                svc[s_] = svc_at[min(P for P in ps if P >= s_)]
+                svc[s_] = int(fit[min(P for P in ps if P >= s_)]["S"])
             else:
-                svc[s_] = int(np.interp(s_, ps, [svc_at[P] for P in ps]))
+                svc[s_] = int(np.interp(s_, ps, [fit[P]["S"] for P in ps]))
         svc[0] = svc[1]
         tables.append(svc.tolist())
-        measured[f"queue{qi}"] = {str(P): round(svc_at[P] / 1e3, 2) for P in ps}
+        alphas.append(alpha)
+        tails.append(tail)
+        us = lambda v: round(v / 1e3, 2)
+        measured[f"queue{qi}"] = {"chain_us": us(alpha), "tail_us": us(tail),
+                                  "per_batch_us": {str(P): us(fit[P]["S"]) for P in ps},
+                                  "lone_batch_chain_us": {str(P): us(fit[P]["c1"]) for P in ps},
+                                  "back_to_back_one_per_window_us": {str(P): us(fit[P]["T1"]) for P in ps},
+                                  "back_to_back_window_us": {str(P): us(fit[P]["TW"] / fit[P]["windows"])
+                                                             for P in ps}}
     lctx = rb.Ctx(-1)
-    ld = Deployment(w, lctx, device=False, service_ns=tables, with_params=False)
-    lat = {"clock": "simulated", "service_us_by_batch_size": measured}
+    ld = Deployment(w, lctx, device=False, service_ns=tables, window_ns=alphas, window_tail_ns=tails,
+                    window_batches=window, with_params=False)
+    lat = {"clock": "simulated", "device_model": f"launch windows of up to {window} batches: chain time per queue "
+                                                  "+ time per batch of device occupancy, and a chain tail until the "
+                                                  "results are complete; fitted to a lone batch's launch chain and to "
+                                                  "back-to-back windows of one and of the full window of batches",
+           "service": measured}
+
+    def busy_of(lg):
+        # simulated device occupancy of every launch window (the batches of a
+        # window share its dispatch time): chain times of its queues plus its
+        # batches' times; the tails overlap the next window
+        wins = collections.defaultdict(list)
+        for qid, P, d0 in zip(lg["b_queue"].tolist(), lg["b_padded"].tolist(), lg["b_dispatch_ns"].tolist()):
+            wins[d0].append((ld.qindex[qid], P))
+        busy = 0
+        for members in wins.values():
+            busy += sum(alphas[qi] for qi in {m[0] for m in members}) + sum(tables[qi][P] for qi, P in members)
+        return busy, len(wins)
+
+    def pct(lg, tr):
+        v = lg["req_done_ns"] - tr.arrival_ns
+        return round(nearest_rank(v, 0.5) / 1e3, 2), round(nearest_rank(v, 0.99) / 1e3, 2)
     try:
         timed = any(q.timeout_ns is not None for q in w.queues)
-        lg0 = ld.replay_meta(t)
-        busy = sum(tables[ld.qindex[int(qid)]][int(P)] for qid, P in zip(lg0["b_queue"], lg0["b_padded"]))
+        min_chain = min(min(v["lone_batch_chain_us"].values()) for v in measured.values())
+        lat["shortest_lone_batch_chain_us"] = min_chain
         if timed:
-            v = lg0["req_done_ns"] - t.arrival_ns
-            span = int(lg0["req_done_ns"].max() - t.arrival_ns.min())
+            check_tr = t
+            lg = ld.replay_meta(t)
+            busy, nw = busy_of(lg)
+            span = int(lg["req_done_ns"].max() - t.arrival_ns.min())
+            p50, p99 = pct(lg, t)
             lat["trace_arrivals"] = {"arrival_rate_req_s": w.rate_per_s, "utilization": round(busy / span, 3),
-                                     "p50_us": round(nearest_rank(v, 0.5) / 1e3, 2),
-                                     "p99_us": round(nearest_rank(v, 0.99) / 1e3, 2)}
+                                     "windows": nw, "mean_batches_per_window": round(lg["n_batches"] / nw, 2),
+                                     "p50_us": p50, "p99_us": p99}
         else:
+            sat = dataclasses.replace(t, arrival_ns=np.zeros(t.n, np.int64))
+            busy, _ = busy_of(ld.replay_meta(sat))
             cap = t.n / (busy * 1e-9)
             lat["capacity_req_s"] = round(cap, 1)
+            lat["capacity_examples_s"] = round(int(t.n_rows.sum()) / (busy * 1e-9), 1)
             for rho in (0.5, 0.9):
                 tr = synth.trace(w, rate_per_s=rho * cap)
                 lg = ld.replay_meta(tr)
-                v = lg["req_done_ns"] - tr.arrival_ns
-                lat[f"rho{rho}"] = {"arrival_rate_req_s": round(rho * cap, 1), "utilization": rho,
-                                    "p50_us": round(nearest_rank(v, 0.5) / 1e3, 2),
-                                    "p99_us": round(nearest_rank(v, 0.99) / 1e3, 2)}
+                b_, nw = busy_of(lg)
+                p50, p99 = pct(lg, tr)
+                lat[f"rho{rho}"] = {"arrival_rate_req_s": round(rho * cap, 1), "utilization": rho, "windows": nw,
+                                    "mean_batches_per_window": round(lg["n_batches"] / nw, 2),
+                                    "p50_us": p50, "p99_us": p99}
+                check_tr = tr
+        # the same arrivals on the GPU, running exactly the clock's windows
+        cdep = Deployment(w, ctx, device=True, window_batches=window, service_ns=tables, window_ns=alphas,
+                          window_tail_ns=tails, clocked_windows=True, models=dep.models, seq_pack=seq_pack,
+                          n_streams=n_streams)
+        try:
+            cdt = dataclasses.replace(dt, arrival_ns=check_tr.arrival_ns)
+            lg = cdep.replay(cdt)
+            cdep.sched.sync()
+            torch.cuda.synchronize()
+            t0 = time.perf_counter()
+            lg = cdep.replay(cdt)
+            cdep.sched.sync()
+            el = time.perf_counter() - t0
+            busy, nw = busy_of(lg)
+            lat["model_check"] = {"arrivals": "rho0.9" if not timed else "trace", "windows": nw,
+                                  "simulated_busy_ms": round(busy / 1e6, 3), "measured_ms": round(el * 1e3, 3),
+                                  "measured_over_simulated": round(el * 1e9 / busy, 3)}
+        finally:
+            cdep.destroy()
     finally:
         ld.destroy()
         lctx.destroy()
-    return lat
+    return lat, tables, alphas, tails
 
 
 def main():
@@ -508,7 +672,7 @@ def main():
     pdep = make(args.window, profile=1)
     pdep.replay(dt)
     pdep.sched.sync()
-    work = algorithmic_work(w, t, a, logd, dep.qindex)
+    work = algorithmic_work(w, t, a, logd, dep.qindex, args.window)
     kernels = {}
     for k in KERNELS:
         n, ms = pdep.sched.kernel_stats(k)
@@ -575,15 +739,21 @@ def main():
         log(f"window {sw}: {el * 1e3:.2f} ms/step, {examples / el / 1e6:.2f} M rows/s")
         d2.destroy()
 
-    latency = None
+    latency, tables, alphas, tails = None, None, None, None
     if not args.no_latency:
-        latency = calibrate_latency(w, t, a, dt, ctx, dep, args.window, args.seq_pack)
+        latency, tables, alphas, tails = calibrate_latency(w, t, a, dt, ctx, dep, args.window, args.seq_pack,
+                                                           args.streams)
         log(f"latency: {json.dumps(latency)}")
 
     serving = None
     if args.serving_requests > 0:
         log(f"serving API with host payloads ({args.serving_requests} requests)")
-        serving = serving_rate(w, t, a, ctx, shared["m"], args.serving_requests, args.seq_pack)
+        # offered load above the simulated device's capacity: the clock keeps
+        # a backlog, so its launch windows fill up
+        cap = None if latency is None else latency.get("capacity_req_s")
+        serving = serving_rate(w, t, a, ctx, shared["m"], args.serving_requests, args.seq_pack,
+                               window=args.window if latency is not None else 1, tables=tables, alpha=alphas,
+                               tail=tails, rate=None if cap is None else 2.0 * cap)
         log(f"serving: {json.dumps(serving)}")
 
     swap = None

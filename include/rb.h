@@ -43,6 +43,9 @@ typedef int32_t rb_status;
 #define RB_ENOMEM (-8)  /* host or device allocation failed */
 #define RB_ERANGE (-9)  /* the device found an id or length outside its bounds */
 
+/* The name of a status code (a static string; "unknown status" for codes
+ * not listed above): the outcome of the batching calls of paper section
+ * 2.2.1, for messages. */
 const char* rb_status_str(rb_status s);
 
 typedef struct rb_ctx rb_ctx;
@@ -52,11 +55,16 @@ typedef struct rb_queue rb_queue;
 
 /* ---------------------------------------------------------------- context */
 
-/* hip_device >= 0: bind to that GPU. hip_device < 0: host-only context; models
+/* The single shared device that the batching queues are scheduled onto
+ * (paper section 2.2.1), with the manager thread that frees servable memory
+ * off the inference path (section 2.1.2).
+ * hip_device >= 0: bind to that GPU. hip_device < 0: host-only context; models
  * and schedulers created in it can only run in RB_MODE_NO_DEVICE.
- * RB_EDEVICE if the device cannot be initialised. */
+ * *out is written on RB_OK and owned by the caller (rb_ctx_destroy).
+ * RB_EINVAL if out is NULL; RB_EDEVICE if the device cannot be initialised. */
 rb_status rb_ctx_create(int32_t hip_device, rb_ctx** out);
-/* RB_EBUSY while models or schedulers created in it are alive. */
+/* Ends the context's manager thread and frees it (paper section 2.1.2).
+ * RB_EBUSY while models or schedulers created in it are alive. */
 rb_status rb_ctx_destroy(rb_ctx* ctx);
 
 /* ---------------------------------------------------------------- models */
@@ -102,13 +110,24 @@ typedef struct {
   rb_layer_desc head;
 } rb_model_desc;
 
+/* Load a servable version into device memory (a Loader's load, paper
+ * section 2.1; the servable is a black box to the queues and the scheduler,
+ * section 2.1). Safe to call on a thread of its own while a scheduler serves:
+ * the upload runs on a private non-blocking stream, so loading is insulated
+ * from inference (section 2.1.2, isolated load and inference threads).
+ * *out is owned by the caller (rb_model_destroy). RB_EINVAL on inconsistent
+ * shapes or NULL arguments; RB_ENOMEM / RB_EDEVICE on device failures. */
 rb_status rb_model_create(rb_ctx* ctx, const rb_model_desc* desc, rb_model** out);
-/* d_in: floats per request row (tokens: per token); d_out: floats per output row
- * (seqpool: per sequence). */
+/* The servable's request interface (paper section 2.1: what a caller's
+ * tensors must look like). d_in: floats per request row (tokens: per token);
+ * d_out: floats per output row (seqpool: per sequence). RB_EINVAL on NULL. */
 rb_status rb_model_info(const rb_model* m, int32_t* d_in, int32_t* d_out);
-/* RB_EBUSY while a queue is bound to the model. Device memory is released by
- * the context's deleter thread once work already enqueued has finished, never
- * on the caller's thread (a large free must not stall inference). */
+/* Unload a servable version (paper section 2.1.2: reference-counted servable
+ * handles whose memory is freed in a manager thread, not an inference
+ * thread). The caller's handle is invalid on return. RB_EBUSY while a queue
+ * is bound to the model. Batches already dispatched to it keep references of
+ * their own: its device memory is released by the context's deleter thread
+ * once the last of them has finished, never on the caller's thread. */
 rb_status rb_model_destroy(rb_model* m);
 
 /* ---------------------------------------------------------------- scheduler */
@@ -150,21 +169,29 @@ typedef struct {
   int32_t clocked_windows;
 } rb_sched_opts;
 
-/* One scheduler owns one HIP stream of the context's device (device mode),
- * plus opts->n_streams streams for concurrent launch chains in replays, and
- * round-robins its queues onto the device. */
+/* The scheduler that serves the batching queues round-robin on one shared
+ * device (paper section 2.2.1). It owns one HIP stream of the context's device
+ * (device mode), plus opts->n_streams streams for concurrent launch chains in
+ * replays, and a simulated clock (int64 ns) on which batches close, are
+ * dispatched in launch windows and complete. *out is owned by the caller
+ * (rb_sched_destroy). RB_EINVAL on a bad option; RB_EDEVICE when device mode
+ * is asked of a host-only context or stream creation fails. */
 rb_status rb_sched_create(rb_ctx* ctx, const rb_sched_opts* opts, rb_sched** out);
-/* RB_EBUSY while queues exist. Waits for the scheduler's device work. */
+/* Frees the scheduler after waiting for its device work (paper section
+ * 2.2.1). RB_EBUSY while queues exist. */
 rb_status rb_sched_destroy(rb_sched* s);
-/* Blocks until all device work of the scheduler has finished. RB_ERANGE if a
- * kernel found an id or a sequence length outside its request's bounds since
- * the last rb_sync (the offending values contributed nothing). */
+/* Blocks until all device work of the scheduler has finished (the batched
+ * Run() calls of paper section 2.2.1 have returned). RB_ERANGE if a kernel
+ * found an id or a sequence length outside its request's bounds since the
+ * last rb_sync (the offending values contributed nothing). */
 rb_status rb_sync(rb_sched* s);
-/* Kernel timings of a profiling scheduler since its creation (after rb_sync):
- * kernel names are those of rb_k_* without the prefix ("embbag", ...). */
+/* Kernel timings of a profiling scheduler since its creation (after rb_sync),
+ * for measuring the batched Run() of paper section 2.2.1: kernel names are
+ * those of rb_k_* without the prefix ("embbag", ...). RB_EINVAL on NULL. */
 rb_status rb_sched_kernel_stats(rb_sched* s, const char* kernel, int64_t* launches, double* total_ms);
-/* The scheduler's HIP stream (hipStream_t), for callers that order their own
- * work after the scheduler's. */
+/* The scheduler's HIP stream (hipStream_t) on the shared device (paper
+ * section 2.2.1), for callers that order their own work after the
+ * scheduler's; NULL in RB_MODE_NO_DEVICE. RB_EINVAL on NULL. */
 rb_status rb_sched_stream(rb_sched* s, void** stream);
 
 /* ---------------------------------------------------------------- queues */
@@ -182,21 +209,34 @@ typedef struct {
    * 0 <= P <= max_batch_size (n_service = max_batch_size + 1); NULL: 0. */
   const int64_t* service_ns;
   int32_t n_service;
-  /* Simulated fixed time of this queue's launch chain in a launch window
-   * (>= 0): a window taking batches of this queue costs window_ns once plus
-   * service_ns[P] per batch. */
+  /* Simulated fixed device time of this queue's launch chain in a launch
+   * window (>= 0): a window taking batches of this queue holds the device for
+   * window_ns once plus service_ns[P] per batch. */
   int64_t window_ns;
+  /* Simulated further time (>= 0) until that chain's results are complete
+   * once the device has moved on to the next window (a chain's fixed latency
+   * that the device overlaps with the next window's work). */
+  int64_t window_tail_ns;
 } rb_queue_opts;
 
-/* Queues may be created and destroyed while the scheduler runs (the set of
- * queues follows the servables and versions being served); queue ids are
- * assigned in creation order and round-robin follows them. */
+/* A batching queue for one servable version (paper section 2.2.1: one queue
+ * per servable or version, the set of queues dynamic as versions come and
+ * go). Queues may be created and destroyed while the scheduler runs; queue
+ * ids are assigned in creation order and round-robin follows them. The queue
+ * binds m (rb_model_destroy then returns RB_EBUSY). *out is owned by the
+ * caller (rb_queue_destroy). RB_EINVAL unless allowed_batch_sizes is strictly
+ * ascending with last == max_batch_size (or empty), bucket_len is given
+ * exactly for seqpool models, and the service table has max_batch_size + 1
+ * non-negative entries. */
 rb_status rb_queue_create(rb_sched* s, rb_model* m, const rb_queue_opts* opts, rb_queue** out);
-/* RB_EBUSY while the queue holds requests that have not run. */
+/* Remove a queue (paper section 2.2.1, queues removed as versions go).
+ * RB_EBUSY while the queue holds requests that have not run. */
 rb_status rb_queue_destroy(rb_queue* q);
+/* The queue's id, its place in the round-robin order (paper section 2.2.1).
+ * RB_EINVAL on NULL. */
 rb_status rb_queue_id(const rb_queue* q, int32_t* id);
 /* Version transition (the version transition policies of the paper's
- * Aspired Versions Manager, section 2.1): batches the queue dispatches after
+ * Aspired Versions Manager, section 2.1.2): batches the queue dispatches after
  * this call run model m. m must have the bound model's kind, dtype, input and
  * output widths and table count (RB_EINVAL otherwise); it may be created on
  * another thread while the scheduler serves (rb_model_create uploads on a
@@ -233,15 +273,29 @@ typedef struct {
   int64_t n_ids;
 } rb_request;
 
-/* Enqueue a request arriving at arrival_ns (non-decreasing per scheduler).
- * Timeouts due at or before arrival_ns fire first. RB_EINVAL if n_rows < 1 or
- * > max_batch_size, shapes mismatch, an id is outside its table, or a
+/* Enqueue one inference request on its servable's batching queue (paper
+ * section 2.2.1: requests are merged into batches by concatenating their
+ * input tensors; section 2.2: the caller's Run()). The payload is copied
+ * before the call returns; the caller keeps ownership of r.
+ * The simulated clock first runs its events before arrival_ns (timeouts, and
+ * launch windows dispatched whenever the simulated device is free), then the
+ * timeouts due at arrival_ns, then the arrival: next-fit in arrival order (the
+ * open batch closes when the request would overflow it, the request opens the
+ * next one, and a batch closes once full). Dispatches at arrival_ns wait for
+ * rb_run_next / rb_run_window / rb_advance, so every request of one timestamp
+ * should be submitted before those are called.
+ * arrival_ns must be >= the clock (RB_EINVAL otherwise). RB_EINVAL if n_rows
+ * < 1 or > max_batch_size, shapes mismatch, an id is outside its table, or a
  * sequence is longer than the queue's bucket. Request ids are dense per
  * scheduler, in submission order. */
 rb_status rb_submit(rb_queue* q, const rb_request* r, int64_t arrival_ns, uint64_t* out_req_id);
-/* Advance the simulated clock, firing batch timeouts due at or before now_ns. */
+/* Advance the simulated clock to now_ns, running its events up to and
+ * including now_ns: batch timeouts (a batch must not wait unduly, paper
+ * section 2.2.1) and the launch windows the simulated device dispatches.
+ * RB_EINVAL if now_ns is before the clock. */
 rb_status rb_advance(rb_sched* s, int64_t now_ns);
-/* Close the queue's open batch now (no-op if empty). */
+/* Close the queue's open batch at the current clock (no-op if empty; paper
+ * section 2.2.1, the end of a stream of requests). RB_EINVAL on NULL. */
 rb_status rb_flush(rb_queue* q);
 
 typedef struct {
@@ -254,10 +308,16 @@ typedef struct {
   const uint64_t* req_ids; /* valid until the next rb_run_next */
 } rb_batch_info;
 
-/* Run the next batch the simulated clock has dispatched (see below) and, in
- * device mode, enqueue its assemble -> forward -> split on the scheduler's
- * stream (asynchronous). RB_EEMPTY if the clock has dispatched nothing that
- * has not run. */
+/* Run one merged request (paper section 2.2.1: the batching wrapper forwards
+ * the concatenated inputs to the wrapped Run() once). The clock first runs
+ * its events up to and including the current time; then the next batch it
+ * has dispatched (oldest launch window first, batches of a window in their
+ * round-robin order) runs on its own: in device mode its payloads are staged
+ * to the device and assemble -> forward -> split is enqueued on the
+ * scheduler's stream (asynchronous; rb_collect waits for it). *out is valid
+ * until the next rb_run_next / rb_run_window call. RB_EEMPTY if the clock has
+ * dispatched nothing that has not run; RB_EDEVICE / RB_ENOMEM on device
+ * failures. */
 rb_status rb_run_next(rb_sched* s, rb_batch_info* out);
 
 /* The batches of one launch window (valid until the next rb_run_next or
@@ -267,15 +327,23 @@ typedef struct {
   const rb_batch_info* batches;
 } rb_window_info;
 
-/* Run the next launch window the simulated clock has dispatched: all of its
- * batches, one launch chain per queue, their payloads staged to the device in
- * one copy and their outputs copied back in one. RB_EEMPTY if nothing
- * dispatched is waiting. */
+/* Run the next launch window the simulated clock has dispatched (paper
+ * section 2.2.1, several merged requests of the queues sharing the device):
+ * the clock first runs its events up to and including the current time;
+ * then all batches of the oldest dispatched window run, one launch chain per
+ * queue, their payloads staged to the device in one copy and their outputs
+ * copied back in one (asynchronous). *out is valid until the next
+ * rb_run_next / rb_run_window call. RB_EEMPTY if nothing dispatched is
+ * waiting; RB_EDEVICE / RB_ENOMEM on device failures. */
 rb_status rb_run_window(rb_sched* s, rb_window_info* out);
-/* Copy request req_id's output rows ([n_rows, d_out] fp32) to dst (host).
- * RB_EAGAIN if its batch has not finished; RB_ESIZE if dst_bytes is too
- * small; RB_ENOENT if unknown or already collected. The library drops its copy
- * after a successful collect. */
+/* Hand a caller its own part of a merged run (paper section 2.2.1: each
+ * caller gets exactly its rows back): copy request req_id's output rows
+ * ([n_rows, d_out] fp32, in the request's row order) to dst (host). Keyed by
+ * the scheduler because request ids are dense per scheduler (a request keeps
+ * its id while its queue changes version or is held). RB_EAGAIN if its batch
+ * has not finished; RB_ESIZE if dst_bytes is too small; RB_ENOENT if unknown
+ * or already collected; RB_EDEVICE without a device. The library drops its
+ * copy after a successful collect. */
 rb_status rb_collect(rb_sched* s, uint64_t req_id, float* dst, size_t dst_bytes, int32_t* out_rows);
 
 /* ---------------------------------------------------------------- trace replay */
@@ -331,12 +399,19 @@ typedef struct {
   int32_t* b_reqs;
 } rb_log;
 
-/* Replay a trace through the queues with the simulated clock (events at one
- * timestamp: timeouts in queue-id order, then arrivals in request order, then
- * the end-of-trace close of count-only queues at the last arrival, then
- * dispatch while the simulated device is free), and in device mode enqueue
- * every batch's device work (asynchronous; rb_sync waits). The queues must be
- * empty; the replay leaves them empty. RB_ESIZE if max_batches is too small. */
+/* Replay a whole request trace through the batching queues (paper section
+ * 2.2.1: per-servable queues, merged requests, round-robin onto one device)
+ * with the simulated clock, starting idle: events at one timestamp are
+ * timeouts in queue-id order, then arrivals in request order, then the
+ * end-of-trace close of count-only queues at the last arrival, then launch
+ * windows dispatched while the simulated device is free. In device mode every
+ * batch's device work is enqueued (asynchronous; rb_sync waits): in windows of
+ * window_batches consecutive dispatched batches, or with clocked_windows in
+ * the clock's own windows. The log is written by the caller's arrays.
+ * RB_EBUSY if any queue of the scheduler still holds a request (open, closed
+ * or dispatched but not run) or a queue of the replay is held; the replay
+ * leaves its queues empty. RB_ESIZE if max_batches is too small; RB_EINVAL on
+ * inconsistent arrays (shapes, offsets, arrival order, unknown servables). */
 rb_status rb_sim_run(rb_sched* s, const rb_servable* servables, int32_t n_servables,
                      const rb_trace* trace, rb_log* log);
 
@@ -373,8 +448,10 @@ typedef struct {
   int64_t src, aux, lens, out;
 } rb_k_row;
 
-/* Row routing (exclusive prefix scans; the concatenation of a batch's request
- * tensors in the paper's batching section): fills rows[row_base .. row_base + P)
+/* Row routing (paper section 2.2.1, a merged request concatenates its
+ * requests' input tensors; here as exclusive prefix scans of row counts and,
+ * fused in the same kernel, of bag lengths or token counts): fills
+ * rows[row_base .. row_base + P)
  * of every batch (P <= RB_MAX_BATCH_ROWS; every request has >= 1 row). kind = RB_MODEL_*; d_in floats per row (per token for
  * seqpool); d_out floats per output row; n_tables bags per ranking row.
  * A request whose payload does not match its n_rows (dense length, bag
@@ -383,8 +460,10 @@ typedef struct {
 rb_status rb_k_route(void* stream, int32_t kind, const rb_k_batch* batches, int32_t n_batches,
                      const rb_k_req* reqs, const int32_t* lens, int32_t d_in, int32_t d_out,
                      int32_t n_tables, rb_k_row* rows, int32_t* err);
-/* Gather rows into X [n_rows_total, ldx] (ldx >= d_in, columns [d_in, ldx)
- * zeroed), padding rows set to pad; out_bf16 != 0 writes bf16 (RNE), else fp32.
+/* Concatenate and pad a batch (paper section 2.2.1, concatenating the input
+ * tensors): gather rows into X [n_rows_total, ldx] (ldx >= d_in, columns
+ * [d_in, ldx) zeroed), padding rows set to pad; out_bf16 != 0 writes bf16
+ * (RNE), else fp32.
  * Seqpool (seq_T > 0): row r*T + t is token t of sequence slot r (pad past L).
  * seq_real_only == 1 (seqpool, fp32 out, n_rows_total a multiple of seq_T):
  * rows t >= L and every row of a padding slot are not written and keep
@@ -396,7 +475,10 @@ rb_status rb_k_route(void* stream, int32_t kind, const rb_k_batch* batches, int3
 rb_status rb_k_assemble(void* stream, const rb_k_row* rows, int32_t n_rows_total, int32_t seq_T,
                         int32_t seq_real_only, const float* dense, int64_t dense_len, int32_t d_in, void* X,
                         int32_t ldx, int32_t out_bf16, float pad, int32_t* err);
-/* Ranking input: X[r] = [bf16(sum of bag f of row r from table f), f = 0..n_tables-1 |
+/* The ranking servable's input layer on a merged batch (paper section
+ * 2.2.1, the wrapped Run() on the concatenated examples; section 2.2, the
+ * examples' sparse features): X[r] = [bf16(sum of bag f of row r from table
+ * f), f = 0..n_tables-1 |
  * bf16(dense) | 0 ...] with row stride ldx; tables: n_tables device pointers
  * (in a device array) to [table_rows, emb_dim] bf16. emb_dim must be 64,
  * n_dense <= 256. ids_len is the length of the ids arena (reads stay below it).
@@ -405,14 +487,17 @@ rb_status rb_k_embbag(void* stream, const rb_k_row* rows, int32_t n_rows_total, 
                       const int32_t* ids, int64_t ids_len, const void* const* tables, int32_t n_tables,
                       int64_t table_rows, int32_t emb_dim, const float* dense, int32_t n_dense, void* X,
                       int32_t ldx, float pad, int32_t* err);
-/* Y[M, N] = act(X[M, K] W[N, K]^T + b), bf16 X and W (row strides ldx, ldw,
+/* A dense layer of the served model run once on a merged batch (paper
+ * section 2.2.1, the wrapped Run() on the concatenated inputs):
+ * Y[M, N] = act(X[M, K] W[N, K]^T + b), bf16 X and W (row strides ldx, ldw,
  * ldx and ldw < 2^22), fp32 accumulation; Y bf16 (out_f32 == 0) or fp32, row
  * stride ldy (a multiple of 8; Y 16-byte aligned). K % 64 == 0, N % 128 == 0.
  * act: RB_ACT_NONE, RB_ACT_RELU or RB_ACT_SIGMOID. */
 rb_status rb_k_gemm_bf16(void* stream, const void* X, int32_t ldx, const void* W, int32_t ldw,
                          const float* b, void* Y, int32_t ldy, int32_t M, int32_t N, int32_t K,
                          int32_t act, int32_t out_f32);
-/* fp32 variant (fp32 MFMA, same k order for every M): K % 32 == 0, N % 64 == 0;
+/* A dense layer on a merged batch (paper section 2.2.1), fp32 variant (fp32
+ * MFMA, same k order for every M): K % 32 == 0, N % 64 == 0;
  * ldx, ldw and ldy multiples of 4 with X, W and Y 16-byte aligned; ldx and
  * ldw < 2^23. Optional tile skip for
  * sequence groups: with skip_rows (the per-slot row map, aux = sequence length)
@@ -423,12 +508,16 @@ rb_status rb_k_gemm_bf16(void* stream, const void* X, int32_t ldx, const void* W
 rb_status rb_k_gemm_f32(void* stream, const float* X, int32_t ldx, const float* W, int32_t ldw,
                         const float* b, float* Y, int32_t ldy, int32_t M, int32_t N, int32_t K, int32_t act,
                         const rb_k_row* skip_rows, int32_t skip_T);
-/* Narrow last layer fused with the split: out[rows[r].out] = act(H[r, :K] . w + b)
+/* The merged run's last layer handed back to the callers (paper section
+ * 2.2.1: each caller gets its own rows): a narrow last layer fused with the
+ * split, out[rows[r].out] = act(H[r, :K] . w + b)
  * for real rows (act RB_ACT_SIGMOID or RB_ACT_NONE); H bf16 [n_rows_total, ldh],
  * w bf16 [K]. */
 rb_status rb_k_head(void* stream, const rb_k_row* rows, int32_t n_rows_total, const void* H, int32_t ldh,
                     const void* w, float b, int32_t K, int32_t act, float* out);
-/* Seqpool head fused with the split: per sequence slot r with L = rows[r].aux
+/* A sequence model's pooling and head on a merged batch, unbatched per
+ * sequence (paper section 2.2.1, sub-graph batching of sequence models with
+ * Batch/Unbatch), fused with the split: per sequence slot r with L = rows[r].aux
  * real tokens (clamped to [0, seq_T]), pooled = mean of H[r*T + t, :D] over t < L (fp32; tokens past L
  * are never read), then out[rows[r].out + j] = act(Wh pooled + bh)[j], j < n_out
  * (act RB_ACT_SOFTMAX or RB_ACT_NONE; D <= 1024, n_out <= 16).
@@ -437,7 +526,9 @@ rb_status rb_k_head(void* stream, const rb_k_row* rows, int32_t n_rows_total, co
 rb_status rb_k_seqpool(void* stream, const rb_k_row* rows, int32_t n_seqs, int32_t seq_T, int64_t packed_rows,
                        const float* H, int32_t ldh, int32_t D, const float* Wh, const float* bh, int32_t n_out,
                        int32_t act, float* out);
-/* Split: out[rows[r].out + j] = Y[r, j] for real rows, j < d_out. */
+/* Split a merged run's output back to its callers (paper section 2.2.1,
+ * each caller gets exactly its own rows): out[rows[r].out + j] = Y[r, j] for
+ * real rows, j < d_out; padding rows are never copied. */
 rb_status rb_k_split(void* stream, const rb_k_row* rows, int32_t n_rows_total, const float* Y, int32_t ldy,
                      int32_t d_out, float* out);
 

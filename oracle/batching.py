@@ -24,10 +24,13 @@ here are (each is a named choice in the design notes):
     batches one at a time, each time the oldest closed batch of the next queue
     holding one (queue ids scanned cyclically from the one after the
     last-served queue), until it has W of them or none is left; every batch of
-    the window is dispatched then and completes when the window does, after
-    the sum over the window's queues of window_ns[queue] (a fixed time per
-    launch chain) plus the sum over its batches of service_ns[queue][P]
-    nanoseconds. W = 1 and window_ns = 0 is one batch at a time;
+    the window is dispatched then; the device is busy with it for the sum
+    over the window's queues of window_ns[queue] (a fixed time per launch
+    chain) plus the sum over its batches of service_ns[queue][P] nanoseconds,
+    and its batches complete window_tail_ns[queue] (summed over its queues)
+    after that: a launch chain's fixed latency that the device overlaps with
+    the next window. W = 1, window_ns = 0 and window_tail_ns = 0 is one batch
+    at a time;
   * events at one timestamp: timeouts (queue id order), then arrivals
     (request id order), then the end-of-trace close, then dispatch;
   * within a batch, requests keep arrival order; request r's rows are rows
@@ -103,12 +106,15 @@ class SimResult:
 
 def simulate(queues: Sequence[QueueCfg], req_queue: Sequence[int], arrival_ns: Sequence[int],
              n_rows: Sequence[int], service_ns: Sequence[Sequence[int]], window: int = 1,
-             window_ns: Optional[Sequence[int]] = None) -> SimResult:
+             window_ns: Optional[Sequence[int]] = None,
+             window_tail_ns: Optional[Sequence[int]] = None) -> SimResult:
     """Batch formation per queue plus round-robin dispatch on one simulated
     serial device that takes launch windows of up to `window` closed batches.
     service_ns[q][P] is the device time of a batch of padded size P from queue
-    q, window_ns[q] (default 0) the fixed time of queue q's launch chain in a
-    window. Returns the batches in dispatch order."""
+    q, window_ns[q] (default 0) the fixed device time of queue q's launch
+    chain in a window, window_tail_ns[q] (default 0) the further time until
+    that chain's results are complete. Returns the batches in dispatch
+    order."""
     if window < 1:
         raise ValueError("window must be >= 1")
     N = len(arrival_ns)
@@ -135,6 +141,7 @@ def simulate(queues: Sequence[QueueCfg], req_queue: Sequence[int], arrival_ns: S
         open_s[q] = 0
 
     wns = [0] * nq if window_ns is None else [int(x) for x in window_ns]
+    tails = [0] * nq if window_tail_ns is None else [int(x) for x in window_tail_ns]
     last_served = -1
     n_windows = 0
     device_free = -(2 ** 62)
@@ -204,11 +211,12 @@ def simulate(queues: Sequence[QueueCfg], req_queue: Sequence[int], arrival_ns: S
                         break
                 win.append(closed[q].popleft())
                 last_served = q
-            busy = sum(int(wns[q]) for q in sorted({b.queue for b in win}))
-            busy += sum(int(service_ns[b.queue][b.P]) for b in win)
+            qs_in = sorted({b.queue for b in win})
+            busy = sum(wns[q] for q in qs_in) + sum(int(service_ns[b.queue][b.P]) for b in win)
+            tail = sum(tails[q] for q in qs_in)
             for b in win:
                 b.dispatch_ns = t
-                b.done_ns = t + busy
+                b.done_ns = t + busy + tail
                 b.window = n_windows
                 for r in b.reqs:
                     done[r] = b.done_ns

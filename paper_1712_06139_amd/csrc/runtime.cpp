@@ -63,8 +63,7 @@ inline uint16_t host_f2bf(float f) {
   return (uint16_t)(u >> 16);
 }
 
-struct DevFree {
-  std::vector<hipEvent_t> events;
+struct DevFree {  // device memory of a released model, for the deleter thread
   std::vector<void*> ptrs;
 };
 
@@ -76,7 +75,6 @@ struct rb_ctx {
   int device = -1;
   int n_models = 0, n_scheds = 0;
   int64_t next_model_id = 1;
-  std::vector<rb_model*> models;  // live models (a destroyed scheduler's stream leaves their use lists)
   // deleter thread: frees device memory after the events it waits on
   std::thread deleter;
   std::mutex mu;
@@ -113,7 +111,11 @@ struct rb_model {
   int64_t lineage = 0;
   hipStream_t upload = nullptr;  // private non-blocking stream of rb_model_create
   std::vector<void*> allocs;
-  std::vector<hipStream_t> used;  // streams that ran this model
+  // references: the caller's handle (until rb_model_destroy) and one per
+  // staging slot whose device work runs the model (until the slot retires,
+  // after that work has finished); the last one hands the device memory to
+  // the context's deleter thread
+  std::atomic<int64_t> refs{1};
 };
 
 namespace {
@@ -168,6 +170,8 @@ struct Slot {
   char* host = nullptr;
   char* dev = nullptr;
   size_t cap = 0;
+  // models its device work runs (one reference each, dropped on retire)
+  std::vector<rb_model*> models;
   // serving mode: payload arenas and the output staging of one batch
   std::vector<int64_t> serving_reqs;
   float* host_out = nullptr;
@@ -208,7 +212,8 @@ struct rb_queue {
   int64_t open_t = 0;
   std::deque<Batch> closed;
   int64_t undispatched = 0;  // requests in the open batch or in closed batches
-  int64_t window_ns = 0;     // simulated fixed time of its launch chain in a window
+  int64_t window_ns = 0;     // simulated fixed device time of its launch chain in a window
+  int64_t window_tail = 0;   // simulated further time until that chain's results are complete
   int64_t pending_run = 0;   // serving: batches the clock dispatched that have not run yet
 };
 
@@ -273,10 +278,6 @@ void deleter_main(rb_ctx* c) {
     DevFree f = std::move(c->pending.front());
     c->pending.pop_front();
     lk.unlock();
-    for (hipEvent_t e : f.events) {
-      hipEventSynchronize(e);
-      hipEventDestroy(e);
-    }
     for (void* p : f.ptrs) hipFree(p);
     lk.lock();
   }
@@ -334,6 +335,27 @@ rb_status upload_layer(rb_model* m, const rb_layer_desc& L, DevLayer& d, bool bf
 void free_model_now(rb_model* m) {
   for (void* p : m->allocs) hipFree(p);
   m->allocs.clear();
+}
+
+void model_ref(rb_model* m) { m->refs.fetch_add(1, std::memory_order_relaxed); }
+
+// Drop a reference; the last one hands the model's device memory to the
+// context's deleter thread (never freed on the calling thread, which may be
+// an inference thread) and frees the host object. Every device use of the
+// model holds a reference until it has finished, so nothing waits here.
+void model_unref(rb_model* m) {
+  if (m->refs.fetch_sub(1, std::memory_order_acq_rel) != 1) return;
+  rb_ctx* c = m->ctx;
+  if (!m->allocs.empty()) {
+    DevFree f;
+    f.ptrs = std::move(m->allocs);
+    {
+      std::lock_guard<std::mutex> lk(c->mu);
+      c->pending.push_back(std::move(f));
+    }
+    c->cv.notify_all();
+  }
+  delete m;
 }
 
 int padded_size(const rb_queue* q, int s) {
@@ -408,10 +430,10 @@ bool has_pickable(const rb_sched* s) {
 
 // One dispatch of the simulated device at time t (the device is free): a
 // launch window of up to window_batches closed batches, each the oldest
-// closed batch of the next queue in round-robin order that holds one. Every
-// batch of the window completes when the window does: after the window_ns of
-// each queue it takes batches from, plus service_ns[P] per batch. Returns
-// false when no queue holds a closed batch.
+// closed batch of the next queue in round-robin order that holds one. The
+// window holds the device for the window_ns of each queue it takes batches
+// from plus service_ns[P] per batch; its batches complete the queues'
+// window_tail later. Returns false when no queue holds a closed batch.
 bool clock_dispatch(rb_sched* s, int64_t t, std::vector<Disp>& win) {
   win.clear();
   const int W = s->opts.window_batches;
@@ -430,14 +452,17 @@ bool clock_dispatch(rb_sched* s, int64_t t, std::vector<Disp>& win) {
     win.push_back(std::move(d));
   }
   if (win.empty()) return false;
-  int64_t busy = 0;
+  int64_t busy = 0, tail = 0;
   for (size_t i = 0; i < win.size(); ++i) {
     bool first = true;
     for (size_t j = 0; j < i && first; ++j) first = win[j].q != win[i].q;
-    if (first) busy += win[i].q->window_ns;
+    if (first) {
+      busy += win[i].q->window_ns;
+      tail += win[i].q->window_tail;
+    }
     busy += service(win[i].q, win[i].b.P);
   }
-  for (Disp& d : win) d.b.done_ns = t + busy;
+  for (Disp& d : win) d.b.done_ns = t + busy + tail;
   s->device_free = t + busy;
   s->window_seq++;
   return true;
@@ -594,7 +619,6 @@ rb_status run_group(rb_sched* s, hipStream_t st_h, int slot, const Group& g, con
   Work* w = nullptr;
   rb_status st = ensure_work(s, m, slot, M, slots, &w);
   if (st != RB_OK) return st;
-  if (std::find(m->used.begin(), m->used.end(), st_h) == m->used.end()) m->used.push_back(st_h);
   void* hs = (void*)st_h;
   const float pad = s->opts.pad_value;
   RB_LAUNCH(s, st_h, "route", rb_k_route(hs, m->kind, d_batches, (int)g.batches.size(), d_reqs, lens, m->d_in,
@@ -658,7 +682,16 @@ void retire_slot(rb_sched* s, Slot& sl) {
     r.slot = -1;
   }
   sl.serving_reqs.clear();
+  for (rb_model* m : sl.models) model_unref(m);
+  sl.models.clear();
   sl.busy = false;
+}
+
+// The slot's device work runs model m: hold a reference until it retires.
+void slot_hold(Slot& sl, rb_model* m) {
+  if (std::find(sl.models.begin(), sl.models.end(), m) != sl.models.end()) return;
+  model_ref(m);
+  sl.models.push_back(m);
 }
 
 // Reuse a staging slot: wait for its previous work, retire it, and make room
@@ -717,6 +750,8 @@ rb_status flush_chunk(rb_sched* s) {
       offs.push_back({o1, off});
       off += round_up((int64_t)rr, 256);
     }
+  for (auto& win : s->chunk)
+    for (Group& g : win) slot_hold(*sl, g.q->m);
   if (!hip_ok(hipMemcpyAsync(sl->dev, sl->host, off, hipMemcpyHostToDevice, s->stream))) return RB_EDEVICE;
   // lanes start after the copy; the main stream (and the slot's event) after
   // every lane's chains
@@ -972,7 +1007,6 @@ rb_status rb_model_create(rb_ctx* ctx, const rb_model_desc* d, rb_model** out) {
   {
     std::lock_guard<std::mutex> lk(ctx->mu);
     ctx->n_models++;
-    ctx->models.push_back(m);
   }
   *out = m;
   return RB_OK;
@@ -989,28 +1023,12 @@ rb_status rb_model_destroy(rb_model* m) {
   if (!m) return RB_OK;
   if (m->bound) return RB_EBUSY;
   rb_ctx* c = m->ctx;
-  if (c->device >= 0 && !m->allocs.empty()) {
-    DevFree f;
-    f.ptrs = std::move(m->allocs);
-    for (hipStream_t st : m->used) {
-      hipEvent_t e = nullptr;
-      if (hip_ok(hipEventCreateWithFlags(&e, hipEventDisableTiming))) {
-        hipEventRecord(e, st);
-        f.events.push_back(e);
-      }
-    }
-    {
-      std::lock_guard<std::mutex> lk(c->mu);
-      c->pending.push_back(std::move(f));
-    }
-    c->cv.notify_all();
-  }
   {
     std::lock_guard<std::mutex> lk(c->mu);
     c->n_models--;
-    c->models.erase(std::remove(c->models.begin(), c->models.end(), m), c->models.end());
   }
-  delete m;
+  // the caller's reference; dispatched work may still hold others
+  model_unref(m);
   return RB_OK;
 }
 
@@ -1068,6 +1086,9 @@ rb_status rb_sched_destroy(rb_sched* s) {
   if (s->n_live_queues) return RB_EBUSY;
   if (s->stream) {
     sync_all(s);
+    // the device work is done: slots drop their model references
+    for (Slot& sl : s->slots)
+      if (sl.busy) retire_slot(s, sl);
     for (auto& kv : s->work) {
       Work& w = kv.second;
       hipFree(w.X);
@@ -1089,14 +1110,6 @@ rb_status rb_sched_destroy(rb_sched* s) {
     for (hipEvent_t e : s->ev_pool) hipEventDestroy(e);
     hipFree(s->err_dev);
     if (s->scrub) hipFree(s->scrub);
-    // the streams are drained: models no longer need to wait on them
-    std::vector<hipStream_t> mine = s->lanes;
-    mine.push_back(s->stream);
-    {
-      std::lock_guard<std::mutex> lk(s->ctx->mu);
-      for (rb_model* m : s->ctx->models)
-        for (hipStream_t st : mine) m->used.erase(std::remove(m->used.begin(), m->used.end(), st), m->used.end());
-    }
     for (hipStream_t l : s->lanes) hipStreamDestroy(l);
     for (hipEvent_t e : s->lane_done) hipEventDestroy(e);
     if (s->ev_copy) hipEventDestroy(s->ev_copy);
@@ -1155,7 +1168,7 @@ rb_status rb_queue_create(rb_sched* s, rb_model* m, const rb_queue_opts* o, rb_q
   if (o->service_ns)
     for (int i = 0; i < o->n_service; ++i)
       if (o->service_ns[i] < 0) return RB_EINVAL;
-  if (o->window_ns < 0) return RB_EINVAL;
+  if (o->window_ns < 0 || o->window_tail_ns < 0) return RB_EINVAL;
   rb_queue* q = new (std::nothrow) rb_queue();
   if (!q) return RB_ENOMEM;
   q->s = s;
@@ -1168,6 +1181,7 @@ rb_status rb_queue_create(rb_sched* s, rb_model* m, const rb_queue_opts* o, rb_q
   q->bucket = o->bucket_len;
   if (o->service_ns) q->svc.assign(o->service_ns, o->service_ns + o->n_service);
   q->window_ns = o->window_ns;
+  q->window_tail = o->window_tail_ns;
   s->queues.push_back(q);
   s->n_live_queues++;
   m->bound++;
@@ -1387,6 +1401,7 @@ static rb_status run_serving_window(rb_sched* s, const std::vector<Disp>& win) {
     offs.push_back({o1, off});
     off += round_up((int64_t)rr, 256);
   }
+  for (Group& g : groups) slot_hold(*sl, g.q->m);
   if (!hip_ok(hipMemcpyAsync(sl->dev, sl->host, o_out, hipMemcpyHostToDevice, s->stream))) return RB_EDEVICE;
   float* dout = (float*)(sl->dev + o_out);
   for (size_t gi = 0; gi < groups.size(); ++gi) {

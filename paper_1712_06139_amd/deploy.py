@@ -39,7 +39,8 @@ class Deployment:
     def __init__(self, w, ctx: rb.Ctx, device: bool = True, window_batches: int = 1, pad_value: float = 0.0,
                  profile: int = 0, service_ns: Optional[Sequence[Sequence[int]]] = None,
                  with_params: bool = True, models: Optional[List[rb.Model]] = None, n_streams: int = 1,
-                 seq_pack: bool = False, window_ns: Optional[Sequence[int]] = None, clocked_windows: bool = False):
+                 seq_pack: bool = False, window_ns: Optional[Sequence[int]] = None,
+                 window_tail_ns: Optional[Sequence[int]] = None, clocked_windows: bool = False):
         import synth
         self.w = w
         self.ctx = ctx
@@ -66,7 +67,8 @@ class Deployment:
             svc = None if service_ns is None else service_ns[qi]
             self.queues.append(rb.Queue(self.sched, self.models[q.servable], q.max_batch_size, q.allowed,
                                         q.timeout_ns, q.bucket_len, svc,
-                                        0 if window_ns is None else int(window_ns[qi])))
+                                        0 if window_ns is None else int(window_ns[qi]),
+                                        0 if window_tail_ns is None else int(window_tail_ns[qi])))
         self.servables = [[self.queues[qi] for qi, q in enumerate(w.queues) if q.servable == s]
                           for s in range(len(w.models))]
         self.qindex = {q.id: i for i, q in enumerate(self.queues)}

@@ -58,7 +58,7 @@ class rb_sched_opts(C.Structure):
 class rb_queue_opts(C.Structure):
     _fields_ = [("max_batch_size", C.c_int32), ("allowed_batch_sizes", p_i32), ("n_allowed", C.c_int32),
                 ("batch_timeout_ns", C.c_int64), ("bucket_len", C.c_int32), ("service_ns", p_i64),
-                ("n_service", C.c_int32), ("window_ns", C.c_int64)]
+                ("n_service", C.c_int32), ("window_ns", C.c_int64), ("window_tail_ns", C.c_int64)]
 
 
 class rb_request(C.Structure):
@@ -285,12 +285,13 @@ class Model:
 class Queue:
     def __init__(self, sched: "Sched", model: Model, max_batch_size: int, allowed: Sequence[int] = (),
                  timeout_ns: Optional[int] = None, bucket_len: int = 0,
-                 service_ns: Optional[Sequence[int]] = None, window_ns: int = 0):
+                 service_ns: Optional[Sequence[int]] = None, window_ns: int = 0, window_tail_ns: int = 0):
         al = np.ascontiguousarray(allowed, dtype=np.int32)
         sv = None if service_ns is None else np.ascontiguousarray(service_ns, dtype=np.int64)
         o = rb_queue_opts(max_batch_size, _ptr(al, p_i32) if al.size else C.cast(None, p_i32), int(al.size),
                           INT64_MAX if timeout_ns is None else int(timeout_ns), bucket_len,
-                          _ptr(sv, p_i64), 0 if sv is None else int(sv.size), int(window_ns))
+                          _ptr(sv, p_i64), 0 if sv is None else int(sv.size), int(window_ns),
+                          int(window_tail_ns))
         h = C.c_void_p()
         check(_lib().rb_queue_create(sched.h, model.h, C.byref(o), C.byref(h)), "rb_queue_create")
         self.h = h

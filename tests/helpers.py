@@ -26,9 +26,9 @@ def service_table(w, base=20_000, per_row=100):
     return [[base + per_row * P for P in range(q.max_batch_size + 1)] for q in w.queues]
 
 
-def oracle_sim(w, t, svc, window=1, window_ns=None):
+def oracle_sim(w, t, svc, window=1, window_ns=None, window_tail_ns=None):
     return ob.simulate(oracle_queues(w), oracle_req_queue(w, t).tolist(), t.arrival_ns, t.n_rows, svc, window,
-                       window_ns)
+                       window_ns, window_tail_ns)
 
 
 def lib_batches(log, qindex):

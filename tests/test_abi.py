@@ -29,6 +29,24 @@ def test_every_declared_symbol_is_exported_and_bound():
     assert sorted(rb.EXPORTS) == names
 
 
+def test_every_declared_call_cites_its_passage():
+    # each exported call's own comment block names the paper section that
+    # defines the operation
+    src = open(os.path.join(ROOT, "include", "rb.h")).read()
+    decl = re.compile(r"^(?:rb_status|const char\*)\s+(rb_\w+)\(", re.M)
+    names = []
+    prev_end = 0
+    for m in decl.finditer(src):
+        block = src[prev_end:m.start()]
+        comments = re.findall(r"/\*.*?\*/", block, re.S)
+        assert comments, m.group(1)
+        text = re.sub(r"\s*\n\s*\*?\s*", " ", comments[-1])
+        assert re.search(r"section \d+(\.\d+)*", text), m.group(1)
+        names.append(m.group(1))
+        prev_end = src.index(";", m.end()) + 1
+    assert set(names) == set(rb.EXPORTS)
+
+
 def test_status_strings():
     for code in (rb.RB_OK, rb.RB_EINVAL, rb.RB_EBUSY, rb.RB_EAGAIN, rb.RB_EEMPTY, rb.RB_ESIZE, rb.RB_ENOENT,
                  rb.RB_EDEVICE, rb.RB_ENOMEM, rb.RB_ERANGE):
@@ -237,13 +255,15 @@ def test_serving_api_formation_matches_oracle(ctx, seed):
         cfg.append(ob.QueueCfg(B, (), T))
     svc = [[int(rng.integers(0, 40)) for _ in range(c.max_batch_size + 1)] for c in cfg]
     wns = [int(rng.integers(0, 30)) for _ in range(nq)]
+    tails = [int(rng.integers(0, 60)) for _ in range(nq)]
     N = 300
     arrival = np.cumsum(rng.integers(0, 20, size=N))
     rq = rng.integers(0, nq, size=N)
     n = np.array([int(rng.integers(1, cfg[q].max_batch_size + 1)) for q in rq])
     s = rb.Sched(ctx, device=False, window_batches=W)
     m = mlp(ctx)
-    qs = [rb.Queue(s, m, c.max_batch_size, (), c.timeout_ns, 0, svc[i], wns[i]) for i, c in enumerate(cfg)]
+    qs = [rb.Queue(s, m, c.max_batch_size, (), c.timeout_ns, 0, svc[i], wns[i], tails[i])
+          for i, c in enumerate(cfg)]
     got = []
 
     def drain():
@@ -276,7 +296,7 @@ def test_serving_api_formation_matches_oracle(ctx, seed):
         drain()
     s.advance(int(arrival[-1]) + 10 ** 12)   # past every timeout and the device's backlog
     drain()
-    ref = ob.simulate(cfg, rq.tolist(), arrival.tolist(), n.tolist(), svc, W, wns)
+    ref = ob.simulate(cfg, rq.tolist(), arrival.tolist(), n.tolist(), svc, W, wns, tails)
     assert got == [(b.queue, list(b.reqs), b.close_ns, b.dispatch_ns, b.done_ns) for b in ref.batches]
     for q in qs:
         q.destroy()

@@ -215,6 +215,43 @@ def test_serving_api_launch_windows(ctx, name, n):
     print(f"{name}: {len(sizes)} windows, largest {max(sizes)} batches")
 
 
+def test_destroy_old_version_while_its_batches_run(ctx):
+    # availability-preserving swap right after an asynchronous replay, with no
+    # sync: the old version is destroyed while its batches may still be
+    # running. They hold references of their own, so its memory goes to the
+    # deleter thread only after they finish; 2 GB of fresh allocations filled
+    # with NaN right after the destroy must not reach any output, which must
+    # equal an undisturbed replay's bit for bit. The new version then serves.
+    name = "large_mlp"
+    n = 1500
+    w = synth.workload(name)
+    t, a = trace_and_arenas(name, n)
+    *_, out_ref, out_off = run(ctx, name, n, window=4)
+    dep = Deployment(w, ctx, device=True, window_batches=4, service_ns=service_table(w))
+    try:
+        p_new = synth.next_version(synth.model_params(w, 0))
+        new = dep.build_model(0, p_new)
+        dt = dep.upload(t, a)
+        dep.replay(dt)
+        old = dep.swap(0, new)
+        old.destroy()
+        junk = [torch.full((64 << 20,), float("nan"), device="cuda") for _ in range(8)]
+        dep.sched.sync()
+        torch.cuda.synchronize()
+        assert np.array_equal(dt.out.cpu().numpy(), out_ref)
+        del junk
+        dep.replay(dt)
+        dep.sched.sync()
+        out = dt.out.cpu().numpy()
+        om_new = OracleModel(w.models[0], p_new)
+        for r in range(0, n, 97):
+            ref = om_new.forward(a.payload(r))
+            y = out[out_off[r]:out_off[r + 1]].reshape(ref.shape)
+            assert row_scaled_err(y, ref.astype(np.float64)) <= RTOL["bf16"], r
+    finally:
+        dep.destroy()
+
+
 def test_serving_api_ranking_and_seqpool(ctx):
     for name, n, pack in (("ranking", 120, False), ("ragged_seq", 60, False), ("ragged_seq", 60, True)):
         w = synth.workload(name)

@@ -17,7 +17,7 @@ def _run_case(c):
     qs = [ob.QueueCfg(q["max_batch_size"], tuple(q["allowed"]), q["timeout_ns"]) for q in c["queues"]]
     req = c["requests"]
     return ob.simulate(qs, [r[1] for r in req], [r[0] for r in req], [r[2] for r in req], c["service_ns"],
-                       c.get("window", 1), c.get("window_ns"))
+                       c.get("window", 1), c.get("window_ns"), c.get("window_tail_ns"))
 
 
 def test_hand_worked_schedules(golden_dir):
@@ -207,7 +207,9 @@ def _random_windowed(seed, n_req=400):
     qs, rq, arrival, n, svc, _ = _random_sim(seed, n_req)
     W = int(rng.integers(2, 7))
     wns = [int(rng.integers(0, 300)) for _ in qs]
-    return qs, rq, arrival, n, svc, W, wns, ob.simulate(qs, rq.tolist(), arrival.tolist(), n.tolist(), svc, W, wns)
+    tails = [int(rng.integers(0, 500)) if seed % 2 else 0 for _ in qs]
+    res = ob.simulate(qs, rq.tolist(), arrival.tolist(), n.tolist(), svc, W, wns, tails)
+    return qs, rq, arrival, n, svc, W, (wns, tails), res
 
 
 @pytest.mark.parametrize("seed", range(25))
@@ -215,9 +217,10 @@ def test_launch_window_invariants(seed):
     # the windowed device restated declaratively from the batches' close
     # times alone: each window starts when the device frees up (or at the
     # next close when nothing waits), takes min(W, waiting) batches in
-    # round-robin order (FIFO within a queue), and lasts the sum of its
-    # queues' chain times and its batches' service times
-    qs, rq, arrival, n, svc, W, wns, res = _random_windowed(seed)
+    # round-robin order (FIFO within a queue), holds the device for the sum
+    # of its queues' chain times and its batches' service times, and its
+    # batches complete its queues' tails after that
+    qs, rq, arrival, n, svc, W, (wns, tails), res = _random_windowed(seed)
     nq = len(qs)
     wins = []
     for b in res.batches:
@@ -243,7 +246,8 @@ def test_launch_window_invariants(seed):
             picked.append(b)
             last = q
         busy = sum(wns[q] for q in {b.queue for b in w}) + sum(svc[b.queue][b.P] for b in w)
-        assert all(b.dispatch_ns == t and b.done_ns == t + busy for b in w)
+        tail = sum(tails[q] for q in {b.queue for b in w})
+        assert all(b.dispatch_ns == t and b.done_ns == t + busy + tail for b in w)
         done_prev = t + busy
         k += len(w)
     assert sorted(r for b in res.batches for r in b.reqs) == list(range(len(arrival)))
@@ -252,7 +256,7 @@ def test_launch_window_invariants(seed):
 @pytest.mark.parametrize("seed", range(10))
 def test_window_of_one_adds_chain_time_to_service(seed):
     # W = 1 with chain times a_q is the one-batch device with service S + a_q
-    qs, rq, arrival, n, svc, W, wns, _ = _random_windowed(seed)
+    qs, rq, arrival, n, svc, W, (wns, _), _ = _random_windowed(seed)
     r1 = ob.simulate(qs, rq.tolist(), arrival.tolist(), n.tolist(), svc, 1, wns)
     svc2 = [[s + wns[q] for s in row] for q, row in enumerate(svc)]
     r2 = ob.simulate(qs, rq.tolist(), arrival.tolist(), n.tolist(), svc2)
@@ -263,7 +267,7 @@ def test_window_of_one_adds_chain_time_to_service(seed):
 
 @pytest.mark.parametrize("seed", range(5))
 def test_littles_law_with_windows(seed):
-    qs, rq, arrival, n, svc, W, wns, res = _random_windowed(seed, n_req=300)
+    qs, rq, arrival, n, svc, W, _, res = _random_windowed(seed, n_req=300)
     lat = res.latency_ns(arrival)
     ev = sorted([(int(a), 1) for a in arrival] + [(int(d), -1) for d in res.done_ns])
     area, cnt, t_prev = 0, 0, ev[0][0]

@@ -29,12 +29,13 @@ def test_full_trace_log_matches_oracle(ctx, name, window):
     t = synth.trace(w)
     svc = service_table(w)
     wns = [3_000 + 1_000 * i for i in range(len(w.queues))]
+    tails = [0 if window == 1 else 50_000 + 7_000 * i for i in range(len(w.queues))]
     dep = Deployment(w, ctx, device=False, service_ns=svc, with_params=False, window_batches=window,
-                     window_ns=wns)
+                     window_ns=wns, window_tail_ns=tails)
     try:
         log = dep.replay_meta(t)
         ours = lib_batches(log, dep.qindex)
-        ref = oracle_sim(w, t, svc, window, wns)
+        ref = oracle_sim(w, t, svc, window, wns, tails)
         assert ours == oracle_batches(ref)
         assert np.array_equal(log["req_done_ns"], ref.done_ns)
         # a second replay on the same scheduler starts a fresh clock
@@ -50,7 +51,9 @@ def test_hand_worked_schedules_through_library(ctx, golden_dir):
         sched = rb.Sched(ctx, device=False, window_batches=c.get("window", 1))
         m = rb.Model(ctx, "mlp", "f32", [(None, None, "none")], shapes=[(4, 4)])
         wns = c.get("window_ns", [0] * len(c["queues"]))
-        qs = [rb.Queue(sched, m, q["max_batch_size"], q["allowed"], q["timeout_ns"], 0, c["service_ns"][i], wns[i])
+        tails = c.get("window_tail_ns", [0] * len(c["queues"]))
+        qs = [rb.Queue(sched, m, q["max_batch_size"], q["allowed"], q["timeout_ns"], 0, c["service_ns"][i], wns[i],
+                       tails[i])
               for i, q in enumerate(c["queues"])]
         req = c["requests"]
         log = sched.sim_run([[q] for q in qs], np.array([r[1] for r in req]), np.array([r[0] for r in req]),
@@ -83,10 +86,11 @@ def test_random_traces_match_oracle(ctx, seed):
     svc = [[int(rng.integers(0, 200)) for _ in range(c.max_batch_size + 1)] for c in cfg]
     W = 1 if seed < 10 else int(rng.integers(2, 9))
     wns = [0] * nq if seed < 10 else [int(rng.integers(0, 300)) for _ in range(nq)]
-    ref = ob.simulate(cfg, rq.tolist(), arrival.tolist(), n.tolist(), svc, W, wns)
+    tails = [0] * nq if seed < 15 else [int(rng.integers(0, 900)) for _ in range(nq)]
+    ref = ob.simulate(cfg, rq.tolist(), arrival.tolist(), n.tolist(), svc, W, wns, tails)
     sched = rb.Sched(ctx, device=False, window_batches=W)
     m = rb.Model(ctx, "mlp", "f32", [(None, None, "none")], shapes=[(4, 4)])
-    qs = [rb.Queue(sched, m, c.max_batch_size, c.allowed, c.timeout_ns, 0, svc[i], wns[i])
+    qs = [rb.Queue(sched, m, c.max_batch_size, c.allowed, c.timeout_ns, 0, svc[i], wns[i], tails[i])
           for i, c in enumerate(cfg)]
     log = sched.sim_run([[q] for q in qs], rq, arrival, n)
     assert lib_batches(log, {q.id: i for i, q in enumerate(qs)}) == oracle_batches(ref)
