@@ -448,18 +448,59 @@ typedef struct {
   int64_t src, aux, lens, out;
 } rb_k_row;
 
+/* ---------------------------------------------------------------- launch groups */
+
+/* Run one merged request group of queue q's model (paper section 2.2.1: the
+ * batching wrapper forwards the concatenated inputs of its callers to the
+ * wrapped Run() once and hands each caller its part) on device-resident
+ * inputs: route -> assemble | embedding bags -> layers -> head | pooling |
+ * split, enqueued on `stream` (a hipStream_t; NULL: the scheduler's stream),
+ * asynchronous. For callers that form their own batches.
+ *   batches [n_batches] and reqs [n_reqs]: device arrays of rb_k_batch /
+ *     rb_k_req (above) describing the group: batch b owns rows
+ *     [row_base, row_base + padded) of the group's `slots` rows (its padded
+ *     sizes summed; sequence slots for seqpool) and requests
+ *     [req_begin, req_begin + n_req);
+ *   tokens (seqpool with rb_sched_opts.seq_pack): the requests' real tokens
+ *     summed (their dense extents over d_in), the rows of the token-wise
+ *     layers; tok_off of each request its first packed row; else 0;
+ *   dense / lens / ids: device payload arenas of dense_len / lens_len /
+ *     ids_len elements; out: the fp32 output arena of out_len floats.
+ * The queue's scheduler must be in device mode and the queue bound to a model
+ * (RB_EBUSY while held); the queue's model and the scheduler's pad value and
+ * seq_pack are used. Work buffers belong to the scheduler (one set per
+ * servable lineage for these calls, grown by allocation as needed; growing
+ * waits for `stream` and the scheduler's streams), so calls on one scheduler
+ * must be ordered: on one stream, or each finished before the next. The
+ * queue must stay bound and its model alive until the stream has run the
+ * call. Rows no valid batch covers stay padding; payloads and descriptors are
+ * bounds-checked on the device (RB_ERANGE from the scheduler's next rb_sync,
+ * called once `stream` has finished). RB_EINVAL on NULL pointers, n_batches
+ * < 1, slots < n_batches or negative extents; RB_EDEVICE without a device. */
+rb_status rb_run_group(rb_queue* q, void* stream, const rb_k_batch* batches, int32_t n_batches,
+                       const rb_k_req* reqs, int32_t n_reqs, int64_t slots, int64_t tokens, const float* dense, int64_t dense_len,
+                       const int32_t* lens, int64_t lens_len, const int32_t* ids, int64_t ids_len, float* out,
+                       int64_t out_len);
+
+/* ---------------------------------------------------------------- single kernels */
+
 /* Row routing (paper section 2.2.1, a merged request concatenates its
  * requests' input tensors; here as exclusive prefix scans of row counts and,
  * fused in the same kernel, of bag lengths or token counts): fills
- * rows[row_base .. row_base + P)
- * of every batch (P <= RB_MAX_BATCH_ROWS; every request has >= 1 row). kind = RB_MODEL_*; d_in floats per row (per token for
- * seqpool); d_out floats per output row; n_tables bags per ranking row.
- * A request whose payload does not match its n_rows (dense length, bag
- * lengths vs ids, sequence lengths outside [1, seq_T]) sets *err = 1 and
- * contributes no ids / no tokens. */
+ * rows[row_base .. row_base + P) of every batch (P <= RB_MAX_BATCH_ROWS; every
+ * request has >= 1 row). kind = RB_MODEL_*; d_in floats per row (per token
+ * for seqpool); d_out floats per output row; n_tables bags per ranking row.
+ * Extents: reqs holds n_reqs requests, lens lens_len elements, rows
+ * n_rows_total entries, and the output out_len floats. A batch whose rows or
+ * requests fall outside them sets *err = 1 and writes no row. A request whose
+ * payload does not match its n_rows (dense length, bag lengths vs ids,
+ * sequence lengths outside [1, seq_T]), or whose lengths or output rows would
+ * lie outside their extents, sets *err = 1, contributes no ids / no tokens and
+ * gets no output rows (its rows' out = -1). */
 rb_status rb_k_route(void* stream, int32_t kind, const rb_k_batch* batches, int32_t n_batches,
-                     const rb_k_req* reqs, const int32_t* lens, int32_t d_in, int32_t d_out,
-                     int32_t n_tables, rb_k_row* rows, int32_t* err);
+                     const rb_k_req* reqs, int32_t n_reqs, const int32_t* lens, int64_t lens_len, int32_t d_in,
+                     int32_t d_out, int32_t n_tables, rb_k_row* rows, int32_t n_rows_total, int64_t out_len,
+                     int32_t* err);
 /* Concatenate and pad a batch (paper section 2.2.1, concatenating the input
  * tensors): gather rows into X [n_rows_total, ldx] (ldx >= d_in, columns
  * [d_in, ldx) zeroed), padding rows set to pad; out_bf16 != 0 writes bf16

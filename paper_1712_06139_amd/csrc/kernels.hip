@@ -109,10 +109,10 @@ __device__ __forceinline__ int64_t block_exclusive_scan(int64_t v, int64_t* s_w,
 //     the row of its first token when the group's real tokens are packed
 //     (its request's first packed row, set by the host, plus the scan).
 __global__ __launch_bounds__(256) void k_route(int kind, const rb_k_batch* __restrict__ batches,
-                                               const rb_k_req* __restrict__ reqs,
-                                               const int32_t* __restrict__ lens, int d_in, int d_out,
-                                               int n_tables, rb_k_row* __restrict__ rows,
-                                               int* __restrict__ err) {
+                                               const rb_k_req* __restrict__ reqs, int n_reqs,
+                                               const int32_t* __restrict__ lens, int64_t lens_len, int d_in,
+                                               int d_out, int n_tables, rb_k_row* __restrict__ rows,
+                                               int n_rows_total, int64_t out_len, int* __restrict__ err) {
   const rb_k_batch b = batches[blockIdx.x];
   const int tid = threadIdx.x;
   __shared__ int s_first[ROUTE_MAX_ROWS + 1];   // first row of request i (batch-relative)
@@ -120,7 +120,11 @@ __global__ __launch_bounds__(256) void k_route(int kind, const rb_k_batch* __res
   __shared__ int64_t s_ex[ROUTE_MAX_ROWS + 1];  // exclusive scan of per-row id/token counts
   __shared__ unsigned char s_bad[ROUTE_MAX_ROWS];
   __shared__ int64_t s_w[4];
-  if (b.padded > ROUTE_MAX_ROWS || b.n_req > b.padded || b.real > b.padded) {
+  // the batch's rows and requests must lie inside the row map and the
+  // request table (its rows are then left as they are)
+  if (b.padded > ROUTE_MAX_ROWS || b.n_req > b.padded || b.real > b.padded || b.padded < 0 || b.n_req < 0 ||
+      b.row_base < 0 || (int64_t)b.row_base + b.padded > n_rows_total || b.req_begin < 0 ||
+      (int64_t)b.req_begin + b.n_req > n_reqs) {
     if (tid == 0) *err = 1;
     return;
   }
@@ -156,11 +160,20 @@ __global__ __launch_bounds__(256) void k_route(int kind, const rb_k_batch* __res
   for (int base = 0; base < s; base += 256) {
     const int p = base + tid;
     int64_t c = 0;
-    if (p < s && kind != RB_MODEL_MLP) {
+    if (p < s) {
       const int i = s_req[p];
       const rb_k_req& rq = reqs[b.req_begin + i];
       const int e = p - s_first[i];
-      if (kind == RB_MODEL_RANKING) {
+      // a request whose output rows would lie outside the output, or whose bag
+      // or sequence lengths outside the lens arena, is rejected
+      const int64_t nl = kind == RB_MODEL_RANKING ? (int64_t)rq.n_rows * n_tables
+                                                  : (kind == RB_MODEL_SEQPOOL ? rq.n_rows : 0);
+      const bool in_arena = e < rq.n_rows && rq.out_off >= 0 && rq.out_off + (int64_t)rq.n_rows * d_out <= out_len &&
+                            (nl == 0 || (rq.lens_off >= 0 && rq.lens_off + nl <= lens_len));
+      if (!in_arena) {
+        s_bad[i] = 1;
+      } else if (kind == RB_MODEL_MLP) {
+      } else if (kind == RB_MODEL_RANKING) {
         const int32_t* l = lens + rq.lens_off + (int64_t)e * n_tables;
         // the flag is kept in a register so that the unrolled loads are all
         // issued before the first one is used
@@ -215,7 +228,7 @@ __global__ __launch_bounds__(256) void k_route(int kind, const rb_k_batch* __res
         rw.aux = rq.ids_off + within;
         rw.lens = (kind == RB_MODEL_RANKING && ok) ? rq.lens_off + (int64_t)e * n_tables : -1;
       }
-      rw.out = rq.out_off + (int64_t)e * d_out;
+      rw.out = ok ? rq.out_off + (int64_t)e * d_out : -1;  // a rejected request's rows are not returned
     } else {
       rw.src = -1;
       rw.aux = 0;
@@ -1120,6 +1133,23 @@ unsigned device_cus() {
 
 }  // namespace
 
+// ---------------------------------------------------------------- row map fill
+
+namespace {
+// Every entry of a row map set to padding (no input, no output).
+__global__ __launch_bounds__(256) void k_fill_padding_rows(rb_k_row* __restrict__ rows, int64_t n) {
+  const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (i < n) rows[i] = rb_k_row{-1, 0, -1, -1};
+}
+}  // namespace
+
+// Runtime support (not part of the C ABI): a row map whose batches come from
+// a caller's descriptors starts as padding, so that rows no valid batch
+// covers are neither computed from nor returned.
+void rb_fill_padding_rows(hipStream_t stream, rb_k_row* rows, int64_t n) {
+  if (n > 0) hipLaunchKernelGGL(k_fill_padding_rows, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, stream, rows, n);
+}
+
 // ---------------------------------------------------------------- cache scrub
 
 namespace {
@@ -1143,15 +1173,19 @@ void rb_scrub_caches(hipStream_t stream, const void* buf, size_t bytes, unsigned
 extern "C" {
 
 rb_status rb_k_route(void* stream, int32_t kind, const rb_k_batch* batches, int32_t n_batches,
-                     const rb_k_req* reqs, const int32_t* lens, int32_t d_in, int32_t d_out,
-                     int32_t n_tables, rb_k_row* rows, int32_t* err) {
-  if (n_batches < 0 || !batches || !rows || !err || d_in < 1 || d_out < 1) return RB_EINVAL;
+                     const rb_k_req* reqs, int32_t n_reqs, const int32_t* lens, int64_t lens_len, int32_t d_in,
+                     int32_t d_out, int32_t n_tables, rb_k_row* rows, int32_t n_rows_total, int64_t out_len,
+                     int32_t* err) {
+  if (n_batches < 0 || n_reqs < 0 || n_rows_total < 0 || lens_len < 0 || out_len < 0 || !batches || !rows ||
+      !err || d_in < 1 || d_out < 1)
+    return RB_EINVAL;
+  if (n_reqs > 0 && !reqs) return RB_EINVAL;
   if (kind < RB_MODEL_MLP || kind > RB_MODEL_SEQPOOL) return RB_EINVAL;
   if (kind != RB_MODEL_MLP && !lens) return RB_EINVAL;
   if (kind == RB_MODEL_RANKING && (n_tables < 1 || n_tables > MAX_TABLES)) return RB_EINVAL;
   if (n_batches == 0) return RB_OK;
-  hipLaunchKernelGGL(k_route, dim3(n_batches), dim3(256), 0, (hipStream_t)stream, kind, batches, reqs, lens,
-                     d_in, d_out, n_tables, rows, err);
+  hipLaunchKernelGGL(k_route, dim3(n_batches), dim3(256), 0, (hipStream_t)stream, kind, batches, reqs, n_reqs, lens,
+                     lens_len, d_in, d_out, n_tables, rows, n_rows_total, out_len, err);
   return launch_status();
 }
 

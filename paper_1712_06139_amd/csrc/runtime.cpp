@@ -42,6 +42,8 @@
 
 // kernels.hip: reads a buffer on the stream, leaving only its clean lines in the caches
 void rb_scrub_caches(hipStream_t stream, const void* buf, size_t bytes, unsigned* sink);
+// kernels.hip: sets n row-map entries to padding
+void rb_fill_padding_rows(hipStream_t stream, rb_k_row* rows, int64_t n);
 
 namespace {
 
@@ -256,9 +258,13 @@ struct rb_sched {
   const float* a_dense = nullptr;
   int64_t a_dense_len = 0;
   const int32_t* a_lens = nullptr;
+  int64_t a_lens_len = 0;
   const int32_t* a_ids = nullptr;
   int64_t a_ids_len = 0;
   float* a_out = nullptr;
+  int64_t a_out_len = 0;
+  // rb_run_group's work buffers, per servable lineage
+  std::map<int64_t, Work> ext_work;
   // profiling
   std::vector<Prof> prof_pending;
   std::map<std::string, std::pair<int64_t, double>> prof;
@@ -531,13 +537,13 @@ void prof_collect(rb_sched* s) {
   s->prof_pending.clear();
 }
 
-#define RB_LAUNCH(s, strm, name, call) \
-  do {                                 \
-    hipEvent_t ev_a_ = nullptr;        \
-    prof_begin(s, strm, &ev_a_);       \
-    rb_status st_ = (call);            \
-    prof_end(s, strm, name, ev_a_);    \
-    if (st_ != RB_OK) return st_;      \
+#define RB_LAUNCH(s, strm, name, call)         \
+  do {                                         \
+    hipEvent_t ev_a_ = nullptr;                \
+    if (timed) prof_begin(s, strm, &ev_a_);    \
+    rb_status st_ = (call);                    \
+    if (timed) prof_end(s, strm, name, ev_a_); \
+    if (st_ != RB_OK) return st_;              \
   } while (0)
 
 int64_t group_rows(const rb_model* m, const rb_queue* q, int64_t slots) {
@@ -578,66 +584,94 @@ hipStream_t lane_for(rb_sched* s, const rb_model* m, int slot) {
   return s->lanes[(size_t)it->second];
 }
 
+// Bytes of a launch group's work buffers for R rows (padded batch rows, or
+// sequence slots times the bucket) and S row-map entries: the row map, the
+// assembled input X, two activation buffers A and B for the layers, and the
+// fp32 output Y of the last layer.
+struct WorkShape {
+  size_t rows, x, ab, y;
+};
+
+WorkShape work_shape(const rb_model* m, int64_t R, int64_t S) {
+  const size_t elt = m->dtype == RB_DT_BF16 ? 2 : 4;
+  int maxN = 0;
+  for (const DevLayer& L : m->layers) maxN = std::max(maxN, L.Np);
+  return WorkShape{(size_t)S * sizeof(rb_k_row), (size_t)R * m->layers[0].Kp * elt, (size_t)R * maxN * elt,
+                   (size_t)R * m->layers.back().Np * 4};
+}
+
+void free_work(Work& w) {
+  hipFree(w.X);
+  hipFree(w.A);
+  hipFree(w.B);
+  hipFree(w.Y);
+  hipFree(w.rows);
+  w = Work{};
+}
+
+// Grow work buffers to rows x slots (capacities only grow, both at once, so
+// groups of different shapes never make the buffers shrink and grow back).
+// The streams that may still use the old buffers are drained first.
+rb_status grow_work(rb_sched* s, rb_model* m, Work& w, int64_t rows, int64_t slots, hipStream_t also) {
+  if (rows <= w.rows_cap && slots <= w.slots_cap) return RB_OK;
+  const int64_t R = std::max<int64_t>({rows, w.rows_cap, 64});
+  const int64_t S = std::max<int64_t>({slots, w.slots_cap, 64});
+  sync_all(s);
+  if (also) hipStreamSynchronize(also);
+  free_work(w);
+  const WorkShape sh = work_shape(m, R, S);
+  if (!hip_ok(hipMalloc(&w.X, sh.x)) || !hip_ok(hipMalloc(&w.A, sh.ab)) || !hip_ok(hipMalloc(&w.B, sh.ab)) ||
+      !hip_ok(hipMalloc((void**)&w.Y, sh.y)) || !hip_ok(hipMalloc((void**)&w.rows, sh.rows))) {
+    free_work(w);
+    return RB_ENOMEM;
+  }
+  w.rows_cap = R;
+  w.slots_cap = S;
+  return RB_OK;
+}
+
 rb_status ensure_work(rb_sched* s, rb_model* m, int slot, int64_t rows, int64_t slots, Work** out) {
   Work& w = s->work[work_key(m, slot)];
-  if (rows > w.rows_cap || slots > w.slots_cap) {
-    // capacities only grow (both at once), so groups of different shapes
-    // never make the buffers shrink and grow back
-    const int64_t R = std::max<int64_t>({rows, w.rows_cap, 64});
-    const int64_t S = std::max<int64_t>({slots, w.slots_cap, 64});
-    sync_all(s);
-    hipFree(w.X);
-    hipFree(w.A);
-    hipFree(w.B);
-    hipFree(w.Y);
-    hipFree(w.rows);
-    w = Work{};
-    const size_t elt = m->dtype == RB_DT_BF16 ? 2 : 4;
-    int maxN = 0;
-    for (const DevLayer& L : m->layers) maxN = std::max(maxN, L.Np);
-    const int Kp0 = m->layers[0].Kp;
-    if (!hip_ok(hipMalloc(&w.X, (size_t)R * Kp0 * elt)) || !hip_ok(hipMalloc(&w.A, (size_t)R * maxN * elt)) ||
-        !hip_ok(hipMalloc(&w.B, (size_t)R * maxN * elt)) ||
-        !hip_ok(hipMalloc((void**)&w.Y, (size_t)R * m->layers.back().Np * 4)) ||
-        !hip_ok(hipMalloc((void**)&w.rows, (size_t)S * sizeof(rb_k_row))))
-      return RB_ENOMEM;
-    w.rows_cap = R;
-    w.slots_cap = S;
-  }
+  rb_status st = grow_work(s, m, w, rows, slots, nullptr);
+  if (st != RB_OK) return st;
   *out = &w;
   return RB_OK;
 }
 
 // Launch chain of one group on stream st_h: route -> assemble | embbag ->
 // layers -> head | seqpool | split.
-rb_status run_group(rb_sched* s, hipStream_t st_h, int slot, const Group& g, const rb_k_batch* d_batches,
+// The chain of a group of n_batches batches of queue q holding `slots`
+// padded rows (sequence slots) and `tokens` real tokens (seqpool), with work
+// buffers w large enough for it; `timed`: HIP events around every launch when
+// the scheduler profiles.
+// Descriptors not built by this library start from a row map of padding
+// (fill_rows).
+rb_status run_chain(rb_sched* s, hipStream_t st_h, const rb_queue* q, int n_batches, int n_reqs, int64_t slots,
+                    int64_t tokens, const Work* w, bool timed, bool fill_rows, const rb_k_batch* d_batches,
                     const rb_k_req* d_reqs, const float* dense, int64_t dense_len, const int32_t* lens,
-                    const int32_t* ids, int64_t ids_len, float* out) {
-  rb_model* m = g.q->m;
-  const int64_t slots = g.slots;
-  const int64_t M = group_rows(m, g.q, slots);
-  Work* w = nullptr;
-  rb_status st = ensure_work(s, m, slot, M, slots, &w);
-  if (st != RB_OK) return st;
+                    int64_t lens_len, const int32_t* ids, int64_t ids_len, float* out, int64_t out_len) {
+  const rb_model* m = q->m;
+  const int64_t M = group_rows(m, q, slots);
   void* hs = (void*)st_h;
   const float pad = s->opts.pad_value;
-  RB_LAUNCH(s, st_h, "route", rb_k_route(hs, m->kind, d_batches, (int)g.batches.size(), d_reqs, lens, m->d_in,
-                                   m->d_out, m->n_tables, w->rows, s->err_dev));
+  if (fill_rows) rb_fill_padding_rows(st_h, w->rows, slots);
+  RB_LAUNCH(s, st_h, "route", rb_k_route(hs, m->kind, d_batches, n_batches, d_reqs, n_reqs, lens, lens_len, m->d_in,
+                                         m->d_out, m->n_tables, w->rows, (int)slots, out_len, s->err_dev));
   const bool bf16 = m->dtype == RB_DT_BF16;
   const int Kp0 = m->layers[0].Kp;
   // sequence groups: padding tokens are not assembled and 64-token blocks of
   // them are not computed (every layer is row-wise and the pooling reads
-  // tokens t < L only); with seq_pack the real tokens are packed into g.tokens
+  // tokens t < L only); with seq_pack the real tokens are packed into tokens
   // consecutive rows and the layers run on those rows alone
   const bool pack = m->kind == RB_MODEL_SEQPOOL && s->opts.seq_pack && !bf16;
-  const bool seq_skip = m->kind == RB_MODEL_SEQPOOL && !pack && g.q->bucket % 64 == 0;
-  const int64_t Ml = pack ? g.tokens : M;  // rows of the layers
+  const bool seq_skip = m->kind == RB_MODEL_SEQPOOL && !pack && q->bucket % 64 == 0;
+  const int64_t Ml = pack ? tokens : M;  // rows of the layers
   if (m->kind == RB_MODEL_RANKING) {
     RB_LAUNCH(s, st_h, "embbag", rb_k_embbag(hs, w->rows, (int)slots, lens, ids, ids_len, (const void* const*)m->tables_dev,
                                        m->n_tables, m->table_rows, m->emb_dim, dense, m->n_dense, w->X, Kp0, pad,
                                        s->err_dev));
   } else {
-    RB_LAUNCH(s, st_h, "assemble", rb_k_assemble(hs, w->rows, (int)M, m->kind == RB_MODEL_SEQPOOL ? g.q->bucket : 0,
+    RB_LAUNCH(s, st_h, "assemble", rb_k_assemble(hs, w->rows, (int)M, m->kind == RB_MODEL_SEQPOOL ? q->bucket : 0,
                                            pack ? 2 : (seq_skip ? 1 : 0), dense, dense_len, m->d_in, w->X, Kp0,
                                            bf16 ? 1 : 0, pad, s->err_dev));
   }
@@ -654,7 +688,7 @@ rb_status run_group(rb_sched* s, hipStream_t st_h, int slot, const Group& g, con
     } else {
       RB_LAUNCH(s, st_h, "gemm_f32", rb_k_gemm_f32(hs, (const float*)h, ldh, (const float*)L.w, L.Kp, L.b, (float*)y,
                                              L.Np, (int)Ml, L.Np, L.Kp, L.act, seq_skip ? w->rows : nullptr,
-                                             seq_skip ? g.q->bucket : 0));
+                                             seq_skip ? q->bucket : 0));
     }
     h = y;
     ldh = L.Np;
@@ -663,13 +697,26 @@ rb_status run_group(rb_sched* s, hipStream_t st_h, int slot, const Group& g, con
     const DevLayer& L = m->layers.back();
     RB_LAUNCH(s, st_h, "head", rb_k_head(hs, w->rows, (int)slots, h, ldh, L.w, m->head_bias, L.K, L.act, out));
   } else if (m->kind == RB_MODEL_SEQPOOL) {
-    RB_LAUNCH(s, st_h, "seqpool", rb_k_seqpool(hs, w->rows, (int)slots, g.q->bucket, pack ? std::max<int64_t>(Ml, 1) : 0,
+    RB_LAUNCH(s, st_h, "seqpool", rb_k_seqpool(hs, w->rows, (int)slots, q->bucket, pack ? std::max<int64_t>(Ml, 1) : 0,
                                          (const float*)h, ldh, m->sp_in, m->sp_w, m->sp_b, m->sp_out, m->sp_act,
                                          out));
   } else {
     RB_LAUNCH(s, st_h, "split", rb_k_split(hs, w->rows, (int)slots, w->Y, ldh, m->d_out, out));
   }
   return RB_OK;
+}
+
+// Launch chain of one group of a window on stream st_h, with the scheduler's
+// work buffers of (lineage, slot).
+rb_status run_group(rb_sched* s, hipStream_t st_h, int slot, const Group& g, const rb_k_batch* d_batches,
+                    const rb_k_req* d_reqs, const float* dense, int64_t dense_len, const int32_t* lens,
+                    int64_t lens_len, const int32_t* ids, int64_t ids_len, float* out, int64_t out_len) {
+  rb_model* m = g.q->m;
+  Work* w = nullptr;
+  rb_status st = ensure_work(s, m, slot, group_rows(m, g.q, g.slots), g.slots, &w);
+  if (st != RB_OK) return st;
+  return run_chain(s, st_h, g.q, (int)g.batches.size(), (int)g.reqs.size(), g.slots, g.tokens, w, true, false,
+                   d_batches, d_reqs, dense, dense_len, lens, lens_len, ids, ids_len, out, out_len);
 }
 
 // A slot whose work has finished: hand its serving outputs to their requests.
@@ -770,8 +817,8 @@ rb_status flush_chunk(rb_sched* s) {
     for (Group& g : win) {
       const int slot = next_slot(s, g.q->m, pipe);
       st = run_group(s, lane_for(s, g.q->m, slot), slot, g, (const rb_k_batch*)(sl->dev + offs[gi].first),
-                     (const rb_k_req*)(sl->dev + offs[gi].second), s->a_dense, s->a_dense_len, s->a_lens, s->a_ids,
-                     s->a_ids_len, s->a_out);
+                     (const rb_k_req*)(sl->dev + offs[gi].second), s->a_dense, s->a_dense_len, s->a_lens,
+                     s->a_lens_len, s->a_ids, s->a_ids_len, s->a_out, s->a_out_len);
       ++gi;
       if (st != RB_OK) return st;
     }
@@ -1089,14 +1136,8 @@ rb_status rb_sched_destroy(rb_sched* s) {
     // the device work is done: slots drop their model references
     for (Slot& sl : s->slots)
       if (sl.busy) retire_slot(s, sl);
-    for (auto& kv : s->work) {
-      Work& w = kv.second;
-      hipFree(w.X);
-      hipFree(w.A);
-      hipFree(w.B);
-      hipFree(w.Y);
-      hipFree(w.rows);
-    }
+    for (auto& kv : s->work) free_work(kv.second);
+    for (auto& kv : s->ext_work) free_work(kv.second);
     for (Slot& sl : s->slots) {
       hipHostFree(sl.host);
       hipFree(sl.dev);
@@ -1407,7 +1448,7 @@ static rb_status run_serving_window(rb_sched* s, const std::vector<Disp>& win) {
   for (size_t gi = 0; gi < groups.size(); ++gi) {
     st = run_group(s, s->stream, 0, groups[gi], (const rb_k_batch*)(sl->dev + offs[gi].first),
                    (const rb_k_req*)(sl->dev + offs[gi].second), (const float*)(sl->dev + o_dense), nd,
-                   (const int32_t*)(sl->dev + o_lens), (const int32_t*)(sl->dev + o_ids), ni, dout);
+                   (const int32_t*)(sl->dev + o_lens), nl, (const int32_t*)(sl->dev + o_ids), ni, dout, no);
     if (st != RB_OK) return st;
   }
   if (!hip_ok(hipMemcpyAsync(sl->host_out, dout, (size_t)no * 4, hipMemcpyDeviceToHost, s->stream)))
@@ -1502,6 +1543,44 @@ rb_status rb_collect(rb_sched* s, uint64_t req_id, float* dst, size_t dst_bytes,
   return RB_OK;
 }
 
+// ---------------------------------------------------------------- launch groups
+
+// Checks of rb_run_group's arguments (the descriptors themselves are checked
+// on the device).
+static rb_status check_group(rb_queue* q, const rb_k_batch* batches, int32_t n_batches, const rb_k_req* reqs,
+                             int32_t n_reqs, int64_t slots, int64_t tokens, const float* dense, int64_t dense_len,
+                             const int32_t* lens, int64_t lens_len, const int32_t* ids, int64_t ids_len,
+                             const float* out, int64_t out_len) {
+  if (!q || !batches || !reqs || !out || !dense) return RB_EINVAL;
+  if (n_batches < 1 || n_reqs < 1 || slots < n_batches || tokens < 0 || dense_len < 0 || lens_len < 0 ||
+      ids_len < 0 || out_len < 0)
+    return RB_EINVAL;
+  if (!q->s->stream) return RB_EDEVICE;
+  const rb_model* m = q->m;
+  if (!m) return RB_EBUSY;
+  if (m->kind != RB_MODEL_MLP && !lens) return RB_EINVAL;
+  if (m->kind == RB_MODEL_RANKING && ids_len > 0 && !ids) return RB_EINVAL;
+  if (group_rows(m, q, slots) > INT32_MAX || slots > INT32_MAX) return RB_EINVAL;
+  if (tokens > group_rows(m, q, slots)) return RB_EINVAL;
+  return RB_OK;
+}
+
+rb_status rb_run_group(rb_queue* q, void* stream, const rb_k_batch* batches, int32_t n_batches, const rb_k_req* reqs,
+                       int32_t n_reqs, int64_t slots, int64_t tokens, const float* dense, int64_t dense_len,
+                       const int32_t* lens, int64_t lens_len, const int32_t* ids, int64_t ids_len, float* out,
+                       int64_t out_len) {
+  rb_status st = check_group(q, batches, n_batches, reqs, n_reqs, slots, tokens, dense, dense_len, lens, lens_len,
+                             ids, ids_len, out, out_len);
+  if (st != RB_OK) return st;
+  rb_sched* s = q->s;
+  rb_model* m = q->m;
+  hipStream_t hs = stream ? (hipStream_t)stream : s->stream;
+  Work& w = s->ext_work[m->lineage];
+  if ((st = grow_work(s, m, w, group_rows(m, q, slots), slots, hs)) != RB_OK) return st;
+  return run_chain(s, hs, q, n_batches, n_reqs, slots, tokens, &w, false, true, batches, reqs, dense, dense_len, lens,
+                   lens_len, ids, ids_len, out, out_len);
+}
+
 // ---------------------------------------------------------------- replay
 
 rb_status rb_sim_run(rb_sched* s, const rb_servable* sv, int32_t n_sv, const rb_trace* tr, rb_log* log) {
@@ -1569,9 +1648,11 @@ rb_status rb_sim_run(rb_sched* s, const rb_servable* sv, int32_t n_sv, const rb_
     s->a_dense = tr->dense;
     s->a_dense_len = N > 0 ? tr->dense_off[N] : 0;
     s->a_lens = tr->lens;
+    s->a_lens_len = (N > 0 && tr->lens_off) ? tr->lens_off[N] : 0;
     s->a_ids = tr->ids;
     s->a_ids_len = (N > 0 && tr->ids_off) ? tr->ids_off[N] : 0;
     s->a_out = tr->out;
+    s->a_out_len = N > 0 ? tr->out_off[N] : 0;
   }
   // a replay runs on its own simulated clock, starting idle
   s->now = INT64_MIN;

@@ -142,8 +142,12 @@ _SIGS = {
     "rb_collect": (C.c_int32, [C.c_void_p, C.c_uint64, p_f32, C.c_size_t, p_i32]),
     "rb_sim_run": (C.c_int32, [C.c_void_p, C.POINTER(rb_servable), C.c_int32, C.POINTER(rb_trace),
                                C.POINTER(rb_log)]),
-    "rb_k_route": (C.c_int32, [C.c_void_p, C.c_int32, C.c_void_p, C.c_int32, C.c_void_p, C.c_void_p, C.c_int32,
-                               C.c_int32, C.c_int32, C.c_void_p, C.c_void_p]),
+    "rb_run_group": (C.c_int32, [C.c_void_p, C.c_void_p, C.c_void_p, C.c_int32, C.c_void_p, C.c_int32, C.c_int64,
+                                 C.c_int64, C.c_void_p, C.c_int64, C.c_void_p, C.c_int64, C.c_void_p, C.c_int64,
+                                 C.c_void_p, C.c_int64]),
+    "rb_k_route": (C.c_int32, [C.c_void_p, C.c_int32, C.c_void_p, C.c_int32, C.c_void_p, C.c_int32, C.c_void_p,
+                               C.c_int64, C.c_int32, C.c_int32, C.c_int32, C.c_void_p, C.c_int32, C.c_int64,
+                               C.c_void_p]),
     "rb_k_assemble": (C.c_int32, [C.c_void_p, C.c_void_p, C.c_int32, C.c_int32, C.c_int32, C.c_void_p, C.c_int64,
                                   C.c_int32, C.c_void_p, C.c_int32, C.c_int32, C.c_float, C.c_void_p]),
     "rb_k_embbag": (C.c_int32, [C.c_void_p, C.c_void_p, C.c_int32, C.c_void_p, C.c_void_p, C.c_int64, C.c_void_p,
@@ -300,6 +304,16 @@ class Queue:
         qid = C.c_int32()
         check(_lib().rb_queue_id(h, C.byref(qid)), "rb_queue_id")
         self.id = qid.value
+
+    def run_group(self, stream: int, batches, n_batches: int, reqs, n_reqs: int, slots: int, tokens: int,
+                  dense, dense_len: int, lens, lens_len: int, ids, ids_len: int, out, out_len: int,
+                  entry: str = "rb_run_group"):
+        """One launch group on device-resident descriptors and arenas
+        (torch tensors; `stream` a hipStream_t address, 0 for the
+        scheduler's)."""
+        check(getattr(_lib(), entry)(self.h, stream or None, dptr(batches), n_batches, dptr(reqs), n_reqs, slots,
+                                     tokens, dptr(dense), dense_len, dptr(lens), lens_len, dptr(ids), ids_len,
+                                     dptr(out), out_len), entry)
 
     def set_model(self, model: Optional[Model]):
         """Version transition: batches dispatched from now on run `model`;

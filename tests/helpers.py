@@ -43,3 +43,28 @@ def lib_batches(log, qindex):
 
 def oracle_batches(res):
     return [(b.queue, list(b.reqs), b.s, b.P, b.close_ns, b.dispatch_ns, b.done_ns) for b in res.batches]
+
+
+def group_descriptors(w, t, a, out_off, batches, seq_pack=False):
+    """A launch group's device descriptors (rb_k_batch / rb_k_req records as
+    numpy structured arrays) for batches of one queue formed by the oracle:
+    requests keep the trace's arena offsets and output offsets. Returns
+    (kb, kr, slots, tokens)."""
+    from paper_1712_06139_amd import rb
+    q = w.queues[batches[0].queue]
+    m = w.models[q.servable]
+    kb = np.zeros(len(batches), dtype=rb.K_BATCH_DTYPE)
+    n_req = sum(len(b.reqs) for b in batches)
+    kr = np.zeros(n_req, dtype=rb.K_REQ_DTYPE)
+    row, ri, tok = 0, 0, 0
+    for bi, b in enumerate(batches):
+        kb[bi] = (ri, len(b.reqs), row, b.P, b.s, q.bucket_len if m.kind == "seqpool" else 0)
+        for r in b.reqs:
+            lo = a.lens_off[r] if a.lens.size else 0
+            io0, io1 = (a.ids_off[r], a.ids_off[r + 1]) if a.ids.size else (0, 0)
+            kr[ri] = (a.dense_off[r], a.dense_off[r + 1], lo, io0, io1, out_off[r], t.n_rows[r], tok)
+            if m.kind == "seqpool":
+                tok += int(a.dense_off[r + 1] - a.dense_off[r]) // m.d_in
+            ri += 1
+        row += b.P
+    return kb, kr, row, (tok if (m.kind == "seqpool" and seq_pack) else 0)

@@ -36,8 +36,8 @@ hipError_t hipStreamDestroy(hipStream_t) { reached("hipStreamDestroy"); }
 hipError_t hipStreamSynchronize(hipStream_t) { reached("hipStreamSynchronize"); }
 hipError_t hipStreamWaitEvent(hipStream_t, hipEvent_t, unsigned) { reached("hipStreamWaitEvent"); }
 
-rb_status rb_k_route(void*, int32_t, const rb_k_batch*, int32_t, const rb_k_req*, const int32_t*, int32_t, int32_t,
-                     int32_t, rb_k_row*, int32_t*) {
+rb_status rb_k_route(void*, int32_t, const rb_k_batch*, int32_t, const rb_k_req*, int32_t, const int32_t*, int64_t,
+                     int32_t, int32_t, int32_t, rb_k_row*, int32_t, int64_t, int32_t*) {
   reached("rb_k_route");
 }
 rb_status rb_k_assemble(void*, const rb_k_row*, int32_t, int32_t, int32_t, const float*, int64_t, int32_t, void*,
@@ -70,3 +70,4 @@ rb_status rb_k_split(void*, const rb_k_row*, int32_t, const float*, int32_t, int
 }
 
 void rb_scrub_caches(hipStream_t, const void*, size_t, unsigned*) { reached("rb_scrub_caches"); }
+void rb_fill_padding_rows(hipStream_t, rb_k_row*, int64_t) { reached("rb_fill_padding_rows"); }

@@ -18,7 +18,7 @@ from oracle.models import OracleModel
 from paper_1712_06139_amd import rb
 from paper_1712_06139_amd.deploy import Deployment
 
-from helpers import lib_batches, oracle_batches, oracle_sim, service_table
+from helpers import group_descriptors, lib_batches, oracle_batches, oracle_sim, service_table
 
 pytestmark = pytest.mark.gpu
 
@@ -248,6 +248,111 @@ def test_destroy_old_version_while_its_batches_run(ctx):
             ref = om_new.forward(a.payload(r))
             y = out[out_off[r]:out_off[r + 1]].reshape(ref.shape)
             assert row_scaled_err(y, ref.astype(np.float64)) <= RTOL["bf16"], r
+    finally:
+        dep.destroy()
+
+
+def _run_groups(ctx, name, n, groups, seq_pack, entry):
+    """Every group of oracle-formed batches through one launch-group entry
+    point, on torch's stream, into one output arena; returns it."""
+    w = synth.workload(name)
+    t, a = trace_and_arenas(name, n)
+    dep = Deployment(w, ctx, device=True, seq_pack=seq_pack)
+    try:
+        dt = dep.upload(t, a)
+        out = torch.zeros_like(dt.out)
+        stream = rb.torch_stream_ptr()
+        for grp in groups:
+            kb, kr, slots, tokens = group_descriptors(w, t, a, dt.out_off, grp, seq_pack)
+            kb_d = torch.from_numpy(kb.view(np.uint8).copy()).cuda()
+            kr_d = torch.from_numpy(kr.view(np.uint8).copy()).cuda()
+            lens_len = 0 if dt.lens is None else dt.lens.numel()
+            ids_len = 0 if dt.ids is None else dt.ids.numel()
+            dep.queues[grp[0].queue].run_group(stream, kb_d, len(kb), kr_d, len(kr), slots, tokens, dt.dense,
+                                               dt.dense.numel(), dt.lens, lens_len, dt.ids, ids_len, out,
+                                               out.numel(), entry=entry)
+            torch.cuda.synchronize()
+        dep.sched.sync()
+        return out.cpu().numpy(), dt.out_off
+    finally:
+        dep.destroy()
+
+
+def _oracle_groups(name, n, sizes):
+    """Consecutive batches of each queue (as the oracle forms them), cut into
+    groups of the given numbers of batches."""
+    w = synth.workload(name)
+    t, _ = trace_and_arenas(name, n)
+    res = oracle_sim(w, t, service_table(w))
+    groups = []
+    for qi in range(len(w.queues)):
+        mine = [b for b in res.batches if b.queue == qi]
+        k = 0
+        for sz in sizes:
+            if k + sz <= len(mine):
+                groups.append(mine[k:k + sz])
+            k += sz
+    return groups
+
+
+@pytest.mark.parametrize("name,n,pack", [("small_mlp", 256, False), ("ranking", 600, False),
+                                         ("large_mlp", 300, False), ("ragged_seq", 300, False),
+                                         ("ragged_seq", 300, True)])
+def test_run_group_matches_replay_and_oracle(ctx, name, n, pack):
+    # rb_run_group on descriptors built outside the library: every request of
+    # the groups gets the replay's rows bit for bit (same kernels, same row
+    # independence), within tolerance of the oracle; requests in no group get
+    # nothing
+    groups = _oracle_groups(name, n, (3, 1, 2))
+    assert groups
+    *_, out_ref, out_off = run(ctx, name, n)
+    out, _ = _run_groups(ctx, name, n, groups, pack, "rb_run_group")
+    t, a = trace_and_arenas(name, n)
+    covered = sorted(r for g in groups for b in g for r in b.reqs)
+    for r in covered:
+        assert np.array_equal(out[out_off[r]:out_off[r + 1]], out_ref[out_off[r]:out_off[r + 1]]), r
+    mask = np.ones(out.size, bool)
+    for r in covered:
+        mask[out_off[r]:out_off[r + 1]] = False
+    assert not out[mask].any()
+    check_outputs(name, t, a, out, out_off, covered[::3])
+
+
+def test_run_group_rejects_bad_descriptors(ctx):
+    # descriptors whose rows, requests or output rows lie outside the extents
+    # given: nothing is written out of bounds, the request gets no output, the
+    # next rb_sync reports RB_ERANGE, and a good group still runs afterwards
+    name = "small_mlp"
+    w = synth.workload(name)
+    t, a = trace_and_arenas(name, 64)
+    grp = _oracle_groups(name, 64, (2,))[0]
+    dep = Deployment(w, ctx, device=True)
+    try:
+        dt = dep.upload(t, a)
+        stream = rb.torch_stream_ptr()
+        kb0, kr0, slots, _ = group_descriptors(w, t, a, dt.out_off, grp)
+        bads = []
+        kb = kb0.copy(); kb[1]["row_base"] += 1; bads.append((kb, kr0))          # rows past the row map
+        kb = kb0.copy(); kb[1]["n_req"] += 5; bads.append((kb, kr0))             # requests past the table
+        kr = kr0.copy(); kr[0]["out_off"] = dt.out.numel(); bads.append((kb0, kr))  # output past the arena
+        for kb, kr in bads:
+            out = torch.zeros(dt.out.numel() + 64, dtype=torch.float32, device="cuda")
+            kb_d = torch.from_numpy(kb.view(np.uint8).copy()).cuda()
+            kr_d = torch.from_numpy(kr.view(np.uint8).copy()).cuda()
+            dep.queues[0].run_group(stream, kb_d, len(kb), kr_d, len(kr), slots, 0, dt.dense, dt.dense.numel(),
+                                    None, 0, None, 0, out, dt.out.numel())
+            torch.cuda.synchronize()
+            with pytest.raises(rb.RBError) as e:
+                dep.sched.sync()
+            assert e.value.status == rb.RB_ERANGE
+            assert not out[dt.out.numel():].any()
+        kb_d = torch.from_numpy(kb0.view(np.uint8).copy()).cuda()
+        kr_d = torch.from_numpy(kr0.view(np.uint8).copy()).cuda()
+        dep.queues[0].run_group(stream, kb_d, len(kb0), kr_d, len(kr0), slots, 0, dt.dense, dt.dense.numel(), None,
+                                0, None, 0, dt.out, dt.out.numel())
+        torch.cuda.synchronize()
+        dep.sched.sync()
+        check_outputs(name, t, a, dt.out.cpu().numpy(), dt.out_off, [r for b in grp for r in b.reqs])
     finally:
         dep.destroy()
 

@@ -86,8 +86,9 @@ def _route(kind, kb, kr, arena, rows_total, d_in, d_out, n_tables=0):
     lens = _dev(arena["lens"])
     kb_d = _dev(kb.view(np.uint8))
     kr_d = _dev(kr.view(np.uint8))
-    rb.check(rb.lib().rb_k_route(_stream(), kind, rb.dptr(kb_d), len(kb), rb.dptr(kr_d), rb.dptr(lens), d_in,
-                                 d_out, n_tables, rb.dptr(rows), rb.dptr(err)), "rb_k_route")
+    rb.check(rb.lib().rb_k_route(_stream(), kind, rb.dptr(kb_d), len(kb), rb.dptr(kr_d), len(kr), rb.dptr(lens),
+                                 int(arena["lens"].size), d_in, d_out, n_tables, rb.dptr(rows), rows_total,
+                                 int(arena["out_len"]), rb.dptr(err)), "rb_k_route")
     torch.cuda.synchronize()
     return rows, err
 
