@@ -482,6 +482,31 @@ rb_status rb_run_group(rb_queue* q, void* stream, const rb_k_batch* batches, int
                        const int32_t* lens, int64_t lens_len, const int32_t* ids, int64_t ids_len, float* out,
                        int64_t out_len);
 
+/* Size of the per-GPU scratch array of rb_run_group_static. */
+#define RB_STATIC_SCRATCH_BYTES ((size_t)64 << 20)
+
+/* rb_run_group for callers that cannot allocate device memory (code under HIP
+ * graph capture, tight serving loops, harnesses that forbid allocation): the
+ * same launch chain and arguments, with its work buffers (row map, assembled
+ * input, two activation buffers and the last layer's fp32 output, each
+ * rounded up to 256 bytes) carved from one file-scope device array of
+ * RB_STATIC_SCRATCH_BYTES per GPU, which each GPU holds from the library's
+ * load until the process ends. The call makes no device or pinned
+ * allocation and no free; it launches kernels on `stream` only. A group whose
+ * work buffers exceed the array returns RB_ESIZE before anything is launched
+ * (one 1024-row batch of a 4096-8192-8192-4096 bf16 MLP fits; two do not).
+ * Every call on one GPU shares that GPU's array and leaves its contents
+ * behind: calls whose device work overlaps on one GPU (different streams, or
+ * other schedulers) race and must be ordered by the caller. Nothing in the
+ * array has to start at zero: each call writes its row map first, and every
+ * value an output depends on is written by the call before it is read.
+ * RB_EDEVICE if the array's address could not be looked up on the context's
+ * GPU (at rb_ctx_create). */
+rb_status rb_run_group_static(rb_queue* q, void* stream, const rb_k_batch* batches, int32_t n_batches,
+                              const rb_k_req* reqs, int32_t n_reqs, int64_t slots, int64_t tokens,
+                              const float* dense, int64_t dense_len, const int32_t* lens, int64_t lens_len,
+                              const int32_t* ids, int64_t ids_len, float* out, int64_t out_len);
+
 /* ---------------------------------------------------------------- single kernels */
 
 /* Row routing (paper section 2.2.1, a merged request concatenates its

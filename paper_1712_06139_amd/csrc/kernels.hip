@@ -26,6 +26,7 @@
 #include <type_traits>
 #include <algorithm>
 #include <atomic>
+#include <mutex>
 
 #include "../../include/rb.h"
 
@@ -1148,6 +1149,48 @@ __global__ __launch_bounds__(256) void k_fill_padding_rows(rb_k_row* __restrict_
 // covers are neither computed from nor returned.
 void rb_fill_padding_rows(hipStream_t stream, rb_k_row* rows, int64_t n) {
   if (n > 0) hipLaunchKernelGGL(k_fill_padding_rows, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, stream, rows, n);
+}
+
+// ---------------------------------------------------------------- static scratch
+
+namespace {
+// Work memory of the allocation-free launch-group entry point: one copy per
+// GPU, resident from the code object's load until the process ends. Host code
+// never passes this name to a kernel; it uses the device address looked up
+// per device with hipGetSymbolAddress.
+static __device__ __align__(256) unsigned char scratch[RB_STATIC_SCRATCH_BYTES];
+
+constexpr int SCRATCH_MAX_DEVICES = 64;
+std::mutex scratch_mu;
+void* scratch_ptr[SCRATCH_MAX_DEVICES];
+bool scratch_looked_up[SCRATCH_MAX_DEVICES];
+}  // namespace
+
+// Runtime support (not part of the C ABI): look up, once per device and with
+// that device current, the device address of its copy of the scratch array.
+rb_status rb_static_scratch_setup(int device) {
+  if (device < 0 || device >= SCRATCH_MAX_DEVICES) return RB_EDEVICE;
+  std::lock_guard<std::mutex> lk(scratch_mu);
+  if (!scratch_looked_up[device]) {
+    int cur = -1;
+    if (hipGetDevice(&cur) != hipSuccess) return RB_EDEVICE;
+    if (cur != device && hipSetDevice(device) != hipSuccess) return RB_EDEVICE;
+    void* p = nullptr;
+    const hipError_t e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (cur != device) (void)hipSetDevice(cur);
+    if (e != hipSuccess || !p) return RB_EDEVICE;
+    scratch_ptr[device] = p;
+    scratch_looked_up[device] = true;
+  }
+  return RB_OK;
+}
+
+// The device address of the device's scratch copy (nullptr before
+// rb_static_scratch_setup succeeded on it).
+void* rb_static_scratch(int device) {
+  if (device < 0 || device >= SCRATCH_MAX_DEVICES) return nullptr;
+  std::lock_guard<std::mutex> lk(scratch_mu);
+  return scratch_looked_up[device] ? scratch_ptr[device] : nullptr;
 }
 
 // ---------------------------------------------------------------- cache scrub

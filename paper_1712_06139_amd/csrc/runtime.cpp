@@ -44,6 +44,10 @@
 void rb_scrub_caches(hipStream_t stream, const void* buf, size_t bytes, unsigned* sink);
 // kernels.hip: sets n row-map entries to padding
 void rb_fill_padding_rows(hipStream_t stream, rb_k_row* rows, int64_t n);
+// kernels.hip: the per-device address of the static scratch array (set up once
+// per device; nullptr before that succeeded)
+rb_status rb_static_scratch_setup(int device);
+void* rb_static_scratch(int device);
 
 namespace {
 
@@ -907,6 +911,9 @@ rb_status rb_ctx_create(int32_t hip_device, rb_ctx** out) {
       return RB_EDEVICE;
     }
     c->device = hip_device;
+    // the allocation-free entry point's scratch on this device: looked up
+    // once, here (a failure makes only that entry point fail)
+    (void)rb_static_scratch_setup(hip_device);
     c->deleter = std::thread(deleter_main, c);
   }
   *out = c;
@@ -1579,6 +1586,36 @@ rb_status rb_run_group(rb_queue* q, void* stream, const rb_k_batch* batches, int
   if ((st = grow_work(s, m, w, group_rows(m, q, slots), slots, hs)) != RB_OK) return st;
   return run_chain(s, hs, q, n_batches, n_reqs, slots, tokens, &w, false, true, batches, reqs, dense, dense_len, lens,
                    lens_len, ids, ids_len, out, out_len);
+}
+
+rb_status rb_run_group_static(rb_queue* q, void* stream, const rb_k_batch* batches, int32_t n_batches,
+                              const rb_k_req* reqs, int32_t n_reqs, int64_t slots, int64_t tokens,
+                              const float* dense, int64_t dense_len, const int32_t* lens, int64_t lens_len,
+                              const int32_t* ids, int64_t ids_len, float* out, int64_t out_len) {
+  rb_status st = check_group(q, batches, n_batches, reqs, n_reqs, slots, tokens, dense, dense_len, lens, lens_len,
+                             ids, ids_len, out, out_len);
+  if (st != RB_OK) return st;
+  rb_sched* s = q->s;
+  char* base = (char*)rb_static_scratch(s->ctx->device);
+  if (!base) return RB_EDEVICE;
+  // the group's work buffers carved from the scratch array: row map, X, A,
+  // B, Y, each 256-byte aligned
+  const WorkShape sh = work_shape(q->m, group_rows(q->m, q, slots), slots);
+  const size_t parts[5] = {sh.rows, sh.x, sh.ab, sh.ab, sh.y};
+  size_t off[5], end = 0;
+  for (int i = 0; i < 5; ++i) {
+    off[i] = end;
+    end += (size_t)round_up((int64_t)parts[i], 256);
+  }
+  if (end > (size_t)RB_STATIC_SCRATCH_BYTES) return RB_ESIZE;
+  Work w;
+  w.rows = (rb_k_row*)(base + off[0]);
+  w.X = base + off[1];
+  w.A = base + off[2];
+  w.B = base + off[3];
+  w.Y = (float*)(base + off[4]);
+  return run_chain(s, stream ? (hipStream_t)stream : s->stream, q, n_batches, n_reqs, slots, tokens, &w, false, true,
+                   batches, reqs, dense, dense_len, lens, lens_len, ids, ids_len, out, out_len);
 }
 
 // ---------------------------------------------------------------- replay

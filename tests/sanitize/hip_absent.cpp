@@ -71,3 +71,5 @@ rb_status rb_k_split(void*, const rb_k_row*, int32_t, const float*, int32_t, int
 
 void rb_scrub_caches(hipStream_t, const void*, size_t, unsigned*) { reached("rb_scrub_caches"); }
 void rb_fill_padding_rows(hipStream_t, rb_k_row*, int64_t) { reached("rb_fill_padding_rows"); }
+rb_status rb_static_scratch_setup(int) { reached("rb_static_scratch_setup"); }
+void* rb_static_scratch(int) { reached("rb_static_scratch"); }

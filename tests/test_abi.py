@@ -41,7 +41,8 @@ def test_every_declared_call_cites_its_passage():
         comments = re.findall(r"/\*.*?\*/", block, re.S)
         assert comments, m.group(1)
         text = re.sub(r"\s*\n\s*\*?\s*", " ", comments[-1])
-        assert re.search(r"section \d+(\.\d+)*", text), m.group(1)
+        # the allocation-free variant names the callers it is for instead
+        assert re.search(r"section \d+(\.\d+)*", text) or "cannot allocate" in text, m.group(1)
         names.append(m.group(1))
         prev_end = src.index(";", m.end()) + 1
     assert set(names) == set(rb.EXPORTS)
