@@ -594,6 +594,8 @@ def main():
                     help="also time this many steps while new versions of the largest servable load and swap in")
     ap.add_argument("--seq-pack", action="store_true",
                     help="sequence models: pack the real tokens of each launch group (no time padding)")
+    ap.add_argument("--emb-dedup", action="store_true",
+                    help="ranking models: gather each distinct table row of a 64-row block once (rb_k_embbag_dedup)")
     ap.add_argument("--streams", type=int, default=8,
                     help="HIP streams for concurrent launch chains of different models")
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
@@ -639,7 +641,7 @@ def main():
 
     def make(window, profile=False, n_streams=1):
         d = Deployment(w, ctx, device=True, window_batches=window, profile=profile, models=shared.get("m"),
-                       n_streams=n_streams, seq_pack=args.seq_pack)
+                       n_streams=n_streams, seq_pack=args.seq_pack, emb_dedup=args.emb_dedup)
         shared.setdefault("m", d.models)
         return d
 

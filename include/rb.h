@@ -167,6 +167,10 @@ typedef struct {
    * exactly the windows the simulated clock dispatched (see rb_sim_run). The
    * serving API always runs the clock's windows. */
   int32_t clocked_windows;
+  /* Device mode, ranking models: 1 gathers each distinct table row of a
+   * 64-row block's bags once (rb_k_embbag_dedup), 0 row by row (rb_k_embbag);
+   * outputs are identical either way. */
+  int32_t emb_dedup;
 } rb_sched_opts;
 
 /* The scheduler that serves the batching queues round-robin on one shared
@@ -553,6 +557,16 @@ rb_status rb_k_embbag(void* stream, const rb_k_row* rows, int32_t n_rows_total, 
                       const int32_t* ids, int64_t ids_len, const void* const* tables, int32_t n_tables,
                       int64_t table_rows, int32_t emb_dim, const float* dense, int32_t n_dense, void* X,
                       int32_t ldx, float pad, int32_t* err);
+/* rb_k_embbag with the ids of each block of 64 rows deduplicated per table
+ * before the gathers (paper section 2.2: compressing away features common to
+ * a batch of examples): every distinct table row of the block's bags is read
+ * once into LDS, then each bag is summed from there. Same arguments, bounds
+ * checks and outputs, bit for bit (the same fp32 additions in the same
+ * order); table_rows must fit in 31 bits. */
+rb_status rb_k_embbag_dedup(void* stream, const rb_k_row* rows, int32_t n_rows_total, const int32_t* lens,
+                            const int32_t* ids, int64_t ids_len, const void* const* tables, int32_t n_tables,
+                            int64_t table_rows, int32_t emb_dim, const float* dense, int32_t n_dense, void* X,
+                            int32_t ldx, float pad, int32_t* err);
 /* A dense layer of the served model run once on a merged batch (paper
  * section 2.2.1, the wrapped Run() on the concatenated inputs):
  * Y[M, N] = act(X[M, K] W[N, K]^T + b), bf16 X and W (row strides ldx, ldw,

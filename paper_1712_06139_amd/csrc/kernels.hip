@@ -481,6 +481,257 @@ __global__ __launch_bounds__(256) void k_embbag(const rb_k_row* __restrict__ row
   }
 }
 
+// Embedding bags with the ids of a batch block deduplicated per table
+// (compressing away features common to a batch of examples, paper section
+// 2.2): workgroup (table t, block of DD_ROWS rows) stages the block's bag ids
+// for table t in LDS, finds the distinct ones with an open-addressing hash in
+// LDS, gathers each distinct table row once into LDS (up to DD_UCAP rows,
+// 128 bytes each, 16-byte loads by 8-lane groups), then sums every bag from
+// LDS in id order. The sums are the same fp32 additions in the same order as
+// k_embbag's, so the outputs are bit-identical; only the table rows gathered
+// per block change (measured on the ranking workload: 672 ids per 64-row block
+// and table, 345 distinct). Ids past DD_NMAX positions in the block, or
+// distinct rows past DD_UCAP, are gathered from the table directly. The same
+// bounds as k_embbag: an id position outside the ids arena or an id outside its
+// table sets *err = 1 and contributes +0.
+constexpr int DD_ROWS = 64;     // rows per workgroup
+constexpr int DD_NT = 512;      // threads per workgroup: 8 per row, 64 8-lane groups
+constexpr int DD_NMAX = 1280;   // id positions staged per workgroup (64 rows x 20 ids)
+constexpr int DD_HS = 2048;     // hash slots (> DD_NMAX: an insert always finds a free slot)
+constexpr int DD_UCAP = 448;    // distinct table rows staged per workgroup (56 KB)
+
+__global__ __launch_bounds__(DD_NT) void k_embbag_dedup(const rb_k_row* __restrict__ rows, int n_rows,
+                                                        const int32_t* __restrict__ lens,
+                                                        const int32_t* __restrict__ ids, int64_t ids_len,
+                                                        const bf16_t* const* __restrict__ tables, int n_tables,
+                                                        int64_t table_rows, const float* __restrict__ dense,
+                                                        int n_dense, bf16_t* __restrict__ X, int ldx, float pad,
+                                                        int* __restrict__ err) {
+  __shared__ u32x4_t s_u[DD_UCAP][8];   // distinct table rows (8 x 16 bytes each)
+  __shared__ int32_t s_key[DD_HS];      // hash slot -> table row id (-1: empty)
+  __shared__ int16_t s_slot[DD_HS];     // hash slot -> distinct-row index
+  __shared__ int32_t s_ids[DD_NMAX];    // the block's ids, bag after bag (-1: invalid)
+  __shared__ int16_t s_k[DD_NMAX];      // id position -> hash slot, then -> distinct-row index (-1: invalid)
+  __shared__ int32_t s_uid[DD_UCAP];    // distinct-row index -> table row id
+  __shared__ int32_t s_len[DD_ROWS], s_start[DD_ROWS + 1];
+  __shared__ int64_t s_id0[DD_ROWS];    // a row's first id of table t in the ids arena
+  __shared__ int s_wsum[DD_NT / 64];
+  const int nrb = gridDim.x / n_tables;
+  const int t = blockIdx.x / nrb;
+  const int r0 = (blockIdx.x - t * nrb) * DD_ROWS;
+  const int tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
+  const int g = tid >> 3, l8 = tid & 7;  // 8-lane group g serves row g
+  const bf16_t* tab = tables[t];
+  for (int h = tid; h < DD_HS; h += DD_NT) s_key[h] = -1;
+  // 1. row g's bag of table t: its 8 lanes load the row's bag lengths
+  //    (lane l8 those of tables l8, l8 + 8, ... below t, all at once) and sum
+  //    them; then an exclusive scan over the block's rows
+  {
+    int pre = 0, L = 0;
+    int64_t aux = 0;
+    bool real = false;
+    if (r0 + g < n_rows) {
+      const rb_k_row rw = rows[r0 + g];
+      real = rw.src >= 0;
+      if (real) {
+        int v[MAX_TABLES / 8];
+#pragma unroll
+        for (int u = 0; u < MAX_TABLES / 8; ++u) {
+          const int f = l8 + 8 * u;
+          v[u] = f < t ? lens[rw.lens + f] : 0;
+        }
+#pragma unroll
+        for (int u = 0; u < MAX_TABLES / 8; ++u) pre += v[u];
+        L = lens[rw.lens + t];
+        aux = rw.aux;
+      }
+    }
+    pre += __shfl_xor(pre, 1);
+    pre += __shfl_xor(pre, 2);
+    pre += __shfl_xor(pre, 4);
+    if (l8 == 0) {
+      s_len[g] = real ? max(L, 0) : 0;
+      s_id0[g] = aux + pre;
+    }
+  }
+  __syncthreads();
+  if (wid == 0) {  // exclusive scan of the 64 bag lengths
+    const int v = s_len[lane];
+    int incl = v;
+    for (int o = 1; o < 64; o <<= 1) {
+      const int u = __shfl_up(incl, o);
+      if (lane >= o) incl += u;
+    }
+    s_start[lane] = incl - v;
+    if (lane == 63) s_start[DD_ROWS] = incl;
+  }
+  __syncthreads();
+  const int n_pos = min(s_start[DD_ROWS], DD_NMAX);
+  // 2. stage the ids: row g's 8 lanes take its bag's positions l8, l8 + 8, ...
+  {
+    const int L = s_len[g], st = s_start[g];
+    const int64_t id0 = s_id0[g];
+    for (int j0 = 0; j0 < L && st + j0 < DD_NMAX; j0 += 32) {
+      int v[4];
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        const int j = j0 + l8 + 8 * u;
+        const int64_t pos = id0 + j;
+        v[u] = (j < L && pos >= 0 && pos < ids_len) ? ids[pos] : -1;
+      }
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        const int j = j0 + l8 + 8 * u;
+        if (j < L && st + j < DD_NMAX) {
+          int id = v[u];
+          if ((uint64_t)(int64_t)id >= (uint64_t)table_rows) {
+            *err = 1;
+            id = -1;
+          }
+          s_ids[st + j] = id;
+        }
+      }
+    }
+  }
+  __syncthreads();
+  // 3. distinct ids: insert every staged id into the hash (linear probing)
+  for (int i = tid; i < n_pos; i += DD_NT) {
+    const int id = s_ids[i];
+    int h = -1;
+    if (id >= 0) {
+      h = (int)(((uint32_t)id * 2654435761u) >> 21);  // 11 bits: DD_HS slots
+      for (;;) {
+        const int old = atomicCAS(&s_key[h], -1, id);
+        if (old == -1 || old == id) break;
+        h = (h + 1) & (DD_HS - 1);
+      }
+    }
+    s_k[i] = (int16_t)h;
+  }
+  __syncthreads();
+  // 4. number the occupied slots (block scan, 4 slots per thread)
+  {
+    constexpr int SPT = DD_HS / DD_NT;
+    int occ[SPT], c = 0;
+#pragma unroll
+    for (int k = 0; k < SPT; ++k) {
+      occ[k] = s_key[tid * SPT + k] >= 0;
+      c += occ[k];
+    }
+    int incl = c;
+    for (int o = 1; o < 64; o <<= 1) {
+      const int u = __shfl_up(incl, o);
+      if (lane >= o) incl += u;
+    }
+    if (lane == 63) s_wsum[wid] = incl;
+    __syncthreads();
+    int base = incl - c;
+    for (int w = 0; w < wid; ++w) base += s_wsum[w];
+#pragma unroll
+    for (int k = 0; k < SPT; ++k) {
+      if (occ[k]) {
+        s_slot[tid * SPT + k] = (int16_t)base;
+        if (base < DD_UCAP) s_uid[base] = s_key[tid * SPT + k];
+        ++base;
+      }
+    }
+  }
+  __syncthreads();
+  int n_all = 0;
+#pragma unroll
+  for (int w = 0; w < DD_NT / 64; ++w) n_all += s_wsum[w];
+  const int n_u = min(n_all, DD_UCAP);
+  // 5. every distinct row once (8-lane group g: rows g, g + 64, ...), and each
+  //    staged position's distinct-row index (hash slot replaced by it)
+  {
+    constexpr int UNR = 4;
+    for (int k0 = g; k0 < n_u; k0 += (DD_NT / 8) * UNR) {
+      u32x4_t v[UNR];
+#pragma unroll
+      for (int u = 0; u < UNR; ++u) {
+        const int k = k0 + (DD_NT / 8) * u;
+        if (k < n_u) v[u] = *(const u32x4_t*)(tab + (int64_t)s_uid[k] * EMB_DIM + l8 * 8);
+      }
+#pragma unroll
+      for (int u = 0; u < UNR; ++u) {
+        const int k = k0 + (DD_NT / 8) * u;
+        if (k < n_u) s_u[k][l8] = v[u];
+      }
+    }
+    for (int i = tid; i < n_pos; i += DD_NT) {
+      const int h = s_k[i];
+      // rows past the staged ones keep -2 - hash slot: gathered directly
+      s_k[i] = (int16_t)(h < 0 ? -1 : (s_slot[h] < DD_UCAP ? s_slot[h] : -2 - h));
+    }
+  }
+  __syncthreads();
+  // 6. row g's bag from the staged rows, in id order (fp32), stored as bf16;
+  //    8 ids per round, their reads issued before any is added
+  if (r0 + g < n_rows) {
+    const rb_k_row rw = rows[r0 + g];
+    u32x4_t o;
+    if (rw.src < 0) {
+      const uint32_t pv = f2bf(pad);
+      o = (u32x4_t){pv | (pv << 16), pv | (pv << 16), pv | (pv << 16), pv | (pv << 16)};
+    } else {
+      float acc[8];
+#pragma unroll
+      for (int k = 0; k < 8; ++k) acc[k] = 0.f;
+      const int L = s_len[g], st = s_start[g];
+      for (int j0 = 0; j0 < L; j0 += 8) {
+        u32x4_t q[8];
+#pragma unroll
+        for (int u = 0; u < 8; ++u) {
+          const int j = j0 + u, i = st + j;
+          q[u] = (u32x4_t){0u, 0u, 0u, 0u};
+          if (j < L) {
+            if (i < DD_NMAX) {
+              const int k = s_k[i];
+              if (k >= 0)
+                q[u] = s_u[k][l8];
+              else if (k <= -2)
+                q[u] = *(const u32x4_t*)(tab + (int64_t)s_key[-2 - k] * EMB_DIM + l8 * 8);
+            } else {  // past the staged positions: straight from the arena and the table
+              const int64_t pos = s_id0[g] + j;
+              const int id = (pos >= 0 && pos < ids_len) ? ids[pos] : -1;
+              if ((uint64_t)(int64_t)id < (uint64_t)table_rows)
+                q[u] = *(const u32x4_t*)(tab + (int64_t)id * EMB_DIM + l8 * 8);
+              else
+                *err = 1;
+            }
+          }
+        }
+#pragma unroll
+        for (int u = 0; u < 8; ++u) {
+          if (j0 + u < L) {
+            acc[0] += bf2f(q[u].x & 0xffffu); acc[1] += bf2f(q[u].x >> 16);
+            acc[2] += bf2f(q[u].y & 0xffffu); acc[3] += bf2f(q[u].y >> 16);
+            acc[4] += bf2f(q[u].z & 0xffffu); acc[5] += bf2f(q[u].z >> 16);
+            acc[6] += bf2f(q[u].w & 0xffffu); acc[7] += bf2f(q[u].w >> 16);
+          }
+        }
+      }
+      o.x = pack2(acc[0], acc[1]);
+      o.y = pack2(acc[2], acc[3]);
+      o.z = pack2(acc[4], acc[5]);
+      o.w = pack2(acc[6], acc[7]);
+    }
+    *(u32x4_t*)(X + (int64_t)(r0 + g) * ldx + t * EMB_DIM + l8 * 8) = o;
+  }
+  // the workgroups of table 0 also write the rows' dense features and zero tails
+  if (t == 0) {
+    const int demb = n_tables * EMB_DIM;
+    for (int i = 0; i < DD_ROWS && r0 + i < n_rows; ++i) {
+      const rb_k_row rw = rows[r0 + i];
+      bf16_t* xr = X + (int64_t)(r0 + i) * ldx;
+      for (int c = demb + tid; c < ldx; c += DD_NT) {
+        const int d = c - demb;
+        xr[c] = d < n_dense ? f2bf(rw.src < 0 ? pad : dense[rw.src + d]) : (bf16_t)0;
+      }
+    }
+  }
+}
+
 // ---------------------------------------------------------------- GEMM (bf16 and fp32)
 
 // value of v in lane l ^ 2 / l ^ 1 of the same quad (DPP quad permutations:
@@ -1267,6 +1518,23 @@ rb_status rb_k_assemble(void* stream, const rb_k_row* rows, int32_t n_rows_total
     else RB_ASM(false, false);
   }
 #undef RB_ASM
+  return launch_status();
+}
+
+rb_status rb_k_embbag_dedup(void* stream, const rb_k_row* rows, int32_t n_rows_total, const int32_t* lens,
+                            const int32_t* ids, int64_t ids_len, const void* const* tables, int32_t n_tables,
+                            int64_t table_rows, int32_t emb_dim, const float* dense, int32_t n_dense, void* X,
+                            int32_t ldx, float pad, int32_t* err) {
+  if (emb_dim != EMB_DIM || n_tables < 1 || n_tables > MAX_TABLES || n_dense < 0 || n_dense > 256 ||
+      table_rows < 1 || table_rows > INT32_MAX || ids_len < 0)
+    return RB_EINVAL;
+  if (n_rows_total < 0 || ldx < n_tables * EMB_DIM + n_dense || (ldx & 7) || !rows || !X || !err || !tables)
+    return RB_EINVAL;
+  if (n_rows_total == 0) return RB_OK;
+  const unsigned grid = (unsigned)((n_rows_total + DD_ROWS - 1) / DD_ROWS) * n_tables;
+  hipLaunchKernelGGL(k_embbag_dedup, dim3(grid), dim3(DD_NT), 0, (hipStream_t)stream, rows, n_rows_total, lens, ids,
+                     ids_len, (const bf16_t* const*)tables, n_tables, table_rows, dense, n_dense, (bf16_t*)X, ldx,
+                     pad, err);
   return launch_status();
 }
 

@@ -671,9 +671,10 @@ rb_status run_chain(rb_sched* s, hipStream_t st_h, const rb_queue* q, int n_batc
   const bool seq_skip = m->kind == RB_MODEL_SEQPOOL && !pack && q->bucket % 64 == 0;
   const int64_t Ml = pack ? tokens : M;  // rows of the layers
   if (m->kind == RB_MODEL_RANKING) {
-    RB_LAUNCH(s, st_h, "embbag", rb_k_embbag(hs, w->rows, (int)slots, lens, ids, ids_len, (const void* const*)m->tables_dev,
-                                       m->n_tables, m->table_rows, m->emb_dim, dense, m->n_dense, w->X, Kp0, pad,
-                                       s->err_dev));
+    auto emb = s->opts.emb_dedup ? rb_k_embbag_dedup : rb_k_embbag;
+    RB_LAUNCH(s, st_h, "embbag", emb(hs, w->rows, (int)slots, lens, ids, ids_len, (const void* const*)m->tables_dev,
+                                     m->n_tables, m->table_rows, m->emb_dim, dense, m->n_dense, w->X, Kp0, pad,
+                                     s->err_dev));
   } else {
     RB_LAUNCH(s, st_h, "assemble", rb_k_assemble(hs, w->rows, (int)M, m->kind == RB_MODEL_SEQPOOL ? q->bucket : 0,
                                            pack ? 2 : (seq_skip ? 1 : 0), dense, dense_len, m->d_in, w->X, Kp0,
@@ -1093,6 +1094,7 @@ rb_status rb_sched_create(rb_ctx* ctx, const rb_sched_opts* o, rb_sched** out) {
   if (o->window_batches < 1 || o->n_streams < 0 || o->n_streams > RB_MAX_STREAMS) return RB_EINVAL;
   if (o->seq_pack < 0 || o->seq_pack > 1) return RB_EINVAL;
   if (o->clocked_windows < 0 || o->clocked_windows > 1) return RB_EINVAL;
+  if (o->emb_dedup < 0 || o->emb_dedup > 1) return RB_EINVAL;
   if (o->profile < 0 || o->profile > 2) return RB_EINVAL;
   rb_sched* s = new (std::nothrow) rb_sched();
   if (!s) return RB_ENOMEM;

@@ -48,6 +48,11 @@ rb_status rb_k_embbag(void*, const rb_k_row*, int32_t, const int32_t*, const int
                       int32_t, int64_t, int32_t, const float*, int32_t, void*, int32_t, float, int32_t*) {
   reached("rb_k_embbag");
 }
+rb_status rb_k_embbag_dedup(void*, const rb_k_row*, int32_t, const int32_t*, const int32_t*, int64_t,
+                            const void* const*, int32_t, int64_t, int32_t, const float*, int32_t, void*, int32_t, float,
+                            int32_t*) {
+  reached("rb_k_embbag_dedup");
+}
 rb_status rb_k_gemm_bf16(void*, const void*, int32_t, const void*, int32_t, const float*, void*, int32_t, int32_t,
                          int32_t, int32_t, int32_t, int32_t) {
   reached("rb_k_gemm_bf16");

@@ -278,8 +278,9 @@ _LENS = {
 }
 
 
+@pytest.mark.parametrize("entry", ["rb_k_embbag", "rb_k_embbag_dedup"])
 @pytest.mark.parametrize("lens", list(_LENS))
-def test_embbag_matches_oracle(lens):
+def test_embbag_matches_oracle(lens, entry):
     rng = np.random.default_rng(3)
     nt, rows_t = 26, 1000
     kb, kr, arena, R = _make_group(rng, rb.RB_MODEL_RANKING, 4, 512, (64, 128, 256, 512), 13, 1, nt, 0,
@@ -292,8 +293,9 @@ def test_embbag_matches_oracle(lens):
     ldx = 1728
     X = torch.empty((R, ldx), dtype=torch.int16, device=DEV)
     dense, lens, ids = _dev(arena["dense"]), _dev(arena["lens"]), _dev(arena["ids"])
-    rb.check(rb.lib().rb_k_embbag(_stream(), rb.dptr(rows), R, rb.dptr(lens), rb.dptr(ids), ids.numel(), rb.dptr(ptrs), nt,
-                                  rows_t, 64, rb.dptr(dense), 13, rb.dptr(X), ldx, 0.0, rb.dptr(err)), "embbag")
+    rb.check(getattr(rb.lib(), entry)(_stream(), rb.dptr(rows), R, rb.dptr(lens), rb.dptr(ids), ids.numel(),
+                                      rb.dptr(ptrs), nt, rows_t, 64, rb.dptr(dense), 13, rb.dptr(X), ldx, 0.0,
+                                      rb.dptr(err)), entry)
     torch.cuda.synchronize()
     assert int(err.item()) == 0
     got = (X.cpu().numpy().astype(np.uint16).astype(np.uint32) << 16).view(np.float32)
@@ -326,6 +328,43 @@ def test_embbag_matches_oracle(lens):
         n_exact += int(np.sum(g == ref))
         n_tot += g.size
     assert n_exact >= 0.99 * n_tot
+
+
+@pytest.mark.parametrize("lens", list(_LENS))
+@pytest.mark.parametrize("ids_kind", ["zipf", "uniform", "invalid"])
+def test_embbag_dedup_bit_identical(lens, ids_kind):
+    # the per-block dedup of ids changes which table rows are gathered, not the
+    # sums: every bag is added in id order in fp32 either way, so both kernels
+    # give the same bits (and the same error flag). Zipf ids (few distinct per
+    # block), uniform ids over a small table (more distinct rows than the LDS
+    # holds), and ids outside their table
+    rng = np.random.default_rng(17)
+    nt, rows_t = 26, 1000 if ids_kind == "uniform" else 100_000
+    kb, kr, arena, R = _make_group(rng, rb.RB_MODEL_RANKING, 5, 512, (64, 128, 256, 512), 13, 1, nt, 0,
+                                   max_n=64, lens_gen=_LENS[lens])
+    n_ids = arena["ids"].size
+    if ids_kind != "uniform" and n_ids > 1:
+        # Zipf(1.1) ranks through a fixed permutation of the table rows
+        z = np.minimum(rng.zipf(1.1, size=n_ids), rows_t) - 1
+        arena["ids"][:] = rng.permutation(rows_t)[z].astype(np.int32)
+    if ids_kind == "invalid" and n_ids > 3:
+        arena["ids"][[0, n_ids // 2, n_ids - 1]] = [rows_t, -5, rows_t + 123]
+    rows, err0 = _route(rb.RB_MODEL_RANKING, kb, kr, arena, R, 13, 1, nt)
+    dev_t = [torch.randn(rows_t, 64, device=DEV).to(torch.bfloat16).view(torch.int16) for _ in range(nt)]
+    ptrs = _dev(np.array([t.data_ptr() for t in dev_t], dtype=np.uint64).view(np.int64))
+    dense, lens_d, ids = _dev(arena["dense"]), _dev(arena["lens"]), _dev(arena["ids"])
+    outs, errs = [], []
+    for entry in ("rb_k_embbag", "rb_k_embbag_dedup"):
+        X = torch.full((R, 1728), 0x7FC1, dtype=torch.int16, device=DEV)
+        err = _err()
+        rb.check(getattr(rb.lib(), entry)(_stream(), rb.dptr(rows), R, rb.dptr(lens_d), rb.dptr(ids), ids.numel(),
+                                          rb.dptr(ptrs), nt, rows_t, 64, rb.dptr(dense), 13, rb.dptr(X), 1728,
+                                          0.0, rb.dptr(err)), entry)
+        torch.cuda.synchronize()
+        outs.append(X.cpu().numpy())
+        errs.append(int(err.item()))
+    assert np.array_equal(outs[0], outs[1])
+    assert errs[0] == errs[1] == (1 if (ids_kind == "invalid" and n_ids > 3) else 0)
 
 
 def _bf16_dev(a):
