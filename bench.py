@@ -36,9 +36,11 @@ sys.path.insert(0, ROOT)
 
 METRIC = "examples/sec per MI355X (batched MLP/embedding model); p50/p99 request latency"
 HBM_PEAK_GBS = 8000.0
+# L2 read peak: 8 XCDs x 16 channels x 128 bytes per clock at 2.4 GHz
+L2_PEAK_GBS = 8 * 16 * 128 * 2.4
 BF16_PEAK_TFLOPS = 2500.0
 F32_PEAK_TFLOPS = 157.3
-KERNELS = ("route", "assemble", "embbag", "gemm_bf16", "gemm_f32", "head", "seqpool", "split")
+KERNELS = ("route", "assemble", "embbag", "gemm_bf16", "gemm_f32", "mlp_tail", "head", "seqpool", "split")
 
 DESCRIPTION = {
     "ranking": "ranking: 26 Zipf(1.1) embedding bags over 100k x 64 bf16 tables + 13 dense -> MLP "
@@ -64,7 +66,16 @@ def nearest_rank(v, q):
     return int(v[max(1, int(math.ceil(q * len(v)))) - 1])
 
 
-def algorithmic_work(w, t, a, logd, qindex, window):
+def fused_tail(m):
+    """With the fused tail on, the library runs a bf16 model's last two hidden
+    layers and its narrow head as one kernel (mlp_tail) when they are ReLU
+    layers of 512 and 256 outputs ahead of a 256-input head."""
+    L = m.layers
+    return (m.dtype == "bf16" and len(L) >= 4 and L[-1].fan_out == 1 and L[-3].fan_out == 512 and
+            L[-3].act == "relu" and L[-2].fan_out == 256 and L[-2].act == "relu")
+
+
+def algorithmic_work(w, t, a, logd, qindex, window, fused=False):
     """Algorithmic bytes / flops of one replay, per kernel. Real model
     dimensions; padded rows count as rows, since the method pads them and
     computes them. Sequence groups: padding tokens are not written by the
@@ -104,6 +115,9 @@ def algorithmic_work(w, t, a, logd, qindex, window):
             work["assemble"]["bytes"] += (int(n_dense[b]) * 4 + Mw * m.d_in * (2 if bf16 else 4)
                                           + (P if m.kind == "seqpool" else M) * row_desc)
         layers = m.layers[:-1] if (m.kind == "ranking" and bf16 and m.layers[-1].fan_out == 1) else m.layers
+        tail = fused and fused_tail(m)
+        if tail:
+            layers = m.layers[:-3]
         key = "gemm_bf16" if bf16 else "gemm_f32"
         Mg = int(n_dense[b]) // m.d_in if m.kind == "seqpool" else M  # rows the layers must compute
         # a launch group (one queue's batches in one launch window) reads each
@@ -117,7 +131,14 @@ def algorithmic_work(w, t, a, logd, qindex, window):
             work[key]["flops"] += 2 * Mg * L.fan_in * L.fan_out
             work[key]["bytes"] += ((Mg * L.fan_in + Mg * L.fan_out + (L.fan_in * L.fan_out if first_in_group else 0))
                                    * (2 if bf16 else 4))
-        if m.kind == "ranking" and len(layers) < len(m.layers):
+        if tail:
+            # hidden input, the two layers' and the head's weights once per
+            # launch group, one output per real row, the row map
+            l2, l3, hd = m.layers[-3], m.layers[-2], m.layers[-1]
+            work["mlp_tail"]["flops"] += 2 * P * (l2.fan_in * l2.fan_out + l3.fan_in * l3.fan_out + hd.fan_in)
+            wts = (l2.fan_in * l2.fan_out + l3.fan_in * l3.fan_out + hd.fan_in) * 2 if first_in_group else 0
+            work["mlp_tail"]["bytes"] += P * l2.fan_in * 2 + wts + s * 4 + P * row_desc
+        elif m.kind == "ranking" and len(layers) < len(m.layers):
             last = m.layers[-1]
             work["head"]["bytes"] += P * row_desc + P * last.fan_in * 2 + last.fan_in * 2 + s * 4
             work["head"]["flops"] += 2 * P * last.fan_in
@@ -128,6 +149,43 @@ def algorithmic_work(w, t, a, logd, qindex, window):
         else:
             work["split"]["bytes"] += P * row_desc + s * m.d_out * 8
     return work
+
+
+def embbag_figures(w, a, logd, window, e, sample_windows=4):
+    """Two bounds for the embedding-bag launches that hold where the plain
+    HBM one does not (table rows hit L2 and the Infinity Cache):
+      gathered bytes per launch (every id's 128-byte table row, as the
+      kernel reads them) against the L2 read peak, and
+      the launch's bytes with each distinct table row counted once per launch
+      window (a lower bound on what must come from HBM) against the HBM peak.
+    Distinct rows per window are counted on the host over the first
+    `sample_windows` windows and scaled by their share of the ids."""
+    m = next(m for m in w.models if m.kind == "ranking")
+    nt, dim = m.n_tables, m.emb_dim
+    nb = logd["n_batches"]
+    beg = logd["b_req_begin"][:nb + 1]
+    reqs = logd["b_reqs"][:beg[-1]]
+    launches = e["launches"]
+    ids_total = int(a.ids_off[-1])
+    gathered = ids_total * dim * 2 / launches
+    uniq = ids_s = 0
+    for wi in range(min(sample_windows, -(-nb // window))):
+        rs = reqs[beg[wi * window]:beg[min((wi + 1) * window, nb)]]
+        lens = np.concatenate([a.lens[a.lens_off[r]:a.lens_off[r + 1]] for r in rs]).astype(np.int64)
+        ids = np.concatenate([a.ids[a.ids_off[r]:a.ids_off[r + 1]] for r in rs]).astype(np.int64)
+        table = np.repeat(np.tile(np.arange(nt), lens.size // nt), lens)
+        uniq += np.unique(table << 32 | ids).size
+        ids_s += ids.size
+    per_launch = e["bytes_per_launch"]
+    unique_bytes = per_launch - gathered + (uniq / ids_s) * (ids_total / launches) * dim * 2
+    secs = e["avg_us"] * 1e-6
+    return {"gathered_bytes_per_launch": round(gathered), "l2_read_peak_gbs": L2_PEAK_GBS,
+            "gathered_gbs": round(gathered / secs / 1e9, 1), "l2_frac": round(gathered / secs / 1e9 / L2_PEAK_GBS, 4),
+            "distinct_rows_per_id": round(uniq / ids_s, 4),
+            "bytes_with_distinct_rows_once_per_launch": round(unique_bytes),
+            "distinct_gbs": round(unique_bytes / secs / 1e9, 1),
+            "hbm_frac_distinct": round(unique_bytes / secs / 1e9 / HBM_PEAK_GBS, 4),
+            "sample": f"distinct (table, id) pairs of the first {min(sample_windows, -(-nb // window))} launch windows"}
 
 
 def recorded_traffic(workload, kernel):
@@ -596,6 +654,8 @@ def main():
                     help="sequence models: pack the real tokens of each launch group (no time padding)")
     ap.add_argument("--emb-dedup", action="store_true",
                     help="ranking models: gather each distinct table row of a 64-row block once (rb_k_embbag_dedup)")
+    ap.add_argument("--fused-tail", action="store_true",
+                    help="run the ranking MLP's last two layers and head as one kernel (rb_k_mlp_tail)")
     ap.add_argument("--streams", type=int, default=8,
                     help="HIP streams for concurrent launch chains of different models")
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
@@ -641,7 +701,8 @@ def main():
 
     def make(window, profile=False, n_streams=1):
         d = Deployment(w, ctx, device=True, window_batches=window, profile=profile, models=shared.get("m"),
-                       n_streams=n_streams, seq_pack=args.seq_pack, emb_dedup=args.emb_dedup)
+                       n_streams=n_streams, seq_pack=args.seq_pack, emb_dedup=args.emb_dedup,
+                       fused_tail=args.fused_tail)
         shared.setdefault("m", d.models)
         return d
 
@@ -674,7 +735,7 @@ def main():
     pdep = make(args.window, profile=1)
     pdep.replay(dt)
     pdep.sched.sync()
-    work = algorithmic_work(w, t, a, logd, dep.qindex, args.window)
+    work = algorithmic_work(w, t, a, logd, dep.qindex, args.window, args.fused_tail)
     kernels = {}
     for k in KERNELS:
         n, ms = pdep.sched.kernel_stats(k)
@@ -703,10 +764,16 @@ def main():
             if wk.get("bytes"):
                 e["cold_gbs"] = round(wk["bytes"] / (ms * 1e-3) / 1e9, 1)
         cdep.destroy()
+    emb = None
+    if "embbag" in kernels:
+        ke = dict(kernels["embbag"])
+        ke["bytes_per_launch"] = work["embbag"]["bytes"] / ke["launches"]
+        emb = embbag_figures(w, a, logd, args.window, ke)
+        log(f"embbag: {json.dumps(emb)}")
     dom = max(kernels, key=lambda k: kernels[k]["total_ms"])
     dk, wk = kernels[dom], work[dom]
-    if dom.startswith("gemm"):
-        peak = BF16_PEAK_TFLOPS if dom == "gemm_bf16" else F32_PEAK_TFLOPS
+    if dom.startswith("gemm") or dom == "mlp_tail":
+        peak = F32_PEAK_TFLOPS if dom == "gemm_f32" else BF16_PEAK_TFLOPS
         ach = wk["flops"] / (dk["total_ms"] * 1e-3) / 1e12
         roof = {"bound": "mfma", "achieved": round(ach, 2), "peak": peak, "unit": "TFLOP/s",
                 "frac": round(ach / peak, 4)}
@@ -784,6 +851,7 @@ def main():
         "device_ms_per_step": round(dev_ms / args.steps, 3),
         "kernels": kernels,
         "roofline": roof,
+        **({"embbag_roofline": emb} if emb is not None else {}),
         "cpu_baseline": cpu,
         "serving_pcie": serving,
         **({"version_swap": swap} if swap is not None else {}),

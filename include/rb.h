@@ -171,6 +171,11 @@ typedef struct {
    * 64-row block's bags once (rb_k_embbag_dedup), 0 row by row (rb_k_embbag);
    * outputs are identical either way. */
   int32_t emb_dedup;
+  /* Device mode, bf16 models whose last two hidden layers are ReLU layers of
+   * 512 and 256 outputs ahead of a narrow head (the ranking MLP): 1 runs them
+   * and the head as one kernel (rb_k_mlp_tail), 0 as three; outputs are
+   * identical either way. */
+  int32_t fuse_mlp_tail;
 } rb_sched_opts;
 
 /* The scheduler that serves the batching queues round-robin on one shared
@@ -595,6 +600,18 @@ rb_status rb_k_gemm_f32(void* stream, const float* X, int32_t ldx, const float* 
  * w bf16 [K]. */
 rb_status rb_k_head(void* stream, const rb_k_row* rows, int32_t n_rows_total, const void* H, int32_t ldh,
                     const void* w, float b, int32_t K, int32_t act, float* out);
+/* The last two hidden layers and the narrow head of a bf16 MLP run once on a
+ * merged batch (paper section 2.2.1) and handed back to the callers (each
+ * caller gets its own rows), in one kernel per block of 128 rows:
+ * Y2 = relu(H1[:, :K2] W2^T + b2) (512 outputs, bf16), Y3 = relu(Y2 W3^T +
+ * b3) (256 outputs, bf16), out[rows[r].out] = act(Y3[r] . w4 + b4) for real
+ * rows (act RB_ACT_SIGMOID or RB_ACT_NONE). H1 bf16 [n_rows_total, ldh1];
+ * W2 bf16 [512, ldw2]; W3 bf16 [256, ldw3 >= 512]; w4 bf16 [256]; b2, b3 fp32.
+ * K2 % 32 == 0; row strides multiples of 8 and operands 16-byte aligned.
+ * Bit-identical to rb_k_gemm_bf16 twice and rb_k_head. */
+rb_status rb_k_mlp_tail(void* stream, const rb_k_row* rows, int32_t n_rows_total, const void* H1, int32_t ldh1,
+                        int32_t K2, const void* W2, int32_t ldw2, const float* b2, const void* W3, int32_t ldw3,
+                        const float* b3, const void* w4, float b4, int32_t act, float* out);
 /* A sequence model's pooling and head on a merged batch, unbatched per
  * sequence (paper section 2.2.1, sub-graph batching of sequence models with
  * Batch/Unbatch), fused with the split: per sequence slot r with L = rows[r].aux

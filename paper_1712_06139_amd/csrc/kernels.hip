@@ -1213,6 +1213,244 @@ __global__ __launch_bounds__(256) void k_head(const rb_k_row* __restrict__ rows,
   if (l == 0 && o >= 0) out[o] = act_fn<ACT>(s + b);
 }
 
+// ---------------------------------------------------------------- fused MLP tail
+
+// The last two hidden layers (ReLU, N2 = 512 then N3 = 256 outputs) and the
+// narrow head of a bf16 model, fused per block of MT_BM rows: the first layer's
+// k-steps stream H1 rows and W2 rows through two LDS stages; its outputs
+// (bias, ReLU, bf16) stay in LDS as the second layer's input while W3 streams
+// through two more stages; the second layer's outputs (bias, ReLU, bf16) go to
+// LDS and the head reads them there. Each output is accumulated in the same k
+// order with the same 32x32x16 bf16 MFMA as k_gemm_bf16, rounded the same way,
+// and the head sums exactly as k_head does (16 lanes per row, 8 consecutive
+// elements of every 128 per lane, then a 16-lane butterfly), so the results
+// are bit-identical to running the two layers and the head separately; only
+// the two hidden layers' round trips through memory and two launches go away.
+// 8 waves: 2 x 4 over the 128 x 512 tile of the first layer (64 x 128 each),
+// 2 x 4 over the 128 x 256 tile of the second (64 x 64 each). Operand rows of
+// 64 bytes per k-step sit in LDS with their four 16-byte chunks permuted by
+// row, and the 1024-byte rows of the first layer's output with their 64 chunks
+// permuted by row, so that a fragment read's 32 rows spread over the banks.
+constexpr int MT_BM = 128, MT_NT = 512, MT_N2 = 512, MT_N3 = 256, MT_KS = 32;
+constexpr int MT_A_BYTES = MT_BM * 64, MT_B_BYTES = MT_N2 * 64;           // one stage of the first layer
+constexpr int MT_Y2 = 0;                                                // [MT_BM][MT_N2] bf16, 128 KB
+constexpr int MT_W3 = MT_BM * MT_N2 * 2;                                // two stages of [MT_N3][64 B]
+constexpr int MT_LDS = MT_W3 + 2 * MT_N3 * 64;                          // 160 KB
+static_assert(2 * (MT_A_BYTES + MT_B_BYTES) <= MT_W3, "first-layer stages fit below the W3 stages");
+
+__device__ __forceinline__ uint32_t mt_addr4(int row, int c) { return (uint32_t)(row * 64 + ((c ^ ((row >> 2) & 3)) << 4)); }
+__device__ __forceinline__ uint32_t mt_addr_y2(int row, int c) { return (uint32_t)(row * 1024 + ((c ^ (row & 63)) << 4)); }
+
+template <int ACT>
+__global__ __launch_bounds__(MT_NT) void k_mlp_tail(const bf16_t* __restrict__ H1, int ldh1, int K2,
+                                                    const bf16_t* __restrict__ W2, int ldw2,
+                                                    const float* __restrict__ b2, const bf16_t* __restrict__ W3,
+                                                    int ldw3, const float* __restrict__ b3,
+                                                    const bf16_t* __restrict__ w4, float b4,
+                                                    const rb_k_row* __restrict__ rows, int M,
+                                                    float* __restrict__ out) {
+  __shared__ __align__(16) unsigned char lds[MT_LDS];
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wid = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int wm = wid >> 2, wn = wid & 3;
+  const int m0 = blockIdx.x * MT_BM;
+  const int lrow = tid >> 2, lc = tid & 3;  // the row (of 128) and chunk this thread loads
+  // ---- first layer: Y2 = relu(H1 W2^T + b2) on rows [m0, m0 + 128)
+  const bf16_t* a_src = H1 + (int64_t)(m0 + min(lrow, M - 1 - m0)) * ldh1 + lc * 8;  // rows past M: a copy
+  // k-step operands go global -> registers -> LDS, loaded two k-steps ahead
+  // into two register sets (the k loops are unrolled by two so that each set
+  // stays in registers)
+  struct Op1 {
+    u32x4_t a, b[4];
+  };
+  auto load1 = [&](Op1& r, int kt) {
+    const int k0 = kt * MT_KS;
+    r.a = *(const u32x4_t*)(a_src + k0);
+#pragma unroll
+    for (int i = 0; i < 4; ++i) r.b[i] = *(const u32x4_t*)(W2 + (int64_t)(lrow + 128 * i) * ldw2 + k0 + lc * 8);
+  };
+  auto store1 = [&](const Op1& r, int st) {
+    unsigned char* base = lds + st * (MT_A_BYTES + MT_B_BYTES);
+    *(u32x4_t*)(base + mt_addr4(lrow, lc)) = r.a;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) *(u32x4_t*)(base + MT_A_BYTES + mt_addr4(lrow + 128 * i, lc)) = r.b[i];
+  };
+  floatx16_t acc[2][4];
+#pragma unroll
+  for (int i = 0; i < 2; ++i)
+#pragma unroll
+    for (int j = 0; j < 4; ++j)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
+  auto mma1 = [&](int st) {
+    const unsigned char* base = lds + st * (MT_A_BYTES + MT_B_BYTES);
+#pragma unroll
+    for (int kk = 0; kk < 2; ++kk) {
+      const int c = kk * 2 + (lane >> 5);
+      u32x4_t fa[2], fb[4];
+#pragma unroll
+      for (int i = 0; i < 2; ++i) fa[i] = *(const u32x4_t*)(base + mt_addr4(wm * 64 + i * 32 + (lane & 31), c));
+#pragma unroll
+      for (int j = 0; j < 4; ++j)
+        fb[j] = *(const u32x4_t*)(base + MT_A_BYTES + mt_addr4(wn * 128 + j * 32 + (lane & 31), c));
+#pragma unroll
+      for (int i = 0; i < 2; ++i)
+#pragma unroll
+        for (int j = 0; j < 4; ++j)
+          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8_t, fa[i]),
+                                                              __builtin_bit_cast(bf16x8_t, fb[j]), acc[i][j], 0, 0, 0);
+    }
+  };
+  // k-step kt: load kt + 2 into the set kt held, multiply stage kt % 2, store
+  // kt + 1 (loaded a k-step ago) into the other stage
+  auto step1 = [&](int kt, int nk, Op1& mine, Op1& next) {
+    if (kt + 2 < nk) load1(mine, kt + 2);
+    mma1(kt & 1);
+    if (kt + 1 < nk) store1(next, (kt + 1) & 1);
+    __syncthreads();
+  };
+  const int nk = K2 / MT_KS;
+  Op1 r0, r1;
+  load1(r0, 0);
+  if (nk > 1) load1(r1, 1);
+  store1(r0, 0);
+  __syncthreads();
+  for (int kt = 0; kt < nk; kt += 2) {
+    step1(kt, nk, r0, r1);
+    if (kt + 1 < nk) step1(kt + 1, nk, r1, r0);
+  }
+  // W3's first two k-steps load while the first layer's outputs go to LDS
+  struct Op2 {
+    u32x4_t b[2];
+  };
+  auto load2 = [&](Op2& r, int kt) {
+    const int k0 = kt * MT_KS;
+#pragma unroll
+    for (int i = 0; i < 2; ++i) r.b[i] = *(const u32x4_t*)(W3 + (int64_t)(lrow + 128 * i) * ldw3 + k0 + lc * 8);
+  };
+  auto store2 = [&](const Op2& r, int st) {
+    unsigned char* base = lds + MT_W3 + st * (MT_N3 * 64);
+#pragma unroll
+    for (int i = 0; i < 2; ++i) *(u32x4_t*)(base + mt_addr4(lrow + 128 * i, lc)) = r.b[i];
+  };
+  Op2 w0, w1;
+  load2(w0, 0);
+  load2(w1, 1);
+  // accumulator (i, j) register r of lane l: row 8 (r / 4) + 4 (l / 32) + r % 4,
+  // column l % 32 of its 32 x 32 block; bias and ReLU per column, then each
+  // group of four rows transposed across the quad so a lane holds four
+  // consecutive columns of one row (as k_gemm_bf16's epilogue), rounded to bf16
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    const int col0 = wn * 128 + j * 32;
+    const float bb = b2[col0 + (lane & 31)];
+    const int colq = col0 + (lane & 28);
+#pragma unroll
+    for (int i = 0; i < 2; ++i)
+#pragma unroll
+      for (int g = 0; g < 4; ++g) {
+        float q[4];
+#pragma unroll
+        for (int k = 0; k < 4; ++k) q[k] = act_fn<RB_ACT_RELU>(acc[i][j][4 * g + k] + bb);
+        quad_transpose4(q, lane);
+        const int row = wm * 64 + i * 32 + 8 * g + 4 * (lane >> 5) + (lane & 3);
+        const u32x2_t o = {pack2_rne(q[0], q[1]), pack2_rne(q[2], q[3])};
+        *(u32x2_t*)(lds + MT_Y2 + mt_addr_y2(row, colq >> 3) + ((colq & 4) ? 8 : 0)) = o;
+      }
+  }
+  store2(w0, 0);
+  __syncthreads();
+  // ---- second layer: Y3 = relu(Y2 W3^T + b3)
+  floatx16_t acc3[2][2];
+#pragma unroll
+  for (int i = 0; i < 2; ++i)
+#pragma unroll
+    for (int j = 0; j < 2; ++j)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) acc3[i][j][r] = 0.f;
+  auto mma2 = [&](int kt) {
+    const unsigned char* base = lds + MT_W3 + (kt & 1) * (MT_N3 * 64);
+#pragma unroll
+    for (int kk = 0; kk < 2; ++kk) {
+      const int c = kk * 2 + (lane >> 5);
+      u32x4_t fa[2], fb[2];
+#pragma unroll
+      for (int i = 0; i < 2; ++i) {
+        const int row = wm * 64 + i * 32 + (lane & 31);
+        fa[i] = *(const u32x4_t*)(lds + MT_Y2 + mt_addr_y2(row, kt * 4 + c));
+      }
+#pragma unroll
+      for (int j = 0; j < 2; ++j) fb[j] = *(const u32x4_t*)(base + mt_addr4(wn * 64 + j * 32 + (lane & 31), c));
+#pragma unroll
+      for (int i = 0; i < 2; ++i)
+#pragma unroll
+        for (int j = 0; j < 2; ++j)
+          acc3[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8_t, fa[i]),
+                                                               __builtin_bit_cast(bf16x8_t, fb[j]), acc3[i][j], 0, 0, 0);
+    }
+  };
+  constexpr int nk3 = MT_N2 / MT_KS;
+  auto step2 = [&](int kt, Op2& mine, Op2& next) {
+    if (kt + 2 < nk3) load2(mine, kt + 2);
+    mma2(kt);
+    if (kt + 1 < nk3) store2(next, (kt + 1) & 1);
+    __syncthreads();
+  };
+  for (int kt = 0; kt < nk3; kt += 2) {
+    step2(kt, w0, w1);
+    step2(kt + 1, w1, w0);
+  }
+  // Y3 (bias, ReLU, bf16) to LDS, row-major [MT_BM][MT_N3] over the first
+  // layer's outputs (no longer read)
+  unsigned char* y3 = lds;
+#pragma unroll
+  for (int j = 0; j < 2; ++j) {
+    const int col0 = wn * 64 + j * 32;
+    const float bb = b3[col0 + (lane & 31)];
+    const int colq = col0 + (lane & 28);
+#pragma unroll
+    for (int i = 0; i < 2; ++i)
+#pragma unroll
+      for (int g = 0; g < 4; ++g) {
+        float q[4];
+#pragma unroll
+        for (int k = 0; k < 4; ++k) q[k] = act_fn<RB_ACT_RELU>(acc3[i][j][4 * g + k] + bb);
+        quad_transpose4(q, lane);
+        const int row = wm * 64 + i * 32 + 8 * g + 4 * (lane >> 5) + (lane & 3);
+        const u32x2_t o = {pack2_rne(q[0], q[1]), pack2_rne(q[2], q[3])};
+        *(u32x2_t*)(y3 + row * (MT_N3 * 2) + colq * 2) = o;
+      }
+  }
+  __syncthreads();
+  // ---- head, as k_head: 16 lanes per row, lane l taking elements
+  // [8 l + 128 i, 8 l + 128 i + 8), then a 16-lane butterfly
+  const int l16 = tid & 15;
+#pragma unroll
+  for (int pass = 0; pass < MT_BM / (MT_NT / 16); ++pass) {
+    const int row = pass * (MT_NT / 16) + (tid >> 4);
+    float s = 0.f;
+    for (int k = l16 * 8; k < MT_N3; k += 128) {
+      const u32x4_t hv = *(const u32x4_t*)(y3 + row * (MT_N3 * 2) + k * 2), wv = *(const u32x4_t*)(w4 + k);
+      s += bf2f(hv.x & 0xffffu) * bf2f(wv.x & 0xffffu);
+      s += bf2f(hv.x >> 16) * bf2f(wv.x >> 16);
+      s += bf2f(hv.y & 0xffffu) * bf2f(wv.y & 0xffffu);
+      s += bf2f(hv.y >> 16) * bf2f(wv.y >> 16);
+      s += bf2f(hv.z & 0xffffu) * bf2f(wv.z & 0xffffu);
+      s += bf2f(hv.z >> 16) * bf2f(wv.z >> 16);
+      s += bf2f(hv.w & 0xffffu) * bf2f(wv.w & 0xffffu);
+      s += bf2f(hv.w >> 16) * bf2f(wv.w >> 16);
+    }
+    s += __shfl_xor(s, 1);
+    s += __shfl_xor(s, 2);
+    s += __shfl_xor(s, 4);
+    s += __shfl_xor(s, 8);
+    if (l16 == 0 && m0 + row < M) {
+      const int64_t o = rows[m0 + row].out;
+      if (o >= 0) out[o] = act_fn<ACT>(s + b4);
+    }
+  }
+}
+
 constexpr int POOL_MAX_D = 1024, POOL_MAX_OUT = 16;
 
 // One workgroup per sequence slot. Wave w sums the slot's real tokens
@@ -1663,6 +1901,27 @@ rb_status rb_k_head(void* stream, const rb_k_row* rows, int32_t n_rows_total, co
   else
     hipLaunchKernelGGL(k_head<RB_ACT_NONE>, dim3(g), dim3(256), 0, (hipStream_t)stream, rows, n_rows_total,
                        (const bf16_t*)H, ldh, (const bf16_t*)w, b, K, vec, out);
+  return launch_status();
+}
+
+rb_status rb_k_mlp_tail(void* stream, const rb_k_row* rows, int32_t n_rows_total, const void* H1, int32_t ldh1,
+                        int32_t K2, const void* W2, int32_t ldw2, const float* b2, const void* W3, int32_t ldw3,
+                        const float* b3, const void* w4, float b4, int32_t act, float* out) {
+  if (n_rows_total < 0 || K2 < MT_KS || K2 % MT_KS || ldh1 < K2 || ldw2 < K2 || ldw3 < MT_N2) return RB_EINVAL;
+  if ((ldh1 & 7) || (ldw2 & 7) || (ldw3 & 7) || !rows || !H1 || !W2 || !b2 || !W3 || !b3 || !w4 || !out)
+    return RB_EINVAL;
+  if (((uintptr_t)H1 & 15) || ((uintptr_t)W2 & 15) || ((uintptr_t)W3 & 15) || ((uintptr_t)w4 & 15)) return RB_EINVAL;
+  if (act != RB_ACT_NONE && act != RB_ACT_SIGMOID) return RB_EINVAL;
+  if (n_rows_total == 0) return RB_OK;
+  const unsigned g = (unsigned)((n_rows_total + MT_BM - 1) / MT_BM);
+  if (act == RB_ACT_SIGMOID)
+    hipLaunchKernelGGL(k_mlp_tail<RB_ACT_SIGMOID>, dim3(g), dim3(MT_NT), 0, (hipStream_t)stream, (const bf16_t*)H1,
+                       ldh1, K2, (const bf16_t*)W2, ldw2, b2, (const bf16_t*)W3, ldw3, b3, (const bf16_t*)w4, b4, rows,
+                       n_rows_total, out);
+  else
+    hipLaunchKernelGGL(k_mlp_tail<RB_ACT_NONE>, dim3(g), dim3(MT_NT), 0, (hipStream_t)stream, (const bf16_t*)H1,
+                       ldh1, K2, (const bf16_t*)W2, ldw2, b2, (const bf16_t*)W3, ldw3, b3, (const bf16_t*)w4, b4, rows,
+                       n_rows_total, out);
   return launch_status();
 }
 

@@ -644,6 +644,18 @@ rb_status ensure_work(rb_sched* s, rb_model* m, int slot, int64_t rows, int64_t 
 
 // Launch chain of one group on stream st_h: route -> assemble | embbag ->
 // layers -> head | seqpool | split.
+// A bf16 model whose last two hidden layers are ReLU layers of 512 and 256
+// outputs ahead of a narrow head of 256 inputs: rb_k_mlp_tail runs them.
+bool fused_tail(const rb_model* m) {
+  if (m->dtype != RB_DT_BF16 || !m->head_last || m->layers.size() < 3) return false;
+  const size_t nL = m->layers.size() - 1;
+  const DevLayer& L2 = m->layers[nL - 2];
+  const DevLayer& L3 = m->layers[nL - 1];
+  const DevLayer& H = m->layers.back();
+  return L2.Np == 512 && L2.act == RB_ACT_RELU && L2.Kp % 32 == 0 && L3.Np == 256 && L3.Kp == 512 &&
+         L3.act == RB_ACT_RELU && H.K == 256;
+}
+
 // The chain of a group of n_batches batches of queue q holding `slots`
 // padded rows (sequence slots) and `tokens` real tokens (seqpool), with work
 // buffers w large enough for it; `timed`: HIP events around every launch when
@@ -681,9 +693,12 @@ rb_status run_chain(rb_sched* s, hipStream_t st_h, const rb_queue* q, int n_batc
                                            bf16 ? 1 : 0, pad, s->err_dev));
   }
   const size_t nL = m->layers.size() - (m->head_last ? 1 : 0);
+  // the last two hidden layers and the head in one kernel when they have its
+  // shapes (bit-identical either way)
+  const bool tail = fused_tail(m) && s->opts.fuse_mlp_tail;
   void* h = w->X;
   int ldh = Kp0;
-  for (size_t i = 0; i < nL; ++i) {
+  for (size_t i = 0; i < nL - (tail ? 2 : 0); ++i) {
     const DevLayer& L = m->layers[i];
     const bool last = (i + 1 == nL) && !m->head_last;
     void* y = last ? (void*)w->Y : (i % 2 == 0 ? w->A : w->B);
@@ -698,7 +713,13 @@ rb_status run_chain(rb_sched* s, hipStream_t st_h, const rb_queue* q, int n_batc
     h = y;
     ldh = L.Np;
   }
-  if (m->head_last) {
+  if (tail) {
+    const DevLayer& L2 = m->layers[nL - 2];
+    const DevLayer& L3 = m->layers[nL - 1];
+    const DevLayer& H = m->layers.back();
+    RB_LAUNCH(s, st_h, "mlp_tail", rb_k_mlp_tail(hs, w->rows, (int)slots, h, ldh, L2.Kp, L2.w, L2.Kp, L2.b, L3.w,
+                                                 L3.Kp, L3.b, H.w, m->head_bias, H.act, out));
+  } else if (m->head_last) {
     const DevLayer& L = m->layers.back();
     RB_LAUNCH(s, st_h, "head", rb_k_head(hs, w->rows, (int)slots, h, ldh, L.w, m->head_bias, L.K, L.act, out));
   } else if (m->kind == RB_MODEL_SEQPOOL) {
@@ -1095,6 +1116,7 @@ rb_status rb_sched_create(rb_ctx* ctx, const rb_sched_opts* o, rb_sched** out) {
   if (o->seq_pack < 0 || o->seq_pack > 1) return RB_EINVAL;
   if (o->clocked_windows < 0 || o->clocked_windows > 1) return RB_EINVAL;
   if (o->emb_dedup < 0 || o->emb_dedup > 1) return RB_EINVAL;
+  if (o->fuse_mlp_tail < 0 || o->fuse_mlp_tail > 1) return RB_EINVAL;
   if (o->profile < 0 || o->profile > 2) return RB_EINVAL;
   rb_sched* s = new (std::nothrow) rb_sched();
   if (!s) return RB_ENOMEM;

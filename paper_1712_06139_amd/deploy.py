@@ -41,7 +41,7 @@ class Deployment:
                  with_params: bool = True, models: Optional[List[rb.Model]] = None, n_streams: int = 1,
                  seq_pack: bool = False, window_ns: Optional[Sequence[int]] = None,
                  window_tail_ns: Optional[Sequence[int]] = None, clocked_windows: bool = False,
-                 emb_dedup: bool = False):
+                 emb_dedup: bool = False, fused_tail: bool = False):
         import synth
         self.w = w
         self.ctx = ctx
@@ -62,7 +62,7 @@ class Deployment:
                                             shapes=shapes, table_rows=m.table_rows))
         self.sched = rb.Sched(ctx, device=device, window_batches=window_batches, pad_value=pad_value,
                               profile=profile, n_streams=n_streams, seq_pack=seq_pack,
-                              clocked_windows=clocked_windows, emb_dedup=emb_dedup)
+                              clocked_windows=clocked_windows, emb_dedup=emb_dedup, fused_tail=fused_tail)
         self.queues: List[rb.Queue] = []
         for qi, q in enumerate(w.queues):
             svc = None if service_ns is None else service_ns[qi]

@@ -52,7 +52,7 @@ class rb_model_desc(C.Structure):
 class rb_sched_opts(C.Structure):
     _fields_ = [("mode", C.c_int32), ("window_batches", C.c_int32), ("pad_value", C.c_float),
                 ("profile", C.c_int32), ("n_streams", C.c_int32), ("seq_pack", C.c_int32),
-                ("clocked_windows", C.c_int32), ("emb_dedup", C.c_int32)]
+                ("clocked_windows", C.c_int32), ("emb_dedup", C.c_int32), ("fuse_mlp_tail", C.c_int32)]
 
 
 class rb_queue_opts(C.Structure):
@@ -166,6 +166,9 @@ _SIGS = {
                                   C.c_void_p, C.c_int32]),
     "rb_k_head": (C.c_int32, [C.c_void_p, C.c_void_p, C.c_int32, C.c_void_p, C.c_int32, C.c_void_p, C.c_float,
                               C.c_int32, C.c_int32, C.c_void_p]),
+    "rb_k_mlp_tail": (C.c_int32, [C.c_void_p, C.c_void_p, C.c_int32, C.c_void_p, C.c_int32, C.c_int32, C.c_void_p,
+                                  C.c_int32, C.c_void_p, C.c_void_p, C.c_int32, C.c_void_p, C.c_void_p, C.c_float,
+                                  C.c_int32, C.c_void_p]),
     "rb_k_seqpool": (C.c_int32, [C.c_void_p, C.c_void_p, C.c_int32, C.c_int32, C.c_int64, C.c_void_p, C.c_int32,
                                  C.c_int32, C.c_void_p, C.c_void_p, C.c_int32, C.c_int32, C.c_void_p]),
     "rb_k_split": (C.c_int32, [C.c_void_p, C.c_void_p, C.c_int32, C.c_void_p, C.c_int32, C.c_int32,
@@ -336,9 +339,10 @@ class Queue:
 class Sched:
     def __init__(self, ctx: Ctx, device: bool = True, window_batches: int = 1, pad_value: float = 0.0,
                  profile: int = 0, n_streams: int = 1, seq_pack: bool = False, clocked_windows: bool = False,
-                 emb_dedup: bool = False):
+                 emb_dedup: bool = False, fused_tail: bool = False):
         o = rb_sched_opts(RB_MODE_DEVICE if device else RB_MODE_NO_DEVICE, window_batches, pad_value,
-                          int(profile), n_streams, int(seq_pack), int(clocked_windows), int(emb_dedup))
+                          int(profile), n_streams, int(seq_pack), int(clocked_windows), int(emb_dedup),
+                          int(fused_tail))
         h = C.c_void_p()
         check(_lib().rb_sched_create(ctx.h, C.byref(o), C.byref(h)), "rb_sched_create")
         self.h = h

@@ -51,12 +51,13 @@ def row_scaled_err(y, ref):
     return float(np.max(np.abs(y.astype(np.float64) - ref) / scale))
 
 
-def run(ctx, name, n, window=1, pad=0.0, profile=False, n_streams=1, seq_pack=False, emb_dedup=False):
+def run(ctx, name, n, window=1, pad=0.0, profile=False, n_streams=1, seq_pack=False, emb_dedup=False,
+        fused_tail=False):
     w = synth.workload(name)
     t, a = trace_and_arenas(name, n)
     svc = service_table(w)
     dep = Deployment(w, ctx, device=True, window_batches=window, pad_value=pad, service_ns=svc, profile=profile,
-                     n_streams=n_streams, seq_pack=seq_pack, emb_dedup=emb_dedup)
+                     n_streams=n_streams, seq_pack=seq_pack, emb_dedup=emb_dedup, fused_tail=fused_tail)
     try:
         dt = dep.upload(t, a)
         log = dep.replay(dt)
@@ -133,6 +134,17 @@ def test_embedding_dedup_bit_identical(ctx, name, window):
     *_, out2, _ = run(ctx, name, n, window=window, emb_dedup=True, pad=float("nan"))
     assert lib_batches(log0, qindex) == lib_batches(log1, qindex)
     assert np.array_equal(out0, out1) and np.array_equal(out0, out2)
+
+
+@pytest.mark.parametrize("name,window", [("ranking", 1), ("ranking", 16), ("multi_tenant", 16)])
+def test_fused_mlp_tail_bit_identical(ctx, name, window):
+    # the ranking MLP's last two layers and head in one kernel or three: the
+    # same batches and the same output bits
+    n = min(PREFIX[name], 1500)
+    w, t, a, qindex, log0, out0, out_off = run(ctx, name, n, window=window)
+    _, _, _, _, log1, out1, _ = run(ctx, name, n, window=window, fused_tail=True)
+    assert lib_batches(log0, qindex) == lib_batches(log1, qindex)
+    assert np.array_equal(out0, out1)
 
 
 @pytest.mark.parametrize("window,pad", [(1, 0.0), (16, float("nan"))])

@@ -542,6 +542,57 @@ def test_head_and_split(K, ldh):
     assert np.all(o[~keep] == -7.0)
 
 
+@pytest.mark.parametrize("M,K2,act", [(1, 1024, rb.RB_ACT_SIGMOID), (77, 1024, rb.RB_ACT_SIGMOID),
+                                       (128, 192, rb.RB_ACT_NONE), (300, 1024, rb.RB_ACT_SIGMOID),
+                                       (4500, 1024, rb.RB_ACT_SIGMOID), (32768, 1024, rb.RB_ACT_SIGMOID)])
+def test_mlp_tail_bit_identical_to_separate_kernels(M, K2, act):
+    # the fused last two layers + head against rb_k_gemm_bf16 twice and
+    # rb_k_head on the same operands: the same bits in every output, rows
+    # whose output is -1 skipped, ragged last blocks; and within the fp64
+    # bound of the definition
+    rng = np.random.default_rng(23)
+    ldh = K2 + 64
+    H1d, H1 = _bf16_dev(np.maximum(rng.standard_normal((M, ldh)), 0))
+    W2d, W2 = _bf16_dev(rng.standard_normal((512, K2)) / np.sqrt(K2))
+    W3d, W3 = _bf16_dev(rng.standard_normal((256, 512)) / np.sqrt(512))
+    w4d, w4 = _bf16_dev(rng.standard_normal(256) / 16)
+    b2 = (rng.uniform(-0.5, 0.5, 512)).astype(np.float32)
+    b3 = (rng.uniform(-0.5, 0.5, 256)).astype(np.float32)
+    b2d, b3d = _dev(b2), _dev(b3)
+    out_idx = np.where(rng.random(M) < 0.9, np.arange(M) * 2, -1)
+    rows = _rows_dev(np.zeros(M), np.zeros(M), out_idx)
+    st = _stream()
+    Y2 = torch.empty((M, 512), dtype=torch.int16, device=DEV)
+    Y3 = torch.empty((M, 256), dtype=torch.int16, device=DEV)
+    ref = torch.full((M * 2,), -7.0, device=DEV)
+    got = torch.full((M * 2,), -7.0, device=DEV)
+    rb.check(rb.lib().rb_k_gemm_bf16(st, rb.dptr(H1d), ldh, rb.dptr(W2d), K2, rb.dptr(b2d), rb.dptr(Y2), 512, M, 512,
+                                     K2, rb.RB_ACT_RELU, 0), "gemm 2")
+    rb.check(rb.lib().rb_k_gemm_bf16(st, rb.dptr(Y2), 512, rb.dptr(W3d), 512, rb.dptr(b3d), rb.dptr(Y3), 256, M, 256,
+                                     512, rb.RB_ACT_RELU, 0), "gemm 3")
+    rb.check(rb.lib().rb_k_head(st, rb.dptr(rows), M, rb.dptr(Y3), 256, rb.dptr(w4d), 0.125, 256, act,
+                                rb.dptr(ref)), "head")
+    rb.check(rb.lib().rb_k_mlp_tail(st, rb.dptr(rows), M, rb.dptr(H1d), ldh, K2, rb.dptr(W2d), K2, rb.dptr(b2d),
+                                    rb.dptr(W3d), 512, rb.dptr(b3d), rb.dptr(w4d), 0.125, act, rb.dptr(got)),
+             "mlp_tail")
+    torch.cuda.synchronize()
+    g, r = got.cpu().numpy(), ref.cpu().numpy()
+    assert np.array_equal(g, r)
+    keep = np.zeros(M * 2, bool)
+    keep[out_idx[out_idx >= 0]] = True
+    assert np.all(g[~keep] == -7.0) and np.all(g[keep] != -7.0)
+    # the definition in fp64 with the bf16 storage roundings, on a sample of rows
+    sel = rng.choice(M, size=min(M, 64), replace=False)
+    h = H1[sel, :K2].astype(np.float64)
+    y2 = nx.round_bf16(np.maximum(h @ W2.astype(np.float64).T + b2, 0))
+    y3 = nx.round_bf16(np.maximum(y2 @ W3.astype(np.float64).T + b3, 0))
+    z = y3 @ w4.astype(np.float64) + 0.125
+    want = nx.sigmoid(z) if act == rb.RB_ACT_SIGMOID else z
+    for i, rr in enumerate(sel):
+        if out_idx[rr] >= 0:
+            assert abs(g[out_idx[rr]] - want[i]) <= 2e-2 * max(abs(want[i]), 1e-3), (rr, g[out_idx[rr]], want[i])
+
+
 @pytest.mark.parametrize("S,T,D", [(50, 64, 256), (20, 512, 256), (30, 64, 100), (10, 128, 1000)])
 def test_seqpool_matches_oracle(S, T, D):
     # float4 path (D % 4 == 0), scalar path, long sequences split over waves
