@@ -778,6 +778,16 @@ def main():
         roof = {"bound": "mfma", "achieved": round(ach, 2), "peak": peak, "unit": "TFLOP/s",
                 "frac": round(ach / peak, 4)}
         roof["algorithmic_flops_per_launch"] = round(wk["flops"] / dk["launches"])
+    elif dom == "embbag":
+        # the gathered table rows are mostly L2 / Infinity Cache hits, so the
+        # bytes that must cross HBM are the launch's other bytes plus each
+        # distinct table row once; the gathered-bytes rate against the L2 peak
+        # is in embbag_roofline
+        per_launch = emb["bytes_with_distinct_rows_once_per_launch"]
+        ach = per_launch / (dk["avg_us"] * 1e-6) / 1e9
+        roof = {"bound": "hbm", "achieved": round(ach, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                "frac": round(ach / HBM_PEAK_GBS, 4), "algorithmic_bytes_per_launch": per_launch,
+                "bytes_note": "distinct table rows once per launch window"}
     else:
         ach = wk["bytes"] / (dk["total_ms"] * 1e-3) / 1e9
         roof = {"bound": "hbm", "achieved": round(ach, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
