@@ -14,12 +14,22 @@ and every batch's device work (route -> assemble or embedding-bag -> dense
 layers -> head / pooling / split), with the request payloads already resident
 in HBM and the outputs left there.
 
-Printed: one JSON line with examples/s, p50/p99 request latency on the
-simulated clock (ranking: service times measured on this GPU, Poisson
-arrivals at 90% of the simulated device's capacity), the dominant kernel
-against its roofline (HIP events on the library's stream during a profiled
-replay), every kernel's figures, and the CPU oracle timed on a bounded sample
-of the same trace.
+Printed: one JSON line with
+  * examples/s of the replay, launch windows of 64 dispatched batches;
+  * p50/p99 request latency on the simulated clock, with the device modelled
+    as the library runs it (launch windows whose chain, per-batch and tail
+    times are measured on this GPU from lone launch chains and back-to-back
+    windows; Poisson arrivals at 90% of the simulated device's capacity for
+    count-only workloads, the trace's own arrivals otherwise), and a check of
+    the simulated busy time against the GPU running the clock's windows;
+  * the dominant kernel against its roofline (HIP events on the library's
+    stream during a profiled replay; algorithmic bytes count each layer's
+    weights once per launch group) with the HBM traffic from the committed
+    counter passes, every kernel's figures, and for ranking the embedding
+    bag against the L2 read peak and, with distinct table rows, against HBM;
+  * the CPU oracle timed on one thread on a bounded sample of the same trace;
+  * the serving API's rate with host payloads (PCIe in and out), never the
+    headline value.
 """
 import argparse
 import collections

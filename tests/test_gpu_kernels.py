@@ -319,7 +319,9 @@ def test_embbag_matches_oracle(lens, entry):
         ref = om.ranking_input(dn[None, :], ln[None, :], ii)[0]
         g = got[r, :nt * 64 + 13].astype(np.float64)
         # fp32 summation of n terms is within (n - 1) 2^-24 sum|x| of the exact
-        # sum (any order); bf16 rounding then adds at most one bf16 ulp
+        # sum to first order (any order); bf16 rounding then adds at most one
+        # bf16 ulp. The factor 2 covers the exact bound's second-order term and
+        # an ulp taken at the oracle's value rather than the larger of the two
         sabs = om_abs.ranking_input(dn[None, :], ln[None, :], ii)[0]
         nterm = np.concatenate([np.repeat(np.maximum(ln - 1, 0), 64), np.zeros(13)])
         ulp = np.maximum(np.abs(ref), 2.0 ** -126) * 2.0 ** -7
