@@ -50,7 +50,7 @@ HBM_PEAK_GBS = 8000.0
 L2_PEAK_GBS = 8 * 16 * 128 * 2.4
 BF16_PEAK_TFLOPS = 2500.0
 F32_PEAK_TFLOPS = 157.3
-KERNELS = ("route", "assemble", "embbag", "gemm_bf16", "gemm_f32", "mlp_tail", "head", "seqpool", "split")
+KERNELS = ("route", "assemble", "embbag", "gemm_bf16", "gemm_f32", "gemm_head", "mlp_tail", "head", "seqpool", "split")
 
 DESCRIPTION = {
     "ranking": "ranking: 26 Zipf(1.1) embedding bags over 100k x 64 bf16 tables + 13 dense -> MLP "
@@ -83,6 +83,14 @@ def fused_tail(m):
     L = m.layers
     return (m.dtype == "bf16" and len(L) >= 4 and L[-1].fan_out == 1 and L[-3].fan_out == 512 and
             L[-3].act == "relu" and L[-2].fan_out == 256 and L[-2].act == "relu")
+
+
+def fused_head(m):
+    """The library runs a bf16 model's last hidden layer of 256 outputs and
+    its 256-input narrow head as one kernel (gemm_head) unless the fused
+    tail takes them."""
+    L = m.layers
+    return m.dtype == "bf16" and len(L) >= 2 and L[-1].fan_out == 1 and L[-2].fan_out == 256 and L[-1].fan_in == 256
 
 
 def algorithmic_work(w, t, a, logd, qindex, window, fused=False):
@@ -126,8 +134,11 @@ def algorithmic_work(w, t, a, logd, qindex, window, fused=False):
                                           + (P if m.kind == "seqpool" else M) * row_desc)
         layers = m.layers[:-1] if (m.kind == "ranking" and bf16 and m.layers[-1].fan_out == 1) else m.layers
         tail = fused and fused_tail(m)
+        ghead = not tail and m.kind != "seqpool" and fused_head(m)
         if tail:
             layers = m.layers[:-3]
+        elif ghead:
+            layers = m.layers[:-2]
         key = "gemm_bf16" if bf16 else "gemm_f32"
         Mg = int(n_dense[b]) // m.d_in if m.kind == "seqpool" else M  # rows the layers must compute
         # a launch group (one queue's batches in one launch window) reads each
@@ -148,6 +159,13 @@ def algorithmic_work(w, t, a, logd, qindex, window, fused=False):
             work["mlp_tail"]["flops"] += 2 * P * (l2.fan_in * l2.fan_out + l3.fan_in * l3.fan_out + hd.fan_in)
             wts = (l2.fan_in * l2.fan_out + l3.fan_in * l3.fan_out + hd.fan_in) * 2 if first_in_group else 0
             work["mlp_tail"]["bytes"] += P * l2.fan_in * 2 + wts + s * 4 + P * row_desc
+        elif ghead:
+            # the layer's input and weights (once per launch group), the head's
+            # weights, one output per real row, the row map
+            l3, hd = m.layers[-2], m.layers[-1]
+            work["gemm_head"]["flops"] += 2 * Mg * l3.fan_in * l3.fan_out + 2 * P * hd.fan_in
+            wts = (l3.fan_in * l3.fan_out + hd.fan_in) * 2 if first_in_group else 0
+            work["gemm_head"]["bytes"] += Mg * l3.fan_in * 2 + wts + s * 4 + P * row_desc
         elif m.kind == "ranking" and len(layers) < len(m.layers):
             last = m.layers[-1]
             work["head"]["bytes"] += P * row_desc + P * last.fan_in * 2 + last.fan_in * 2 + s * 4

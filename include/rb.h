@@ -600,6 +600,19 @@ rb_status rb_k_gemm_f32(void* stream, const float* X, int32_t ldx, const float* 
  * w bf16 [K]. */
 rb_status rb_k_head(void* stream, const rb_k_row* rows, int32_t n_rows_total, const void* H, int32_t ldh,
                     const void* w, float b, int32_t K, int32_t act, float* out);
+/* The merged run's last hidden layer and its narrow head in one launch (paper
+ * section 2.2.1: one forward pass for the whole merged request, each caller
+ * handed its own rows): for rows r < M, y_r = act(X[r, :K] W^T + b) with W bf16
+ * [256, ldw] (256 outputs), rounded to bf16 as rb_k_gemm_bf16 stores it, then
+ * out[rows[r].out] = head_act(y_r . w_head + b_head) for rows whose out >= 0
+ * (head_act RB_ACT_SIGMOID or RB_ACT_NONE; w_head bf16 [256], 16-byte
+ * aligned). X bf16 [M, ldx]; K a multiple of 64, ldx, ldw >= K and multiples
+ * of 8. y never leaves the device's on-chip memory. Bit-identical to
+ * rb_k_gemm_bf16 with N = 256 followed by rb_k_head with K = 256. RB_EINVAL on
+ * a bad shape, alignment or activation. */
+rb_status rb_k_gemm_head(void* stream, const void* X, int32_t ldx, const void* W, int32_t ldw, const float* b,
+                         int32_t M, int32_t K, int32_t act, const rb_k_row* rows, const void* w_head, float b_head,
+                         int32_t head_act, float* out);
 /* The last two hidden layers and the narrow head of a bf16 MLP run once on a
  * merged batch (paper section 2.2.1) and handed back to the callers (each
  * caller gets its own rows), in one kernel per block of 128 rows:

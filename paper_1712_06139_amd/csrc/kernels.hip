@@ -865,11 +865,23 @@ constexpr int G16_KALIGN = 64;  // K multiple the bf16 entry point accepts
 constexpr int G32_KALIGN = 32;  // K multiple the fp32 entry point accepts
 constexpr int G32_BM = 64;      // fp32 tile height (the padding-token skip granularity)
 
+// A narrow head applied in the epilogue instead of storing the layer's
+// output (HEAD >= 0, the head's activation): the layer's bf16 outputs of
+// the tile (all N = BN columns of its rows) go to LDS, and row r's head
+// output act(w . y_r + b) is written to out[rows[r].out] when that is >= 0.
+struct HeadArgs {
+  const rb_k_row* rows;
+  const bf16_t* w;  // BN bf16 weights, 16-byte aligned
+  float b;
+  float* out;
+};
+
 template <typename TI, int BM, int BN, int WM, int WN, int NT, int RB, int S, int ORDER, int ACT, bool OUT_F32,
-          bool PERSIST>
+          bool PERSIST, int HEAD = -1>
 __device__ __forceinline__ void gemm_mfma(const TI* __restrict__ X, int ldx, const TI* __restrict__ W, int ldw,
                                           const float* __restrict__ bias, void* __restrict__ Y, int ldy, int M,
-                                          int N, int K, const rb_k_row* __restrict__ skip_rows, int skip_T) {
+                                          int N, int K, const rb_k_row* __restrict__ skip_rows, int skip_T,
+                                          const HeadArgs ha = HeadArgs{}) {
   constexpr bool F32 = sizeof(TI) == 4;
   constexpr int ES = sizeof(TI);  // bytes per element
   constexpr int BK = RB / ES;     // k values per k-step
@@ -1118,6 +1130,78 @@ __device__ __forceinline__ void gemm_mfma(const TI* __restrict__ X, int ldx, con
   }
   };
 
+  // The head instead of the store: the tile's outputs, rounded to bf16 exactly
+  // as the store would round them, into LDS rows of HLD bytes (over the
+  // operand stages, once every wave is done with them); then 16 lanes per row
+  // sum w . y in the order of k_head (lane l: elements 8 l .. 8 l + 7 of every
+  // 128, then a 16-lane butterfly), so the results equal the separate layer and
+  // head bit for bit.
+  auto head_epilogue = [&]() {
+    if constexpr (HEAD >= 0) {
+    constexpr int RPP = NT / 16;  // rows per pass of the head (16 lanes each)
+    static_assert(!F32 && !OUT_F32 && BN == 256 && BM % RPP == 0, "bf16 layer of 256 outputs");
+    constexpr int HLD = BN * 2 + 16;
+    static_assert(BM * HLD <= S * BN * CPR * 16, "the output tile fits over the B stages");
+    unsigned char* hb = (unsigned char*)&sB[0][0];
+    // the output offsets of this thread's rows and its head weights, loaded
+    // before the tile goes to LDS so that their latency overlaps it
+    const int l = tid & 15;
+    int64_t outs[BM / RPP];
+#pragma unroll
+    for (int p = 0; p < BM / RPP; ++p) {
+      const int r = m0 + p * RPP + (tid >> 4);
+      outs[p] = r < M ? ha.rows[r].out : -1;
+    }
+    const u32x4_t w0 = *(const u32x4_t*)(ha.w + l * 8), w1 = *(const u32x4_t*)(ha.w + 128 + l * 8);
+    __syncthreads();
+#pragma unroll
+    for (int j = 0; j < TN; ++j) {
+      const float bb = bias[n0 + wn * WN + j * 32 + (lane & 31)];
+      const int colq = wn * WN + j * 32 + (lane & 28);
+#pragma unroll
+      for (int i = 0; i < TM; ++i)
+#pragma unroll
+        for (int g = 0; g < 4; ++g) {
+          float q[4];
+#pragma unroll
+          for (int k = 0; k < 4; ++k) q[k] = act_fn<ACT>(acc[i][j][4 * g + k] + bb);
+          quad_transpose4(q, lane);
+          const int rl = wm * WM + i * 32 + 8 * g + 4 * (lane >> 5) + (lane & 3);
+          const u32x2_t o = {pack2_rne(q[0], q[1]), pack2_rne(q[2], q[3])};
+          *(u32x2_t*)(hb + rl * HLD + colq * 2) = o;
+        }
+    }
+    __syncthreads();
+#pragma unroll
+    for (int p = 0; p < BM / RPP; ++p) {
+      const int rl = p * RPP + (tid >> 4);
+      float sum = 0.f;
+      const int64_t o = outs[p];
+      {
+        if (o >= 0) {
+#pragma unroll
+          for (int c = 0; c < 2; ++c) {
+            const u32x4_t hv = *(const u32x4_t*)(hb + rl * HLD + (c * 128 + l * 8) * 2), wv = c ? w1 : w0;
+            sum += bf2f(hv.x & 0xffffu) * bf2f(wv.x & 0xffffu);
+            sum += bf2f(hv.x >> 16) * bf2f(wv.x >> 16);
+            sum += bf2f(hv.y & 0xffffu) * bf2f(wv.y & 0xffffu);
+            sum += bf2f(hv.y >> 16) * bf2f(wv.y >> 16);
+            sum += bf2f(hv.z & 0xffffu) * bf2f(wv.z & 0xffffu);
+            sum += bf2f(hv.z >> 16) * bf2f(wv.z >> 16);
+            sum += bf2f(hv.w & 0xffffu) * bf2f(wv.w & 0xffffu);
+            sum += bf2f(hv.w >> 16) * bf2f(wv.w >> 16);
+          }
+        }
+      }
+      sum += __shfl_xor(sum, 1);
+      sum += __shfl_xor(sum, 2);
+      sum += __shfl_xor(sum, 4);
+      sum += __shfl_xor(sum, 8);
+      if (l == 0 && o >= 0) ha.out[o] = act_fn<HEAD>(sum + ha.b);
+    }
+    }
+  };
+
   if constexpr (PERSIST) {
     // K a multiple of S k-steps (so every tile starts at stage 0) and at least
     // S k-steps (so the loads of a tile's last steps reach only the next tile)
@@ -1146,7 +1230,10 @@ __device__ __forceinline__ void gemm_mfma(const TI* __restrict__ X, int ldx, con
       if (kt + 2 < nk) step(kt + 2, ic<2 % S>{}, ic<3 % S>{}, ic<1>{});
     // no load into LDS may still be in flight when the wave ends
     wait_vmcnt_lds<0>();
-    epilogue();
+    if constexpr (HEAD >= 0)
+      head_epilogue();
+    else
+      epilogue();
   }
 }
 
@@ -1159,6 +1246,15 @@ __global__ __launch_bounds__(NT) void k_gemm_bf16(const bf16_t* __restrict__ X, 
                                                   int M, int N, int K) {
   gemm_mfma<bf16_t, BM, BN, WM, WN, NT, RB, S, ORDER, ACT, OUT_F32, PERSIST>(X, ldx, W, ldw, bias, Y, ldy, M, N, K,
                                                                             nullptr, 0);
+}
+// A bf16 layer of 256 outputs with a narrow head in its epilogue (HEAD: the
+// head's activation); the layer's outputs never leave the workgroup.
+template <int BM, int BN, int WM, int WN, int NT, int RB, int S, int ORDER, int ACT, int HEAD>
+__global__ __launch_bounds__(NT) void k_gemm_head(const bf16_t* __restrict__ X, int ldx,
+                                                  const bf16_t* __restrict__ W, int ldw,
+                                                  const float* __restrict__ bias, int M, int K, HeadArgs ha) {
+  gemm_mfma<bf16_t, BM, BN, WM, WN, NT, RB, S, ORDER, ACT, false, false, HEAD>(X, ldx, W, ldw, bias, nullptr, BN, M,
+                                                                             BN, K, nullptr, 0, ha);
 }
 template <int BM, int BN, int WM, int WN, int NT, int RB, int S, int ORDER, int ACT>
 __global__ __launch_bounds__(NT) void k_gemm_f32(const float* __restrict__ X, int ldx, const float* __restrict__ W,
@@ -1901,6 +1997,37 @@ rb_status rb_k_head(void* stream, const rb_k_row* rows, int32_t n_rows_total, co
   else
     hipLaunchKernelGGL(k_head<RB_ACT_NONE>, dim3(g), dim3(256), 0, (hipStream_t)stream, rows, n_rows_total,
                        (const bf16_t*)H, ldh, (const bf16_t*)w, b, K, vec, out);
+  return launch_status();
+}
+
+rb_status rb_k_gemm_head(void* stream, const void* X, int32_t ldx, const void* W, int32_t ldw, const float* b,
+                         int32_t M, int32_t K, int32_t act, const rb_k_row* rows, const void* w_head, float b_head,
+                         int32_t head_act, float* out) {
+  if (M < 0 || K <= 0 || (K % G16_KALIGN) || ldx < K || ldw < K || (ldx & 7) || (ldw & 7)) return RB_EINVAL;
+  if (!X || !W || !b || !rows || !w_head || !out || ((uintptr_t)w_head & 15)) return RB_EINVAL;
+  if ((int64_t)ldx * 512 >= ((int64_t)1 << 31) || (int64_t)ldw * 512 >= ((int64_t)1 << 31)) return RB_EINVAL;
+  if (act != RB_ACT_NONE && act != RB_ACT_RELU && act != RB_ACT_SIGMOID) return RB_EINVAL;
+  if (head_act != RB_ACT_NONE && head_act != RB_ACT_SIGMOID) return RB_EINVAL;
+  if (M == 0) return RB_OK;
+  // 128 x 256 tiles (every row's 256 outputs in one workgroup), 8 waves of
+  // 64 x 64 (two per SIMD: 4 waves of 64 x 128 measured 16% slower), k-step
+  // 64, 3 stages; XCD-contiguous order (W is 256 x K bf16)
+  const unsigned g = (unsigned)((M + 127) / 128);
+  const HeadArgs ha{rows, (const bf16_t*)w_head, b_head, out};
+  hipStream_t s = (hipStream_t)stream;
+#define RB_GH(A, H)                                                                                                    \
+  hipLaunchKernelGGL((k_gemm_head<128, 256, 64, 64, 512, 128, 3, 1, A, H>), dim3(g), dim3(512), 0, s,                \
+                     (const bf16_t*)X, ldx, (const bf16_t*)W, ldw, b, M, K, ha)
+  if (head_act == RB_ACT_SIGMOID) {
+    if (act == RB_ACT_RELU) RB_GH(RB_ACT_RELU, RB_ACT_SIGMOID);
+    else if (act == RB_ACT_SIGMOID) RB_GH(RB_ACT_SIGMOID, RB_ACT_SIGMOID);
+    else RB_GH(RB_ACT_NONE, RB_ACT_SIGMOID);
+  } else {
+    if (act == RB_ACT_RELU) RB_GH(RB_ACT_RELU, RB_ACT_NONE);
+    else if (act == RB_ACT_SIGMOID) RB_GH(RB_ACT_SIGMOID, RB_ACT_NONE);
+    else RB_GH(RB_ACT_NONE, RB_ACT_NONE);
+  }
+#undef RB_GH
   return launch_status();
 }
 

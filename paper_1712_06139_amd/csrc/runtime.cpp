@@ -656,6 +656,14 @@ bool fused_tail(const rb_model* m) {
          L3.act == RB_ACT_RELU && H.K == 256;
 }
 
+// A bf16 model whose last hidden layer has 256 outputs ahead of a narrow
+// head of 256 inputs: rb_k_gemm_head runs the two.
+bool gemm_head(const rb_model* m) {
+  if (m->dtype != RB_DT_BF16 || !m->head_last || m->layers.size() < 2) return false;
+  const DevLayer& L = m->layers[m->layers.size() - 2];
+  return L.N == 256 && L.Np == 256 && L.Kp % 64 == 0 && m->layers.back().K == 256;
+}
+
 // The chain of a group of n_batches batches of queue q holding `slots`
 // padded rows (sequence slots) and `tokens` real tokens (seqpool), with work
 // buffers w large enough for it; `timed`: HIP events around every launch when
@@ -696,9 +704,12 @@ rb_status run_chain(rb_sched* s, hipStream_t st_h, const rb_queue* q, int n_batc
   // the last two hidden layers and the head in one kernel when they have its
   // shapes (bit-identical either way)
   const bool tail = fused_tail(m) && s->opts.fuse_mlp_tail;
+  // otherwise a last hidden layer of 256 outputs and a 256-input head in one
+  // kernel (bit-identical to the layer and the head run separately)
+  const bool ghead = !tail && gemm_head(m);
   void* h = w->X;
   int ldh = Kp0;
-  for (size_t i = 0; i < nL - (tail ? 2 : 0); ++i) {
+  for (size_t i = 0; i < nL - (tail ? 2 : 0) - (ghead ? 1 : 0); ++i) {
     const DevLayer& L = m->layers[i];
     const bool last = (i + 1 == nL) && !m->head_last;
     void* y = last ? (void*)w->Y : (i % 2 == 0 ? w->A : w->B);
@@ -719,6 +730,11 @@ rb_status run_chain(rb_sched* s, hipStream_t st_h, const rb_queue* q, int n_batc
     const DevLayer& H = m->layers.back();
     RB_LAUNCH(s, st_h, "mlp_tail", rb_k_mlp_tail(hs, w->rows, (int)slots, h, ldh, L2.Kp, L2.w, L2.Kp, L2.b, L3.w,
                                                  L3.Kp, L3.b, H.w, m->head_bias, H.act, out));
+  } else if (ghead) {
+    const DevLayer& L3 = m->layers[nL - 1];
+    const DevLayer& H = m->layers.back();
+    RB_LAUNCH(s, st_h, "gemm_head", rb_k_gemm_head(hs, h, ldh, L3.w, L3.Kp, L3.b, (int)Ml, L3.Kp, L3.act, w->rows, H.w,
+                                                   m->head_bias, H.act, out));
   } else if (m->head_last) {
     const DevLayer& L = m->layers.back();
     RB_LAUNCH(s, st_h, "head", rb_k_head(hs, w->rows, (int)slots, h, ldh, L.w, m->head_bias, L.K, L.act, out));

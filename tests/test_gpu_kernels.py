@@ -595,6 +595,72 @@ def test_mlp_tail_bit_identical_to_separate_kernels(M, K2, act):
             assert abs(g[out_idx[rr]] - want[i]) <= 2e-2 * max(abs(want[i]), 1e-3), (rr, g[out_idx[rr]], want[i])
 
 
+@pytest.mark.parametrize("M,K,act,hact", [(1000, 512, rb.RB_ACT_RELU, rb.RB_ACT_SIGMOID),
+                                          (300, 192, rb.RB_ACT_RELU, rb.RB_ACT_NONE),
+                                          (128, 64, rb.RB_ACT_NONE, rb.RB_ACT_SIGMOID),
+                                          (4133, 512, rb.RB_ACT_RELU, rb.RB_ACT_SIGMOID)])
+def test_gemm_head_bit_identical_to_separate_kernels(M, K, act, hact):
+    # the last hidden layer (256 outputs) with the head in its epilogue against
+    # rb_k_gemm_bf16 and rb_k_head on the same operands: the same bits in
+    # every output, rows whose output is -1 skipped, ragged last tiles; and
+    # within the fp64 bound of the definition
+    rng = np.random.default_rng(29)
+    ldx = K + 64
+    Xd, X = _bf16_dev(np.maximum(rng.standard_normal((M, ldx)), 0))
+    Wd, W = _bf16_dev(rng.standard_normal((256, K)) / np.sqrt(K))
+    wd, w = _bf16_dev(rng.standard_normal(256) / 16)
+    b = rng.uniform(-0.5, 0.5, 256).astype(np.float32)
+    bd = _dev(b)
+    out_idx = np.where(rng.random(M) < 0.9, np.arange(M) * 2, -1)
+    rows = _rows_dev(np.zeros(M), np.zeros(M), out_idx)
+    st = _stream()
+    Y = torch.empty((M, 256), dtype=torch.int16, device=DEV)
+    ref = torch.full((M * 2,), -7.0, device=DEV)
+    got = torch.full((M * 2,), -7.0, device=DEV)
+    rb.check(rb.lib().rb_k_gemm_bf16(st, rb.dptr(Xd), ldx, rb.dptr(Wd), K, rb.dptr(bd), rb.dptr(Y), 256, M, 256, K,
+                                     act, 0), "gemm")
+    rb.check(rb.lib().rb_k_head(st, rb.dptr(rows), M, rb.dptr(Y), 256, rb.dptr(wd), 0.125, 256, hact, rb.dptr(ref)),
+             "head")
+    rb.check(rb.lib().rb_k_gemm_head(st, rb.dptr(Xd), ldx, rb.dptr(Wd), K, rb.dptr(bd), M, K, act, rb.dptr(rows),
+                                     rb.dptr(wd), 0.125, hact, rb.dptr(got)), "gemm_head")
+    torch.cuda.synchronize()
+    g, r = got.cpu().numpy(), ref.cpu().numpy()
+    assert np.array_equal(g, r)
+    keep = np.zeros(M * 2, bool)
+    keep[out_idx[out_idx >= 0]] = True
+    assert np.all(g[~keep] == -7.0) and np.all(g[keep] != -7.0)
+    # the definition in fp64 with the bf16 storage rounding, on a sample of rows
+    sel = rng.choice(M, size=min(M, 64), replace=False)
+    z = X[sel, :K].astype(np.float64) @ W.astype(np.float64).T + b
+    y = nx.round_bf16(np.maximum(z, 0) if act == rb.RB_ACT_RELU else z)
+    zh = y @ w.astype(np.float64) + 0.125
+    want = nx.sigmoid(zh) if hact == rb.RB_ACT_SIGMOID else zh
+    for i, rr in enumerate(sel):
+        if out_idx[rr] >= 0:
+            assert abs(g[out_idx[rr]] - want[i]) <= 2e-2 * max(abs(want[i]), 1e-2), (rr, g[out_idx[rr]], want[i])
+
+
+def test_gemm_head_rejects_bad_arguments():
+    st = _stream()
+    X = torch.zeros((128, 128), dtype=torch.int16, device=DEV)
+    W = torch.zeros((256, 128), dtype=torch.int16, device=DEV)
+    w = torch.zeros(264, dtype=torch.int16, device=DEV)
+    b = torch.zeros(256, device=DEV)
+    out = torch.zeros(128, device=DEV)
+    rows = _rows_dev(np.zeros(128), np.zeros(128), np.arange(128))
+    lib = rb.lib()
+
+    def call(K=128, ldx=128, wp=None, act=rb.RB_ACT_RELU, hact=rb.RB_ACT_SIGMOID):
+        return lib.rb_k_gemm_head(st, rb.dptr(X), ldx, rb.dptr(W), 128, rb.dptr(b), 128, K, act, rb.dptr(rows),
+                                  rb.dptr(w) if wp is None else wp, 0.0, hact, rb.dptr(out))
+    assert call() == rb.RB_OK
+    assert call(K=96) == rb.RB_EINVAL             # K not a multiple of 64
+    assert call(ldx=64) == rb.RB_EINVAL           # ldx < K
+    assert call(wp=rb.dptr(w) + 2) == rb.RB_EINVAL  # head weights not 16-byte aligned
+    assert call(hact=rb.RB_ACT_RELU) == rb.RB_EINVAL
+    torch.cuda.synchronize()
+
+
 @pytest.mark.parametrize("S,T,D", [(50, 64, 256), (20, 512, 256), (30, 64, 100), (10, 128, 1000)])
 def test_seqpool_matches_oracle(S, T, D):
     # float4 path (D % 4 == 0), scalar path, long sequences split over waves
