@@ -1,0 +1,94 @@
+"""The algorithmic work behind bench.py's roofline figures, counted again from
+the batch log of a no-device replay: every dense layer's flops from the padded
+batch sizes and the model's real dimensions, the weights once per launch group
+(one queue's batches inside one launch window), and the split of the layers
+between the kernels that run them (two GEMM layers and the fused last layer
+with its head for the ranking MLP, the opt-in fused tail, the three layers of
+the large MLP)."""
+import numpy as np
+import pytest
+
+import bench
+import synth
+from paper_1712_06139_amd import rb
+from paper_1712_06139_amd.deploy import Deployment
+
+W = 64
+
+
+@pytest.fixture(scope="module")
+def ctx():
+    return rb.Ctx(-1)
+
+
+def _replay(ctx, name, n):
+    w = synth.workload(name)
+    t = synth.trace(w, n)
+    a = synth.arenas(t)
+    dep = Deployment(w, ctx, device=False, with_params=False, window_batches=W)
+    try:
+        logd = dep.replay_meta(t)
+        qindex = dict(dep.qindex)
+    finally:
+        dep.destroy()
+    return w, t, a, logd, qindex
+
+
+def _padded(logd):
+    nb = int(logd["n_batches"])
+    return np.asarray(logd["b_padded"][:nb], np.int64), np.asarray(logd["b_queue"][:nb])
+
+
+def _groups(logd):
+    # (launch window, queue) pairs: consecutive windows of W dispatched batches
+    P, q = _padded(logd)
+    return len({(b // W, int(q[b])) for b in range(len(P))})
+
+
+def test_ranking_layers_split_between_gemm_and_fused_head(ctx):
+    w, t, a, logd, qindex = _replay(ctx, "ranking", 3000)
+    P, _ = _padded(logd)
+    m = w.models[0]
+    dims = [(L.fan_in, L.fan_out) for L in m.layers]
+    assert dims == [(1677, 1024), (1024, 512), (512, 256), (256, 1)]
+    work = bench.algorithmic_work(w, t, a, logd, qindex, W)
+    rows = int(P.sum())
+    assert work["gemm_bf16"]["flops"] == 2 * rows * (1677 * 1024 + 1024 * 512)
+    assert work["gemm_head"]["flops"] == 2 * rows * (512 * 256) + 2 * rows * 256
+    assert "head" not in work and "mlp_tail" not in work
+    g = _groups(logd)
+    # inputs and outputs of every row plus the two layers' weights once per group
+    assert work["gemm_bf16"]["bytes"] == 2 * (rows * (1677 + 1024 + 1024 + 512) + g * (1677 * 1024 + 1024 * 512))
+    real = int(t.n_rows.sum())
+    assert work["gemm_head"]["bytes"] == rows * 512 * 2 + g * (512 * 256 + 256) * 2 + real * 4 + rows * 32
+    # the embedding bags: every id's 4-byte index and 128-byte table row, the
+    # lengths and dense features of real rows, the bf16 output and row map of
+    # every padded row
+    n_ids = int(a.ids_off[-1])
+    assert work["embbag"]["bytes"] == (rows * 32 + real * (26 * 4 + 13 * 4) + n_ids * (4 + 128)
+                                       + rows * (26 * 64 + 13) * 2)
+
+
+def test_ranking_fused_tail_accounting(ctx):
+    w, t, a, logd, qindex = _replay(ctx, "ranking", 2000)
+    P, _ = _padded(logd)
+    rows = int(P.sum())
+    work = bench.algorithmic_work(w, t, a, logd, qindex, W, fused=True)
+    assert work["gemm_bf16"]["flops"] == 2 * rows * 1677 * 1024
+    assert work["mlp_tail"]["flops"] == 2 * rows * (1024 * 512 + 512 * 256 + 256)
+    assert "gemm_head" not in work
+
+
+def test_large_mlp_weights_once_per_launch_group(ctx):
+    w, t, a, logd, qindex = _replay(ctx, "large_mlp", 600)
+    P, _ = _padded(logd)
+    rows = int(P.sum())
+    work = bench.algorithmic_work(w, t, a, logd, qindex, W)
+    layers = [(4096, 8192), (8192, 8192), (8192, 4096)]
+    assert work["gemm_bf16"]["flops"] == sum(2 * rows * k * n for k, n in layers)
+    g = _groups(logd)
+    assert work["gemm_bf16"]["bytes"] == 2 * sum(rows * (k + n) + g * k * n for k, n in layers)
+    real = int(t.n_rows.sum())
+    # real fp32 inputs read once, every padded row written in bf16, the row map
+    assert work["assemble"]["bytes"] == real * 4096 * 4 + rows * 4096 * 2 + rows * 32
+    assert work["split"]["bytes"] == rows * 32 + real * 4096 * 8
