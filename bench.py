@@ -148,10 +148,18 @@ def algorithmic_work(w, t, a, logd, qindex, window, fused=False):
         seen_in_window.add(qid)
         if (b + 1) % window == 0:
             seen_in_window = set()
-        for L in layers:
+        # a chain that ends in the split writes its last layer's real rows
+        # (fp32, d_out columns) straight into the requests' outputs through
+        # the row map
+        rows_out = m.kind != "seqpool" and len(layers) == len(m.layers)
+        es = 2 if bf16 else 4
+        for li, L in enumerate(layers):
             work[key]["flops"] += 2 * Mg * L.fan_in * L.fan_out
-            work[key]["bytes"] += ((Mg * L.fan_in + Mg * L.fan_out + (L.fan_in * L.fan_out if first_in_group else 0))
-                                   * (2 if bf16 else 4))
+            w_bytes = L.fan_in * L.fan_out * es if first_in_group else 0
+            if rows_out and li == len(layers) - 1:
+                work[key]["bytes"] += Mg * L.fan_in * es + w_bytes + s * m.d_out * 4 + P * row_desc
+            else:
+                work[key]["bytes"] += (Mg * L.fan_in + Mg * L.fan_out) * es + w_bytes
         if tail:
             # hidden input, the two layers' and the head's weights once per
             # launch group, one output per real row, the row map
@@ -174,8 +182,6 @@ def algorithmic_work(w, t, a, logd, qindex, window, fused=False):
             D = m.head.fan_in
             work["seqpool"]["bytes"] += (int(n_dense[b]) // m.d_in) * D * 4 + P * row_desc + s * m.d_out * 4
             work["seqpool"]["flops"] += (int(n_dense[b]) // m.d_in) * D + 2 * s * D * m.d_out
-        else:
-            work["split"]["bytes"] += P * row_desc + s * m.d_out * 8
     return work
 
 

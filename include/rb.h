@@ -593,6 +593,23 @@ rb_status rb_k_gemm_bf16(void* stream, const void* X, int32_t ldx, const void* W
 rb_status rb_k_gemm_f32(void* stream, const float* X, int32_t ldx, const float* W, int32_t ldw,
                         const float* b, float* Y, int32_t ldy, int32_t M, int32_t N, int32_t K, int32_t act,
                         const rb_k_row* skip_rows, int32_t skip_T);
+/* The merged run's last layer handed back to the callers in the same launch
+ * (paper section 2.2.1: each caller gets exactly its own rows): the layer of
+ * rb_k_gemm_bf16 (bf16 X and W, out_f32) or rb_k_gemm_f32 (fp32 X and W, no
+ * padding-token skip), with row r's first d_out fp32 outputs written to
+ * out[rows[r].out, rows[r].out + d_out) when rows[r].out >= 0 instead of to a
+ * Y matrix; padding rows and columns past d_out are never written. Same shape
+ * rules as those calls; 1 <= d_out <= N. Bit-identical to the layer followed by
+ * rb_k_split. RB_EINVAL on a bad shape, pointer or activation. */
+rb_status rb_k_gemm_bf16_rows(void* stream, const void* X, int32_t ldx, const void* W, int32_t ldw, const float* b,
+                              int32_t M, int32_t N, int32_t K, int32_t act, const rb_k_row* rows, int32_t d_out,
+                              float* out);
+/* The same for an fp32 layer (paper section 2.2.1, the split of the merged
+ * run fused into its last layer): the layer of rb_k_gemm_f32 without the
+ * padding-token skip, outputs through the row map as above. */
+rb_status rb_k_gemm_f32_rows(void* stream, const float* X, int32_t ldx, const float* W, int32_t ldw, const float* b,
+                             int32_t M, int32_t N, int32_t K, int32_t act, const rb_k_row* rows, int32_t d_out,
+                             float* out);
 /* The merged run's last layer handed back to the callers (paper section
  * 2.2.1: each caller gets its own rows): a narrow last layer fused with the
  * split, out[rows[r].out] = act(H[r, :K] . w + b)

@@ -876,12 +876,22 @@ struct HeadArgs {
   float* out;
 };
 
+// fp32 outputs written through a row map instead of to Y (rows != nullptr):
+// row r's first d_out columns go to out[rows[r].out ...] when that is >= 0
+// (the merged run's split fused into its last layer); padding rows and
+// columns past d_out are dropped.
+struct OutMap {
+  const rb_k_row* rows;
+  float* out;
+  int d_out;
+};
+
 template <typename TI, int BM, int BN, int WM, int WN, int NT, int RB, int S, int ORDER, int ACT, bool OUT_F32,
           bool PERSIST, int HEAD = -1>
 __device__ __forceinline__ void gemm_mfma(const TI* __restrict__ X, int ldx, const TI* __restrict__ W, int ldw,
                                           const float* __restrict__ bias, void* __restrict__ Y, int ldy, int M,
                                           int N, int K, const rb_k_row* __restrict__ skip_rows, int skip_T,
-                                          const HeadArgs ha = HeadArgs{}) {
+                                          const HeadArgs ha = HeadArgs{}, const OutMap om = OutMap{}) {
   constexpr bool F32 = sizeof(TI) == 4;
   constexpr int ES = sizeof(TI);  // bytes per element
   constexpr int BK = RB / ES;     // k values per k-step
@@ -1101,6 +1111,19 @@ __device__ __forceinline__ void gemm_mfma(const TI* __restrict__ X, int ldx, con
   // consecutive columns of one row and stores them at once (8 bytes bf16, 16
   // bytes fp32) instead of four single elements.
   auto epilogue = [&]() {
+  // with an output row map: the output offsets of this lane's rows, loaded
+  // all at once before any is needed
+  const bool mapped = OUT_F32 && om.rows != nullptr;  // uniform
+  int64_t ro[TM][4];
+  if (mapped) {
+#pragma unroll
+    for (int i = 0; i < TM; ++i)
+#pragma unroll
+      for (int g = 0; g < 4; ++g) {
+        const int r = m0 + wm * WM + i * 32 + 8 * g + 4 * (lane >> 5) + (lane & 3);
+        ro[i][g] = r < M ? om.rows[r].out : -1;
+      }
+  }
 #pragma unroll
   for (int j = 0; j < TN; ++j) {
     const float bb = bias[n0 + wn * WN + j * 32 + (lane & 31)];
@@ -1117,6 +1140,23 @@ __device__ __forceinline__ void gemm_mfma(const TI* __restrict__ X, int ldx, con
         // streaming (nontemporal) stores: the whole chip writes its tiles'
         // outputs at about the same time, and these drain faster than
         // stores that allocate in L2
+        if constexpr (OUT_F32) {
+          if (mapped) {
+            const int64_t o = ro[i][g];
+            if (o >= 0) {
+              float* dst = om.out + o + colq;
+              if (colq + 3 < om.d_out && ((o + colq) & 3) == 0) {
+                const f32x4_t v = {q[0], q[1], q[2], q[3]};
+                __builtin_nontemporal_store(v, (f32x4_t*)dst);
+              } else {
+#pragma unroll
+                for (int k = 0; k < 4; ++k)
+                  if (colq + k < om.d_out) dst[k] = q[k];
+              }
+            }
+            continue;
+          }
+        }
         if (row < M) {
           if (OUT_F32) {
             const f32x4_t o = {q[0], q[1], q[2], q[3]};
@@ -1243,9 +1283,9 @@ template <int BM, int BN, int WM, int WN, int NT, int RB, int S, int ORDER, int 
 __global__ __launch_bounds__(NT) void k_gemm_bf16(const bf16_t* __restrict__ X, int ldx,
                                                   const bf16_t* __restrict__ W, int ldw,
                                                   const float* __restrict__ bias, void* __restrict__ Y, int ldy,
-                                                  int M, int N, int K) {
+                                                  int M, int N, int K, OutMap om) {
   gemm_mfma<bf16_t, BM, BN, WM, WN, NT, RB, S, ORDER, ACT, OUT_F32, PERSIST>(X, ldx, W, ldw, bias, Y, ldy, M, N, K,
-                                                                            nullptr, 0);
+                                                                            nullptr, 0, HeadArgs{}, om);
 }
 // A bf16 layer of 256 outputs with a narrow head in its epilogue (HEAD: the
 // head's activation); the layer's outputs never leave the workgroup.
@@ -1260,9 +1300,9 @@ template <int BM, int BN, int WM, int WN, int NT, int RB, int S, int ORDER, int 
 __global__ __launch_bounds__(NT) void k_gemm_f32(const float* __restrict__ X, int ldx, const float* __restrict__ W,
                                                  int ldw, const float* __restrict__ bias, void* __restrict__ Y,
                                                  int ldy, int M, int N, int K,
-                                                 const rb_k_row* __restrict__ skip_rows, int skip_T) {
+                                                 const rb_k_row* __restrict__ skip_rows, int skip_T, OutMap om) {
   gemm_mfma<float, BM, BN, WM, WN, NT, RB, S, ORDER, ACT, true, false>(X, ldx, W, ldw, bias, Y, ldy, M, N, K,
-                                                                       skip_rows, skip_T);
+                                                                       skip_rows, skip_T, HeadArgs{}, om);
 }
 
 // ---------------------------------------------------------------- heads and split
@@ -1668,13 +1708,13 @@ namespace {
 template <typename TI, int BM, int BN, int WM, int WN, int NT, int RB, int S, int ORDER, bool PERSIST = false>
 void launch_gemm(hipStream_t s, const TI* x, int ldx, const TI* w, int ldw, const float* b, void* Y, int ldy,
                  int M, int N, int K, int act, bool out_f32, const rb_k_row* skip_rows, int skip_T,
-                 unsigned cap = 0) {
+                 unsigned cap = 0, OutMap om = OutMap{}) {
   const unsigned tiles = (unsigned)(((M + BM - 1) / BM) * (N / BN));
   const unsigned g = PERSIST ? std::min(tiles, cap) : tiles;
   if constexpr (sizeof(TI) == 4) {
 #define RB_G(A)                                                                                                     \
   hipLaunchKernelGGL((k_gemm_f32<BM, BN, WM, WN, NT, RB, S, ORDER, A>), dim3(g), dim3(NT), 0, s, x, ldx, w, ldw, b, \
-                     Y, ldy, M, N, K, skip_rows, skip_T)
+                     Y, ldy, M, N, K, skip_rows, skip_T, om)
     if (act == RB_ACT_RELU) RB_G(RB_ACT_RELU);
     else if (act == RB_ACT_SIGMOID) RB_G(RB_ACT_SIGMOID);
     else RB_G(RB_ACT_NONE);
@@ -1682,7 +1722,7 @@ void launch_gemm(hipStream_t s, const TI* x, int ldx, const TI* w, int ldw, cons
   } else {
 #define RB_G(A, F)                                                                                             \
   hipLaunchKernelGGL((k_gemm_bf16<BM, BN, WM, WN, NT, RB, S, ORDER, A, F, PERSIST>), dim3(g), dim3(NT), 0, s, x, ldx, w, \
-                     ldw, b, Y, ldy, M, N, K)
+                     ldw, b, Y, ldy, M, N, K, om)
     if (out_f32) {
       if (act == RB_ACT_RELU) RB_G(RB_ACT_RELU, true);
       else if (act == RB_ACT_SIGMOID) RB_G(RB_ACT_SIGMOID, true);
@@ -1699,9 +1739,9 @@ void launch_gemm(hipStream_t s, const TI* x, int ldx, const TI* w, int ldw, cons
 // bf16 operands, k-step BK bf16 values
 template <int BM, int BN, int WM, int WN, int NT, int BK, int S, int ORDER, bool PERSIST>
 void launch_gemm_bf16(hipStream_t s, const bf16_t* x, int ldx, const bf16_t* w, int ldw, const float* b, void* Y,
-                      int ldy, int M, int N, int K, int act, int out_f32, unsigned cap) {
+                      int ldy, int M, int N, int K, int act, int out_f32, unsigned cap, OutMap om) {
   launch_gemm<bf16_t, BM, BN, WM, WN, NT, BK * 2, S, ORDER, PERSIST>(s, x, ldx, w, ldw, b, Y, ldy, M, N, K, act,
-                                                                    out_f32 != 0, nullptr, 0, cap);
+                                                                    out_f32 != 0, nullptr, 0, cap, om);
 }
 
 // compute units of the current device (cached per device)
@@ -1892,10 +1932,12 @@ rb_status rb_k_embbag(void* stream, const rb_k_row* rows, int32_t n_rows_total, 
   return launch_status();
 }
 
-rb_status rb_k_gemm_bf16(void* stream, const void* X, int32_t ldx, const void* W, int32_t ldw, const float* b,
-                         void* Y, int32_t ldy, int32_t M, int32_t N, int32_t K, int32_t act, int32_t out_f32) {
-  if (M < 0 || N <= 0 || K <= 0 || (N % 128) || (K % G16_KALIGN) || ldx < K || ldw < K || ldy < N) return RB_EINVAL;
-  if ((ldx & 7) || (ldw & 7) || (ldy & 7) || ((uintptr_t)Y & 15) || !X || !W || !b || !Y) return RB_EINVAL;
+namespace {
+rb_status gemm_bf16_impl(void* stream, const void* X, int32_t ldx, const void* W, int32_t ldw, const float* b,
+                         void* Y, int32_t ldy, int32_t M, int32_t N, int32_t K, int32_t act, int32_t out_f32,
+                         OutMap om) {
+  if (M < 0 || N <= 0 || K <= 0 || (N % 128) || (K % G16_KALIGN) || ldx < K || ldw < K) return RB_EINVAL;
+  if ((ldx & 7) || (ldw & 7) || !X || !W || !b) return RB_EINVAL;
   // operand byte offsets within a 256-row tile are 32-bit
   if ((int64_t)ldx * 512 >= ((int64_t)1 << 31) || (int64_t)ldw * 512 >= ((int64_t)1 << 31)) return RB_EINVAL;
   if (act != RB_ACT_NONE && act != RB_ACT_RELU && act != RB_ACT_SIGMOID) return RB_EINVAL;
@@ -1928,9 +1970,9 @@ rb_status rb_k_gemm_bf16(void* stream, const void* X, int32_t ldx, const void* W
 #define RB_PICK(BM, BN, WM, WN, NT, BK, S, P)                                                                   \
   do {                                                                                                          \
     if (xcd)                                                                                                    \
-      launch_gemm_bf16<BM, BN, WM, WN, NT, BK, S, 1, P>(s, x, ldx, w, ldw, b, Y, ldy, M, N, K, act, out_f32, cus); \
+      launch_gemm_bf16<BM, BN, WM, WN, NT, BK, S, 1, P>(s, x, ldx, w, ldw, b, Y, ldy, M, N, K, act, out_f32, cus, om); \
     else                                                                                                        \
-      launch_gemm_bf16<BM, BN, WM, WN, NT, BK, S, 0, P>(s, x, ldx, w, ldw, b, Y, ldy, M, N, K, act, out_f32, cus); \
+      launch_gemm_bf16<BM, BN, WM, WN, NT, BK, S, 0, P>(s, x, ldx, w, ldw, b, Y, ldy, M, N, K, act, out_f32, cus, om); \
   } while (0)
   auto persist = [&](int bm, int bn, int bk, int st) {
     const int64_t tiles = ((M + bm - 1) / bm) * (int64_t)(N / bn);
@@ -1953,13 +1995,28 @@ rb_status rb_k_gemm_bf16(void* stream, const void* X, int32_t ldx, const void* W
 #undef RB_PICK
   return launch_status();
 }
+}  // namespace
 
-rb_status rb_k_gemm_f32(void* stream, const float* X, int32_t ldx, const float* W, int32_t ldw, const float* b,
+rb_status rb_k_gemm_bf16(void* stream, const void* X, int32_t ldx, const void* W, int32_t ldw, const float* b,
+                         void* Y, int32_t ldy, int32_t M, int32_t N, int32_t K, int32_t act, int32_t out_f32) {
+  if (ldy < N || (ldy & 7) || ((uintptr_t)Y & 15) || !Y) return RB_EINVAL;
+  return gemm_bf16_impl(stream, X, ldx, W, ldw, b, Y, ldy, M, N, K, act, out_f32, OutMap{});
+}
+
+rb_status rb_k_gemm_bf16_rows(void* stream, const void* X, int32_t ldx, const void* W, int32_t ldw, const float* b,
+                              int32_t M, int32_t N, int32_t K, int32_t act, const rb_k_row* rows, int32_t d_out,
+                              float* out) {
+  if (!rows || !out || d_out < 1 || d_out > N) return RB_EINVAL;
+  return gemm_bf16_impl(stream, X, ldx, W, ldw, b, nullptr, N, M, N, K, act, 1, OutMap{rows, out, d_out});
+}
+
+namespace {
+rb_status gemm_f32_impl(void* stream, const float* X, int32_t ldx, const float* W, int32_t ldw, const float* b,
                         float* Y, int32_t ldy, int32_t M, int32_t N, int32_t K, int32_t act,
-                        const rb_k_row* skip_rows, int32_t skip_T) {
-  if (M < 0 || N <= 0 || K <= 0 || (N % 64) || (K % G32_KALIGN) || ldx < K || ldw < K || ldy < N) return RB_EINVAL;
-  if ((ldx & 3) || (ldw & 3) || (ldy & 3) || !X || !W || !b || !Y) return RB_EINVAL;
-  if (((uintptr_t)X & 15) || ((uintptr_t)W & 15) || ((uintptr_t)Y & 15)) return RB_EINVAL;
+                        const rb_k_row* skip_rows, int32_t skip_T, OutMap om) {
+  if (M < 0 || N <= 0 || K <= 0 || (N % 64) || (K % G32_KALIGN) || ldx < K || ldw < K) return RB_EINVAL;
+  if ((ldx & 3) || (ldw & 3) || !X || !W || !b) return RB_EINVAL;
+  if (((uintptr_t)X & 15) || ((uintptr_t)W & 15)) return RB_EINVAL;
   // operand byte offsets within a 64-row tile are 32-bit
   if ((int64_t)ldx * 4 * G32_BM >= ((int64_t)1 << 31) || (int64_t)ldw * 4 * 64 >= ((int64_t)1 << 31)) return RB_EINVAL;
   if (act != RB_ACT_NONE && act != RB_ACT_RELU && act != RB_ACT_SIGMOID) return RB_EINVAL;
@@ -1976,11 +2033,26 @@ rb_status rb_k_gemm_f32(void* stream, const float* X, int32_t ldx, const float* 
   const bool xcd = (int64_t)N * K * 4 <= (4 << 20);
   if (xcd)
     launch_gemm<float, G32_BM, 64, 32, 32, 256, 64, 3, 1>(s, X, ldx, W, ldw, b, Y, ldy, M, N, K, act, true, skip_rows,
-                                                          skip_T);
+                                                          skip_T, 0, om);
   else
     launch_gemm<float, G32_BM, 64, 32, 32, 256, 64, 3, 0>(s, X, ldx, W, ldw, b, Y, ldy, M, N, K, act, true, skip_rows,
-                                                          skip_T);
+                                                          skip_T, 0, om);
   return launch_status();
+}
+}  // namespace
+
+rb_status rb_k_gemm_f32(void* stream, const float* X, int32_t ldx, const float* W, int32_t ldw, const float* b,
+                        float* Y, int32_t ldy, int32_t M, int32_t N, int32_t K, int32_t act,
+                        const rb_k_row* skip_rows, int32_t skip_T) {
+  if (ldy < N || (ldy & 3) || ((uintptr_t)Y & 15) || !Y) return RB_EINVAL;
+  return gemm_f32_impl(stream, X, ldx, W, ldw, b, Y, ldy, M, N, K, act, skip_rows, skip_T, OutMap{});
+}
+
+rb_status rb_k_gemm_f32_rows(void* stream, const float* X, int32_t ldx, const float* W, int32_t ldw, const float* b,
+                             int32_t M, int32_t N, int32_t K, int32_t act, const rb_k_row* rows, int32_t d_out,
+                             float* out) {
+  if (!rows || !out || d_out < 1 || d_out > N) return RB_EINVAL;
+  return gemm_f32_impl(stream, X, ldx, W, ldw, b, nullptr, N, M, N, K, act, nullptr, 0, OutMap{rows, out, d_out});
 }
 
 rb_status rb_k_head(void* stream, const rb_k_row* rows, int32_t n_rows_total, const void* H, int32_t ldh,

@@ -707,13 +707,23 @@ rb_status run_chain(rb_sched* s, hipStream_t st_h, const rb_queue* q, int n_batc
   // otherwise a last hidden layer of 256 outputs and a 256-input head in one
   // kernel (bit-identical to the layer and the head run separately)
   const bool ghead = !tail && gemm_head(m);
+  // a chain that ends in the split writes its last layer straight into the
+  // requests' output rows (bit-identical to the layer and the split)
+  const bool rows_out = !m->head_last && m->kind != RB_MODEL_SEQPOOL;
   void* h = w->X;
   int ldh = Kp0;
   for (size_t i = 0; i < nL - (tail ? 2 : 0) - (ghead ? 1 : 0); ++i) {
     const DevLayer& L = m->layers[i];
     const bool last = (i + 1 == nL) && !m->head_last;
     void* y = last ? (void*)w->Y : (i % 2 == 0 ? w->A : w->B);
-    if (bf16) {
+    if (last && rows_out) {
+      if (bf16)
+        RB_LAUNCH(s, st_h, "gemm_bf16", rb_k_gemm_bf16_rows(hs, h, ldh, L.w, L.Kp, L.b, (int)Ml, L.Np, L.Kp, L.act,
+                                                            w->rows, m->d_out, out));
+      else
+        RB_LAUNCH(s, st_h, "gemm_f32", rb_k_gemm_f32_rows(hs, (const float*)h, ldh, (const float*)L.w, L.Kp, L.b,
+                                                          (int)Ml, L.Np, L.Kp, L.act, w->rows, m->d_out, out));
+    } else if (bf16) {
       RB_LAUNCH(s, st_h, "gemm_bf16", rb_k_gemm_bf16(hs, h, ldh, L.w, L.Kp, L.b, y, L.Np, (int)Ml, L.Np, L.Kp, L.act,
                                                last ? 1 : 0));
     } else {
@@ -742,8 +752,6 @@ rb_status run_chain(rb_sched* s, hipStream_t st_h, const rb_queue* q, int n_batc
     RB_LAUNCH(s, st_h, "seqpool", rb_k_seqpool(hs, w->rows, (int)slots, q->bucket, pack ? std::max<int64_t>(Ml, 1) : 0,
                                          (const float*)h, ldh, m->sp_in, m->sp_w, m->sp_b, m->sp_out, m->sp_act,
                                          out));
-  } else {
-    RB_LAUNCH(s, st_h, "split", rb_k_split(hs, w->rows, (int)slots, w->Y, ldh, m->d_out, out));
   }
   return RB_OK;
 }

@@ -65,6 +65,14 @@ rb_status rb_k_head(void*, const rb_k_row*, int32_t, const void*, int32_t, const
                     float*) {
   reached("rb_k_head");
 }
+rb_status rb_k_gemm_bf16_rows(void*, const void*, int32_t, const void*, int32_t, const float*, int32_t, int32_t,
+                              int32_t, int32_t, const rb_k_row*, int32_t, float*) {
+  reached("rb_k_gemm_bf16_rows");
+}
+rb_status rb_k_gemm_f32_rows(void*, const float*, int32_t, const float*, int32_t, const float*, int32_t, int32_t,
+                             int32_t, int32_t, const rb_k_row*, int32_t, float*) {
+  reached("rb_k_gemm_f32_rows");
+}
 rb_status rb_k_gemm_head(void*, const void*, int32_t, const void*, int32_t, const float*, int32_t, int32_t, int32_t,
                          const rb_k_row*, const void*, float, int32_t, float*) {
   reached("rb_k_gemm_head");

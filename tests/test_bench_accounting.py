@@ -4,7 +4,7 @@ batch sizes and the model's real dimensions, the weights once per launch group
 (one queue's batches inside one launch window), and the split of the layers
 between the kernels that run them (two GEMM layers and the fused last layer
 with its head for the ranking MLP, the opt-in fused tail, the three layers of
-the large MLP)."""
+the large MLP, the last of which writes the requests' outputs itself)."""
 import numpy as np
 import pytest
 
@@ -87,8 +87,11 @@ def test_large_mlp_weights_once_per_launch_group(ctx):
     layers = [(4096, 8192), (8192, 8192), (8192, 4096)]
     assert work["gemm_bf16"]["flops"] == sum(2 * rows * k * n for k, n in layers)
     g = _groups(logd)
-    assert work["gemm_bf16"]["bytes"] == 2 * sum(rows * (k + n) + g * k * n for k, n in layers)
     real = int(t.n_rows.sum())
+    # the last layer writes only the real rows' fp32 outputs, through the row
+    # map, into the requests' output rows (no separate split)
+    assert "split" not in work
+    assert work["gemm_bf16"]["bytes"] == (2 * sum(rows * (k + n) + g * k * n for k, n in layers[:-1])
+                                          + 2 * (rows * 8192 + g * 8192 * 4096) + real * 4096 * 4 + rows * 32)
     # real fp32 inputs read once, every padded row written in bf16, the row map
     assert work["assemble"]["bytes"] == real * 4096 * 4 + rows * 4096 * 2 + rows * 32
-    assert work["split"]["bytes"] == rows * 32 + real * 4096 * 8

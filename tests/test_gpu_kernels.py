@@ -705,6 +705,69 @@ def test_seqpool_matches_oracle(S, T, D):
         assert np.max(np.abs(o[s] - ref)) <= 1e-5 * np.max(np.abs(ref)), s
 
 
+@pytest.mark.parametrize("dt,M,N,K,d_out,gap", [
+    ("bf16", 1000, 512, 256, 512, 0), ("bf16", 300, 4096, 512, 4096, 0), ("bf16", 4133, 256, 1728, 250, 3),
+    ("bf16", 77, 128, 64, 7, 1), ("f32", 700, 64, 64, 16, 0), ("f32", 1234, 1024, 256, 1000, 2),
+    ("f32", 33, 64, 32, 3, 5)])
+def test_gemm_rows_out_bit_identical_to_gemm_and_split(dt, M, N, K, d_out, gap):
+    # the last layer writing each real row's first d_out fp32 outputs through
+    # the row map against the layer into Y followed by rb_k_split: the same
+    # bits at every output position, nothing written for padding rows, past
+    # d_out or between rows (gaps leave output offsets that are not multiples
+    # of 4 floats: the element path)
+    rng = np.random.default_rng(31)
+    gaps = rng.integers(0, gap + 1, size=M)
+    off = np.cumsum(np.concatenate([[0], (d_out + gaps)[:-1]]))
+    out_idx = np.where(rng.random(M) < 0.85, off, -1)
+    rows = _rows_dev(np.zeros(M), np.zeros(M), out_idx)
+    n_out = int(off[-1]) + d_out + 8
+    b = _dev(rng.uniform(-0.5, 0.5, N).astype(np.float32))
+    st = _stream()
+    Y = torch.empty((M, N), dtype=torch.float32, device=DEV)
+    ref = torch.full((n_out,), -7.0, device=DEV)
+    got = torch.full((n_out,), -7.0, device=DEV)
+    lib = rb.lib()
+    if dt == "bf16":
+        Xd, _ = _bf16_dev(rng.standard_normal((M, K)))
+        Wd, _ = _bf16_dev(rng.standard_normal((N, K)) / np.sqrt(K))
+        rb.check(lib.rb_k_gemm_bf16(st, rb.dptr(Xd), K, rb.dptr(Wd), K, rb.dptr(b), rb.dptr(Y), N, M, N, K,
+                                    rb.RB_ACT_NONE, 1), "gemm")
+        rb.check(lib.rb_k_gemm_bf16_rows(st, rb.dptr(Xd), K, rb.dptr(Wd), K, rb.dptr(b), M, N, K, rb.RB_ACT_NONE,
+                                         rb.dptr(rows), d_out, rb.dptr(got)), "gemm rows")
+    else:
+        Xd = _dev(rng.standard_normal((M, K)).astype(np.float32))
+        Wd = _dev((rng.standard_normal((N, K)) / np.sqrt(K)).astype(np.float32))
+        rb.check(lib.rb_k_gemm_f32(st, rb.dptr(Xd), K, rb.dptr(Wd), K, rb.dptr(b), rb.dptr(Y), N, M, N, K,
+                                   rb.RB_ACT_RELU, None, 0), "gemm")
+        rb.check(lib.rb_k_gemm_f32_rows(st, rb.dptr(Xd), K, rb.dptr(Wd), K, rb.dptr(b), M, N, K, rb.RB_ACT_RELU,
+                                        rb.dptr(rows), d_out, rb.dptr(got)), "gemm rows")
+    rb.check(lib.rb_k_split(st, rb.dptr(rows), M, rb.dptr(Y), N, d_out, rb.dptr(ref)), "split")
+    torch.cuda.synchronize()
+    g, r = got.cpu().numpy(), ref.cpu().numpy()
+    assert np.array_equal(g.view(np.uint32), r.view(np.uint32))
+    assert np.sum(g != -7.0) <= int(np.sum(out_idx >= 0)) * d_out
+
+
+def test_gemm_rows_out_rejects_bad_arguments():
+    st = _stream()
+    X = torch.zeros((64, 64), dtype=torch.int16, device=DEV)
+    W = torch.zeros((128, 64), dtype=torch.int16, device=DEV)
+    b = torch.zeros(128, device=DEV)
+    out = torch.zeros(64 * 128, device=DEV)
+    rows = _rows_dev(np.zeros(64), np.zeros(64), np.arange(64) * 128)
+    lib = rb.lib()
+
+    def call(N=128, d_out=128, rp=None):
+        return lib.rb_k_gemm_bf16_rows(st, rb.dptr(X), 64, rb.dptr(W), 64, rb.dptr(b), 64, N, 64, rb.RB_ACT_NONE,
+                                       rb.dptr(rows) if rp is None else rp, d_out, rb.dptr(out))
+    assert call() == rb.RB_OK
+    assert call(d_out=129) == rb.RB_EINVAL   # more outputs than the layer has
+    assert call(d_out=0) == rb.RB_EINVAL
+    assert call(rp=0) == rb.RB_EINVAL        # no row map
+    assert call(N=96) == rb.RB_EINVAL        # N not a multiple of 128 (bf16)
+    torch.cuda.synchronize()
+
+
 @pytest.mark.parametrize("d_out,ldy", [(64, 64), (4096, 4096), (32, 64), (7, 8)])
 def test_split_vector_and_scalar_paths(d_out, ldy):
     # output offsets mix multiples of 4 floats (16-byte path) and others
