@@ -12,10 +12,16 @@
 //   assemble  gather request rows into the padded batch tensor (optional
 //             fp32 -> bf16 cast), or
 //   embbag    sum-pool each row's embedding bags (ranking models)
-//   gemm      dense layers with fused bias + activation (bf16 or fp32 MFMA)
+//   gemm      dense layers with fused bias + activation (bf16 or fp32 MFMA);
+//             the last layer of a chain without a head writes its real rows
+//             straight into the requests' outputs through the row map (the
+//             split fused in)
+//   gemm_head the last hidden layer of 256 outputs and a narrow head in one
+//             kernel, or
 //   head /    narrow last layer or masked mean-pool + softmax head, writing
 //   seqpool   straight to each request's output rows
-//   split     copy real rows to their requests' outputs (padding dropped)
+//   split     copy real rows to their requests' outputs (padding dropped;
+//             the unfused form, kept for the C ABI)
 //
 // Every row is computed the same way whatever batch it sits in (one tile
 // shape and k order per layer, no row-count-dependent split of the sum), so a

@@ -643,7 +643,8 @@ rb_status ensure_work(rb_sched* s, rb_model* m, int slot, int64_t rows, int64_t 
 }
 
 // Launch chain of one group on stream st_h: route -> assemble | embbag ->
-// layers -> head | seqpool | split.
+// layers -> head (alone or fused with the last hidden layer) | seqpool, or a
+// last layer that writes the requests' outputs itself.
 // A bf16 model whose last two hidden layers are ReLU layers of 512 and 256
 // outputs ahead of a narrow head of 256 inputs: rb_k_mlp_tail runs them.
 bool fused_tail(const rb_model* m) {
