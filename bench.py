@@ -450,8 +450,9 @@ def version_swap(w, t, a, dt, ctx, args):
 def _chain_ns(sched, run, reps):
     """Median device time (ns) of `run` (one replay), each repetition on its
     own: the device drained before and after it, HIP events on the
-    scheduler's stream around it (the host's enqueueing included, as a
-    served batch would see it)."""
+    scheduler's stream around it (the library's host work of building and
+    enqueueing the chain included, as a served batch would see it; the
+    binding's argument marshalling done beforehand)."""
     import torch
     st = torch.cuda.ExternalStream(sched.stream())
     e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
@@ -543,8 +544,8 @@ def calibrate_latency(w, t, a, dt, ctx, dep, window, seq_pack=False, n_streams=1
                         out_off = cdep.out_offsets(st)
                         out = torch.empty(int(out_off[-1]), dtype=torch.float32, device="cuda")
 
-                        def run(k, cdep=cdep, out=out, out_off=out_off):
-                            return cdep.sched.sim_run(
+                        def prep(k, cdep=cdep, out=out, out_off=out_off):
+                            return cdep.sched.prepare_sim_run(
                                 cdep.servables, np.zeros(k, np.int32), np.zeros(k, np.int64), st.n_rows[:k],
                                 None if st.seq_lens is None else cdep.max_len(st)[:k], dense=dt.dense,
                                 dense_off=a.dense_off[:k + 1], lens=dt.lens,
@@ -554,23 +555,26 @@ def calibrate_latency(w, t, a, dt, ctx, dep, window, seq_pack=False, n_streams=1
                     else:
                         sdt = cdep.upload(st, sa)
 
-                        def run(k, cdep=cdep, sdt=sdt):
-                            return cdep.sched.sim_run(
+                        def prep(k, cdep=cdep, sdt=sdt):
+                            return cdep.sched.prepare_sim_run(
                                 cdep.servables, np.zeros(k, np.int32), np.zeros(k, np.int64), sdt.n_rows[:k],
                                 None if sdt.max_len is None else sdt.max_len[:k], dense=sdt.dense,
                                 dense_off=sdt.dense_off[:k + 1], lens=sdt.lens,
                                 lens_off=None if sdt.lens_off is None else sdt.lens_off[:k + 1], ids=sdt.ids,
                                 ids_off=None if sdt.ids_off is None else sdt.ids_off[:k + 1], out=sdt.out,
                                 out_off=sdt.out_off[:k + 1])
+                    # the calls' arguments are marshalled beforehand, so the
+                    # timings hold the library call and the device work only
                     if win == 1:
                         k1 = ends[n1 - 1]
-                        run(k1)
-                        times["c1"] = _chain_ns(cdep.sched, lambda: run(ends[0]), 20)
-                        times["T1"] = _chain_ns(cdep.sched, lambda: run(k1), 3) / n1
+                        run1, runk = prep(ends[0]), prep(k1)
+                        runk()
+                        times["c1"] = _chain_ns(cdep.sched, run1, 20)
+                        times["T1"] = _chain_ns(cdep.sched, runk, 3) / n1
                     else:
-                        kall = len(idx)
-                        run(kall)
-                        times["TW"] = _chain_ns(cdep.sched, lambda: [run(kall) for _ in range(reps)], 3) / reps
+                        runa = prep(len(idx))
+                        runa()
+                        times["TW"] = _chain_ns(cdep.sched, lambda: [runa() for _ in range(reps)], 3) / reps
                 finally:
                     cdep.destroy()
             S = max(1.0, (times["TW"] - nw * times["T1"]) / (nb - nw)) if nb > nw else times["T1"]

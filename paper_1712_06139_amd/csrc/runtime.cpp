@@ -851,29 +851,46 @@ rb_status flush_chunk(rb_sched* s) {
   for (auto& win : s->chunk)
     for (Group& g : win) slot_hold(*sl, g.q->m);
   if (!hip_ok(hipMemcpyAsync(sl->dev, sl->host, off, hipMemcpyHostToDevice, s->stream))) return RB_EDEVICE;
-  // lanes start after the copy; the main stream (and the slot's event) after
-  // every lane's chains
-  if (!s->lanes.empty()) {
-    hipEventRecord(s->ev_copy, s->stream);
-    for (hipStream_t l : s->lanes) hipStreamWaitEvent(l, s->ev_copy, 0);
-  }
   std::vector<int64_t> lin;
   for (auto& win : s->chunk)
     for (Group& g : win) lin.push_back(g.q->m->lineage);
   std::sort(lin.begin(), lin.end());
   const size_t n_lin = (size_t)(std::unique(lin.begin(), lin.end()) - lin.begin());
   const bool pipe = s->lanes.size() >= (size_t)PIPE_SLOTS * n_lin;
-  size_t gi = 0;
+  // every group's work-buffer slot and launch stream, in launch order. A
+  // chunk of one group runs on the main stream: nothing could overlap it, and
+  // cross-stream events only add latency (its slot's earlier work on a lane
+  // was joined into the main stream, and later lane work waits for a copy
+  // enqueued after it, so the slot's buffers stay in stream order).
+  std::vector<std::pair<int, hipStream_t>> where;
   for (auto& win : s->chunk)
     for (Group& g : win) {
       const int slot = next_slot(s, g.q->m, pipe);
-      st = run_group(s, lane_for(s, g.q->m, slot), slot, g, (const rb_k_batch*)(sl->dev + offs[gi].first),
+      where.push_back({slot, lane_for(s, g.q->m, slot)});
+    }
+  if (where.size() == 1) where[0].second = s->stream;
+  // the lanes this chunk launches on start after the copy; the main stream
+  // (and the slot's event) after each of them. Lanes the chunk does not use
+  // are left alone: their earlier work was joined by their own chunks.
+  std::vector<size_t> used;
+  if (!s->lanes.empty()) {
+    for (const auto& w : where) {
+      const size_t i = (size_t)(std::find(s->lanes.begin(), s->lanes.end(), w.second) - s->lanes.begin());
+      if (i < s->lanes.size() && std::find(used.begin(), used.end(), i) == used.end()) used.push_back(i);
+    }
+    hipEventRecord(s->ev_copy, s->stream);
+    for (size_t i : used) hipStreamWaitEvent(s->lanes[i], s->ev_copy, 0);
+  }
+  size_t gi = 0;
+  for (auto& win : s->chunk)
+    for (Group& g : win) {
+      st = run_group(s, where[gi].second, where[gi].first, g, (const rb_k_batch*)(sl->dev + offs[gi].first),
                      (const rb_k_req*)(sl->dev + offs[gi].second), s->a_dense, s->a_dense_len, s->a_lens,
                      s->a_lens_len, s->a_ids, s->a_ids_len, s->a_out, s->a_out_len);
       ++gi;
       if (st != RB_OK) return st;
     }
-  for (size_t i = 0; i < s->lanes.size(); ++i) {
+  for (size_t i : used) {
     hipEventRecord(s->lane_done[i], s->lanes[i]);
     hipStreamWaitEvent(s->stream, s->lane_done[i], 0);
   }

@@ -416,6 +416,15 @@ class Sched:
                 lens=None, lens_off=None, ids=None, ids_off=None, out=None, out_off=None) -> dict:
         """Replay a trace. Host arrays are numpy; dense/lens/ids/out are device
         tensors (or None in no-device mode). Returns the batch log."""
+        return self.prepare_sim_run(servables, servable, arrival_ns, n_rows, max_len, dense, dense_off, lens,
+                                    lens_off, ids, ids_off, out, out_off)()
+
+    def prepare_sim_run(self, servables: Sequence[Sequence[Queue]], servable: np.ndarray, arrival_ns: np.ndarray,
+                        n_rows: np.ndarray, max_len: Optional[np.ndarray] = None, dense=None, dense_off=None,
+                        lens=None, lens_off=None, ids=None, ids_off=None, out=None, out_off=None):
+        """The arguments of sim_run marshalled once; returns a function that
+        makes the rb_sim_run call with them (again on every call) and returns
+        the batch log, so that a caller can time the library call alone."""
         n = int(len(n_rows))
         keep = []
 
@@ -453,10 +462,16 @@ class Sched:
         L.max_batches = n
         for k, v in lg.items():
             setattr(L, k, _ptr(v, p_i64 if v.dtype == np.int64 else p_i32))
-        check(_lib().rb_sim_run(self.h, sv, len(servables), C.byref(t), C.byref(L)), "rb_sim_run")
-        nb = int(L.n_batches)
-        res = {k: (v[:nb] if k.startswith("b_") and k != "b_req_begin" and k != "b_reqs" else v)
-               for k, v in lg.items()}
-        res["b_req_begin"] = lg["b_req_begin"][:nb + 1]
-        res["n_batches"] = nb
-        return res
+        f = _lib().rb_sim_run
+        ns = len(servables)
+
+        def call() -> dict:
+            check(f(self.h, sv, ns, C.byref(t), C.byref(L)), "rb_sim_run")
+            nb = int(L.n_batches)
+            res = {k: (v[:nb] if k.startswith("b_") and k != "b_req_begin" and k != "b_reqs" else v)
+                   for k, v in lg.items()}
+            res["b_req_begin"] = lg["b_req_begin"][:nb + 1]
+            res["n_batches"] = nb
+            return res
+        call.keep = keep
+        return call
