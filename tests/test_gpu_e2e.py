@@ -124,6 +124,40 @@ def test_outputs_independent_of_stream_count(ctx, name, n_streams):
     check_outputs(name, t, a, outk, out_off, range(0, t.n, 7))
 
 
+def test_single_group_chunks_and_lanes_share_work_buffers(ctx):
+    # with lanes, a replay chunk of one launch group runs on the scheduler's
+    # own stream while chunks of several groups run on the lanes, with the same
+    # work buffers: replays of both kinds enqueued back to back with no sync in
+    # between give the same bits as one stream
+    name = "ranking"
+    n = min(PREFIX[name], 600)
+    w, t, a, qindex, log1, out1, _ = run(ctx, name, n, window=16)
+    t, a = trace_and_arenas(name, n)
+    dep = Deployment(w, ctx, device=True, window_batches=16, service_ns=service_table(w), n_streams=8)
+    try:
+        dt = dep.upload(t, a)
+        k = 1
+        while k < n and int(t.n_rows[:k + 1].sum()) <= 512:
+            k += 1
+
+        def prefix(k):
+            return dep.sched.sim_run(dep.servables, t.servable[:k], t.arrival_ns[:k], t.n_rows[:k], None,
+                                     dense=dt.dense, dense_off=a.dense_off[:k + 1], lens=dt.lens,
+                                     lens_off=a.lens_off[:k + 1], ids=dt.ids, ids_off=a.ids_off[:k + 1],
+                                     out=dt.out, out_off=dt.out_off[:k + 1])
+        logs = []
+        for _ in range(3):
+            logs.append(dep.replay(dt))
+            assert int(prefix(k)["n_batches"]) == 1
+        logs.append(dep.replay(dt))
+        dep.sched.sync()
+        out8 = dt.out.cpu().numpy()
+    finally:
+        dep.destroy()
+    assert all(lib_batches(lg, qindex) == lib_batches(log1, qindex) for lg in logs)
+    assert np.array_equal(out1, out8)
+
+
 @pytest.mark.parametrize("name,window", [("ranking", 8), ("multi_tenant", 16)])
 def test_embedding_dedup_bit_identical(ctx, name, window):
     # ranking models with each block's distinct table rows gathered once:
