@@ -1151,7 +1151,7 @@ __device__ __forceinline__ void gemm_mfma(const TI* __restrict__ X, int ldx, con
             const int64_t o = ro[i][g];
             if (o >= 0) {
               float* dst = om.out + o + colq;
-              if (colq + 3 < om.d_out && ((o + colq) & 3) == 0) {
+              if (colq + 3 < om.d_out && ((uintptr_t)dst & 15) == 0) {
                 const f32x4_t v = {q[0], q[1], q[2], q[3]};
                 __builtin_nontemporal_store(v, (f32x4_t*)dst);
               } else {
