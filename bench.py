@@ -447,6 +447,16 @@ def version_swap(w, t, a, dt, ctx, args):
             "ms_per_step_loading": {"p50": pct(busy, 50), "p99": pct(busy, 99), "max": round(max(busy), 3)}}
 
 
+def chain_model_fit(c1, T1, TW, nb, nw):
+    """The launch-window device model from three timings: c1 a lone batch's
+    chain (b + S + c), T1 one batch per window back to back (b + S per
+    batch), TW nb batches in nw windows back to back (nw b + nb S). Returns
+    (S, b, c): the per-batch time, the chain's fixed device time and its
+    tail, clamped at S >= 1 ns and b, c >= 0."""
+    S = max(1.0, (TW - nw * T1) / (nb - nw)) if nb > nw else T1
+    return S, max(0.0, T1 - S), max(0.0, c1 - T1)
+
+
 def _chain_ns(sched, run, reps):
     """Median device time (ns) of `run` (one replay), each repetition on its
     own: the device drained before and after it, HIP events on the
@@ -577,9 +587,7 @@ def calibrate_latency(w, t, a, dt, ctx, dep, window, seq_pack=False, n_streams=1
                         times["TW"] = _chain_ns(cdep.sched, lambda: [runa() for _ in range(reps)], 3) / reps
                 finally:
                     cdep.destroy()
-            S = max(1.0, (times["TW"] - nw * times["T1"]) / (nb - nw)) if nb > nw else times["T1"]
-            b_ = max(0.0, times["T1"] - S)
-            c_ = max(0.0, times["c1"] - times["T1"])
+            S, b_, c_ = chain_model_fit(times["c1"], times["T1"], times["TW"], nb, nw)
             fit[P] = {"S": S, "b": b_, "c": c_, "c1": times["c1"], "T1": times["T1"], "TW": times["TW"],
                       "batches": nb, "windows": nw}
         ps = sorted(fit)

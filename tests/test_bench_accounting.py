@@ -4,7 +4,9 @@ batch sizes and the model's real dimensions, the weights once per launch group
 (one queue's batches inside one launch window), and the split of the layers
 between the kernels that run them (two GEMM layers and the fused last layer
 with its head for the ranking MLP, the opt-in fused tail, the three layers of
-the large MLP, the last of which writes the requests' outputs itself)."""
+the large MLP, the last of which writes the requests' outputs itself); and the
+latency calibration's fit of the launch-window device model, tied to the
+library's simulated clock."""
 import numpy as np
 import pytest
 
@@ -95,3 +97,29 @@ def test_large_mlp_weights_once_per_launch_group(ctx):
                                           + 2 * (rows * 8192 + g * 8192 * 4096) + real * 4096 * 4 + rows * 32)
     # real fp32 inputs read once, every padded row written in bf16, the row map
     assert work["assemble"]["bytes"] == real * 4096 * 4 + rows * 4096 * 2 + rows * 32
+
+
+def test_chain_model_fit_recovers_the_device_model(ctx):
+    # the three timings a device with chain time b, per-batch time S and tail
+    # c would give are fitted back to (S, b, c); and the library's simulated
+    # clock, given those values, completes a lone request exactly one lone
+    # chain c1 = b + S + c after it closes
+    b, S, c = 30_000, 5_000, 40_000
+    nb, nw = 100, 2
+    c1, T1, TW = b + S + c, b + S, nw * b + nb * S
+    assert bench.chain_model_fit(c1, T1, TW, nb, nw) == (S, b, c)
+    assert bench.chain_model_fit(c1, T1, nw * T1, nb, nw) == (1.0, T1 - 1.0, c)  # S clamped
+    assert bench.chain_model_fit(T1 - 5, T1, TW, nb, nw)[2] == 0.0                   # tail clamped
+    svc = [0] * 513
+    svc[512] = S
+    sched = rb.Sched(ctx, device=False, window_batches=W)
+    m = rb.Model(ctx, "mlp", "f32", [(None, None, "none")], shapes=[(4, 4)])
+    q = rb.Queue(sched, m, 512, (512,), None, 0, svc, b, c)
+    try:
+        log = sched.sim_run([[q]], np.array([0]), np.array([1_000]), np.array([512]))
+        assert int(log["n_batches"]) == 1
+        assert int(log["req_done_ns"][0]) - 1_000 == c1
+    finally:
+        q.destroy()
+        sched.destroy()
+        m.destroy()
