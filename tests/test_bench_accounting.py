@@ -123,3 +123,18 @@ def test_chain_model_fit_recovers_the_device_model(ctx):
         q.destroy()
         sched.destroy()
         m.destroy()
+
+
+def test_bench_refuses_more_than_one_gpu():
+    # one GPU only: a request for several exits with a message before any
+    # device work (no GPU is needed to check this)
+    import os
+    import subprocess
+    import sys
+    root = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+    for args, env in ((["--gpus", "2"], {}), ([], {"WORLD_SIZE": "4"})):
+        r = subprocess.run([sys.executable, os.path.join(root, "bench.py"), *args], capture_output=True, text=True,
+                           timeout=120, env=dict(os.environ, **env))
+        assert r.returncode != 0
+        assert "one MI355X only" in r.stderr
+        assert r.stdout.strip() == ""
