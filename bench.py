@@ -284,6 +284,42 @@ def cpu_baseline(w, t, a, seconds):
                              "sample": f"first {n2} requests ({ex2} examples), {el2:.1f} s"}}
 
 
+def cpu_latency(w, t, ns_per_example, n_max=20_000):
+    """Per-request latency if the CPU oracle served the trace: one server,
+    requests run unbatched in arrival order (FIFO), each taking n_r times the
+    oracle's measured time per example. Count-only workloads: Poisson arrivals
+    at rho x this server's capacity (rho 0.5 and 0.9), as for the GPU; workloads
+    with batch timeouts: the trace's own arrivals, where a utilization above 1
+    means the queue grows without bound over the trace (reported as unstable,
+    with the percentiles over the simulated requests)."""
+    import synth
+    n = min(n_max, t.n)
+    svc = t.n_rows[:n].astype(np.float64) * ns_per_example
+
+    def fifo(arrival):
+        arrival = np.asarray(arrival[:n], np.float64)
+        lat = np.empty(n)
+        free = -np.inf
+        for r in range(n):
+            free = max(arrival[r], free) + svc[r]
+            lat[r] = free - arrival[r]
+        return round(nearest_rank(lat, 0.5) / 1e3, 1), round(nearest_rank(lat, 0.99) / 1e3, 1)
+    cap = 1e9 / float(svc.mean())
+    out = {"model": "one CPU server, requests unbatched in arrival order, n_r x the measured time per example",
+           "requests": n, "ns_per_example": round(ns_per_example, 1), "capacity_req_s": round(cap, 1)}
+    if any(q.timeout_ns is not None for q in w.queues):
+        util = w.rate_per_s / cap
+        p50, p99 = fifo(t.arrival_ns)
+        out["trace_arrivals"] = {"arrival_rate_req_s": w.rate_per_s, "utilization": round(util, 2),
+                                 "unstable": bool(util >= 1.0), "p50_us": p50, "p99_us": p99}
+    else:
+        for rho in (0.5, 0.9):
+            p50, p99 = fifo(synth.trace(w, n, rate_per_s=rho * cap).arrival_ns)
+            out[f"rho{rho}"] = {"arrival_rate_req_s": round(rho * cap, 1), "utilization": rho,
+                                "p50_us": p50, "p99_us": p99}
+    return out
+
+
 def serving_rate(w, t, a, ctx, models, n, seq_pack=False, window=1, tables=None, alpha=None, tail=None, rate=None):
     """The serving API with host payloads: the first n requests submitted in
     arrival order from host memory (rb_submit copies them), every launch
@@ -891,6 +927,8 @@ def main():
     if not args.no_cpu_baseline:
         log("timing the CPU oracle")
         cpu = cpu_baseline(w, t, a, args.cpu_seconds)
+        cpu["latency"] = cpu_latency(w, t, 1e9 / cpu["value"])
+        log(f"cpu latency: {json.dumps(cpu['latency'])}")
 
     dtypes = {m.dtype for m in w.models}
     out = {

@@ -138,3 +138,32 @@ def test_bench_refuses_more_than_one_gpu():
         assert r.returncode != 0
         assert "one MI355X only" in r.stderr
         assert r.stdout.strip() == ""
+
+
+@pytest.mark.parametrize("name,ns", [("multi_tenant", 2_000.0), ("multi_tenant", 200_000.0), ("small_mlp", 150_000.0)])
+def test_cpu_latency_is_a_fifo_queue(name, ns):
+    # the CPU oracle's latency model against Lindley's recursion for the same
+    # single-server FIFO queue (waiting time W_{r+1} = max(0, W_r + S_r - A_{r+1})
+    # with A the interarrival times): the same percentiles
+    w = synth.workload(name)
+    t = synth.trace(w, min(w.n_requests, 3000))
+    out = bench.cpu_latency(w, t, ns, n_max=3000)
+    n = out["requests"]
+    S = t.n_rows[:n].astype(np.float64) * ns
+
+    def lindley(arr):
+        arr = np.asarray(arr[:n], np.float64)
+        W = np.zeros(n)
+        for r in range(1, n):
+            W[r] = max(0.0, W[r - 1] + S[r - 1] - (arr[r] - arr[r - 1]))
+        lat = W + S
+        return (round(bench.nearest_rank(lat, 0.5) / 1e3, 1), round(bench.nearest_rank(lat, 0.99) / 1e3, 1))
+    if "trace_arrivals" in out:
+        got = out["trace_arrivals"]
+        assert (got["p50_us"], got["p99_us"]) == lindley(t.arrival_ns)
+        assert got["unstable"] == (w.rate_per_s * S.mean() * 1e-9 >= 1.0)
+    else:
+        for rho in (0.5, 0.9):
+            got = out[f"rho{rho}"]
+            arr = synth.trace(w, n, rate_per_s=rho * 1e9 / float(S.mean())).arrival_ns
+            assert (got["p50_us"], got["p99_us"]) == lindley(arr)
