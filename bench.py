@@ -276,12 +276,38 @@ def cpu_baseline(w, t, a, seconds):
     with threadpool_limits(limits=1):
         n, ex, el = run(seconds, t.n)
     n2, ex2, el2 = run(seconds / 4, n)
-    return {"value": ex / el, "unit": "examples/s", "cores": 1, "kind": "oracle",
+    return {"value": ex / el, "unit": "examples/s", "cores": 1, "kind": "oracle", "requests": n,
             "sample": f"first {n} requests ({ex} examples) of the same trace, unbatched fp64 forward per request "
                       f"on one thread, {el:.1f} s",
             "cpu_model": cpu_model(),
             "blas_threads": {"value": ex2 / el2, "cores": int(blas_threads),
                              "sample": f"first {n2} requests ({ex2} examples), {el2:.1f} s"}}
+
+
+def gpu_prefix_rate(dep, dt, n, reps=5):
+    """The GPU's examples/s over the first n requests of the trace (the CPU
+    oracle's sample), replayed in the bench's launch configuration with the
+    payloads in HBM: wall time of `reps` replays, synchronized on both sides."""
+    import torch
+    k = min(n, dt.n)
+
+    def cut(x, m):
+        return None if x is None else x[:m]
+    go = dep.sched.prepare_sim_run(
+        dep.servables, dt.servable[:k], dt.arrival_ns[:k], dt.n_rows[:k], cut(dt.max_len, k),
+        dense=dt.dense, dense_off=dt.dense_off[:k + 1], lens=dt.lens, lens_off=cut(dt.lens_off, k + 1),
+        ids=dt.ids, ids_off=cut(dt.ids_off, k + 1), out=dt.out, out_off=dt.out_off[:k + 1])
+    go()
+    dep.sched.sync()
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(reps):
+        go()
+    dep.sched.sync()
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    return {"value": round(int(dt.n_rows[:k].sum()) * reps / wall, 1), "unit": "examples/s", "requests": k,
+            "sample": f"first {k} requests, replayed {reps} times in the bench's launch configuration"}
 
 
 def cpu_latency(w, t, ns_per_example, n_max=20_000):
@@ -928,6 +954,8 @@ def main():
         log("timing the CPU oracle")
         cpu = cpu_baseline(w, t, a, args.cpu_seconds)
         cpu["latency"] = cpu_latency(w, t, 1e9 / cpu["value"])
+        cpu["gpu_same_sample"] = gpu_prefix_rate(dep, dt, cpu["requests"])
+        log(f"gpu on the cpu sample: {json.dumps(cpu['gpu_same_sample'])}")
         log(f"cpu latency: {json.dumps(cpu['latency'])}")
 
     dtypes = {m.dtype for m in w.models}
