@@ -390,7 +390,9 @@ constexpr int MAX_TABLES = 64;
 constexpr int EMB_SLICES = MAX_TABLES;  // table slices: one table each (up to MAX_TABLES)
 constexpr int EMB_CHUNK = 8;      // ids loaded (one per lane of a group) and gathers issued per round
 static_assert(EMB_CHUNK <= 8, "each of a group's 8 lanes loads one id of a chunk");
-// (16 or 24 ids per round, two or three per lane, measured 1.5x and 1.7x slower)
+// (4 ids per round measured 4% slower; 16 or 24, two or three per lane, 1.5x
+// and 1.7x slower; fewer workgroups per CU, capped through LDS, 1.25x to 2.8x
+// slower: the gather wants every load in flight the registers can hold)
 
 // One 8-lane group per (row, bag); lane l8 owns dims [8 l8, 8 l8 + 8) of the
 // 64-dim table rows. The grid is slice-major: workgroups [x nrb, (x + 1) nrb)
@@ -400,11 +402,15 @@ static_assert(EMB_CHUNK <= 8, "each of a group's 8 lanes loads one id of a chunk
 // hold their hot rows (all tables at once per row measured 1.5x slower, 4 or
 // 8 slices 1.2x slower).
 // A group finds its bag in the row's flat id list (bag after bag) with an
-// 8-lane sum of the preceding bag lengths, then walks the bag EMB_CHUNK ids at
-// a time: lane i loads id c + i, the ids are broadcast within the group and
-// all EMB_CHUNK gathers are issued before any is added. Sums are fp32 in id
-// order (a fixed order that depends on the bag only), stored as bf16. The
-// workgroups of slice 0 also write the rows' dense features and zero tails.
+// 8-lane sum of the preceding bag lengths. The workgroup's 32 bags are then
+// ranked by length through LDS and the group of rank p walks the bag of rank
+// p, so the 8 bags of a wave have similar lengths and its gather instructions
+// keep most lanes busy (uniform 1..20-id bags: 50 gather instructions per
+// workgroup instead of 73; 2-3% faster). A bag is walked EMB_CHUNK ids at a
+// time: lane i loads id c + i, the ids are broadcast within the group and all
+// EMB_CHUNK gathers are issued before any is added. Sums are fp32 in id order
+// (a fixed order that depends on the bag only), stored as bf16. The workgroups
+// of slice 0 also write the rows' dense features and zero tails.
 // Reads stay inside the ids arena and the tables: an id position past the
 // arena or an id outside its table sets *err = 1 and contributes nothing.
 __global__ __launch_bounds__(256) void k_embbag(const rb_k_row* __restrict__ rows, int n_rows,
@@ -420,21 +426,62 @@ __global__ __launch_bounds__(256) void k_embbag(const rb_k_row* __restrict__ row
   const int tid = threadIdx.x, g = tid >> 3, l8 = tid & 7;
   const int gbase = (tid & 63) & ~7;  // this group's first lane in the wave
   const int demb = n_tables * EMB_DIM;
-  const int row = r0 + g / gpr, t = x + n_slices * (g % gpr);
-  if (g < rpw * gpr && row < n_rows && t < n_tables) {
-    const rb_k_row rw = rows[row];
+  // 1. group g's own bag: its length (-1: no bag, -2: a padding row) and its
+  //    first id's position in the ids arena
+  __shared__ int s_key[32];
+  __shared__ int s_bag[32], s_len[32];
+  __shared__ int64_t s_id0[32];
+  int L = -1;
+  int64_t id0 = 0;
+  {
+    const int row = r0 + g / gpr, t = x + n_slices * (g % gpr);
+    if (g < rpw * gpr && row < n_rows && t < n_tables) {
+      const rb_k_row rw = rows[row];
+      if (rw.src < 0) {
+        L = -2;
+      } else {
+        int pre = 0;
+        for (int f = l8; f < t; f += 8) pre += lens[rw.lens + f];
+        pre += __shfl_xor(pre, 1);
+        pre += __shfl_xor(pre, 2);
+        pre += __shfl_xor(pre, 4);
+        L = lens[rw.lens + t];
+        id0 = rw.aux + pre;
+      }
+    }
+  }
+  // 2. the workgroup's 32 bags ranked longest first (ties by group), and
+  //    group p takes the bag of rank p: the 8 bags of a wave then have
+  //    similar lengths, so its gather instructions keep most lanes busy
+  if (l8 == 0) s_key[g] = L;
+  __syncthreads();
+  {
+    int rank = 0;
+    for (int h = l8; h < 32; h += 8) {
+      const int k = s_key[h];
+      rank += (k > L || (k == L && h < g)) ? 1 : 0;
+    }
+    rank += __shfl_xor(rank, 1);
+    rank += __shfl_xor(rank, 2);
+    rank += __shfl_xor(rank, 4);
+    if (l8 == 0) {
+      s_bag[rank] = g;
+      s_len[rank] = L;
+      s_id0[rank] = id0;
+    }
+  }
+  __syncthreads();
+  const int b = s_bag[g];
+  L = s_len[g];
+  id0 = s_id0[g];
+  // 3. the bag's walk
+  if (L != -1) {
+    const int row = r0 + b / gpr, t = x + n_slices * (b % gpr);
     u32x4_t o;
-    if (rw.src < 0) {
+    if (L == -2) {
       const uint32_t p = f2bf(pad);
       o = (u32x4_t){p | (p << 16), p | (p << 16), p | (p << 16), p | (p << 16)};
     } else {
-      int pre = 0;
-      for (int f = l8; f < t; f += 8) pre += lens[rw.lens + f];
-      pre += __shfl_xor(pre, 1);
-      pre += __shfl_xor(pre, 2);
-      pre += __shfl_xor(pre, 4);
-      const int L = lens[rw.lens + t];
-      const int64_t id0 = rw.aux + pre;
       const bf16_t* tab = tables[t];
       float acc[8];
 #pragma unroll

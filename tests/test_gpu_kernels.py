@@ -332,6 +332,43 @@ def test_embbag_matches_oracle(lens, entry):
     assert n_exact >= 0.99 * n_tot
 
 
+@pytest.mark.parametrize("entry", ["rb_k_embbag", "rb_k_embbag_dedup"])
+@pytest.mark.parametrize("cut", [1, 13, 31, 45])
+def test_embbag_ragged_row_count_and_pad_value(cut, entry):
+    # a row count that leaves the last row block part empty (groups with no
+    # bag) and a non-zero pad: real rows are bit-identical to the full call,
+    # padding rows hold pad in every bag and dense-feature column and zeros in
+    # the tail, and rows past the count are not written
+    rng = np.random.default_rng(29)
+    nt, rows_t = 26, 1000
+    kb, kr, arena, R = _make_group(rng, rb.RB_MODEL_RANKING, 4, 512, (64, 128, 256, 512), 13, 1, nt, 0,
+                                   max_n=64, lens_gen=None)
+    rows, _ = _route(rb.RB_MODEL_RANKING, kb, kr, arena, R, 13, 1, nt)
+    dev_t = [torch.randn(rows_t, 64, device=DEV).to(torch.bfloat16).view(torch.int16) for _ in range(nt)]
+    ptrs = _dev(np.array([t.data_ptr() for t in dev_t], dtype=np.uint64).view(np.int64))
+    dense, lens_d, ids = _dev(arena["dense"]), _dev(arena["lens"]), _dev(arena["ids"])
+    outs = []
+    for n, pad in ((R, 0.0), (R - cut, 1.5)):
+        X = torch.full((R, 1728), 0x7FC1, dtype=torch.int16, device=DEV)
+        err = _err()
+        rb.check(getattr(rb.lib(), entry)(_stream(), rb.dptr(rows), n, rb.dptr(lens_d), rb.dptr(ids), ids.numel(),
+                                          rb.dptr(ptrs), nt, rows_t, 64, rb.dptr(dense), 13, rb.dptr(X), 1728,
+                                          pad, rb.dptr(err)), entry)
+        torch.cuda.synchronize()
+        assert int(err.item()) == 0
+        outs.append(X.cpu().numpy())
+    full, part = outs
+    src = _rows_np(rows)["src"]
+    n = R - cut
+    real = src[:n] >= 0
+    assert (~real).any() and real.any()
+    assert np.array_equal(part[:n][real], full[:n][real])
+    pad_bits = np.int16(0x3FC0)  # 1.5 in bf16
+    assert np.all(part[:n][~real][:, :nt * 64 + 13] == pad_bits)
+    assert np.all(part[:n][~real][:, nt * 64 + 13:] == 0)
+    assert np.all(part[n:] == np.int16(0x7FC1))
+
+
 @pytest.mark.parametrize("lens", list(_LENS))
 @pytest.mark.parametrize("ids_kind", ["zipf", "uniform", "invalid"])
 def test_embbag_dedup_bit_identical(lens, ids_kind):
