@@ -351,7 +351,8 @@ rb_status rb_run_window(rb_sched* s, rb_window_info* out);
  * the scheduler because request ids are dense per scheduler (a request keeps
  * its id while its queue changes version or is held). RB_EAGAIN if its batch
  * has not finished; RB_ESIZE if dst_bytes is too small; RB_ENOENT if unknown
- * or already collected; RB_EDEVICE without a device. The library drops its
+ * or already collected; RB_EDEVICE without a device, or (once, after which
+ * the id is unknown) when the run of its window failed. The library drops its
  * copy after a successful collect. */
 rb_status rb_collect(rb_sched* s, uint64_t req_id, float* dst, size_t dst_bytes, int32_t* out_rows);
 

@@ -147,7 +147,7 @@ struct HostReq {
   std::vector<float> dense;
   std::vector<int32_t> lens, ids;
   std::vector<float> out;
-  int state = 0;      // 0 queued, 1 dispatched, 2 done, 3 collected
+  int state = 0;      // 0 queued, 1 dispatched, 2 done, 3 collected, 4 failed (its window's launch failed)
   int slot = -1;      // staging slot holding its output while in flight
   int64_t out_off = 0;  // offset of its rows in the slot's output staging
 };
@@ -848,9 +848,9 @@ rb_status flush_chunk(rb_sched* s) {
       offs.push_back({o1, off});
       off += round_up((int64_t)rr, 256);
     }
+  if (!hip_ok(hipMemcpyAsync(sl->dev, sl->host, off, hipMemcpyHostToDevice, s->stream))) return RB_EDEVICE;
   for (auto& win : s->chunk)
     for (Group& g : win) slot_hold(*sl, g.q->m);
-  if (!hip_ok(hipMemcpyAsync(sl->dev, sl->host, off, hipMemcpyHostToDevice, s->stream))) return RB_EDEVICE;
   std::vector<int64_t> lin;
   for (auto& win : s->chunk)
     for (Group& g : win) lin.push_back(g.q->m->lineage);
@@ -882,14 +882,19 @@ rb_status flush_chunk(rb_sched* s) {
     for (size_t i : used) hipStreamWaitEvent(s->lanes[i], s->ev_copy, 0);
   }
   size_t gi = 0;
-  for (auto& win : s->chunk)
+  for (auto& win : s->chunk) {
     for (Group& g : win) {
       st = run_group(s, where[gi].second, where[gi].first, g, (const rb_k_batch*)(sl->dev + offs[gi].first),
                      (const rb_k_req*)(sl->dev + offs[gi].second), s->a_dense, s->a_dense_len, s->a_lens,
                      s->a_lens_len, s->a_ids, s->a_ids_len, s->a_out, s->a_out_len);
       ++gi;
-      if (st != RB_OK) return st;
+      if (st != RB_OK) break;
     }
+    if (st != RB_OK) break;
+  }
+  // also after a failed launch: the copy out of the slot's host buffer and
+  // any launched work stay fenced by the slot's event, so the buffer is not
+  // rewritten and the models it holds are not released before they finish
   for (size_t i : used) {
     hipEventRecord(s->lane_done[i], s->lanes[i]);
     hipStreamWaitEvent(s->stream, s->lane_done[i], 0);
@@ -897,7 +902,7 @@ rb_status flush_chunk(rb_sched* s) {
   hipEventRecord(sl->ev, s->stream);
   sl->busy = true;
   s->chunk.clear();
-  return RB_OK;
+  return st;
 }
 
 void close_window(rb_sched* s) {
@@ -1515,17 +1520,31 @@ static rb_status run_serving_window(rb_sched* s, const std::vector<Disp>& win) {
     offs.push_back({o1, off});
     off += round_up((int64_t)rr, 256);
   }
+  // a failure from here on: the window's requests fail (rb_collect reports
+  // RB_EDEVICE for them), and whatever was enqueued stays fenced by the
+  // slot's event, so its buffers are not reused before that work is done
+  auto fail = [&](rb_status e) {
+    for (int64_t id : sl->serving_reqs) {
+      HostReq& h = s->hreqs[(size_t)id];
+      h.state = 4;
+      h.slot = -1;
+    }
+    sl->serving_reqs.clear();
+    hipEventRecord(sl->ev, s->stream);
+    sl->busy = true;
+    return e;
+  };
   for (Group& g : groups) slot_hold(*sl, g.q->m);
-  if (!hip_ok(hipMemcpyAsync(sl->dev, sl->host, o_out, hipMemcpyHostToDevice, s->stream))) return RB_EDEVICE;
+  if (!hip_ok(hipMemcpyAsync(sl->dev, sl->host, o_out, hipMemcpyHostToDevice, s->stream))) return fail(RB_EDEVICE);
   float* dout = (float*)(sl->dev + o_out);
   for (size_t gi = 0; gi < groups.size(); ++gi) {
     st = run_group(s, s->stream, 0, groups[gi], (const rb_k_batch*)(sl->dev + offs[gi].first),
                    (const rb_k_req*)(sl->dev + offs[gi].second), (const float*)(sl->dev + o_dense), nd,
                    (const int32_t*)(sl->dev + o_lens), nl, (const int32_t*)(sl->dev + o_ids), ni, dout, no);
-    if (st != RB_OK) return st;
+    if (st != RB_OK) return fail(st);
   }
   if (!hip_ok(hipMemcpyAsync(sl->host_out, dout, (size_t)no * 4, hipMemcpyDeviceToHost, s->stream)))
-    return RB_EDEVICE;
+    return fail(RB_EDEVICE);
   hipEventRecord(sl->ev, s->stream);
   sl->busy = true;
   return RB_OK;
@@ -1597,6 +1616,13 @@ rb_status rb_collect(rb_sched* s, uint64_t req_id, float* dst, size_t dst_bytes,
   if (h.state == 3) return RB_ENOENT;
   if (h.state == 0) return RB_EAGAIN;
   if (!s->stream) return RB_EDEVICE;  // no outputs without a device
+  if (h.state == 4) {  // its window failed: reported once, then forgotten
+    h.state = 3;
+    std::vector<float>().swap(h.dense);
+    std::vector<int32_t>().swap(h.lens);
+    std::vector<int32_t>().swap(h.ids);
+    return RB_EDEVICE;
+  }
   if (h.state == 1) {
     Slot& sl = s->slots[h.slot];
     const hipError_t e = hipEventQuery(sl.ev);
