@@ -402,7 +402,10 @@ static_assert(EMB_CHUNK <= 8, "each of a group's 8 lanes loads one id of a chunk
 // hold their hot rows (all tables at once per row measured 1.5x slower, 4 or
 // 8 slices 1.2x slower).
 // A group finds its bag in the row's flat id list (bag after bag) with an
-// 8-lane sum of the preceding bag lengths. The workgroup's 32 bags are then
+// 8-lane sum of the preceding bag lengths; the row-map entry takes one round
+// trip and all the lengths one more (loaded one after another, as a loop that
+// adds each length as it arrives compiles, they took up to five: the kernel
+// was 4-5% slower on one box). The workgroup's 32 bags are then
 // ranked by length through LDS and the group of rank p walks the bag of rank
 // p, so the 8 bags of a wave have similar lengths and its gather instructions
 // keep most lanes busy (uniform 1..20-id bags: 50 gather instructions per
@@ -436,16 +439,35 @@ __global__ __launch_bounds__(256) void k_embbag(const rb_k_row* __restrict__ row
   {
     const int row = r0 + g / gpr, t = x + n_slices * (g % gpr);
     if (g < rpw * gpr && row < n_rows && t < n_tables) {
-      const rb_k_row rw = rows[row];
+      // the 32-byte entry as two 16-byte loads issued together (the empty asm
+      // uses the second half here, so that its load is not moved after the
+      // test of the first half and waited for separately)
+      const u32x4_t* re = (const u32x4_t*)(rows + row);
+      const u32x4_t e0 = re[0], e1 = re[1];
+      asm volatile("" ::"v"(e1.x), "v"(e1.y));
+      rb_k_row rw;
+      rw.src = (int64_t)((uint64_t)e0.x | ((uint64_t)e0.y << 32));
+      rw.aux = (int64_t)((uint64_t)e0.z | ((uint64_t)e0.w << 32));
+      rw.lens = (int64_t)((uint64_t)e1.x | ((uint64_t)e1.y << 32));
       if (rw.src < 0) {
         L = -2;
       } else {
+        // lane l8 loads the lengths of tables l8, l8 + 8, ... below t and
+        // the bag's own length, all issued before any is used (a loop that
+        // adds each length as it arrives waits for every load in turn)
+        int v[MAX_TABLES / 8];
+#pragma unroll
+        for (int u = 0; u < MAX_TABLES / 8; ++u) {
+          const int f = l8 + 8 * u;
+          v[u] = f < t ? lens[rw.lens + f] : 0;
+        }
+        L = lens[rw.lens + t];
         int pre = 0;
-        for (int f = l8; f < t; f += 8) pre += lens[rw.lens + f];
+#pragma unroll
+        for (int u = 0; u < MAX_TABLES / 8; ++u) pre += v[u];
         pre += __shfl_xor(pre, 1);
         pre += __shfl_xor(pre, 2);
         pre += __shfl_xor(pre, 4);
-        L = lens[rw.lens + t];
         id0 = rw.aux + pre;
       }
     }
