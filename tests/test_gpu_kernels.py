@@ -279,10 +279,13 @@ _LENS = {
 
 
 @pytest.mark.parametrize("entry", ["rb_k_embbag", "rb_k_embbag_dedup"])
-@pytest.mark.parametrize("lens", list(_LENS))
-def test_embbag_matches_oracle(lens, entry):
+@pytest.mark.parametrize("lens,nt", [(k, 26) for k in _LENS] + [("uniform", 1), ("uniform", 5), ("uniform", 64)])
+def test_embbag_matches_oracle(lens, nt, entry):
+    # 26 tables (the ranking model) with every bag-length mix, and 1, 5 and 64
+    # tables (the most a row may have): a bag's start is the sum of the lengths
+    # of the row's earlier bags, loaded up to 8 per lane
     rng = np.random.default_rng(3)
-    nt, rows_t = 26, 1000
+    rows_t = 1000
     kb, kr, arena, R = _make_group(rng, rb.RB_MODEL_RANKING, 4, 512, (64, 128, 256, 512), 13, 1, nt, 0,
                                    max_n=64, lens_gen=_LENS[lens])
     rows, err = _route(rb.RB_MODEL_RANKING, kb, kr, arena, R, 13, 1, nt)
@@ -290,7 +293,7 @@ def test_embbag_matches_oracle(lens, entry):
     tb = [nx.round_bf16(t).astype(np.float32) for t in tables]
     dev_t = [torch.from_numpy((t.view(np.uint32) >> 16).astype(np.uint16).view(np.int16)).to(DEV) for t in tb]
     ptrs = _dev(np.array([t.data_ptr() for t in dev_t], dtype=np.uint64).view(np.int64))
-    ldx = 1728
+    ldx = (nt * 64 + 13 + 63) // 64 * 64
     X = torch.empty((R, ldx), dtype=torch.int16, device=DEV)
     dense, lens, ids = _dev(arena["dense"]), _dev(arena["lens"]), _dev(arena["ids"])
     rb.check(getattr(rb.lib(), entry)(_stream(), rb.dptr(rows), R, rb.dptr(lens), rb.dptr(ids), ids.numel(),
