@@ -545,13 +545,22 @@ __global__ __launch_bounds__(256) void k_embbag(const rb_k_row* __restrict__ row
     *(u32x4_t*)(X + (int64_t)row * ldx + t * EMB_DIM + l8 * 8) = o;
   }
   if (x == 0) {
-    for (int i = 0; i < rpw && r0 + i < n_rows; ++i) {
+    // the dense features and zero tail (columns demb .. ldx, a multiple of 8
+    // wide): one 8-column chunk, a 16-byte store, per thread and pass, so that
+    // the loads of all the block's rows are in flight at once
+    const int cpr = (ldx - demb) >> 3;
+    for (int e = tid; e < rpw * cpr; e += 256) {
+      const int i = e / cpr, c = e - i * cpr;
+      if (r0 + i >= n_rows) break;
       const rb_k_row rw = rows[r0 + i];
-      bf16_t* xr = X + (int64_t)(r0 + i) * ldx;
-      for (int c = demb + tid; c < ldx; c += 256) {
-        const int d = c - demb;
-        xr[c] = d < n_dense ? f2bf(rw.src < 0 ? pad : dense[rw.src + d]) : (bf16_t)0;
+      uint32_t h[8];
+#pragma unroll
+      for (int k = 0; k < 8; ++k) {
+        const int d = 8 * c + k;
+        h[k] = d < n_dense ? (uint32_t)f2bf(rw.src < 0 ? pad : dense[rw.src + d]) : 0u;
       }
+      const u32x4_t o = {h[0] | (h[1] << 16), h[2] | (h[3] << 16), h[4] | (h[5] << 16), h[6] | (h[7] << 16)};
+      *(u32x4_t*)(X + (int64_t)(r0 + i) * ldx + demb + 8 * c) = o;
     }
   }
 }
