@@ -2038,7 +2038,8 @@ rb_status gemm_bf16_impl(void* stream, const void* X, int32_t ldx, const void* W
   // 8 waves of 64 x 128 when fewer (two waves per SIMD hide more of the single
   // round's start and end), else 256 x 128 (8 waves of 64 x 64, k-step
   // 64, 3 stages, 144 KB), else
-  // 128 x 128 (8 waves of 64 x 32, k-step 64, 4 stages, 128 KB). XCD-contiguous
+  // 128 x 128 (8 waves of 64 x 32, k-step 64, 4 stages, 128 KB), 128 x 64 (4
+  // waves of 64 x 32, 96 KB) or 64 x 64 (2 waves of 64 x 32, 64 KB). XCD-contiguous
   // tile order when all of W fits in one XCD's L2 (each XCD then keeps its A
   // row-blocks and W in its own L2); plain order otherwise (contiguous ranges
   // would stream all of W through every XCD).
@@ -2074,7 +2075,17 @@ rb_status gemm_bf16_impl(void* stream, const void* X, int32_t ldx, const void* W
     else
       RB_PICK(256, 128, 64, 64, 512, 64, 3, false);
   } else {
-    RB_PICK(128, 128, 64, 32, 512, 64, 4, false);
+    // fewer tiles than that: the k-loop's latency bounds a launch of a few
+    // batches, so the largest of 128 x 128, 128 x 64 and 64 x 64 tiles that
+    // still gives half the compute units a tile (512 x 1024 x 1728: 12.5 ->
+    // 8.7 us with 64 x 64; 2816 x 512 x 1024: 9.7 -> 7.3 us with 128 x 64)
+    const int64_t rows128 = (M + 127) / 128, half = std::max<int64_t>(cus / 2, 1);
+    if (rows128 * (N / 128) >= half)
+      RB_PICK(128, 128, 64, 32, 512, 64, 4, false);
+    else if (rows128 * (N / 64) >= half)
+      RB_PICK(128, 64, 64, 32, 256, 64, 4, false);
+    else
+      RB_PICK(64, 64, 64, 32, 128, 64, 4, false);
   }
 #undef RB_PICK
   return launch_status();
@@ -2167,13 +2178,22 @@ rb_status rb_k_gemm_head(void* stream, const void* X, int32_t ldx, const void* W
   if (M == 0) return RB_OK;
   // 128 x 256 tiles (every row's 256 outputs in one workgroup), 8 waves of
   // 64 x 64 (two per SIMD: 4 waves of 64 x 128 measured 16% slower), k-step
-  // 64, 3 stages; XCD-contiguous order (W is 256 x K bf16)
-  const unsigned g = (unsigned)((M + 127) / 128);
+  // 64, 3 stages; XCD-contiguous order (W is 256 x K bf16). With fewer such
+  // tiles than half the compute units (a launch of a few batches, bound by
+  // its k-loop's latency), 64 x 256 tiles of 8 waves of 64 x 32.
+  const bool small = (int64_t)(M + 127) / 128 < std::max<int64_t>(device_cus() / 2, 1);
+  const unsigned g = (unsigned)(small ? (M + 63) / 64 : (M + 127) / 128);
   const HeadArgs ha{rows, (const bf16_t*)w_head, b_head, out};
   hipStream_t s = (hipStream_t)stream;
 #define RB_GH(A, H)                                                                                                    \
-  hipLaunchKernelGGL((k_gemm_head<128, 256, 64, 64, 512, 128, 3, 1, A, H>), dim3(g), dim3(512), 0, s,                \
-                     (const bf16_t*)X, ldx, (const bf16_t*)W, ldw, b, M, K, ha)
+  do {                                                                                                                 \
+    if (small)                                                                                                         \
+      hipLaunchKernelGGL((k_gemm_head<64, 256, 64, 32, 512, 128, 3, 1, A, H>), dim3(g), dim3(512), 0, s,             \
+                         (const bf16_t*)X, ldx, (const bf16_t*)W, ldw, b, M, K, ha);                                   \
+    else                                                                                                               \
+      hipLaunchKernelGGL((k_gemm_head<128, 256, 64, 64, 512, 128, 3, 1, A, H>), dim3(g), dim3(512), 0, s,            \
+                         (const bf16_t*)X, ldx, (const bf16_t*)W, ldw, b, M, K, ha);                                   \
+  } while (0)
   if (head_act == RB_ACT_SIGMOID) {
     if (act == RB_ACT_RELU) RB_GH(RB_ACT_RELU, RB_ACT_SIGMOID);
     else if (act == RB_ACT_SIGMOID) RB_GH(RB_ACT_SIGMOID, RB_ACT_SIGMOID);

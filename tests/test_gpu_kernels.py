@@ -430,7 +430,10 @@ def _row_scaled_err(y, ref):
     (2100, 8192, 512, rb.RB_ACT_SIGMOID, 0, 0), (25600 - 37, 384, 192, rb.RB_ACT_RELU, 1, 0),
     # at least two 256 x 256 tiles per compute unit: 4 waves of 128 x 128 (XCD
     # and plain tile order)
-    (8500, 4096, 192, rb.RB_ACT_RELU, 0, 0), (4500 + 11, 8192, 512, rb.RB_ACT_NONE, 1, 0)])
+    (8500, 4096, 192, rb.RB_ACT_RELU, 0, 0), (4500 + 11, 8192, 512, rb.RB_ACT_NONE, 1, 0),
+    # few tiles: 128 x 128 when there are at least half as many as compute
+    # units, else 128 x 64 (1024 x 1024), else 64 x 64 (the small shapes above)
+    (2816 - 5, 1024, 1728, rb.RB_ACT_RELU, 0, 0), (2816 + 3, 512, 1024, rb.RB_ACT_SIGMOID, 1, 0)])
 def test_gemm_bf16_matches_fp64(M, N, K, act, out_f32, pad_y):
     rng = np.random.default_rng(4)
     Xd, X = _bf16_dev(rng.standard_normal((M, K)))
@@ -486,7 +489,7 @@ def test_gemm_rows_independent_of_batch(dtype, N, K):
     # bf16 launch of all rows takes a larger tile than the partial ones: N = 4096
     # and 2048 give the full launch at least two 256 x 256 tiles per compute
     # unit (4 waves of 128 x 128, 2 stages),
-    # while the partial launches take 128 x 128 tiles of 8 waves with 4 stages)
+    # while the partial launches take 128 x 64 or 64 x 64 tiles with 4 stages)
     rng = np.random.default_rng(11)
     M = 16384
     X = rng.standard_normal((M, K)).astype(np.float32)
@@ -638,12 +641,15 @@ def test_mlp_tail_bit_identical_to_separate_kernels(M, K2, act):
 @pytest.mark.parametrize("M,K,act,hact", [(1000, 512, rb.RB_ACT_RELU, rb.RB_ACT_SIGMOID),
                                           (300, 192, rb.RB_ACT_RELU, rb.RB_ACT_NONE),
                                           (128, 64, rb.RB_ACT_NONE, rb.RB_ACT_SIGMOID),
-                                          (4133, 512, rb.RB_ACT_RELU, rb.RB_ACT_SIGMOID)])
+                                          (4133, 512, rb.RB_ACT_RELU, rb.RB_ACT_SIGMOID),
+                                          (20000 + 7, 512, rb.RB_ACT_RELU, rb.RB_ACT_SIGMOID)])
 def test_gemm_head_bit_identical_to_separate_kernels(M, K, act, hact):
     # the last hidden layer (256 outputs) with the head in its epilogue against
     # rb_k_gemm_bf16 and rb_k_head on the same operands: the same bits in
     # every output, rows whose output is -1 skipped, ragged last tiles; and
-    # within the fp64 bound of the definition
+    # within the fp64 bound of the definition. 64-row tiles below 128 x 128
+    # rows (half the compute units' worth of 128-row tiles), 128-row tiles at
+    # 20007 rows
     rng = np.random.default_rng(29)
     ldx = K + 64
     Xd, X = _bf16_dev(np.maximum(rng.standard_normal((M, ldx)), 0))
